@@ -1,0 +1,155 @@
+"""End-to-end draft-and-verify on the float64 oracle decoders.
+
+State of one sequence (the pending-token model):
+
+* ``history`` holds every committed token x_0..x_n; the last one, x_n at
+  position n, is *pending*: it is not yet in the target's KV cache, whose
+  length is n.
+* the draft cache has length len_d <= n; its pending tokens are
+  history[len_d..n] (one token normally, two after a step that accepted all
+  drafts).
+* draft step j feeds the draft model its pending tokens (j = 1) or x~_{j-1}
+  (j > 1) and draws x~_j at position n+j from the last row's logits.
+* verify feeds the target x_n, x~_1..x~_k at positions n..n+k (their K/V are
+  written first, then each row attends causally) and applies the rule.
+* commit with a accepted: the a+1 emitted tokens join the history; the target
+  cache keeps positions <= n+a (length n+a+1); the draft cache keeps
+  min(len_d, n+a+1); rejected positions are dropped in place.
+
+A prompt of P tokens is prefilled into both caches for positions 0..P-2, and
+x_{P-1} is pending.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from .decoder import Decoder, KVList
+from .paging import PagePool
+from . import rule
+
+
+@dataclass
+class SeqState:
+    history: List[int]
+    kv_t: KVList
+    kv_d: KVList
+    drafts: List[int] = field(default_factory=list)
+    zq: List[np.ndarray] = field(default_factory=list)
+    draft_excluded: bool = False
+
+    @property
+    def n(self) -> int:            # position of the pending token
+        return len(self.history) - 1
+
+
+class Session:
+    def __init__(self, target: Decoder, draft: Decoder, num_pages_target: int,
+                 num_pages_draft: int, page_size: int = 16):
+        self.target = target
+        self.draft = draft
+        self.pool_t = PagePool(num_pages_target, page_size)
+        self.pool_d = PagePool(num_pages_draft, page_size)
+        self.seqs: Dict[int, SeqState] = {}
+
+    # ------------------------------------------------------------------
+    def prefill(self, seq_ids: Sequence[int], prompts: Sequence[Sequence[int]]):
+        for sid, prompt in zip(seq_ids, prompts):
+            sid = int(sid)
+            prompt = [int(t) for t in prompt]
+            assert len(prompt) >= 1 and sid not in self.seqs
+            st = SeqState(prompt, self.target.new_kv(), self.draft.new_kv())
+            P = len(prompt)
+            self.pool_t.ensure(sid, P - 1)
+            self.pool_d.ensure(sid, P - 1)
+            if P > 1:
+                self.target.forward(st.kv_t, prompt[:-1], np.arange(P - 1), logits=False)
+                self.draft.forward(st.kv_d, prompt[:-1], np.arange(P - 1), logits=False)
+            self.seqs[sid] = st
+
+    def draft_step(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int,
+                   margins: rule.Margins = rule.Margins()) -> List[int]:
+        out = []
+        for sid, T in zip(seq_ids, temps):
+            st = self.seqs[int(sid)]
+            if st.drafts:
+                toks = [st.drafts[-1]]
+            else:
+                toks = st.history[st.kv_d.length:]
+            start = st.kv_d.length
+            self.pool_d.ensure(int(sid), start + len(toks))
+            z = self.draft.forward(st.kv_d, toks, start + np.arange(len(toks)))[-1]
+            pos = st.n + len(st.drafts) + 1
+            x, bad = rule.sample_draft(z, float(T), seed, int(sid), pos, margins)
+            st.drafts.append(x)
+            st.zq.append(z)
+            st.draft_excluded |= bad
+            out.append(x)
+        return out
+
+    def set_drafts(self, sid: int, drafts: Sequence[int], zq: np.ndarray):
+        """Install externally supplied drafts (tokens and their draft logits)."""
+        st = self.seqs[int(sid)]
+        st.drafts = [int(x) for x in drafts]
+        st.zq = [np.asarray(r, dtype=np.float64) for r in zq]
+
+    def verify(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int,
+               margins: rule.Margins = rule.Margins()):
+        """Returns a list of (VerifyResult, target logits [k+1, V])."""
+        out = []
+        for sid, T in zip(seq_ids, temps):
+            sid = int(sid)
+            st = self.seqs[sid]
+            n, k = st.n, len(st.drafts)
+            self.pool_t.ensure(sid, n + k + 1)
+            rows = [st.history[-1]] + st.drafts
+            zp = self.target.forward(st.kv_t, rows, n + np.arange(k + 1))
+            zq = np.stack(st.zq) if k else np.zeros((0, zp.shape[1]))
+            res = rule.verify(zp, zq, st.drafts, float(T), seed, sid, n, margins)
+            if st.draft_excluded:
+                res.excluded = True
+                res.first_excluded = 0 if res.first_excluded is None else res.first_excluded
+            out.append((res, zp))
+        return out
+
+    def commit(self, seq_ids: Sequence[int], results: Sequence[rule.VerifyResult]):
+        for sid, res in zip(seq_ids, results):
+            sid = int(sid)
+            st = self.seqs[sid]
+            n, a = st.n, res.n_accepted
+            st.history.extend(res.tokens)
+            new_t = n + a + 1
+            new_d = min(st.kv_d.length, new_t)
+            st.kv_t.truncate(new_t)
+            st.kv_d.truncate(new_d)
+            self.pool_t.truncate(sid, new_t)
+            self.pool_d.truncate(sid, new_d)
+            st.drafts, st.zq, st.draft_excluded = [], [], False
+
+    def rollback(self, sid: int, new_len: int):
+        """Truncate both caches to ``new_len`` positions; history[new_len] becomes
+        the pending token.  Outstanding drafts are dropped."""
+        st = self.seqs[int(sid)]
+        assert 0 <= new_len <= st.kv_t.length
+        del st.history[new_len + 1:]
+        st.kv_t.truncate(new_len)
+        st.kv_d.truncate(min(st.kv_d.length, new_len))
+        self.pool_t.truncate(int(sid), new_len)
+        self.pool_d.truncate(int(sid), st.kv_d.length)
+        st.drafts, st.zq, st.draft_excluded = [], [], False
+
+    def release(self, sid: int):
+        self.pool_t.release(int(sid))
+        self.pool_d.release(int(sid))
+        del self.seqs[int(sid)]
+
+    # ------------------------------------------------------------------
+    def lengths(self, sid: int):
+        st = self.seqs[int(sid)]
+        return st.kv_t.length, st.kv_d.length
+
+    def pages(self, sid: int):
+        return list(self.pool_t.tables.get(int(sid), [])), list(self.pool_d.tables.get(int(sid), []))

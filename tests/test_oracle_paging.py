@@ -1,0 +1,71 @@
+"""Pins of the page-assignment simulation and of the session's cache bookkeeping."""
+
+import numpy as np
+import pytest
+
+from oracle.paging import PageOOM, PagePool
+from oracle.decoder import Decoder
+from oracle.session import Session
+from workloads import ModelShape, model_weights
+
+
+def test_lowest_free_first_and_eager_free():
+    p = PagePool(8, page_size=16)
+    p.ensure(1, 33)          # 3 pages
+    p.ensure(2, 16)          # 1 page
+    assert p.tables[1] == [0, 1, 2] and p.tables[2] == [3]
+    p.truncate(1, 17)        # keeps pages for positions 0..16 -> 2 pages
+    assert p.tables[1] == [0, 1]
+    p.ensure(2, 40)          # needs 2 more: lowest free are 2 and 4
+    assert p.tables[2] == [3, 2, 4]
+    assert p.slot(2, 17) == 2 * 16 + 1
+    p.truncate(1, 0)
+    assert p.tables[1] == [] and sorted(p.free) == [0, 1, 5, 6, 7]
+
+
+def test_oom_leaves_state_unchanged():
+    p = PagePool(4, page_size=16)
+    p.ensure(1, 48)
+    before = (list(p.free), {k: list(v) for k, v in p.tables.items()})
+    with pytest.raises(PageOOM):
+        p.ensure(2, 33)
+    assert (list(p.free), {k: list(v) for k, v in p.tables.items()}) == before
+
+
+def test_boundaries():
+    p = PagePool(4, page_size=16)
+    p.ensure(1, 16)
+    assert len(p.tables[1]) == 1
+    p.ensure(1, 17)
+    assert len(p.tables[1]) == 2
+    p.truncate(1, 16)
+    assert len(p.tables[1]) == 1
+    p.ensure(3, 0)
+    assert p.tables[3] == []
+
+
+def test_session_lengths_pages_and_history():
+    """Scripted steps: lengths after commit follow n+a+1 / min(len_d, n+a+1), and
+    page tables cover exactly the cached positions."""
+    sh = ModelShape("pg", 1, 16, 2, 2, 8, 16, 20, 1e4, dtype="f32", init_std=0.3)
+    dec = Decoder(sh, model_weights(sh, 51))
+    sess = Session(dec, dec, 32, 32, page_size=4)
+    sess.prefill([1, 2], [[1, 2, 3, 4, 5], [6, 7]])
+    assert sess.lengths(1) == (4, 4) and sess.lengths(2) == (1, 1)
+    for _ in range(3):
+        sess.draft_step([1, 2], [0.7, 0.7], seed=3)
+    assert sess.lengths(1) == (4, 7)
+    out = sess.verify([1, 2], [0.7, 0.7], seed=3)
+    res = [r for r, _ in out]
+    sess.commit([1, 2], res)
+    for sid, r, n0 in ((1, res[0], 4), (2, res[1], 1)):
+        lt, ld = sess.lengths(sid)
+        assert lt == n0 + r.n_accepted + 1
+        assert ld == min(n0 + 3, n0 + r.n_accepted + 1)
+        pt, pd = sess.pages(sid)
+        assert len(pt) == (lt + 3) // 4 and len(pd) == (ld + 3) // 4
+    sess.rollback(1, 2)
+    assert sess.lengths(1) == (2, 2)
+    assert sess.seqs[1].history == [1, 2, 3]
+    used = sum(len(v) for v in sess.pool_t.tables.values())
+    assert used + len(sess.pool_t.free) == 32
