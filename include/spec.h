@@ -1,0 +1,223 @@
+/*
+ * spec.h - C ABI of the speculative-decoding verify step on MI355X (gfx950).
+ *
+ * The operation is the draft-and-verify generation of CacheSpec (Section 3.4,
+ * "Cache-Miss Branch"; Section 2, speculative-decoding paragraph): a small
+ * draft model proposes k tokens, the target model scores all of them in one
+ * batched forward pass, and speculative sampling accepts each draft x~_j with
+ * probability min(1, p_j(x~_j) / q_j(x~_j)); at the first rejection one token
+ * is drawn from norm(max(0, p_j - q_j)) instead, and if all k are accepted a
+ * bonus token is drawn from p_{k+1}.  Temperature 0 is greedy: drafts are
+ * accepted while they equal the target's argmax.
+ *
+ * Conventions
+ *  - Every pointer documented "device" is a HIP device address; "host" is CPU
+ *    memory.  Sizes are element counts unless stated.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *    calls enqueue work on it and return without waiting, except where a call
+ *    says it blocks.
+ *  - Ownership: the caller owns every device buffer it passes (weights, KV
+ *    pools, workspace, inputs, outputs) and keeps them alive for as long as a
+ *    context that refers to them exists.  The library never frees them.  The
+ *    library owns the context, its host metadata, pinned staging memory and
+ *    events.
+ *  - Errors are returned as spec_status; no exception crosses the ABI.  On any
+ *    error other than SPEC_E_HIP the context's state is unchanged (page
+ *    exhaustion is detected before anything is enqueued).  SPEC_E_HIP is
+ *    sticky: destroy the context.  spec_last_error() explains the last failure.
+ *  - A context is not thread-safe.
+ *
+ * Random numbers: Philox4x32-10 (Salmon et al., SC'11) keyed by the 64-bit
+ * `seed`; the counter is (block, position, seq_id bits 0..31, seq_id bits
+ * 32..55 << 8 | purpose) with purpose DRAFT=0, ACCEPT=1, RESAMPLE=2, BONUS=3.
+ * A uniform is ((word >> 9) + 0.5) * 2^-23; vocabulary noise for token i is
+ * word i & 3 of block i >> 2.  Because noise is keyed by the caller's stable
+ * seq_id and the absolute position of the token being decided, results do not
+ * depend on batch composition or on the order of sequences in a call.
+ */
+#ifndef SPEC_H_
+#define SPEC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPEC_API __attribute__((visibility("default")))
+
+typedef int32_t spec_status;
+enum {
+  SPEC_OK = 0,
+  SPEC_E_INVALID = 1,     /* bad argument (null pointer, size out of range, unknown seq) */
+  SPEC_E_NOPAGES = 2,     /* a KV page pool is exhausted; nothing was changed */
+  SPEC_E_HIP = 3,         /* a HIP runtime call failed; the context is unusable */
+  SPEC_E_STATE = 4,       /* call out of order (verify twice, commit without verify, ...) */
+  SPEC_E_UNSUPPORTED = 5  /* valid but unsupported shape (e.g. head_dim not 64/128) */
+};
+
+enum { SPEC_F32 = 0, SPEC_BF16 = 1 };
+enum { SPEC_DRAFT = 0, SPEC_ACCEPT = 1, SPEC_RESAMPLE = 2, SPEC_BONUS = 3 };
+
+/* One decoder layer's weights (device pointers, element type = model dtype,
+ * row-major with the reduction dimension innermost):
+ *   attn_norm, mlp_norm  [d]
+ *   wqkv       [(Hq + 2*Hkv) * hd, d]   rows: q heads, then k heads, then v heads
+ *   wo         [d, Hq * hd]
+ *   w_gate_up  [2 * ffn, d]             rows 0..ffn-1 gate, ffn..2ffn-1 up
+ *   w_down     [d, ffn]                                                       */
+typedef struct spec_layer_weights {
+  const void* attn_norm;
+  const void* wqkv;
+  const void* wo;
+  const void* mlp_norm;
+  const void* w_gate_up;
+  const void* w_down;
+} spec_layer_weights;
+
+/* A Llama-style decoder: RMSNorm -> QKV -> rotate-half RoPE -> causal GQA
+ * attention -> O (+ residual) -> RMSNorm -> SwiGLU MLP (+ residual); final
+ * RMSNorm and an untied LM head producing fp32 logits.  Residual stream fp32. */
+typedef struct spec_model_desc {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  int32_t dtype;          /* SPEC_F32 or SPEC_BF16: weights, KV cache, GEMM inputs */
+  float rope_theta, rms_eps;
+  const void* embed;      /* device [vocab, d] */
+  const void* final_norm; /* device [d] */
+  const void* lm_head;    /* device [vocab, d] */
+  const spec_layer_weights* layers; /* host array [n_layers]; copied by spec_ctx_create */
+} spec_model_desc;
+
+/* Paged KV cache.  Each pool holds, per layer, K pages [page][Hkv][16][hd] and
+ * V pages stored transposed [page][Hkv][hd][16], element type = model dtype;
+ * size it with spec_kv_pool_bytes(). */
+typedef struct spec_cache_desc {
+  int32_t page_size;          /* must be 16 */
+  int32_t num_pages_target;
+  int32_t num_pages_draft;
+  int32_t max_seqs;           /* live sequences at once */
+  int32_t max_pages_per_seq;
+  int32_t k_max;              /* most drafts per sequence per step (1..15) */
+  int32_t max_rows;           /* most rows per forward launch; prefill is chunked to it */
+  void* kv_target;            /* device */
+  void* kv_draft;             /* device */
+} spec_cache_desc;
+
+typedef struct spec_ctx spec_ctx;
+
+/* Bytes one KV pool of `num_pages` pages needs for model `m`. */
+SPEC_API size_t spec_kv_pool_bytes(const spec_model_desc* m, int32_t num_pages);
+
+/* Create a context for a target/draft pair (same vocabulary and dtype). */
+SPEC_API spec_status spec_ctx_create(const spec_model_desc* target, const spec_model_desc* draft,
+                                     const spec_cache_desc* cache, spec_ctx** out);
+SPEC_API void spec_ctx_destroy(spec_ctx* ctx);
+/* Message of the last failure; owned by ctx (or static for ctx == NULL), valid
+ * until the next call on it. */
+SPEC_API const char* spec_last_error(const spec_ctx* ctx);
+
+/* Device workspace the context needs (activations, logits, draft rows,
+ * attention partials, metadata).  Call spec_set_workspace once before any
+ * compute call; the buffer must be 256-byte aligned and stay alive. */
+SPEC_API size_t spec_workspace_bytes(const spec_ctx* ctx);
+SPEC_API spec_status spec_set_workspace(spec_ctx* ctx, void* dev_ptr, size_t bytes);
+
+/* Prefill: register `n` new sequences (caller-chosen, distinct, stable ids)
+ * with prompts `tokens` (host, packed, prompt_lens[i] >= 1 tokens each) and run
+ * positions 0..P-2 through both models (no LM head).  The last prompt token
+ * becomes the pending token.  Pages: lowest-numbered free page first, in list
+ * order.  Blocks until the work is done. */
+SPEC_API spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
+                                  const int32_t* prompt_lens, const int32_t* tokens, void* stream);
+
+/* One draft step for each listed sequence: the draft model consumes its
+ * pending tokens (the committed tail not yet in the draft cache on the first
+ * step after a commit, else the previous draft) and draws the next draft token
+ * x~_j at position n+j from softmax(z/T) by Gumbel-max with DRAFT noise
+ * (argmax for T == 0).  The draft logits row is kept for the verify.  A
+ * sequence is drafted at most k_max times between verifies.
+ * temperature: host [n], >= 0.  Asynchronous. */
+SPEC_API spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
+                                     const float* temperature, uint64_t seed, void* stream);
+
+/* Replace a sequence's drafts by externally supplied ones: k tokens (host) and
+ * their draft logits rows (device fp32 [k, vocab], which must stay alive until
+ * the verify has run). */
+SPEC_API spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k,
+                                     const int32_t* tokens, const float* q_logits, void* stream);
+
+/* Verify: feed [x_n, x~_1..x~_k] at positions n..n+k through the target (their
+ * K/V are written to the cache first, then each row attends causally), produce
+ * fp32 logits, and apply the speculative sampling rule per sequence with its
+ * own temperature.  Outputs (host): n_accepted[i] = a_i in 0..k_i and
+ * out_tokens[i * (k_max + 1) + j] for j <= a_i (x~_1..x~_a, then the resampled
+ * or bonus token); other entries are -1.  Committed lengths do not change.
+ * Blocks until the outputs are on the host. */
+SPEC_API spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
+                                 const float* temperature, uint64_t seed,
+                                 int32_t* n_accepted, int32_t* out_tokens, void* stream);
+
+/* Commit the last verify of each listed sequence with a accepted drafts
+ * (normally the a returned by spec_verify): the target cache keeps positions
+ * <= n+a, the draft cache keeps min(its length, n+a+1) positions, the emitted
+ * tokens join the history, rejected K/V slots are cleared in place and pages
+ * holding no kept position return to the free pool.  Asynchronous. */
+SPEC_API spec_status spec_kv_commit(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
+                                    const int32_t* n_accepted, void* stream);
+
+/* Truncate both caches of a sequence to `new_len` positions (0 <= new_len <=
+ * target length); history[new_len] becomes the pending token and outstanding
+ * drafts are dropped.  Cleared in place like a commit.  Asynchronous. */
+SPEC_API spec_status spec_kv_rollback(spec_ctx* ctx, int64_t seq_id, int32_t new_len, void* stream);
+
+/* Forget a sequence and free its pages. */
+SPEC_API spec_status spec_seq_release(spec_ctx* ctx, int64_t seq_id);
+
+/* Introspection (host outputs): committed target/draft lengths, pending token
+ * position n, and the page tables (*n_pages_* entries are written, at most
+ * max_pages each).  Useful for checking KV indices. */
+SPEC_API spec_status spec_seq_info(const spec_ctx* ctx, int64_t seq_id, int32_t* target_len,
+                                   int32_t* draft_len, int32_t* pending_pos,
+                                   int32_t* pages_target, int32_t* n_pages_target,
+                                   int32_t* pages_draft, int32_t* n_pages_draft, int32_t max_pages);
+
+/* Device address of the last verify's target logits, fp32 [rows, vocab] in
+ * call order (sequence i's k_i + 1 rows are contiguous), and the row count. */
+SPEC_API spec_status spec_last_logits(const spec_ctx* ctx, const float** logits, int32_t* rows);
+
+/* ---------------------------------------------------------------------------
+ * The decision pass alone, on caller-provided device logits.
+ *
+ * B sequences; sequence b has k[b] drafts (0..15), temperature[b] >= 0,
+ * stable id seq_ids[b] and pending-token position base_pos[b] (all host arrays).
+ * p_logits: device fp32 [sum(k+1), V], sequence b's rows contiguous in order.
+ * q_logits: device fp32 [sum(k), V], likewise.  draft_tokens: device int32
+ * [sum(k)].  Outputs (device): n_accepted[B], out_tokens[B * (k_max + 1)]
+ * where k_max = max k[b].  workspace: device, >= spec_sample_workspace_bytes.
+ * Asynchronous; host arrays are consumed before return. */
+SPEC_API size_t spec_sample_workspace_bytes(int32_t B, int32_t total_rows, int32_t V);
+SPEC_API spec_status spec_sample_verify(int32_t B, const int32_t* k, const float* temperature,
+                                        const int64_t* seq_ids, const int32_t* base_pos,
+                                        const float* p_logits, const float* q_logits,
+                                        const int32_t* draft_tokens, int32_t V, uint64_t seed,
+                                        int32_t* n_accepted, int32_t* out_tokens,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Draw one draft token per row: row i of `logits` (device fp32 [n, V]) is the
+ * draft distribution for position pos[i] of sequence seq_ids[i] (host arrays);
+ * tokens (device int32 [n]) <- Gumbel-max with DRAFT noise, argmax if T == 0. */
+SPEC_API spec_status spec_sample_draft(int32_t n, const float* logits, int32_t V,
+                                       const float* temperature, const int64_t* seq_ids,
+                                       const int32_t* pos, uint64_t seed, int32_t* tokens,
+                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* The generator itself: out (device fp32 [n]) <- uniforms of stream
+ * (seed, seq_id, pos, purpose), words 0..n-1. */
+SPEC_API spec_status spec_philox_uniform(uint64_t seed, int64_t seq_id, int32_t pos, int32_t purpose,
+                                         int32_t n, float* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPEC_H_ */

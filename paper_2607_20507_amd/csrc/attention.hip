@@ -1,0 +1,297 @@
+// Paged causal grouped-query attention on gfx950.
+//
+// Row r of sequence s sits at absolute position pos_r and attends keys
+// 0..pos_r of its own cache (the verify window's K/V are written before this
+// kernel runs, so drafts see each other causally).  Query head h reads kv head
+// h / (Hq / Hkv).  Scale 1/sqrt(hd).
+//
+// KV pages hold 16 tokens: K as [page][Hkv][16][hd] and V transposed as
+// [page][Hkv][hd][16].  The bf16 kernel assigns one wave per (rows of one
+// sequence, kv head, key range) and runs both products on MFMA:
+//   S^T = K Q^T : A = 16 keys x 32 dims of K, B = 32 dims x 16 query vectors.
+//   O^T = V^T P^T: A = 16 dims x 32 keys of V^T, B = P^T.
+// Keys inside each 32-key chunk are permuted (A row i of key tile h reads key
+// 8 (i / 4) + 4 h + i % 4) so that the S^T accumulators a lane ends up with are
+// exactly the 8 consecutive keys it must supply as the P^T operand, and the
+// softmax statistics of query vector (l % 16) stay lane-local: no shuffles of
+// P, no LDS.  Every K and V^T operand is one contiguous 16-byte load.  Long
+// contexts are split into key ranges (multiples of 32) whose unnormalised
+// partials a combine kernel merges.
+
+#include <cmath>
+
+#include "attention.h"
+#include "common.h"
+
+namespace spec {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ uint32_t mask_pair(uint32_t w, int valid) {
+  // keep the first `valid` (0, 1, 2) bf16 halves of a 32-bit word
+  return valid >= 2 ? w : (valid == 1 ? (w & 0xFFFFu) : 0u);
+}
+
+template <int HD, int NT>
+__global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
+  constexpr int DS = HD / 32;   // MFMA k-steps over the head dim
+  constexpr int DPL = HD / 4;   // contiguous dims per lane group
+  constexpr int DT = HD / 16;   // 16-dim output tiles
+  const AttnItem it = items[blockIdx.x];
+  const int gkv = blockIdx.y;
+  const int lane = threadIdx.x, g = lane >> 4, l16 = lane & 15;
+  const int G = a.Hq / a.Hkv;
+  const int M = it.nrows * G;
+  const bf16_t* q = static_cast<const bf16_t*>(a.q);
+  const bf16_t* kp = static_cast<const bf16_t*>(a.kpool);
+  const bf16_t* vp = static_cast<const bf16_t*>(a.vpool);
+  const int32_t* pt = a.page_table + static_cast<size_t>(it.seq) * a.max_pages;
+
+  uint4 qf[NT][DS];
+  int vpos[NT];
+  bool vval[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int m = 16 * nt + l16;
+    vval[nt] = m < M;
+    const int mm = vval[nt] ? m : 0;
+    vpos[nt] = it.pos0 + mm / G;
+    const bf16_t* base =
+        q + (static_cast<size_t>(it.row0 + mm / G) * a.Hq + gkv * G + mm % G) * HD + g * DPL;
+#pragma unroll
+    for (int s = 0; s < DS; ++s)
+      qf[nt][s] = vval[nt] ? reinterpret_cast<const uint4*>(base)[s] : make_uint4(0, 0, 0, 0);
+  }
+  const float scale = kLog2e / sqrtf(static_cast<float>(HD));
+  float mrun[NT], lrun[NT];
+  f32x4 acc[DT][NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    mrun[nt] = -INFINITY;
+    lrun[nt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  for (int c0 = it.t0; c0 < it.t1; c0 += 32) {
+    uint4 kf[2][DS];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int t = min(c0 + 8 * (l16 >> 2) + 4 * hh + (l16 & 3), it.t1 - 1);
+      const bf16_t* kb =
+          kp + (static_cast<size_t>(pt[t >> 4] * a.Hkv + gkv) * 16 + (t & 15)) * HD + g * DPL;
+#pragma unroll
+      for (int s = 0; s < DS; ++s) kf[hh][s] = reinterpret_cast<const uint4*>(kb)[s];
+    }
+    const int tv = c0 + 8 * g;
+    const int nvalid = min(max(it.t1 - tv, 0), 8);
+    const int tvc = min(tv, it.t1 - 1);
+    const bf16_t* vb = vp + static_cast<size_t>(pt[tvc >> 4] * a.Hkv + gkv) * HD * 16 + (tvc & 8);
+
+    uint4 pf[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DS; ++s) {
+        s0 = mfma16x16x32(kf[0][s], qf[nt][s], s0);
+        s1 = mfma16x16x32(kf[1][s], qf[nt][s], s1);
+      }
+      float sv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int t = c0 + 8 * g + j;
+        const float raw = (j < 4) ? s0[j] : s1[j - 4];
+        const bool ok = vval[nt] && t < it.t1 && t <= vpos[nt];
+        sv[j] = ok ? raw * scale : -INFINITY;
+      }
+      float mx = sv[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) mx = fmaxf(mx, sv[j]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float mnew = fmaxf(mrun[nt], mx);
+      float p[8];
+      float alpha = 1.f;
+      if (mnew == -INFINITY) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) p[j] = 0.f;
+      } else {
+        alpha = (mrun[nt] == -INFINITY) ? 0.f : exp2f(mrun[nt] - mnew);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) p[j] = exp2f(sv[j] - mnew);
+      }
+      float ps = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ps += p[j];
+      lrun[nt] = lrun[nt] * alpha + ps;
+      mrun[nt] = mnew;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) acc[dt][nt] *= alpha;
+      pf[nt] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                          pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      uint4 v = *reinterpret_cast<const uint4*>(vb + (16 * dt + l16) * 16);
+      if (nvalid < 8) {
+        v.x = mask_pair(v.x, nvalid);
+        v.y = mask_pair(v.y, nvalid - 2);
+        v.z = mask_pair(v.z, nvalid - 4);
+        v.w = mask_pair(v.w, nvalid - 6);
+      }
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[dt][nt] = mfma16x16x32(v, pf[nt], acc[dt][nt]);
+    }
+  }
+
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float lt = lrun[nt];
+    lt += __shfl_xor(lt, 16, kWave);
+    lt += __shfl_xor(lt, 32, kWave);
+    const int m = 16 * nt + l16;
+    if (m >= M) continue;
+    if (it.part < 0) {
+      const float inv = (lt > 0.f) ? 1.f / lt : 0.f;
+      bf16_t* o = static_cast<bf16_t*>(a.out) +
+                  (static_cast<size_t>(it.row0 + m / G) * a.Hq + gkv * G + m % G) * HD;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const f32x4 v = acc[dt][nt];
+        *reinterpret_cast<uint2*>(o + 16 * dt + 4 * g) =
+            make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+      }
+    } else {
+      const size_t pm = static_cast<size_t>(it.part * a.Hkv + gkv) * 64 + m;
+      float* po = a.part_o + pm * HD;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<float4*>(po + 16 * dt + 4 * g) =
+            make_float4(acc[dt][nt][0], acc[dt][nt][1], acc[dt][nt][2], acc[dt][nt][3]);
+      if (g == 0) {
+        a.part_ml[pm * 2] = mrun[nt];
+        a.part_ml[pm * 2 + 1] = lt;
+      }
+    }
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a, const AttnGroup* __restrict__ groups) {
+  const AttnGroup gr = groups[blockIdx.x];
+  const int gkv = blockIdx.y;
+  const int G = a.Hq / a.Hkv;
+  const int M = gr.nrows * G;
+  for (int e = threadIdx.x; e < M * HD; e += blockDim.x) {
+    const int m = e / HD, d = e % HD;
+    float mx = -INFINITY;
+    for (int c = 0; c < gr.nparts; ++c)
+      mx = fmaxf(mx, a.part_ml[(static_cast<size_t>((gr.part0 + c) * a.Hkv + gkv) * 64 + m) * 2]);
+    float num = 0.f, den = 0.f;
+    if (mx != -INFINITY) {
+      for (int c = 0; c < gr.nparts; ++c) {
+        const size_t pm = static_cast<size_t>((gr.part0 + c) * a.Hkv + gkv) * 64 + m;
+        const float mc = a.part_ml[pm * 2];
+        if (mc == -INFINITY) continue;
+        const float w = exp2f(mc - mx);
+        num += w * a.part_o[pm * HD + d];
+        den += w * a.part_ml[pm * 2 + 1];
+      }
+    }
+    const size_t o = (static_cast<size_t>(gr.row0 + m / G) * a.Hq + gkv * G + m % G) * HD + d;
+    static_cast<bf16_t*>(a.out)[o] = f32_to_bf16(den > 0.f ? num / den : 0.f);
+  }
+}
+
+// fp32: one wave per (row, head); each lane runs an online softmax over keys
+// lane, lane + 64, ...; lanes are merged through LDS.
+template <int HD>
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, const int32_t* __restrict__ row_seq,
+                                                      const int32_t* __restrict__ row_pos) {
+  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int G = a.Hq / a.Hkv, gkv = h / G;
+  const int pos = row_pos[r];
+  const int32_t* pt = a.page_table + static_cast<size_t>(row_seq[r]) * a.max_pages;
+  const float* kp = static_cast<const float*>(a.kpool);
+  const float* vp = static_cast<const float*>(a.vpool);
+  __shared__ float qs[HD];
+  __shared__ float red[kWave][HD + 1];
+  __shared__ float ms[kWave], ls[kWave];
+  const float* qv = static_cast<const float*>(a.q) + (static_cast<size_t>(r) * a.Hq + h) * HD;
+  for (int d = lane; d < HD; d += kWave) qs[d] = qv[d];
+  __syncthreads();
+  const float scale = 1.f / sqrtf(static_cast<float>(HD));
+  float m = -INFINITY, l = 0.f, acc[HD];
+#pragma unroll
+  for (int d = 0; d < HD; ++d) acc[d] = 0.f;
+  for (int t = lane; t <= pos; t += kWave) {
+    const size_t pb = static_cast<size_t>(pt[t >> 4] * a.Hkv + gkv);
+    const float* kr = kp + (pb * 16 + (t & 15)) * HD;
+    float s = 0.f;
+#pragma unroll
+    for (int d = 0; d < HD; ++d) s = fmaf(qs[d], kr[d], s);
+    s *= scale;
+    const float mn = fmaxf(m, s);
+    const float al = (m == -INFINITY) ? 0.f : expf(m - mn);
+    const float p = expf(s - mn);
+    l = l * al + p;
+    const float* vr = vp + pb * HD * 16 + (t & 15);
+#pragma unroll
+    for (int d = 0; d < HD; ++d) acc[d] = acc[d] * al + p * vr[d * 16];
+    m = mn;
+  }
+  ms[lane] = m;
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int i = 0; i < kWave; ++i) mx = fmaxf(mx, ms[i]);
+  const float w = (m == -INFINITY) ? 0.f : expf(m - mx);
+  ls[lane] = l * w;
+#pragma unroll
+  for (int d = 0; d < HD; ++d) red[lane][d] = acc[d] * w;
+  __syncthreads();
+  float den = 0.f;
+  for (int i = 0; i < kWave; ++i) den += ls[i];
+  float* o = static_cast<float*>(a.out) + (static_cast<size_t>(r) * a.Hq + h) * HD;
+  for (int d = lane; d < HD; d += kWave) {
+    float num = 0.f;
+    for (int i = 0; i < kWave; ++i) num += red[i][d];
+    o[d] = num / den;
+  }
+}
+
+template <int HD>
+hipError_t launch_bf16_hd(const AttnArgs& a, const AttnItem* items, int n_items,
+                          const AttnGroup* groups, int n_groups, int nt, hipStream_t st) {
+  dim3 grid(n_items, a.Hkv);
+  if (n_items > 0) {
+    if (nt <= 1) attn_bf16_kernel<HD, 1><<<grid, 64, 0, st>>>(a, items);
+    else if (nt == 2) attn_bf16_kernel<HD, 2><<<grid, 64, 0, st>>>(a, items);
+    else attn_bf16_kernel<HD, 4><<<grid, 64, 0, st>>>(a, items);
+  }
+  if (n_groups > 0) attn_combine_kernel<HD><<<dim3(n_groups, a.Hkv), 256, 0, st>>>(a, groups);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int n_items,
+                                 const AttnGroup* d_groups, int n_groups, int nt, hipStream_t st) {
+  if (nt > 4) return hipErrorInvalidValue;
+  if (a.hd == 128) return launch_bf16_hd<128>(a, d_items, n_items, d_groups, n_groups, nt, st);
+  if (a.hd == 64) return launch_bf16_hd<64>(a, d_items, n_items, d_groups, n_groups, nt, st);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_attention_f32(const AttnArgs& a, int R, const int32_t* d_row_seq,
+                                const int32_t* d_row_pos, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  dim3 grid(R, a.Hq);
+  if (a.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, st>>>(a, d_row_seq, d_row_pos);
+  else if (a.hd == 128) attn_f32_kernel<128><<<grid, 64, 0, st>>>(a, d_row_seq, d_row_pos);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace spec

@@ -1,0 +1,823 @@
+// Host orchestration of the draft-and-verify step: the C ABI of include/spec.h.
+//
+// Sequence model (pending token): a sequence's committed tokens are
+// x_0..x_n; x_n (position n) is pending, i.e. not in the target cache, whose
+// length is n.  The draft cache has length len_d <= n.  Draft step j feeds the
+// draft model the pending tail (j = 1) or x~_{j-1} and draws x~_j at position
+// n + j.  Verify feeds x_n, x~_1..x~_k at positions n..n+k to the target,
+// writes their K/V, and applies the speculative sampling rule.  Commit keeps
+// target positions <= n + a and draft positions < min(len_d, n + a + 1).
+//
+// One metadata block (rows, positions, KV slots, compact page tables,
+// attention work items, decision tables) is uploaded per call through a
+// pinned ring; the decision outputs come back in one small copy per verify.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <functional>
+#include <queue>
+#include <string>
+#include <unordered_map>
+#include <unordered_set>
+#include <vector>
+
+#include "../../include/spec.h"
+#include "attention.h"
+#include "elem.h"
+#include "gemm.h"
+#include "host_util.h"
+#include "pages.h"
+#include "vocab.h"
+
+using namespace spec;
+
+namespace {
+
+constexpr int kMaxParts = 1024;
+constexpr int kMetaRing = 4;
+
+struct Model {
+  spec_model_desc d{};
+  std::vector<spec_layer_weights> layers;
+  int esz = 2;
+  char* kv = nullptr;
+  int num_pages = 0;
+  size_t layer_stride = 0, v_off = 0;  // elements
+  PagePool pool;
+  int dt() const { return d.dtype == SPEC_F32 ? 0 : 1; }
+  int G() const { return d.n_heads / d.n_kv_heads; }
+  int qkvw() const { return (d.n_heads + 2 * d.n_kv_heads) * d.head_dim; }
+  int qdim() const { return d.n_heads * d.head_dim; }
+  void* kl(int l) const { return kv + static_cast<size_t>(l) * layer_stride * esz; }
+  void* vl(int l) const { return kv + (static_cast<size_t>(l) * layer_stride + v_off) * esz; }
+};
+
+struct Seq {
+  int64_t id = 0;
+  int slot = 0;
+  std::vector<int32_t> hist;
+  int len_t = 0, len_d = 0;
+  int written_t = 0;
+  std::vector<int32_t> pages_t, pages_d;
+  int k = 0;
+  std::vector<const float*> qrow;
+  std::vector<int32_t> dsrc;  // >= 0 token id, < 0: -(1 + index into the device draft-token pool)
+  bool external = false;
+  bool verified = false;
+  int a_ver = 0;
+  std::vector<int32_t> emitted;
+  int n() const { return static_cast<int>(hist.size()) - 1; }
+};
+
+struct Ws {
+  size_t h = 0, y = 0, qkv = 0, q = 0, o = 0, u = 0, logits = 0, dq = 0, dtok = 0, rowtok = 0;
+  size_t part_o = 0, part_ml = 0, vocab = 0, draft = 0, nacc = 0, otok = 0, meta = 0;
+  size_t meta_cap = 0, total = 0;
+};
+
+// Host description of one forward launch.
+struct Fwd {
+  std::vector<int32_t> tok_src, pos, slot, seqi;
+  std::vector<AttnSegment> segs;
+  std::vector<int32_t> ptab;
+  int ptab_stride = 1;
+  std::vector<int32_t> lm_rows, lm_map;
+};
+
+struct FwdOff {
+  size_t tok, pos, slot, seqi, pt, items, groups, lmr, lmm;
+  int n_items = 0, n_groups = 0, nt = 1, R = 0, n_lm = 0, ptab_stride = 1;
+  bool lm_map = false;
+};
+
+size_t pool_layer_elems(const spec_model_desc& m, int num_pages) {
+  return static_cast<size_t>(num_pages) * m.n_kv_heads * 16 * m.head_dim * 2;
+}
+
+bool valid_model(const spec_model_desc* m, std::string& why) {
+  if (!m) { why = "null model"; return false; }
+  if (m->n_layers <= 0 || m->d_model <= 0 || m->n_heads <= 0 || m->n_kv_heads <= 0 ||
+      m->head_dim <= 0 || m->ffn_dim <= 0 || m->vocab <= 0) { why = "non-positive model size"; return false; }
+  if (m->n_heads % m->n_kv_heads != 0) { why = "n_heads must be a multiple of n_kv_heads"; return false; }
+  if (m->dtype != SPEC_F32 && m->dtype != SPEC_BF16) { why = "dtype must be SPEC_F32 or SPEC_BF16"; return false; }
+  if (!m->embed || !m->final_norm || !m->lm_head || !m->layers) { why = "null weight pointer"; return false; }
+  for (int l = 0; l < m->n_layers; ++l) {
+    const auto& L = m->layers[l];
+    if (!L.attn_norm || !L.wqkv || !L.wo || !L.mlp_norm || !L.w_gate_up || !L.w_down) {
+      why = "null layer weight pointer"; return false;
+    }
+  }
+  return true;
+}
+
+int unsupported_model(const spec_model_desc* m, std::string& why) {
+  if (m->head_dim != 64 && m->head_dim != 128) { why = "head_dim must be 64 or 128"; return 1; }
+  if (m->dtype == SPEC_BF16) {
+    if (m->d_model % 128 || m->ffn_dim % 128 || (m->n_heads * m->head_dim) % 128) {
+      why = "bf16 models need d_model, ffn_dim and n_heads*head_dim multiples of 128"; return 1;
+    }
+    if (m->n_heads / m->n_kv_heads > 16) { why = "at most 16 query heads per kv head"; return 1; }
+  }
+  return 0;
+}
+
+}  // namespace
+
+struct spec_ctx {
+  Model m[2];  // 0 target, 1 draft
+  spec_cache_desc cache{};
+  int R_max = 0, V = 0, k_max = 0, max_seqs = 0, max_pages = 0;
+  int d_max = 0, qkv_max = 0, q_max = 0, ffn_max = 0, hkv_max = 0, hd_max = 0, esz_max = 2;
+  Ws ws;
+  char* wsp = nullptr;
+  size_t ws_bytes = 0;
+  std::unordered_map<int64_t, Seq> seqs;
+  std::priority_queue<int, std::vector<int>, std::greater<int>> free_slots;
+  Stager stager;
+  int meta_next = 0;
+  int32_t* h_out = nullptr;  // pinned: n_acc [max_seqs] then tokens [max_seqs * (k_max + 1)]
+  hipEvent_t out_ev = nullptr;
+  std::string err;
+  bool broken = false;
+  int last_rows = 0;
+};
+
+static thread_local std::string g_err;
+
+#define FAIL(code, msg)          \
+  do {                           \
+    ctx->err = (msg);            \
+    return (code);               \
+  } while (0)
+
+#define HIPC(expr)                                                              \
+  do {                                                                          \
+    hipError_t e_ = (expr);                                                     \
+    if (e_ != hipSuccess) {                                                     \
+      ctx->broken = true;                                                       \
+      ctx->err = std::string("HIP error in ") + #expr + ": " + hipGetErrorString(e_); \
+      return SPEC_E_HIP;                                                        \
+    }                                                                           \
+  } while (0)
+
+namespace {
+
+void compute_ws(spec_ctx* c) {
+  Ws& w = c->ws;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  const size_t R = c->R_max;
+  const size_t nq = static_cast<size_t>(c->max_seqs) * c->k_max;
+  w.h = take(R * c->d_max * 4);
+  w.y = take(R * std::max(c->d_max, c->q_max) * c->esz_max);
+  w.qkv = take(R * c->qkv_max * 4);
+  w.q = take(R * c->q_max * c->esz_max);
+  w.o = take(R * c->q_max * c->esz_max);
+  w.u = take(R * c->ffn_max * c->esz_max);
+  const size_t vr = static_cast<size_t>(c->max_seqs) * (c->k_max + 1);
+  w.logits = take(vr * c->V * 4);
+  w.dq = take(nq * c->V * 4);
+  w.dtok = take(nq * 4);
+  w.rowtok = take(R * 4);
+  w.part_o = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * c->hd_max * 4);
+  w.part_ml = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * 2 * 4);
+  const int vrows = c->max_seqs * (2 * c->k_max + 1);
+  w.vocab = take(vocab_ws_bytes(vocab_plan(c->max_seqs, vrows, c->V)));
+  w.draft = take(draft_ws_bytes(draft_plan(c->max_seqs, c->V)));
+  w.nacc = take(c->max_seqs * 4);
+  w.otok = take(vr * 4);
+  // metadata bound for one call
+  size_t mc = 0;
+  mc += 6 * align_up(R * 4);
+  mc += align_up(static_cast<size_t>(c->max_seqs) * c->max_pages * 4);
+  mc += align_up((R + kMaxParts) * sizeof(AttnItem)) + align_up(R * sizeof(AttnGroup));
+  mc += align_up(static_cast<size_t>(vrows) * sizeof(VRow)) + align_up(c->max_seqs * sizeof(VSeq));
+  mc += align_up(c->max_seqs * sizeof(DRow));
+  const size_t clears = std::max<size_t>(static_cast<size_t>(c->max_seqs) * (c->k_max + 2),
+                                         static_cast<size_t>(c->max_pages) * 16);
+  mc += 2 * align_up(clears * 4);
+  mc += 16 * 256;
+  w.meta_cap = align_up(mc);
+  w.meta = take(w.meta_cap * kMetaRing);
+  w.total = off;
+}
+
+template <typename T>
+T* wsptr(spec_ctx* c, size_t off) {
+  return reinterpret_cast<T*>(c->wsp + off);
+}
+
+// Upload a metadata block; returns the device base.
+spec_status upload_meta(spec_ctx* ctx, const MetaBlock& mb, hipStream_t st, char** dev) {
+  if (mb.size() > ctx->ws.meta_cap) FAIL(SPEC_E_UNSUPPORTED, "call metadata exceeds its bound");
+  char* base = ctx->wsp + ctx->ws.meta + static_cast<size_t>(ctx->meta_next) * ctx->ws.meta_cap;
+  ctx->meta_next = (ctx->meta_next + 1) % kMetaRing;
+  HIPC(ctx->stager.upload(base, mb.data(), mb.size(), st));
+  *dev = base;
+  return SPEC_OK;
+}
+
+FwdOff add_forward(spec_ctx* ctx, const Model& M, const Fwd& f, MetaBlock& mb) {
+  FwdOff o;
+  o.R = static_cast<int>(f.tok_src.size());
+  o.tok = mb.add(f.tok_src);
+  o.pos = mb.add(f.pos);
+  o.slot = mb.add(f.slot);
+  o.seqi = mb.add(f.seqi);
+  o.pt = mb.add(f.ptab);
+  o.ptab_stride = f.ptab_stride;
+  if (M.dt() == 1) {
+    AttnPlan p = plan_attention(f.segs, M.G(), M.d.n_kv_heads, kMaxParts);
+    o.items = mb.add(p.items);
+    o.groups = mb.add(p.groups);
+    o.n_items = static_cast<int>(p.items.size());
+    o.n_groups = static_cast<int>(p.groups.size());
+    o.nt = p.nt;
+  }
+  o.n_lm = static_cast<int>(f.lm_rows.size());
+  o.lmr = mb.add(f.lm_rows);
+  o.lm_map = !f.lm_map.empty();
+  o.lmm = mb.add(f.lm_map);
+  (void)ctx;
+  return o;
+}
+
+spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const char* dev,
+                           float* logits, hipStream_t st) {
+  const int dt = M.dt();
+  const int R = o.R;
+  const auto& d = M.d;
+  auto I = [&](size_t off) { return reinterpret_cast<const int32_t*>(dev + off); };
+  float* h = wsptr<float>(ctx, ctx->ws.h);
+  void* y = ctx->wsp + ctx->ws.y;
+  float* qkv = wsptr<float>(ctx, ctx->ws.qkv);
+  void* q = ctx->wsp + ctx->ws.q;
+  void* ob = ctx->wsp + ctx->ws.o;
+  void* u = ctx->wsp + ctx->ws.u;
+  HIPC(launch_embed(dt, R, d.d_model, I(o.tok), wsptr<int32_t>(ctx, ctx->ws.dtok), d.embed, h,
+                    wsptr<int32_t>(ctx, ctx->ws.rowtok), st));
+  AttnArgs a;
+  a.dtype = dt;
+  a.Hq = d.n_heads;
+  a.Hkv = d.n_kv_heads;
+  a.hd = d.head_dim;
+  a.q = q;
+  a.page_table = I(o.pt);
+  a.max_pages = o.ptab_stride;
+  a.out = ob;
+  a.part_o = wsptr<float>(ctx, ctx->ws.part_o);
+  a.part_ml = wsptr<float>(ctx, ctx->ws.part_ml);
+  for (int l = 0; l < d.n_layers; ++l) {
+    const auto& L = M.layers[l];
+    HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
+    HIPC(launch_gemm(dt, R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, st));
+    HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, qkv, I(o.pos),
+                        I(o.slot), q, M.kl(l), M.vl(l), st));
+    a.kpool = M.kl(l);
+    a.vpool = M.vl(l);
+    if (dt == 1) {
+      HIPC(launch_attention_bf16(a, reinterpret_cast<const AttnItem*>(dev + o.items), o.n_items,
+                                 reinterpret_cast<const AttnGroup*>(dev + o.groups), o.n_groups,
+                                 o.nt, st));
+    } else {
+      HIPC(launch_attention_f32(a, R, I(o.seqi), I(o.pos), st));
+    }
+    HIPC(launch_gemm(dt, R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, st));
+    HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.mlp_norm, d.rms_eps, y, st));
+    HIPC(launch_gemm(dt, R, d.ffn_dim, d.d_model, y, L.w_gate_up, u, kEpiSwiGLU, st));
+    HIPC(launch_gemm(dt, R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, st));
+  }
+  if (o.n_lm > 0) {
+    HIPC(launch_rmsnorm(dt, o.n_lm, d.d_model, h, I(o.lmr), d.final_norm, d.rms_eps, y, st));
+    HIPC(launch_gemm(dt, o.n_lm, d.vocab, d.d_model, y, d.lm_head, logits, kEpiStoreF32, st,
+                     o.lm_map ? I(o.lmm) : nullptr));
+  }
+  return SPEC_OK;
+}
+
+// Compact page table of the listed sequences (row i = sequence i).
+void build_ptab(const std::vector<const std::vector<int32_t>*>& tabs, Fwd& f) {
+  size_t w = 1;
+  for (auto* t : tabs) w = std::max(w, t->size());
+  f.ptab_stride = static_cast<int>(w);
+  f.ptab.assign(tabs.size() * w, 0);
+  for (size_t i = 0; i < tabs.size(); ++i)
+    std::copy(tabs[i]->begin(), tabs[i]->end(), f.ptab.begin() + i * w);
+}
+
+int32_t dev_tok_ref(int slot, int k_max, int j) { return -(1 + slot * k_max + j); }
+
+bool check_ids(spec_ctx* ctx, int32_t n, const int64_t* ids, bool must_exist) {
+  std::unordered_set<int64_t> seen;
+  for (int i = 0; i < n; ++i) {
+    if (!seen.insert(ids[i]).second) {
+      ctx->err = "duplicate seq_id in call";
+      return false;
+    }
+    if (must_exist && !ctx->seqs.count(ids[i])) {
+      ctx->err = "unknown seq_id " + std::to_string(ids[i]);
+      return false;
+    }
+  }
+  return true;
+}
+
+spec_status launch_clears(spec_ctx* ctx, const std::vector<int32_t>& ct, const std::vector<int32_t>& cd,
+                          hipStream_t st) {
+  if (ct.empty() && cd.empty()) return SPEC_OK;
+  MetaBlock mb;
+  const size_t ot = mb.add(ct), od = mb.add(cd);
+  char* dev = nullptr;
+  spec_status s = upload_meta(ctx, mb, st, &dev);
+  if (s != SPEC_OK) return s;
+  const Model& T = ctx->m[0];
+  const Model& D = ctx->m[1];
+  HIPC(launch_kv_clear(T.dt(), static_cast<int>(ct.size()), reinterpret_cast<const int32_t*>(dev + ot),
+                       T.kv, T.d.n_layers, T.layer_stride, T.v_off, T.d.n_kv_heads, T.d.head_dim, st));
+  HIPC(launch_kv_clear(D.dt(), static_cast<int>(cd.size()), reinterpret_cast<const int32_t*>(dev + od),
+                       D.kv, D.d.n_layers, D.layer_stride, D.v_off, D.d.n_kv_heads, D.d.head_dim, st));
+  return SPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t spec_kv_pool_bytes(const spec_model_desc* m, int32_t num_pages) {
+  if (!m || num_pages < 0) return 0;
+  const size_t esz = m->dtype == SPEC_F32 ? 4 : 2;
+  return static_cast<size_t>(m->n_layers) * pool_layer_elems(*m, num_pages) * esz;
+}
+
+spec_status spec_ctx_create(const spec_model_desc* target, const spec_model_desc* draft,
+                            const spec_cache_desc* cache, spec_ctx** out) {
+  std::string why;
+  if (!out) { g_err = "null out"; return SPEC_E_INVALID; }
+  *out = nullptr;
+  if (!valid_model(target, why) || !valid_model(draft, why)) { g_err = why; return SPEC_E_INVALID; }
+  if (!cache || cache->page_size != 16 || cache->num_pages_target <= 0 || cache->num_pages_draft <= 0 ||
+      cache->max_seqs <= 0 || cache->max_pages_per_seq <= 0 || cache->k_max < 1 || cache->k_max > 15 ||
+      cache->max_rows <= 0 || !cache->kv_target || !cache->kv_draft) {
+    g_err = "invalid cache descriptor (page_size must be 16, k_max in 1..15, pools non-null)";
+    return SPEC_E_INVALID;
+  }
+  if (target->vocab != draft->vocab || target->dtype != draft->dtype) {
+    g_err = "target and draft must share vocab and dtype";
+    return SPEC_E_INVALID;
+  }
+  if (unsupported_model(target, why) || unsupported_model(draft, why)) { g_err = why; return SPEC_E_UNSUPPORTED; }
+  spec_ctx* c = new spec_ctx();
+  const spec_model_desc* ms[2] = {target, draft};
+  void* pools[2] = {cache->kv_target, cache->kv_draft};
+  const int np[2] = {cache->num_pages_target, cache->num_pages_draft};
+  for (int i = 0; i < 2; ++i) {
+    Model& M = c->m[i];
+    M.d = *ms[i];
+    M.layers.assign(ms[i]->layers, ms[i]->layers + ms[i]->n_layers);
+    M.d.layers = nullptr;
+    M.esz = M.d.dtype == SPEC_F32 ? 4 : 2;
+    M.kv = static_cast<char*>(pools[i]);
+    M.num_pages = np[i];
+    M.layer_stride = pool_layer_elems(M.d, np[i]);
+    M.v_off = M.layer_stride / 2;
+    M.pool.reset(np[i], 16);
+    c->d_max = std::max(c->d_max, M.d.d_model);
+    c->qkv_max = std::max(c->qkv_max, M.qkvw());
+    c->q_max = std::max(c->q_max, M.qdim());
+    c->ffn_max = std::max(c->ffn_max, M.d.ffn_dim);
+    c->hkv_max = std::max(c->hkv_max, M.d.n_kv_heads);
+    c->hd_max = std::max(c->hd_max, M.d.head_dim);
+    c->esz_max = std::max(c->esz_max, M.esz);
+  }
+  c->cache = *cache;
+  c->V = target->vocab;
+  c->k_max = cache->k_max;
+  c->max_seqs = cache->max_seqs;
+  c->max_pages = cache->max_pages_per_seq;
+  c->R_max = std::max(cache->max_rows, cache->max_seqs * (cache->k_max + 1));
+  for (int s = 0; s < c->max_seqs; ++s) c->free_slots.push(s);
+  compute_ws(c);
+  hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&c->h_out),
+                               sizeof(int32_t) * c->max_seqs * (c->k_max + 2), hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->out_ev, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    g_err = std::string("hipHostMalloc/hipEventCreate: ") + hipGetErrorString(e);
+    if (c->h_out) (void)hipHostFree(c->h_out);
+    delete c;
+    return SPEC_E_HIP;
+  }
+  *out = c;
+  return SPEC_OK;
+}
+
+void spec_ctx_destroy(spec_ctx* ctx) {
+  if (!ctx) return;
+  ctx->stager.release();
+  if (ctx->h_out) (void)hipHostFree(ctx->h_out);
+  if (ctx->out_ev) (void)hipEventDestroy(ctx->out_ev);
+  delete ctx;
+}
+
+const char* spec_last_error(const spec_ctx* ctx) { return ctx ? ctx->err.c_str() : g_err.c_str(); }
+
+size_t spec_workspace_bytes(const spec_ctx* ctx) { return ctx ? ctx->ws.total : 0; }
+
+spec_status spec_set_workspace(spec_ctx* ctx, void* dev_ptr, size_t bytes) {
+  if (!ctx) return SPEC_E_INVALID;
+  if (!dev_ptr || bytes < ctx->ws.total || (reinterpret_cast<uintptr_t>(dev_ptr) & 255))
+    FAIL(SPEC_E_INVALID, "workspace null, too small or not 256-byte aligned");
+  ctx->wsp = static_cast<char*>(dev_ptr);
+  ctx->ws_bytes = bytes;
+  return SPEC_OK;
+}
+
+#define CHECK_READY()                                                    \
+  do {                                                                   \
+    if (!ctx) return SPEC_E_INVALID;                                     \
+    if (ctx->broken) FAIL(SPEC_E_HIP, "context unusable after a HIP error"); \
+    if (!ctx->wsp) FAIL(SPEC_E_STATE, "spec_set_workspace not called");  \
+  } while (0)
+
+spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const int32_t* prompt_lens,
+                         const int32_t* tokens, void* stream) {
+  CHECK_READY();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n < 0 || (n > 0 && (!seq_ids || !prompt_lens || !tokens))) FAIL(SPEC_E_INVALID, "bad arguments");
+  if (!check_ids(ctx, n, seq_ids, false)) return SPEC_E_INVALID;
+  int need_t = 0, need_d = 0;
+  for (int i = 0; i < n; ++i) {
+    if (ctx->seqs.count(seq_ids[i])) FAIL(SPEC_E_INVALID, "seq_id already live");
+    const int P = prompt_lens[i];
+    if (P < 1) FAIL(SPEC_E_INVALID, "prompt_lens must be >= 1");
+    if (ctx->m[0].pool.pages_for(P + ctx->k_max + 1) > ctx->max_pages)
+      FAIL(SPEC_E_INVALID, "prompt too long for max_pages_per_seq");
+    need_t += ctx->m[0].pool.pages_for(P - 1);
+    need_d += ctx->m[1].pool.pages_for(P - 1);
+  }
+  if (static_cast<int>(ctx->free_slots.size()) < n) FAIL(SPEC_E_INVALID, "more live sequences than max_seqs");
+  if (need_t > ctx->m[0].pool.free_pages() || need_d > ctx->m[1].pool.free_pages())
+    FAIL(SPEC_E_NOPAGES, "KV page pool exhausted");
+  {
+    size_t off = 0;
+    for (int i = 0; i < n; ++i) {
+      for (int j = 0; j < prompt_lens[i]; ++j)
+        if (tokens[off + j] < 0 || tokens[off + j] >= ctx->V) FAIL(SPEC_E_INVALID, "token id out of range");
+      off += prompt_lens[i];
+    }
+  }
+  // commit host state
+  std::vector<Seq*> ss;
+  size_t off = 0;
+  for (int i = 0; i < n; ++i) {
+    Seq s;
+    s.id = seq_ids[i];
+    s.slot = ctx->free_slots.top();
+    ctx->free_slots.pop();
+    s.hist.assign(tokens + off, tokens + off + prompt_lens[i]);
+    off += prompt_lens[i];
+    const int P = prompt_lens[i];
+    ctx->m[0].pool.ensure(s.pages_t, P - 1);
+    ctx->m[1].pool.ensure(s.pages_d, P - 1);
+    s.len_t = s.len_d = s.written_t = P - 1;
+    ss.push_back(&(ctx->seqs[s.id] = std::move(s)));
+  }
+  // chunked forward of positions 0..P-2 through both models
+  struct Piece { Seq* s; int pos0, nrows; };
+  std::vector<Piece> pieces;
+  for (Seq* s : ss)
+    for (int p = 0; p < s->len_t; p += ctx->R_max)
+      pieces.push_back(Piece{s, p, std::min(ctx->R_max, s->len_t - p)});
+  size_t pi = 0;
+  while (pi < pieces.size()) {
+    std::vector<Piece> chunk;
+    int rows = 0;
+    while (pi < pieces.size() && rows + pieces[pi].nrows <= ctx->R_max) {
+      chunk.push_back(pieces[pi]);
+      rows += pieces[pi].nrows;
+      ++pi;
+    }
+    for (int mi = 0; mi < 2; ++mi) {
+      const Model& M = ctx->m[mi];
+      Fwd f;
+      std::vector<const std::vector<int32_t>*> tabs;
+      for (size_t c = 0; c < chunk.size(); ++c) {
+        const Piece& p = chunk[c];
+        const auto& tab = mi == 0 ? p.s->pages_t : p.s->pages_d;
+        tabs.push_back(&tab);
+        f.segs.push_back(AttnSegment{static_cast<int32_t>(c), static_cast<int32_t>(f.tok_src.size()),
+                                     p.nrows, p.pos0});
+        for (int r = 0; r < p.nrows; ++r) {
+          const int pos = p.pos0 + r;
+          f.tok_src.push_back(p.s->hist[pos]);
+          f.pos.push_back(pos);
+          f.slot.push_back(M.pool.slot(tab, pos));
+          f.seqi.push_back(static_cast<int32_t>(c));
+        }
+      }
+      build_ptab(tabs, f);
+      MetaBlock mb;
+      FwdOff o = add_forward(ctx, M, f, mb);
+      char* dev = nullptr;
+      spec_status s = upload_meta(ctx, mb, st, &dev);
+      if (s != SPEC_OK) return s;
+      s = launch_forward(ctx, M, o, dev, nullptr, st);
+      if (s != SPEC_OK) return s;
+    }
+  }
+  HIPC(hipStreamSynchronize(st));
+  return SPEC_OK;
+}
+
+spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                            uint64_t seed, void* stream) {
+  CHECK_READY();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n < 0 || (n > 0 && (!seq_ids || !temperature))) FAIL(SPEC_E_INVALID, "bad arguments");
+  if (n == 0) return SPEC_OK;
+  if (!check_ids(ctx, n, seq_ids, true)) return SPEC_E_INVALID;
+  Model& D = ctx->m[1];
+  int rows = 0, need = 0;
+  for (int i = 0; i < n; ++i) {
+    Seq& s = ctx->seqs[seq_ids[i]];
+    if (!(temperature[i] >= 0.f)) FAIL(SPEC_E_INVALID, "temperature must be >= 0");
+    if (s.verified) FAIL(SPEC_E_STATE, "draft step after verify without commit");
+    if (s.external) FAIL(SPEC_E_STATE, "sequence holds external drafts");
+    if (s.k >= ctx->k_max) FAIL(SPEC_E_STATE, "sequence already has k_max drafts");
+    const int c = s.k == 0 ? s.n() + 1 - s.len_d : 1;
+    rows += c;
+    if (D.pool.pages_for(s.len_d + c) > ctx->max_pages) FAIL(SPEC_E_INVALID, "sequence exceeds max_pages_per_seq");
+    need += D.pool.need(s.pages_d, s.len_d + c);
+  }
+  if (rows > ctx->R_max) FAIL(SPEC_E_UNSUPPORTED, "draft rows exceed max_rows");
+  if (need > D.pool.free_pages()) FAIL(SPEC_E_NOPAGES, "draft KV page pool exhausted");
+  Fwd f;
+  std::vector<const std::vector<int32_t>*> tabs;
+  std::vector<DRow> dr;
+  float* dq = wsptr<float>(ctx, ctx->ws.dq);
+  for (int i = 0; i < n; ++i) {
+    Seq& s = ctx->seqs[seq_ids[i]];
+    const int c = s.k == 0 ? s.n() + 1 - s.len_d : 1;
+    D.pool.ensure(s.pages_d, s.len_d + c);
+    tabs.push_back(&s.pages_d);
+    f.segs.push_back(AttnSegment{i, static_cast<int32_t>(f.tok_src.size()), c, s.len_d});
+    for (int r = 0; r < c; ++r) {
+      const int pos = s.len_d + r;
+      f.tok_src.push_back(s.k == 0 ? s.hist[pos] : s.dsrc[s.k - 1]);
+      f.pos.push_back(pos);
+      f.slot.push_back(D.pool.slot(s.pages_d, pos));
+      f.seqi.push_back(i);
+    }
+    const int qidx = s.slot * ctx->k_max + s.k;
+    f.lm_rows.push_back(static_cast<int32_t>(f.tok_src.size()) - 1);
+    f.lm_map.push_back(qidx);
+    DRow d{};
+    d.ptr = dq + static_cast<size_t>(qidx) * ctx->V;
+    d.t = temperature[i];
+    d.pos = s.n() + s.k + 1;
+    d.seq_lo = static_cast<uint32_t>(static_cast<uint64_t>(s.id));
+    d.seq_hi = static_cast<uint32_t>(static_cast<uint64_t>(s.id) >> 32);
+    d.out = qidx;
+    dr.push_back(d);
+  }
+  build_ptab(tabs, f);
+  MetaBlock mb;
+  FwdOff o = add_forward(ctx, D, f, mb);
+  const size_t odr = mb.add(dr);
+  char* dev = nullptr;
+  spec_status s = upload_meta(ctx, mb, st, &dev);
+  if (s != SPEC_OK) return s;
+  s = launch_forward(ctx, D, o, dev, dq, st);
+  if (s != SPEC_OK) return s;
+  HIPC(launch_draft_sample(draft_plan(n, ctx->V), reinterpret_cast<const DRow*>(dev + odr), seed,
+                           wsptr<int32_t>(ctx, ctx->ws.dtok), ctx->wsp + ctx->ws.draft, st));
+  for (int i = 0; i < n; ++i) {
+    Seq& q = ctx->seqs[seq_ids[i]];
+    const int c = q.k == 0 ? q.n() + 1 - q.len_d : 1;
+    const int qidx = q.slot * ctx->k_max + q.k;
+    q.len_d += c;
+    q.qrow.push_back(dq + static_cast<size_t>(qidx) * ctx->V);
+    q.dsrc.push_back(dev_tok_ref(q.slot, ctx->k_max, q.k));
+    q.k += 1;
+  }
+  return SPEC_OK;
+}
+
+spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k, const int32_t* tokens,
+                            const float* q_logits, void* stream) {
+  CHECK_READY();
+  (void)stream;
+  auto it = ctx->seqs.find(seq_id);
+  if (it == ctx->seqs.end()) FAIL(SPEC_E_INVALID, "unknown seq_id");
+  Seq& s = it->second;
+  if (k < 0 || k > ctx->k_max || (k > 0 && (!tokens || !q_logits))) FAIL(SPEC_E_INVALID, "bad drafts");
+  if (s.verified) FAIL(SPEC_E_STATE, "set_drafts after verify without commit");
+  if (s.k > 0 && !s.external) FAIL(SPEC_E_STATE, "sequence already has drafts from spec_draft_step");
+  for (int j = 0; j < k; ++j)
+    if (tokens[j] < 0 || tokens[j] >= ctx->V) FAIL(SPEC_E_INVALID, "draft token out of range");
+  s.k = k;
+  s.external = k > 0;
+  s.qrow.clear();
+  s.dsrc.clear();
+  for (int j = 0; j < k; ++j) {
+    s.qrow.push_back(q_logits + static_cast<size_t>(j) * ctx->V);
+    s.dsrc.push_back(tokens[j]);
+  }
+  return SPEC_OK;
+}
+
+spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                        uint64_t seed, int32_t* n_accepted, int32_t* out_tokens, void* stream) {
+  CHECK_READY();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n < 0 || (n > 0 && (!seq_ids || !temperature || !n_accepted || !out_tokens)))
+    FAIL(SPEC_E_INVALID, "bad arguments");
+  if (n == 0) return SPEC_OK;
+  if (!check_ids(ctx, n, seq_ids, true)) return SPEC_E_INVALID;
+  Model& T = ctx->m[0];
+  int need = 0;
+  for (int i = 0; i < n; ++i) {
+    Seq& s = ctx->seqs[seq_ids[i]];
+    if (!(temperature[i] >= 0.f)) FAIL(SPEC_E_INVALID, "temperature must be >= 0");
+    if (s.verified) FAIL(SPEC_E_STATE, "verify twice without commit");
+    if (T.pool.pages_for(s.n() + s.k + 1) > ctx->max_pages) FAIL(SPEC_E_INVALID, "sequence exceeds max_pages_per_seq");
+    need += T.pool.need(s.pages_t, s.n() + s.k + 1);
+  }
+  if (need > T.pool.free_pages()) FAIL(SPEC_E_NOPAGES, "target KV page pool exhausted");
+  Fwd f;
+  std::vector<const std::vector<int32_t>*> tabs;
+  std::vector<VRow> prow, qrow;
+  std::vector<VSeq> vs;
+  float* logits = wsptr<float>(ctx, ctx->ws.logits);
+  for (int i = 0; i < n; ++i) {
+    Seq& s = ctx->seqs[seq_ids[i]];
+    const int nn = s.n();
+    T.pool.ensure(s.pages_t, nn + s.k + 1);
+    tabs.push_back(&s.pages_t);
+    const int row0 = static_cast<int>(f.tok_src.size());
+    f.segs.push_back(AttnSegment{i, row0, s.k + 1, nn});
+    const float t = temperature[i];
+    const float it = t > 0.f ? 1.f / t : 0.f;
+    VSeq q{};
+    q.k = s.k;
+    q.p_row = row0;
+    q.q_row = static_cast<int32_t>(qrow.size());
+    q.tok_row = row0 + 1;
+    q.base_pos = nn;
+    q.t = t;
+    q.seq_lo = static_cast<uint32_t>(static_cast<uint64_t>(s.id));
+    q.seq_hi = static_cast<uint32_t>(static_cast<uint64_t>(s.id) >> 32);
+    vs.push_back(q);
+    for (int r = 0; r <= s.k; ++r) {
+      const int pos = nn + r;
+      f.tok_src.push_back(r == 0 ? s.hist[nn] : s.dsrc[r - 1]);
+      f.pos.push_back(pos);
+      f.slot.push_back(T.pool.slot(s.pages_t, pos));
+      f.seqi.push_back(i);
+      f.lm_rows.push_back(row0 + r);
+      prow.push_back(VRow{logits + static_cast<size_t>(row0 + r) * ctx->V, it, t > 0.f ? 0 : 1});
+    }
+    for (int j = 0; j < s.k; ++j) qrow.push_back(VRow{s.qrow[j], it, t > 0.f ? 0 : 1});
+    s.written_t = std::max(s.written_t, nn + s.k + 1);
+  }
+  const int R = static_cast<int>(f.tok_src.size());
+  for (auto& q : vs) q.q_row += R;
+  std::vector<VRow> rows = prow;
+  rows.insert(rows.end(), qrow.begin(), qrow.end());
+  build_ptab(tabs, f);
+  MetaBlock mb;
+  FwdOff o = add_forward(ctx, T, f, mb);
+  const size_t orow = mb.add(rows), oseq = mb.add(vs);
+  char* dev = nullptr;
+  spec_status s = upload_meta(ctx, mb, st, &dev);
+  if (s != SPEC_OK) return s;
+  s = launch_forward(ctx, T, o, dev, logits, st);
+  if (s != SPEC_OK) return s;
+  int32_t* d_nacc = wsptr<int32_t>(ctx, ctx->ws.nacc);
+  int32_t* d_otok = wsptr<int32_t>(ctx, ctx->ws.otok);
+  const VocabPlan vp = vocab_plan(n, static_cast<int>(rows.size()), ctx->V);
+  HIPC(launch_vocab_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
+                         reinterpret_cast<const VSeq*>(dev + oseq), wsptr<int32_t>(ctx, ctx->ws.rowtok),
+                         seed, ctx->k_max, d_nacc, d_otok, ctx->wsp + ctx->ws.vocab, st));
+  const int W = ctx->k_max + 1;
+  HIPC(hipMemcpyAsync(ctx->h_out, d_nacc, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
+  HIPC(hipMemcpyAsync(ctx->h_out + ctx->max_seqs, d_otok, sizeof(int32_t) * n * W, hipMemcpyDeviceToHost, st));
+  HIPC(hipEventRecord(ctx->out_ev, st));
+  HIPC(hipEventSynchronize(ctx->out_ev));
+  std::memcpy(n_accepted, ctx->h_out, sizeof(int32_t) * n);
+  std::memcpy(out_tokens, ctx->h_out + ctx->max_seqs, sizeof(int32_t) * n * W);
+  for (int i = 0; i < n; ++i) {
+    Seq& q = ctx->seqs[seq_ids[i]];
+    q.verified = true;
+    q.a_ver = n_accepted[i];
+    q.emitted.assign(out_tokens + i * W, out_tokens + i * W + q.a_ver + 1);
+  }
+  ctx->last_rows = R;
+  return SPEC_OK;
+}
+
+spec_status spec_kv_commit(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const int32_t* n_accepted,
+                           void* stream) {
+  CHECK_READY();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n < 0 || (n > 0 && (!seq_ids || !n_accepted))) FAIL(SPEC_E_INVALID, "bad arguments");
+  if (!check_ids(ctx, n, seq_ids, true)) return SPEC_E_INVALID;
+  for (int i = 0; i < n; ++i) {
+    const Seq& s = ctx->seqs[seq_ids[i]];
+    if (!s.verified) FAIL(SPEC_E_STATE, "commit without verify");
+    if (n_accepted[i] < 0 || n_accepted[i] > s.a_ver) FAIL(SPEC_E_INVALID, "n_accepted outside 0..verified count");
+  }
+  std::vector<int32_t> ct, cd;
+  for (int i = 0; i < n; ++i) {
+    Seq& s = ctx->seqs[seq_ids[i]];
+    const int a = n_accepted[i];
+    const int nn = s.n();
+    s.hist.insert(s.hist.end(), s.emitted.begin(), s.emitted.begin() + a + 1);
+    const int new_t = nn + a + 1;
+    const int new_d = std::min(s.len_d, new_t);
+    for (int p = new_t; p < s.written_t; ++p) ct.push_back(ctx->m[0].pool.slot(s.pages_t, p));
+    for (int p = new_d; p < s.len_d; ++p) cd.push_back(ctx->m[1].pool.slot(s.pages_d, p));
+    ctx->m[0].pool.truncate(s.pages_t, new_t);
+    ctx->m[1].pool.truncate(s.pages_d, new_d);
+    s.len_t = s.written_t = new_t;
+    s.len_d = new_d;
+    s.k = 0;
+    s.qrow.clear();
+    s.dsrc.clear();
+    s.external = false;
+    s.verified = false;
+    s.emitted.clear();
+  }
+  return launch_clears(ctx, ct, cd, st);
+}
+
+spec_status spec_kv_rollback(spec_ctx* ctx, int64_t seq_id, int32_t new_len, void* stream) {
+  CHECK_READY();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  auto it = ctx->seqs.find(seq_id);
+  if (it == ctx->seqs.end()) FAIL(SPEC_E_INVALID, "unknown seq_id");
+  Seq& s = it->second;
+  if (new_len < 0 || new_len > s.len_t) FAIL(SPEC_E_INVALID, "new_len outside 0..target length");
+  std::vector<int32_t> ct, cd;
+  const int new_d = std::min(s.len_d, new_len);
+  for (int p = new_len; p < s.written_t; ++p) ct.push_back(ctx->m[0].pool.slot(s.pages_t, p));
+  for (int p = new_d; p < s.len_d; ++p) cd.push_back(ctx->m[1].pool.slot(s.pages_d, p));
+  ctx->m[0].pool.truncate(s.pages_t, new_len);
+  ctx->m[1].pool.truncate(s.pages_d, new_d);
+  s.hist.resize(new_len + 1);
+  s.len_t = s.written_t = new_len;
+  s.len_d = new_d;
+  s.k = 0;
+  s.qrow.clear();
+  s.dsrc.clear();
+  s.external = false;
+  s.verified = false;
+  s.emitted.clear();
+  return launch_clears(ctx, ct, cd, st);
+}
+
+spec_status spec_seq_release(spec_ctx* ctx, int64_t seq_id) {
+  if (!ctx) return SPEC_E_INVALID;
+  auto it = ctx->seqs.find(seq_id);
+  if (it == ctx->seqs.end()) FAIL(SPEC_E_INVALID, "unknown seq_id");
+  ctx->m[0].pool.truncate(it->second.pages_t, 0);
+  ctx->m[1].pool.truncate(it->second.pages_d, 0);
+  ctx->free_slots.push(it->second.slot);
+  ctx->seqs.erase(it);
+  return SPEC_OK;
+}
+
+spec_status spec_seq_info(const spec_ctx* ctx, int64_t seq_id, int32_t* target_len, int32_t* draft_len,
+                          int32_t* pending_pos, int32_t* pages_target, int32_t* n_pages_target,
+                          int32_t* pages_draft, int32_t* n_pages_draft, int32_t max_pages) {
+  if (!ctx) return SPEC_E_INVALID;
+  auto it = ctx->seqs.find(seq_id);
+  if (it == ctx->seqs.end()) return SPEC_E_INVALID;
+  const Seq& s = it->second;
+  if (target_len) *target_len = s.len_t;
+  if (draft_len) *draft_len = s.len_d;
+  if (pending_pos) *pending_pos = s.n();
+  auto put = [&](const std::vector<int32_t>& t, int32_t* out, int32_t* cnt) {
+    if (cnt) *cnt = static_cast<int32_t>(t.size());
+    if (out)
+      for (int i = 0; i < static_cast<int>(t.size()) && i < max_pages; ++i) out[i] = t[i];
+  };
+  put(s.pages_t, pages_target, n_pages_target);
+  put(s.pages_d, pages_draft, n_pages_draft);
+  return SPEC_OK;
+}
+
+spec_status spec_last_logits(const spec_ctx* ctx, const float** logits, int32_t* rows) {
+  if (!ctx || !logits || !rows || !ctx->wsp) return SPEC_E_INVALID;
+  *logits = reinterpret_cast<const float*>(ctx->wsp + ctx->ws.logits);
+  *rows = ctx->last_rows;
+  return SPEC_OK;
+}
+
+}  // extern "C"

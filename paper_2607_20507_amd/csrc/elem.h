@@ -1,0 +1,30 @@
+// Embedding gather, RMSNorm, RoPE + paged KV append, KV slot clearing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spec {
+
+// h[r] = E[tok(r)] (fp32), tok(r) = tok_src[r] if >= 0 else tok_pool[-1 - tok_src[r]];
+// the resolved ids are written to row_tok[r].
+hipError_t launch_embed(int dtype, int R, int d, const int32_t* tok_src, const int32_t* tok_pool,
+                        const void* E, float* h, int32_t* row_tok, hipStream_t st);
+
+// y[i] = h[src(i)] / sqrt(mean(h^2) + eps) * w, src(i) = row_idx ? row_idx[i] : i.
+hipError_t launch_rmsnorm(int dtype, int R, int d, const float* h, const int32_t* row_idx,
+                          const void* w, float eps, void* y, hipStream_t st);
+
+// From qkv fp32 [R, (Hq + 2 Hkv) hd]: q <- RoPE(q) [R, Hq, hd]; K page slot
+// slot[r] <- RoPE(k); V^T page slot <- v.  Rotate-half pairs (i, i + hd/2)
+// at angle pos[r] * theta^(-2i/hd), angles and sin/cos evaluated in fp64.
+hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta, const float* qkv,
+                          const int32_t* pos, const int32_t* slot, void* q, void* kpool,
+                          void* vpool, hipStream_t st);
+
+// Zero the K and V entries of `n` flat slots in every layer of a pool whose
+// layer l holds K at kv + l * layer_stride and V at + v_off (elements).
+hipError_t launch_kv_clear(int dtype, int n, const int32_t* slots, void* kv, int n_layers,
+                           size_t layer_stride, size_t v_off, int Hkv, int hd, hipStream_t st);
+
+}  // namespace spec

@@ -1,0 +1,154 @@
+// Row-wise decoder kernels: embedding gather, RMSNorm (Llama definition,
+// x / sqrt(mean(x^2) + eps) * w), rotate-half RoPE fused with the paged KV
+// append, and in-place clearing of rolled-back KV slots.
+
+#include <cmath>
+
+#include "common.h"
+#include "elem.h"
+
+namespace spec {
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(int d, const int32_t* __restrict__ tok_src,
+                                                    const int32_t* __restrict__ tok_pool,
+                                                    const T* __restrict__ E, float* __restrict__ h,
+                                                    int32_t* __restrict__ row_tok) {
+  const int r = blockIdx.x;
+  const int s = tok_src[r];
+  const int tok = s >= 0 ? s : tok_pool[-1 - s];
+  if (threadIdx.x == 0) row_tok[r] = tok;
+  const T* e = E + static_cast<size_t>(tok) * d;
+  float* o = h + static_cast<size_t>(r) * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) o[i] = Elem<T>::to_f32(e[i]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(int d, const float* __restrict__ h,
+                                                      const int32_t* __restrict__ row_idx,
+                                                      const T* __restrict__ w, float eps,
+                                                      T* __restrict__ y) {
+  const int r = blockIdx.x;
+  const int src = row_idx ? row_idx[r] : r;
+  const float* x = h + static_cast<size_t>(src) * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) ss = fmaf(x[i], x[i], ss);
+  ss = wave_sum(ss);
+  __shared__ float part[256 / kWave];
+  if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int k = 0; k < static_cast<int>(blockDim.x) / kWave; ++k) tot += part[k];
+  const float inv = 1.f / sqrtf(tot / static_cast<float>(d) + eps);
+  T* o = y + static_cast<size_t>(r) * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) o[i] = Elem<T>::from_f32(x[i] * inv * Elem<T>::to_f32(w[i]));
+}
+
+// One workgroup per row; thread (head, i) rotates the pair (i, i + hd/2).
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, float theta,
+                                                      const float* __restrict__ qkv,
+                                                      const int32_t* __restrict__ pos,
+                                                      const int32_t* __restrict__ slot,
+                                                      T* __restrict__ q, T* __restrict__ kpool,
+                                                      T* __restrict__ vpool) {
+  const int r = blockIdx.x;
+  const int half = hd / 2;
+  const int width = (Hq + 2 * Hkv) * hd;
+  const float* x = qkv + static_cast<size_t>(r) * width;
+  const double p = static_cast<double>(pos[r]);
+  const int sl = slot[r];
+  const int page = sl >> 4, off = sl & 15;
+  const double lt = log(static_cast<double>(theta));
+  for (int e = threadIdx.x; e < (Hq + Hkv) * half; e += blockDim.x) {
+    const int head = e / half, i = e % half;
+    double sn, cs;
+    sincos(p * exp(-(2.0 * i / hd) * lt), &sn, &cs);
+    const float c = static_cast<float>(cs), s = static_cast<float>(sn);
+    const float* src = x + head * hd;
+    const float a = src[i], b = src[i + half];
+    const float ra = a * c - b * s, rb = b * c + a * s;
+    if (head < Hq) {
+      T* o = q + (static_cast<size_t>(r) * Hq + head) * hd;
+      o[i] = Elem<T>::from_f32(ra);
+      o[i + half] = Elem<T>::from_f32(rb);
+    } else {
+      const int kh = head - Hq;
+      T* o = kpool + ((static_cast<size_t>(page) * Hkv + kh) * 16 + off) * hd;
+      o[i] = Elem<T>::from_f32(ra);
+      o[i + half] = Elem<T>::from_f32(rb);
+    }
+  }
+  const float* v = x + (Hq + Hkv) * hd;
+  for (int e = threadIdx.x; e < Hkv * hd; e += blockDim.x) {
+    const int kh = e / hd, dd = e % hd;
+    vpool[((static_cast<size_t>(page) * Hkv + kh) * hd + dd) * 16 + off] = Elem<T>::from_f32(v[e]);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void kv_clear_kernel(const int32_t* __restrict__ slots, T* __restrict__ kv,
+                                                       size_t layer_stride, size_t v_off, int Hkv, int hd) {
+  const int i = blockIdx.x, l = blockIdx.y;
+  const int sl = slots[i];
+  const int page = sl >> 4, off = sl & 15;
+  T* K = kv + l * layer_stride;
+  T* V = K + v_off;
+  for (int e = threadIdx.x; e < Hkv * hd; e += blockDim.x) {
+    const int h = e / hd, dd = e % hd;
+    K[((static_cast<size_t>(page) * Hkv + h) * 16 + off) * hd + dd] = T(0);
+    V[((static_cast<size_t>(page) * Hkv + h) * hd + dd) * 16 + off] = T(0);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_embed(int dtype, int R, int d, const int32_t* tok_src, const int32_t* tok_pool,
+                        const void* E, float* h, int32_t* row_tok, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (dtype == 0)
+    embed_kernel<float><<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const float*>(E), h, row_tok);
+  else
+    embed_kernel<bf16_t><<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const bf16_t*>(E), h, row_tok);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int dtype, int R, int d, const float* h, const int32_t* row_idx,
+                          const void* w, float eps, void* y, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (dtype == 0)
+    rmsnorm_kernel<float><<<R, 256, 0, st>>>(d, h, row_idx, static_cast<const float*>(w), eps,
+                                             static_cast<float*>(y));
+  else
+    rmsnorm_kernel<bf16_t><<<R, 256, 0, st>>>(d, h, row_idx, static_cast<const bf16_t*>(w), eps,
+                                              static_cast<bf16_t*>(y));
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta, const float* qkv,
+                          const int32_t* pos, const int32_t* slot, void* q, void* kpool,
+                          void* vpool, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (hd % 2 != 0) return hipErrorInvalidValue;
+  if (dtype == 0)
+    rope_kv_kernel<float><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
+                                             static_cast<float*>(kpool), static_cast<float*>(vpool));
+  else
+    rope_kv_kernel<bf16_t><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
+                                              static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool));
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_clear(int dtype, int n, const int32_t* slots, void* kv, int n_layers,
+                           size_t layer_stride, size_t v_off, int Hkv, int hd, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  dim3 grid(n, n_layers);
+  if (dtype == 0)
+    kv_clear_kernel<float><<<grid, 256, 0, st>>>(slots, static_cast<float*>(kv), layer_stride, v_off, Hkv, hd);
+  else
+    kv_clear_kernel<bf16_t><<<grid, 256, 0, st>>>(slots, static_cast<bf16_t*>(kv), layer_stride, v_off, Hkv, hd);
+  return hipGetLastError();
+}
+
+}  // namespace spec

@@ -1,0 +1,60 @@
+// Attention work planning: query tiles and key-range splits.
+
+#include <algorithm>
+
+#include "host_util.h"
+
+namespace spec {
+
+AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, int max_parts,
+                        int target_waves) {
+  AttnPlan p;
+  int max_rows = 1;
+  for (const auto& s : segs) max_rows = std::max(max_rows, s.nrows);
+  // query vectors per tile: rows * G <= 16 * nt, nt in {1, 2, 4}
+  const int want = std::min(max_rows * G, 64);
+  p.nt = want <= 16 ? 1 : (want <= 32 ? 2 : 4);
+  const int qt = std::max(1, 16 * p.nt / G);
+
+  struct Tile {
+    int seq, row0, nrows, pos0, kend;
+  };
+  std::vector<Tile> tiles;
+  long long total_keys = 0;
+  for (const auto& s : segs) {
+    for (int r = 0; r < s.nrows; r += qt) {
+      const int n = std::min(qt, s.nrows - r);
+      const int kend = s.pos0 + r + n;  // keys 0 .. last row's position
+      tiles.push_back(Tile{s.seq, s.row0 + r, n, s.pos0 + r, kend});
+      total_keys += kend;
+    }
+  }
+  long long split = (total_keys * Hkv + target_waves - 1) / std::max(1, target_waves);
+  split = std::max<long long>(64, (split + 31) / 32 * 32);
+  auto parts_for = [&](long long sp) {
+    long long n = 0;
+    for (const auto& t : tiles) {
+      const long long c = (t.kend + sp - 1) / sp;
+      if (c > 1) n += c;
+    }
+    return n;
+  };
+  while (parts_for(split) > max_parts) split *= 2;
+  for (const auto& t : tiles) {
+    const int c = static_cast<int>((t.kend + split - 1) / split);
+    if (c <= 1) {
+      p.items.push_back(AttnItem{t.row0, t.nrows, t.pos0, t.seq, 0, t.kend, -1, 0});
+      continue;
+    }
+    p.groups.push_back(AttnGroup{t.row0, t.nrows, p.n_parts, c});
+    for (int i = 0; i < c; ++i) {
+      const int t0 = static_cast<int>(i * split);
+      const int t1 = static_cast<int>(std::min<long long>(t.kend, (i + 1) * split));
+      p.items.push_back(AttnItem{t.row0, t.nrows, t.pos0, t.seq, t0, t1, p.n_parts + i, 0});
+    }
+    p.n_parts += c;
+  }
+  return p;
+}
+
+}  // namespace spec

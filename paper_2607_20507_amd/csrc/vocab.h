@@ -1,0 +1,67 @@
+// Vocabulary-wide decision pass: row statistics, the acceptance scan, the
+// residual / bonus draw and the draft sampler (host-side launch interface).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace spec {
+
+// One logits row of the decision pass: fp32 pointer and 1/T (0 for greedy).
+struct VRow {
+  const float* ptr;
+  float inv_t;
+  int32_t greedy;
+};
+
+// One sequence of the decision pass.  Rows are indices into the VRow table:
+// target rows p_row .. p_row + k, draft rows q_row .. q_row + k - 1; draft
+// tokens draft_tok[tok_row .. tok_row + k - 1].
+struct VSeq {
+  int32_t k;
+  int32_t p_row;
+  int32_t q_row;
+  int32_t tok_row;
+  int32_t base_pos;
+  float t;
+  uint32_t seq_lo, seq_hi;
+};
+
+// One row of the draft sampler: its logits, temperature, the absolute position
+// of the token being drawn, the sequence id and where the token is written.
+struct DRow {
+  const float* ptr;
+  float t;
+  int32_t pos;
+  uint32_t seq_lo, seq_hi;
+  int32_t out;
+  int32_t pad;
+};
+
+struct VocabPlan {
+  int B = 0, n_rows = 0, V = 0;
+  int chunk1 = 0, n_chunks1 = 0;  // statistics pass
+  int chunk2 = 0, n_chunks2 = 0;  // residual / bonus draw
+};
+
+VocabPlan vocab_plan(int B, int n_rows, int V);
+size_t vocab_ws_bytes(const VocabPlan& p);
+
+// Full decision pass.  Outputs n_acc[B], out_tok[B * (kmax + 1)] (device).
+hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
+                             const int32_t* d_draft_tok, uint64_t seed, int kmax,
+                             int32_t* d_n_acc, int32_t* d_out_tok, void* d_ws, hipStream_t st);
+
+struct DraftPlan {
+  int n = 0, V = 0, chunk = 0, n_chunks = 0;
+};
+DraftPlan draft_plan(int n, int V);
+size_t draft_ws_bytes(const DraftPlan& p);
+hipError_t launch_draft_sample(const DraftPlan& p, const DRow* d_rows, uint64_t seed,
+                               int32_t* d_tokens, void* d_ws, hipStream_t st);
+
+hipError_t launch_philox_uniform(uint64_t seed, uint64_t seq_id, int32_t pos, int32_t purpose,
+                                 int32_t n, float* out, hipStream_t st);
+
+}  // namespace spec

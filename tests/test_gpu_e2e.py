@@ -1,0 +1,166 @@
+"""End-to-end parity of prefill -> draft x k -> verify -> commit / rollback
+between the HIP library (through the C ABI) and the float64 oracle session.
+
+* tiny fp32 pair (2-layer d=256 target, 1-layer drafter, vocab 1024, prompt
+  128, k = 4, 32 steps, T = 1.0 and greedy): accepted counts, emitted tokens,
+  cache lengths and page tables bit-exact; verify logits within 1e-4
+  (normwise per row).  A decision the oracle marks as within its margin ends
+  the comparison of that sequence (counted; must be rare).
+* small bf16 pair shape (12-layer d=1024 target, 2-layer drafter, vocab 32000)
+  with seeded external drafts: verify logits within 2e-2 normwise per row.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import rule
+from oracle.decoder import Decoder
+from oracle.session import Session
+from tests.gpu_util import device, rel_err, say, torch
+from workloads import (SMALL_BF16, TINY_FP32, model_weights, prompt_lengths_uniform,
+                       seq_ids_for, uniform_prompts)
+
+pytestmark = pytest.mark.gpu
+
+
+def _sessions(cfg, max_seqs, pages, max_rows=512, n_layers_t=None, n_layers_d=None):
+    from paper_2607_20507_amd.session import DeviceModel, SpecSession
+    dev = device()
+    tw = model_weights(cfg.target, cfg.seed, n_layers_t)
+    dw = model_weights(cfg.draft, cfg.seed, n_layers_d)
+    gpu = SpecSession(DeviceModel(cfg.target, tw, dev), DeviceModel(cfg.draft, dw, dev), max_seqs=max_seqs,
+                      k_max=max(cfg.k), max_pages_per_seq=pages, num_pages_target=max_seqs * pages,
+                      num_pages_draft=max_seqs * pages, max_rows=max_rows)
+    ora = Session(Decoder(cfg.target, tw), Decoder(cfg.draft, dw), max_seqs * pages, max_seqs * pages)
+    return gpu, ora
+
+
+def _row_rel_errs(zg, zo):
+    return [rel_err(zg[r], zo[r]) for r in range(zo.shape[0])]
+
+
+def _compare_state(gpu, ora, sid):
+    info = gpu.seq_info(sid)
+    lt, ld = ora.lengths(sid)
+    pt, pd = ora.pages(sid)
+    assert (info["target_len"], info["draft_len"]) == (lt, ld)
+    assert info["pages_target"] == pt and info["pages_draft"] == pd
+    assert info["pending_pos"] == len(ora.seqs[sid].history) - 1
+
+
+def run_tiny(temps, steps, seed, n_seqs=1, rollback_at=None):
+    cfg = TINY_FP32
+    k = cfg.k[0]
+    gpu, ora = _sessions(cfg, max_seqs=max(2, n_seqs), pages=40)
+    ids = [int(x) for x in seq_ids_for(cfg.seed + n_seqs, n_seqs)]
+    lens = [128] + [int(x) for x in prompt_lengths_uniform(seed, n_seqs - 1, 1, 100)] if n_seqs > 1 else [128]
+    prompts = uniform_prompts(cfg.seed, lens, cfg.target.vocab)
+    say("tiny e2e prefill", ids, lens, temps)
+    gpu.prefill(ids, prompts)
+    ora.prefill(ids, prompts)
+    for sid in ids:
+        _compare_state(gpu, ora, sid)
+    margins = rule.Margins(accept=1e-4, rel=1e-3, gumbel=1e-4, greedy=5e-4)
+    live = list(ids)
+    stats = {"steps": 0, "excluded": 0, "accepted": 0}
+    for step in range(steps):
+        if not live:
+            break
+        tl = [temps[ids.index(s) % len(temps)] for s in live]
+        for _ in range(k):
+            gpu.draft_step(live, tl, seed + step)
+            ora.draft_step(live, tl, seed + step, margins)
+        na, ot = gpu.verify(live, tl, seed + step)
+        outs = ora.verify(live, tl, seed + step, margins)
+        zg = gpu.last_logits().cpu().numpy()
+        r0 = 0
+        keep = []
+        for i, sid in enumerate(live):
+            res, zp = outs[i]
+            errs = _row_rel_errs(zg[r0:r0 + zp.shape[0]], zp)
+            r0 += zp.shape[0]
+            assert max(errs) < 1e-4, f"step {step} seq {sid}: logits rel err {max(errs)}"
+            if res.excluded:
+                stats["excluded"] += 1
+                continue
+            assert int(na[i]) == res.n_accepted, f"step {step} seq {sid}"
+            assert [int(x) for x in ot[i, :res.n_accepted + 1]] == res.tokens
+            stats["accepted"] += res.n_accepted
+            keep.append(sid)
+        stats["steps"] += 1
+        gpu.commit(live, na)
+        ora.commit(live, [r for r, _ in outs])
+        for sid in keep:
+            _compare_state(gpu, ora, sid)
+        live = keep
+        if rollback_at is not None and step == rollback_at:
+            for sid in live:
+                new_len = max(0, ora.lengths(sid)[0] - 7)
+                gpu.rollback(sid, new_len)
+                ora.rollback(sid, new_len)
+                _compare_state(gpu, ora, sid)
+    gpu.close()
+    return stats
+
+
+@pytest.mark.parametrize("T", [1.0, 0.0])
+def test_tiny_fp32_end_to_end(T):
+    st = run_tiny([T], TINY_FP32.steps, seed=2024)
+    assert st["steps"] >= 8 and st["excluded"] <= 1
+
+
+def test_tiny_fp32_batch_mixed_with_rollback():
+    st = run_tiny([1.0, 0.0, 0.6], 12, seed=7, n_seqs=3, rollback_at=4)
+    assert st["steps"] >= 6
+
+
+def test_tiny_fp32_identical_draft_accepts_all():
+    """Drafter == target: every draft is accepted (p/q = 1) on the GPU too."""
+    from paper_2607_20507_amd.session import DeviceModel, SpecSession
+    dev = device()
+    cfg = TINY_FP32
+    w = model_weights(cfg.target, cfg.seed)
+    gpu = SpecSession(DeviceModel(cfg.target, w, dev), DeviceModel(cfg.target, w, dev), max_seqs=1, k_max=4,
+                      max_pages_per_seq=40, max_rows=256)
+    gpu.prefill([5], [uniform_prompts(1, [30], cfg.target.vocab)[0]])
+    for step in range(5):
+        for _ in range(4):
+            gpu.draft_step([5], [0.8], step)
+        na, ot = gpu.verify([5], [0.8], step)
+        assert int(na[0]) == 4
+        gpu.commit([5], na)
+    assert gpu.seq_info(5)["target_len"] == 29 + 25
+    gpu.close()
+
+
+def test_small_bf16_verify_logits():
+    """Small bf16 pair shape, full depth and width, 2 sequences with short
+    prompts and seeded external drafts: verify logits within 2e-2."""
+    cfg = SMALL_BF16
+    k = cfg.k[0]
+    gpu, ora = _sessions(cfg, max_seqs=2, pages=16, max_rows=256)
+    dev = device()
+    ids = [11, 1 << 33]
+    prompts = uniform_prompts(cfg.seed, [70, 41], cfg.target.vocab)
+    say("small bf16 prefill")
+    gpu.prefill(ids, prompts)
+    ora.prefill(ids, prompts)
+    rng = np.random.default_rng(3)
+    for sid in ids:
+        drafts = rng.integers(0, cfg.target.vocab, size=k).astype(np.int32)
+        zq = (rng.standard_normal((k, cfg.target.vocab)) * 0.5).astype(np.float32)
+        zq_dev = torch.from_numpy(zq).to(dev)
+        gpu.set_drafts(sid, drafts, zq_dev)
+        ora.set_drafts(sid, drafts, zq)
+        setattr(gpu, f"_keep_{sid}", zq_dev)
+    na, ot = gpu.verify(ids, [0.7, 0.7], 5)
+    outs = ora.verify(ids, [0.7, 0.7], 5)
+    zg = gpu.last_logits().cpu().numpy()
+    r0 = 0
+    for i, (res, zp) in enumerate(outs):
+        errs = _row_rel_errs(zg[r0:r0 + k + 1], zp)
+        r0 += k + 1
+        assert max(errs) < 2e-2, errs
+        assert 0 <= int(na[i]) <= k
+    gpu.commit(ids, na)
+    gpu.close()
