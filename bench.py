@@ -1,0 +1,345 @@
+#!/usr/bin/env python3
+"""Verified tokens/s and verify-step latency of draft-and-verify on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the whole hot path on one batch: k draft steps, the
+verify (target forward over the k+1 rows of every sequence, logits, decision
+pass) and the KV commit / rollback.  Inputs (random-init weights, prompts)
+are synthetic, seeded and resident in HBM before the timed region.
+
+Workloads:
+  8b-shaped     32-layer d=4096 target (32/8 heads, ffn 14336, vocab 128256),
+                16-layer d=2048 drafter, batch 1, 2048-token context, k = 5,
+                T = 0.8 (default) or --temperature 0 for greedy.
+  vocab-stress  the decision pass alone: 256 sequences x (7 + 1) rows x 128256.
+
+Prints one JSON line: metric, value (verified tokens/s, whole job), latency,
+roofline of the dominant kernel (live HIP-event timing through the library's
+kernel timer), and the float64 oracle timed on a bounded sample on the host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def cpu_info():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"), default=None)
+    except Exception:
+        pass
+    aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return model, threads or aff, aff
+
+
+# ---------------------------------------------------------------------------
+# 8B-shaped pair, batch 1
+
+def bench_8b(args):
+    import torch
+    from paper_2607_20507_amd import binding as B
+    from paper_2607_20507_amd.session import DeviceModel, SpecSession
+    from workloads import LLAMA8B_SHAPED, seq_ids_for, uniform_prompts
+
+    cfg = LLAMA8B_SHAPED
+    dev = torch.device("cuda:0")
+    k = cfg.k[0]
+    T = args.temperature
+    ctx_len = cfg.context[1]
+    log("drawing weights on device")
+    target = DeviceModel(cfg.target, None, dev, seed=cfg.seed)
+    draft = DeviceModel(cfg.draft, None, dev, seed=cfg.seed + 1)
+    total_steps = args.warmup + args.steps
+    max_len = ctx_len + total_steps * (k + 1) + 64
+    pages = (max_len + 15) // 16
+    sess = SpecSession(target, draft, max_seqs=1, k_max=k, max_pages_per_seq=pages, max_rows=2048)
+    sid = int(seq_ids_for(cfg.seed, 1)[0])
+    prompt = uniform_prompts(cfg.seed, [ctx_len], cfg.target.vocab)[0]
+    log("prefill", ctx_len)
+    sess.prefill([sid], [prompt])
+    stream = torch.cuda.current_stream()
+    acc_hist = []
+    lat = []
+
+    def step(s, record):
+        for _ in range(k):
+            sess.draft_step([sid], [T], cfg.seed + s)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        na, _ = sess.verify([sid], [T], cfg.seed + s)
+        sess.commit([sid], na)
+        e1.record(stream)
+        if record:
+            acc_hist.append(int(na[0]))
+            lat.append((e0, e1))
+        return int(na[0]) + 1
+
+    for s in range(args.warmup):
+        step(s, False)
+    kernel = args.kernel or "gemm_skinny_bf16<1, 2>"
+    B.spec_timing_enable(sess.ctx, kernel)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    tokens = 0
+    for s in range(args.steps):
+        tokens += step(args.warmup + s, True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = ev0.elapsed_time(ev1)
+    k_ms, k_n, k_bytes, k_flops = B.spec_timing_read(sess.ctx)
+    B.spec_timing_enable(sess.ctx, None)
+    lats = sorted(a.elapsed_time(b) for a, b in lat)
+    info = {
+        "tokens": tokens, "wall_s": wall, "event_ms": ev_ms, "acc_hist": acc_hist,
+        "verify_ms_median": float(np.median(lats)), "verify_ms_p90": float(np.percentile(lats, 90)),
+        "kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops,
+        "weights_gb_per_step": (cfg.target.weight_bytes_per_forward() + k * cfg.draft.weight_bytes_per_forward()) / 1e9,
+    }
+    sess.close()
+    return info
+
+
+def cpu_baseline_8b(mean_tokens_per_step):
+    """Time the float64 oracle on a bounded sample of the same step and scale
+    it to a whole step: one target layer on the 6 verify rows over a
+    2048-token synthetic cache, the target LM head and the rule; one drafter
+    layer on one row, the drafter LM head and a draft draw."""
+    from oracle import decoder as OD
+    from oracle import rule
+    from workloads import LLAMA8B_SHAPED
+    from workloads.gen import layer_weights, _normal, _ones
+
+    cfg = LLAMA8B_SHAPED
+    k = cfg.k[0]
+    rng = np.random.default_rng(0)
+
+    def one_layer_model(shape, seed):
+        lm = _normal(seed, shape, "lm_head", 0, (shape.vocab, shape.d_model))
+        return OD.Decoder(shape, {"embed": lm, "final_norm": _ones(shape, shape.d_model), "lm_head": lm,
+                                  "layers": [layer_weights(shape, seed, 0)]})
+
+    def filled_kv(dec, ctx):
+        kv = dec.new_kv()
+        sh = dec.shape
+        kv.append(0, rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim)),
+                  rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim)))
+        return kv
+
+    log("oracle sample: generating one layer + LM head of each model")
+    tdec = one_layer_model(cfg.target, cfg.seed)
+    ddec = one_layer_model(cfg.draft, cfg.seed + 1)
+    ctx = cfg.context[1]
+    toks = rng.integers(0, cfg.target.vocab, size=k + 1)
+
+    def timed(fn):
+        t0 = time.perf_counter()
+        out = fn()
+        return time.perf_counter() - t0, out
+
+    # target: one layer over k+1 rows (hidden only), then LM head + rule
+    t_layer, _ = timed(lambda: tdec.forward(filled_kv(tdec, ctx), toks, ctx + np.arange(k + 1), logits=False))
+    h = rng.standard_normal((k + 1, cfg.target.d_model))
+    t_lm, zp = timed(lambda: OD.matmul_wt(OD.rms_norm(h, tdec.w["final_norm"], 1e-5), tdec.w["lm_head"]))
+    zq = zp[:k] + rng.standard_normal((k, cfg.target.vocab))
+    drafts = [int(np.argmax(z)) for z in zq]
+    t_rule, _ = timed(lambda: rule.verify(zp, zq, drafts, 0.8, 1, 2, ctx))
+    # drafter: one layer on one row, LM head and draw
+    t_dlayer, _ = timed(lambda: ddec.forward(filled_kv(ddec, ctx), toks[:1], np.array([ctx]), logits=False))
+    hd = rng.standard_normal((1, cfg.draft.d_model))
+    t_dlm, zd = timed(lambda: OD.matmul_wt(OD.rms_norm(hd, ddec.w["final_norm"], 1e-5), ddec.w["lm_head"]))
+    t_draw, _ = timed(lambda: rule.sample_draft(zd[0], 0.8, 1, 2, ctx + 1))
+    step_s = (cfg.target.n_layers * t_layer + t_lm + t_rule
+              + k * (cfg.draft.n_layers * t_dlayer + t_dlm + t_draw))
+    sample_s = t_layer + t_lm + t_rule + t_dlayer + t_dlm + t_draw
+    return {
+        "value": mean_tokens_per_step / step_s,
+        "step_s": step_s,
+        "sample_s": sample_s,
+        "sample": ("one verify step estimated from timed pieces: 1 of 32 target layers on 6 rows over a "
+                   "2048-token synthetic cache + LM head + rule, and 1 of 16 drafter layers on 1 row + "
+                   "drafter LM head + draw; scaled to 32/16 layers and k=5 draft steps"),
+    }
+
+
+# ---------------------------------------------------------------------------
+# decision pass alone
+
+def bench_vocab(args):
+    import torch
+    from paper_2607_20507_amd import binding as B
+    from workloads import VOCAB_STRESS, base_positions, seq_ids_for, vocab_temperatures
+
+    cfg = VOCAB_STRESS
+    dev = torch.device("cuda:0")
+    Bn, k, V = cfg.batch, cfg.k, cfg.vocab
+    g = torch.Generator(device=dev)
+    g.manual_seed(cfg.seed)
+    P = torch.randn(Bn * (k + 1), V, generator=g, device=dev) * cfg.p_std
+    Q = P.view(Bn, k + 1, V)[:, :k].reshape(Bn * k, V) + torch.randn(Bn * k, V, generator=g, device=dev) * cfg.q_noise_std
+    temps = vocab_temperatures(Bn, cfg.temperatures)
+    ids = seq_ids_for(cfg.seed, Bn)
+    base = base_positions(cfg.seed, Bn, *cfg.base_pos_range)
+    drafts = torch.zeros(Bn * k, dtype=torch.int32, device=dev)
+    wsd = torch.empty(16 << 20, dtype=torch.uint8, device=dev)
+    B.spec_sample_draft(Q, V, np.repeat(temps, k), np.repeat(ids, k),
+                        np.concatenate([base[s] + 1 + np.arange(k) for s in range(Bn)]), cfg.seed, drafts, wsd)
+    na = torch.zeros(Bn, dtype=torch.int32, device=dev)
+    out = torch.zeros(Bn, k + 1, dtype=torch.int32, device=dev)
+    ws = torch.empty(B.spec_sample_workspace_bytes(Bn, Bn * (2 * k + 1), V), dtype=torch.uint8, device=dev)
+    ks = [k] * Bn
+
+    def step(s):
+        B.spec_sample_verify(ks, temps, ids, base, P, Q, drafts, V, cfg.seed + s, na, out, ws)
+
+    for s in range(args.warmup):
+        step(s)
+    kernel = args.kernel or "stats_kernel<true>"
+    B.spec_timing_enable(None, kernel)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    tokens = 0
+    lats = []
+    for s in range(args.steps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        step(args.warmup + s)
+        b.record(stream)
+        lats.append((a, b))
+        tokens += int(na.sum().item()) + Bn
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_ms, k_n, k_bytes, k_flops = B.spec_timing_read(None)
+    B.spec_timing_enable(None, None)
+    ls = sorted(x.elapsed_time(y) for x, y in lats)
+    return {"tokens": tokens, "wall_s": wall, "event_ms": ev0.elapsed_time(ev1),
+            "verify_ms_median": float(np.median(ls)), "verify_ms_p90": float(np.percentile(ls, 90)),
+            "kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops,
+            "acc_hist": []}
+
+
+def cpu_baseline_vocab(mean_tokens_per_step):
+    """The oracle rule (float64) on a sample of 8 of the 256 sequences."""
+    from oracle import rule
+    from workloads import VOCAB_STRESS, vocab_logits
+
+    cfg = VOCAB_STRESS
+    p, q = vocab_logits(cfg.seed, range(8), cfg.k, cfg.vocab)
+    t0 = time.perf_counter()
+    for s in range(8):
+        T = cfg.temperatures[s % 3]
+        drafts = [rule.sample_draft(q[s, j], T, 1, s, 100 + j + 1)[0] for j in range(cfg.k)]
+        rule.verify(p[s], q[s], drafts, T, 1, s, 100)
+    dt = time.perf_counter() - t0
+    per_seq = dt / 8
+    return {"value": mean_tokens_per_step / (per_seq * cfg.batch), "step_s": per_seq * cfg.batch,
+            "sample_s": dt,
+            "sample": "draft draws + rule on 8 of the 256 sequences, scaled to the full batch"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="8b-shaped", choices=["8b-shaped", "vocab-stress"])
+    ap.add_argument("--temperature", type=float, default=0.8)
+    ap.add_argument("--kernel", default=None, help="kernel to time for the roofline (profiler name)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: sequences shard by data parallelism "
+                                   "with no exchange, so a multi-GPU figure is N independent copies of the "
+                                   "one-GPU line; run with --gpus 1"}))
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+
+    if args.workload == "8b-shaped":
+        info = bench_8b(args)
+        config = {"workload": "8b-shaped target / 1b-shaped drafter, batch 1, context 2048, k=5",
+                  "target": "32L d4096 32q/8kv hd128 ffn14336 V128256", "draft": "16L d2048 32q/8kv hd64 ffn8192",
+                  "batch": 1, "context": 2048, "k": 5, "temperature": args.temperature}
+        bound = "hbm"
+    else:
+        info = bench_vocab(args)
+        config = {"workload": "vocab-stress: decision pass alone, 256 seqs x 8 rows x 128256",
+                  "batch": 256, "k": 7, "vocab": 128256, "temperatures": [0.3, 1.0, 1.5]}
+        bound = "hbm"
+    steps = args.steps
+    value = info["tokens"] / info["wall_s"]
+    per_launch_ms = info["k_ms"] / max(1, info["k_n"])
+    achieved = (info["k_bytes"] / max(1, info["k_n"])) / (per_launch_ms / 1e3) / 1e9 if info["k_n"] else None
+    roofline = {"bound": bound, "kernel": info["kernel"], "achieved": achieved, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": (achieved / HBM_PEAK_GBS) if achieved else None, "traffic": None,
+                "launches": info["k_n"], "avg_launch_us": per_launch_ms * 1e3,
+                "bytes_per_launch": info["k_bytes"] / max(1, info["k_n"])}
+    if info["k_flops"] and info["k_n"]:
+        roofline["tflops"] = info["k_flops"] / (info["k_ms"] / 1e3) / 1e12
+    line = {
+        "metric": "verified tokens/sec + verify-step latency (ms) at 1 MI355X; % MFMA/HBM peak",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": info["wall_s"] * 1e3 / steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded random-init weights and prompts)",
+        "config": config,
+        "verify_ms_median": info["verify_ms_median"], "verify_ms_p90": info["verify_ms_p90"],
+        "event_ms_per_step": info["event_ms"] / steps,
+        "mean_accepted": float(np.mean(info["acc_hist"])) if info["acc_hist"] else None,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        mean_tok = info["tokens"] / steps
+        model, threads, aff = cpu_info()
+        log("timing the oracle on a bounded sample")
+        cb = cpu_baseline_8b(mean_tok) if args.workload == "8b-shaped" else cpu_baseline_vocab(mean_tok)
+        line["cpu_baseline"] = {"value": cb["value"], "unit": "tokens/s", "cores": threads, "kind": "oracle",
+                                "sample": cb["sample"], "sample_s": cb["sample_s"],
+                                "est_step_s": cb["step_s"], "cpu": model, "affinity": aff}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

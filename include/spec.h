@@ -186,6 +186,19 @@ SPEC_API spec_status spec_seq_info(const spec_ctx* ctx, int64_t seq_id, int32_t*
  * call order (sequence i's k_i + 1 rows are contiguous), and the row count. */
 SPEC_API spec_status spec_last_logits(const spec_ctx* ctx, const float** logits, int32_t* rows);
 
+/* Kernel timing for roofline measurement.  While a kernel name is set, the
+ * context records HIP events on the call's stream around every launch of that
+ * kernel (names as the profiler reports them without namespaces and argument
+ * lists, e.g. "gemm_skinny_bf16<1, 2>", "gemm_tiled_bf16<0>",
+ * "attn_bf16_kernel<128, 2>", "stats_kernel<true>") and accumulates the
+ * elapsed time, the launch count and each launch's algorithmic HBM bytes and
+ * flops (weights, activations and KV actually required, each read once).
+ * name NULL or "" disables timing.  spec_timing_read waits for the recorded
+ * events and returns the totals since the last spec_timing_enable. */
+SPEC_API spec_status spec_timing_enable(spec_ctx* ctx, const char* kernel_name);
+SPEC_API spec_status spec_timing_read(spec_ctx* ctx, double* total_ms, int64_t* launches,
+                                      double* bytes, double* flops);
+
 /* ---------------------------------------------------------------------------
  * The decision pass alone, on caller-provided device logits.
  *

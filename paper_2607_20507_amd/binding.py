@@ -73,6 +73,9 @@ SIGNATURES = {
     "spec_seq_release": (c_int32, [_P, c_int64]),
     "spec_seq_info": (c_int32, [_P, c_int64, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, c_int32]),
     "spec_last_logits": (c_int32, [_P, POINTER(c_void_p), _I32P]),
+    "spec_timing_enable": (c_int32, [_P, ctypes.c_char_p]),
+    "spec_timing_read": (c_int32, [_P, POINTER(ctypes.c_double), _I64P, POINTER(ctypes.c_double),
+                                   POINTER(ctypes.c_double)]),
     "spec_sample_workspace_bytes": (c_size_t, [c_int32, c_int32, c_int32]),
     "spec_sample_verify": (c_int32, [c_int32, _I32P, _F32P, _I64P, _I32P, _P, _P, _P, c_int32,
                                      c_uint64, _P, _P, _P, c_size_t, _P]),
@@ -235,6 +238,18 @@ def spec_last_logits(ctx: int):
     r = c_int32()
     check(lib().spec_last_logits(ctx, ctypes.byref(p), ctypes.byref(r)), ctx)
     return p.value, r.value
+
+
+def spec_timing_enable(ctx: int, kernel_name: Optional[str]):
+    check(lib().spec_timing_enable(ctx, kernel_name.encode() if kernel_name else None), ctx)
+
+
+def spec_timing_read(ctx: int):
+    """-> (total_ms, launches, bytes, flops) of the timed kernel since enable."""
+    ms, b, f = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    n = c_int64()
+    check(lib().spec_timing_read(ctx, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b), ctypes.byref(f)), ctx)
+    return ms.value, n.value, b.value, f.value
 
 
 def spec_sample_workspace_bytes(B: int, total_rows: int, V: int) -> int:

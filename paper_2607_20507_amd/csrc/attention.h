@@ -42,4 +42,7 @@ hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int
 hipError_t launch_attention_f32(const AttnArgs& a, int R, const int32_t* d_row_seq,
                                 const int32_t* d_row_pos, hipStream_t st);
 
+// Profiler name of the bf16 attention kernel for (hd, nt).
+const char* attn_kernel_name(int hd, int nt);
+
 }  // namespace spec

@@ -58,10 +58,10 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
     const int mm = vval[nt] ? m : 0;
     vpos[nt] = it.pos0 + mm / G;
     const bf16_t* base =
-        q + (static_cast<size_t>(it.row0 + mm / G) * a.Hq + gkv * G + mm % G) * HD + g * DPL;
+        q + (static_cast<size_t>(it.row0 + mm / G) * a.Hq + gkv * G + mm % G) * HD + g * 8;
 #pragma unroll
     for (int s = 0; s < DS; ++s)
-      qf[nt][s] = vval[nt] ? reinterpret_cast<const uint4*>(base)[s] : make_uint4(0, 0, 0, 0);
+      qf[nt][s] = vval[nt] ? reinterpret_cast<const uint4*>(base)[4 * s] : make_uint4(0, 0, 0, 0);
   }
   const float scale = kLog2e / sqrtf(static_cast<float>(HD));
   float mrun[NT], lrun[NT];
@@ -74,20 +74,29 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
     for (int dt = 0; dt < DT; ++dt) acc[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int c0 = it.t0; c0 < it.t1; c0 += 32) {
-    uint4 kf[2][DS];
+  // K and V^T operands of one 32-key chunk (keys past t1 are clamped to a
+  // valid address; their scores are masked and their V entries zeroed)
+  auto load_chunk = [&](int c0, uint4 (&kf)[2][DS], uint4 (&vf)[DT]) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       const int t = min(c0 + 8 * (l16 >> 2) + 4 * hh + (l16 & 3), it.t1 - 1);
       const bf16_t* kb =
-          kp + (static_cast<size_t>(pt[t >> 4] * a.Hkv + gkv) * 16 + (t & 15)) * HD + g * DPL;
+          kp + (static_cast<size_t>(pt[t >> 4] * a.Hkv + gkv) * 16 + (t & 15)) * HD + g * 8;
 #pragma unroll
-      for (int s = 0; s < DS; ++s) kf[hh][s] = reinterpret_cast<const uint4*>(kb)[s];
+      for (int s = 0; s < DS; ++s) kf[hh][s] = ld_stream(reinterpret_cast<const uint4*>(kb) + 4 * s);
     }
+    const int tvc = min(c0 + 8 * g, it.t1 - 1);
+    const bf16_t* vb = vp + static_cast<size_t>(pt[tvc >> 4] * a.Hkv + gkv) * HD * 16 + (tvc & 8);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[dt] = ld_stream(reinterpret_cast<const uint4*>(vb + (16 * dt + l16) * 16));
+  };
+  uint4 kf[2][DS], vf[DT], kn[2][DS], vn[DT];
+  load_chunk(it.t0, kf, vf);
+  for (int c0 = it.t0; c0 < it.t1; c0 += 32) {
+    const bool more = c0 + 32 < it.t1;
+    if (more) load_chunk(c0 + 32, kn, vn);
     const int tv = c0 + 8 * g;
     const int nvalid = min(max(it.t1 - tv, 0), 8);
-    const int tvc = min(tv, it.t1 - 1);
-    const bf16_t* vb = vp + static_cast<size_t>(pt[tvc >> 4] * a.Hkv + gkv) * HD * 16 + (tvc & 8);
 
     uint4 pf[NT];
 #pragma unroll
@@ -134,7 +143,7 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
     }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      uint4 v = *reinterpret_cast<const uint4*>(vb + (16 * dt + l16) * 16);
+      uint4 v = vf[dt];
       if (nvalid < 8) {
         v.x = mask_pair(v.x, nvalid);
         v.y = mask_pair(v.y, nvalid - 2);
@@ -143,6 +152,14 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
       }
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[dt][nt] = mfma16x16x32(v, pf[nt], acc[dt][nt]);
+    }
+    if (more) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int s = 0; s < DS; ++s) kf[hh][s] = kn[hh][s];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vf[dt] = vn[dt];
     }
   }
 
@@ -178,31 +195,33 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
   }
 }
 
+// One workgroup per (group, kv head, query vector), one thread per head dim:
+// the partials' loads are independent across parts and coalesced across dims.
 template <int HD>
-__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a, const AttnGroup* __restrict__ groups) {
+__global__ __launch_bounds__(HD) void attn_combine_kernel(AttnArgs a, const AttnGroup* __restrict__ groups) {
   const AttnGroup gr = groups[blockIdx.x];
-  const int gkv = blockIdx.y;
+  const int gkv = blockIdx.y, m = blockIdx.z;
   const int G = a.Hq / a.Hkv;
-  const int M = gr.nrows * G;
-  for (int e = threadIdx.x; e < M * HD; e += blockDim.x) {
-    const int m = e / HD, d = e % HD;
-    float mx = -INFINITY;
-    for (int c = 0; c < gr.nparts; ++c)
-      mx = fmaxf(mx, a.part_ml[(static_cast<size_t>((gr.part0 + c) * a.Hkv + gkv) * 64 + m) * 2]);
-    float num = 0.f, den = 0.f;
-    if (mx != -INFINITY) {
-      for (int c = 0; c < gr.nparts; ++c) {
-        const size_t pm = static_cast<size_t>((gr.part0 + c) * a.Hkv + gkv) * 64 + m;
-        const float mc = a.part_ml[pm * 2];
-        if (mc == -INFINITY) continue;
-        const float w = exp2f(mc - mx);
-        num += w * a.part_o[pm * HD + d];
-        den += w * a.part_ml[pm * 2 + 1];
-      }
+  if (m >= gr.nrows * G) return;
+  const int d = threadIdx.x;
+  const size_t base = static_cast<size_t>(gr.part0 * a.Hkv + gkv) * 64 + m;
+  const size_t stride = static_cast<size_t>(a.Hkv) * 64;
+  float mx = -INFINITY;
+#pragma unroll 8
+  for (int c = 0; c < gr.nparts; ++c) mx = fmaxf(mx, a.part_ml[(base + c * stride) * 2]);
+  float num = 0.f, den = 0.f;
+  if (mx != -INFINITY) {
+#pragma unroll 8
+    for (int c = 0; c < gr.nparts; ++c) {
+      const size_t pm = base + c * stride;
+      const float mc = a.part_ml[pm * 2];
+      const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - mx);
+      num += w * a.part_o[pm * HD + d];
+      den += w * a.part_ml[pm * 2 + 1];
     }
-    const size_t o = (static_cast<size_t>(gr.row0 + m / G) * a.Hq + gkv * G + m % G) * HD + d;
-    static_cast<bf16_t*>(a.out)[o] = f32_to_bf16(den > 0.f ? num / den : 0.f);
   }
+  const size_t o = (static_cast<size_t>(gr.row0 + m / G) * a.Hq + gkv * G + m % G) * HD + d;
+  static_cast<bf16_t*>(a.out)[o] = f32_to_bf16(den > 0.f ? num / den : 0.f);
 }
 
 // fp32: one wave per (row, head); each lane runs an online softmax over keys
@@ -270,11 +289,18 @@ hipError_t launch_bf16_hd(const AttnArgs& a, const AttnItem* items, int n_items,
     else if (nt == 2) attn_bf16_kernel<HD, 2><<<grid, 64, 0, st>>>(a, items);
     else attn_bf16_kernel<HD, 4><<<grid, 64, 0, st>>>(a, items);
   }
-  if (n_groups > 0) attn_combine_kernel<HD><<<dim3(n_groups, a.Hkv), 256, 0, st>>>(a, groups);
+  if (n_groups > 0) attn_combine_kernel<HD><<<dim3(n_groups, a.Hkv, 16 * nt), HD, 0, st>>>(a, groups);
   return hipGetLastError();
 }
 
 }  // namespace
+
+const char* attn_kernel_name(int hd, int nt) {
+  static const char* n128[3] = {"attn_bf16_kernel<128, 1>", "attn_bf16_kernel<128, 2>", "attn_bf16_kernel<128, 4>"};
+  static const char* n64[3] = {"attn_bf16_kernel<64, 1>", "attn_bf16_kernel<64, 2>", "attn_bf16_kernel<64, 4>"};
+  const int i = nt <= 1 ? 0 : (nt == 2 ? 1 : 2);
+  return hd == 128 ? n128[i] : n64[i];
+}
 
 hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int n_items,
                                  const AttnGroup* d_groups, int n_groups, int nt, hipStream_t st) {

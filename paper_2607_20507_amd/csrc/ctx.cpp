@@ -91,6 +91,7 @@ struct FwdOff {
   size_t tok, pos, slot, seqi, pt, items, groups, lmr, lmm;
   int n_items = 0, n_groups = 0, nt = 1, R = 0, n_lm = 0, ptab_stride = 1;
   bool lm_map = false;
+  double attn_keys = 0, attn_qk = 0;  // sum of context lengths; sum over rows of (pos + 1)
 };
 
 size_t pool_layer_elems(const spec_model_desc& m, int num_pages) {
@@ -143,6 +144,7 @@ struct spec_ctx {
   std::string err;
   bool broken = false;
   int last_rows = 0;
+  EventTimer timer;
 };
 
 static thread_local std::string g_err;
@@ -241,6 +243,10 @@ FwdOff add_forward(spec_ctx* ctx, const Model& M, const Fwd& f, MetaBlock& mb) {
     o.n_groups = static_cast<int>(p.groups.size());
     o.nt = p.nt;
   }
+  for (const auto& s : f.segs) {
+    o.attn_keys += s.pos0 + s.nrows;
+    for (int r = 0; r < s.nrows; ++r) o.attn_qk += s.pos0 + r + 1;
+  }
   o.n_lm = static_cast<int>(f.lm_rows.size());
   o.lmr = mb.add(f.lm_rows);
   o.lm_map = !f.lm_map.empty();
@@ -274,30 +280,51 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   a.out = ob;
   a.part_o = wsptr<float>(ctx, ctx->ws.part_o);
   a.part_ml = wsptr<float>(ctx, ctx->ws.part_ml);
+  EventTimer& tm = ctx->timer;
+  const double esz = M.esz;
+  // GEMM launch, timed when selected: algorithmic bytes = weights + inputs +
+  // outputs (read-modify-write for the residual add), flops = 2 R N_w K.
+  auto gemm = [&](int rows, int N, int K, const void* X, const void* W, void* Y, int epi,
+                  const int32_t* rm) -> hipError_t {
+    const bool timed = tm.wants(gemm_kernel_name(dt, rows, epi));
+    if (timed) tm.begin(st);
+    const hipError_t e = launch_gemm(dt, rows, N, K, X, W, Y, epi, st, rm);
+    if (timed) {
+      const double nw = epi == kEpiSwiGLU ? 2.0 * N : N;
+      const double ob = epi == kEpiStoreF32 ? 4.0 : (epi == kEpiAddF32 ? 8.0 : esz);
+      tm.end(st, (nw * K + double(rows) * K) * esz + double(rows) * N * ob, 2.0 * rows * nw * K);
+    }
+    return e;
+  };
   for (int l = 0; l < d.n_layers; ++l) {
     const auto& L = M.layers[l];
     HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
-    HIPC(launch_gemm(dt, R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, st));
+    HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr));
     HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, qkv, I(o.pos),
                         I(o.slot), q, M.kl(l), M.vl(l), st));
     a.kpool = M.kl(l);
     a.vpool = M.vl(l);
     if (dt == 1) {
+      // bytes: every cached key and value once, queries in, output out
+      const bool timed = tm.wants(attn_kernel_name(d.head_dim, o.nt));
+      if (timed) tm.begin(st);
       HIPC(launch_attention_bf16(a, reinterpret_cast<const AttnItem*>(dev + o.items), o.n_items,
                                  reinterpret_cast<const AttnGroup*>(dev + o.groups), o.n_groups,
                                  o.nt, st));
+      if (timed)
+        tm.end(st, (o.attn_keys * d.n_kv_heads * 2.0 + 2.0 * R * d.n_heads) * d.head_dim * esz,
+               4.0 * o.attn_qk * d.n_heads * d.head_dim);
     } else {
       HIPC(launch_attention_f32(a, R, I(o.seqi), I(o.pos), st));
     }
-    HIPC(launch_gemm(dt, R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, st));
+    HIPC(gemm(R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, nullptr));
     HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.mlp_norm, d.rms_eps, y, st));
-    HIPC(launch_gemm(dt, R, d.ffn_dim, d.d_model, y, L.w_gate_up, u, kEpiSwiGLU, st));
-    HIPC(launch_gemm(dt, R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, st));
+    HIPC(gemm(R, d.ffn_dim, d.d_model, y, L.w_gate_up, u, kEpiSwiGLU, nullptr));
+    HIPC(gemm(R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, nullptr));
   }
   if (o.n_lm > 0) {
     HIPC(launch_rmsnorm(dt, o.n_lm, d.d_model, h, I(o.lmr), d.final_norm, d.rms_eps, y, st));
-    HIPC(launch_gemm(dt, o.n_lm, d.vocab, d.d_model, y, d.lm_head, logits, kEpiStoreF32, st,
-                     o.lm_map ? I(o.lmm) : nullptr));
+    HIPC(gemm(o.n_lm, d.vocab, d.d_model, y, d.lm_head, logits, kEpiStoreF32, o.lm_map ? I(o.lmm) : nullptr));
   }
   return SPEC_OK;
 }
@@ -532,6 +559,7 @@ spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const
     }
   }
   HIPC(hipStreamSynchronize(st));
+  ctx->timer.flush();
   return SPEC_OK;
 }
 
@@ -704,7 +732,7 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   const VocabPlan vp = vocab_plan(n, static_cast<int>(rows.size()), ctx->V);
   HIPC(launch_vocab_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
                          reinterpret_cast<const VSeq*>(dev + oseq), wsptr<int32_t>(ctx, ctx->ws.rowtok),
-                         seed, ctx->k_max, d_nacc, d_otok, ctx->wsp + ctx->ws.vocab, st));
+                         seed, ctx->k_max, d_nacc, d_otok, ctx->wsp + ctx->ws.vocab, st, &ctx->timer));
   const int W = ctx->k_max + 1;
   HIPC(hipMemcpyAsync(ctx->h_out, d_nacc, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
   HIPC(hipMemcpyAsync(ctx->h_out + ctx->max_seqs, d_otok, sizeof(int32_t) * n * W, hipMemcpyDeviceToHost, st));
@@ -719,6 +747,24 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
     q.emitted.assign(out_tokens + i * W, out_tokens + i * W + q.a_ver + 1);
   }
   ctx->last_rows = R;
+  ctx->timer.flush();
+  return SPEC_OK;
+}
+
+spec_status spec_timing_enable(spec_ctx* ctx, const char* kernel_name) {
+  EventTimer& t = ctx ? ctx->timer : global_timer();
+  t.reset(kernel_name);
+  return SPEC_OK;
+}
+
+spec_status spec_timing_read(spec_ctx* ctx, double* total_ms, int64_t* launches, double* bytes,
+                             double* flops) {
+  EventTimer& t = ctx ? ctx->timer : global_timer();
+  t.flush();
+  if (total_ms) *total_ms = t.ms;
+  if (launches) *launches = t.launches;
+  if (bytes) *bytes = t.bytes;
+  if (flops) *flops = t.flops;
   return SPEC_OK;
 }
 

@@ -18,4 +18,7 @@ enum GemmEpi {
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
                        int epi, hipStream_t st, const int32_t* row_map = nullptr);
 
+// Profiler name of the kernel launch_gemm uses for (dtype, R, epi).
+const char* gemm_kernel_name(int dtype, int R, int epi);
+
 }  // namespace spec

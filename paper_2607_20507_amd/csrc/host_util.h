@@ -7,6 +7,7 @@
 #include <cstdint>
 #include <cstring>
 #include <mutex>
+#include <string>
 #include <vector>
 
 #include "attention.h"
@@ -14,6 +15,82 @@
 namespace spec {
 
 inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+// Optional timing of one kernel's launches: the launcher asks whether the
+// kernel (by its profiler name) is wanted and brackets each launch.
+struct KernelTimer {
+  virtual ~KernelTimer() {}
+  virtual bool wants(const char* kernel) const = 0;
+  virtual void begin(hipStream_t st) = 0;
+  virtual void end(hipStream_t st, double bytes, double flops) = 0;
+};
+
+// Events around the launches of one kernel; elapsed times are collected at
+// the next synchronisation point.
+class EventTimer : public KernelTimer {
+ public:
+  std::string name;
+  double ms = 0, bytes = 0, flops = 0;
+  int64_t launches = 0;
+
+  ~EventTimer() override {
+    flush();
+    for (hipEvent_t e : free_) (void)hipEventDestroy(e);
+  }
+  bool wants(const char* k) const override { return !name.empty() && name == k; }
+  void begin(hipStream_t st) override {
+    cur_ = take();
+    if (cur_) (void)hipEventRecord(cur_, st);
+  }
+  void end(hipStream_t st, double b, double f) override {
+    hipEvent_t e = take();
+    if (!cur_ || !e) return;
+    (void)hipEventRecord(e, st);
+    recs_.push_back(Rec{cur_, e, b, f});
+    cur_ = nullptr;
+  }
+  void flush() {
+    for (auto& r : recs_) {
+      float t = 0.f;
+      if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&t, r.a, r.b) == hipSuccess) {
+        ms += t;
+        bytes += r.bytes;
+        flops += r.flops;
+        ++launches;
+      }
+      free_.push_back(r.a);
+      free_.push_back(r.b);
+    }
+    recs_.clear();
+  }
+  void reset(const char* k) {
+    flush();
+    name = k ? k : "";
+    ms = bytes = flops = 0;
+    launches = 0;
+  }
+
+ private:
+  struct Rec {
+    hipEvent_t a, b;
+    double bytes, flops;
+  };
+  hipEvent_t take() {
+    if (!free_.empty()) {
+      hipEvent_t e = free_.back();
+      free_.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+  }
+  std::vector<hipEvent_t> free_;
+  std::vector<Rec> recs_;
+  hipEvent_t cur_ = nullptr;
+};
+
+// Timer of the context-free entry points (spec_timing_enable with no context).
+EventTimer& global_timer();
 
 // A packed block of host arrays, each 256-byte aligned, uploaded in one copy.
 class MetaBlock {

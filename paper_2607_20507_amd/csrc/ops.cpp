@@ -36,6 +36,13 @@ spec_status hip_status(hipError_t e) {
 
 }  // namespace
 
+namespace spec {
+EventTimer& global_timer() {
+  static EventTimer t;
+  return t;
+}
+}  // namespace spec
+
 extern "C" {
 
 size_t spec_sample_workspace_bytes(int32_t B, int32_t total_rows, int32_t V) {
@@ -100,7 +107,7 @@ spec_status spec_sample_verify(int32_t B, const int32_t* k, const float* tempera
   if (e != hipSuccess) return SPEC_E_HIP;
   e = launch_vocab_pass(vocab_plan(B, rows_n, V), reinterpret_cast<const VRow*>(ws + orow),
                         reinterpret_cast<const VSeq*>(ws + oseq), draft_tokens, seed, kmax, n_accepted,
-                        out_tokens, ws + ovoc, st);
+                        out_tokens, ws + ovoc, st, &global_timer());
   return hip_status(e);
 }
 

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "host_util.h"
+
 namespace spec {
 
 // One logits row of the decision pass: fp32 pointer and 1/T (0 for greedy).
@@ -51,7 +53,8 @@ size_t vocab_ws_bytes(const VocabPlan& p);
 // Full decision pass.  Outputs n_acc[B], out_tok[B * (kmax + 1)] (device).
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax,
-                             int32_t* d_n_acc, int32_t* d_out_tok, void* d_ws, hipStream_t st);
+                             int32_t* d_n_acc, int32_t* d_out_tok, void* d_ws, hipStream_t st,
+                             KernelTimer* timer = nullptr);
 
 struct DraftPlan {
   int n = 0, V = 0, chunk = 0, n_chunks = 0;

@@ -421,7 +421,7 @@ size_t vocab_ws_bytes(const VocabPlan& p) {
 
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax, int32_t* d_n_acc,
-                             int32_t* d_out_tok, void* d_ws, hipStream_t st) {
+                             int32_t* d_out_tok, void* d_ws, hipStream_t st, KernelTimer* timer) {
   if (p.B == 0) return hipSuccess;
   char* ws = static_cast<char*>(d_ws);
   VStat* stats = reinterpret_cast<VStat*>(ws);
@@ -431,10 +431,13 @@ hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq*
   VDec* decs = reinterpret_cast<VDec*>(ws);
   const bool vec = (p.V % 4) == 0;
   dim3 g1(p.n_chunks1, p.n_rows);
+  const bool timed = timer && timer->wants(vec ? "stats_kernel<true>" : "stats_kernel<false>");
+  if (timed) timer->begin(st);
   if (vec)
     stats_kernel<true><<<g1, kThreads, 0, st>>>(d_rows, p.V, p.chunk1, stats, p.n_chunks1);
   else
     stats_kernel<false><<<g1, kThreads, 0, st>>>(d_rows, p.V, p.chunk1, stats, p.n_chunks1);
+  if (timed) timer->end(st, 4.0 * p.n_rows * p.V, 0.0);
   dim3 g2(p.n_chunks2, p.B);
   if (vec)
     decide_kernel<true><<<g2, kThreads, 0, st>>>(d_rows, d_seqs, d_draft_tok, stats, p.n_chunks1,
