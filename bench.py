@@ -197,6 +197,80 @@ def cpu_baseline_8b(mean_tokens_per_step):
 
 
 # ---------------------------------------------------------------------------
+# 8B-shaped pair, serving batch of 64 sequences
+
+def bench_serving(args):
+    import torch
+    from paper_2607_20507_amd import binding as B
+    from paper_2607_20507_amd.session import DeviceModel, SpecSession
+    from workloads import (SERVING_8B, context_lengths_loguniform, draft_lengths, seq_ids_for,
+                           uniform_prompts)
+
+    cfg = SERVING_8B
+    dev = torch.device("cuda:0")
+    T = args.temperature
+    n = cfg.batch
+    ctx = context_lengths_loguniform(cfg.seed, n, cfg.context[1], cfg.context[2])
+    ks = draft_lengths(cfg.seed, n, cfg.k)
+    kmax = int(max(cfg.k))
+    ids = [int(x) for x in seq_ids_for(cfg.seed, n)]
+    log("drawing weights on device")
+    target = DeviceModel(cfg.target, None, dev, seed=cfg.seed)
+    draft = DeviceModel(cfg.draft, None, dev, seed=cfg.seed + 1)
+    total_steps = args.warmup + args.steps
+    max_len = int(ctx.max()) + total_steps * (kmax + 1) + 64
+    pages = (max_len + 15) // 16
+    need = int(sum((int(c) + total_steps * (kmax + 1) + 64 + 15) // 16 for c in ctx))
+    sess = SpecSession(target, draft, max_seqs=n, k_max=kmax, max_pages_per_seq=pages,
+                       num_pages_target=need, num_pages_draft=need, max_rows=4096)
+    prompts = uniform_prompts(cfg.seed, [int(c) for c in ctx], cfg.target.vocab)
+    log("prefill", int(ctx.sum()), "tokens")
+    sess.prefill(ids, prompts)
+    stream = torch.cuda.current_stream()
+    temps = [T] * n
+    acc_hist, lat = [], []
+
+    def step(s, record):
+        for j in range(1, kmax + 1):
+            live = [ids[i] for i in range(n) if ks[i] >= j]
+            sess.draft_step(live, [T] * len(live), cfg.seed + s)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        na, _ = sess.verify(ids, temps, cfg.seed + s)
+        sess.commit(ids, na)
+        e1.record(stream)
+        if record:
+            acc_hist.extend(int(x) for x in na)
+            lat.append((e0, e1))
+        return int(na.sum()) + n
+
+    for s in range(args.warmup):
+        step(s, False)
+    kernel = args.kernel or "gemm_mfma_bf16<2>"
+    B.spec_timing_enable(sess.ctx, kernel)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    tokens = 0
+    for s in range(args.steps):
+        tokens += step(args.warmup + s, True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_ms, k_n, k_bytes, k_flops = B.spec_timing_read(sess.ctx)
+    B.spec_timing_enable(sess.ctx, None)
+    lats = sorted(a.elapsed_time(b) for a, b in lat)
+    sess.close()
+    return {"tokens": tokens, "wall_s": wall, "event_ms": ev0.elapsed_time(ev1), "acc_hist": acc_hist,
+            "verify_ms_median": float(np.median(lats)), "verify_ms_p90": float(np.percentile(lats, 90)),
+            "kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops,
+            "mean_ctx": float(ctx.mean()), "rows_per_verify": int((ks + 1).sum())}
+
+
+# ---------------------------------------------------------------------------
 # decision pass alone
 
 def bench_vocab(args):
@@ -282,7 +356,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="8b-shaped", choices=["8b-shaped", "vocab-stress"])
+    ap.add_argument("--workload", default="8b-shaped", choices=["8b-shaped", "8b-serving", "vocab-stress"])
     ap.add_argument("--temperature", type=float, default=0.8)
     ap.add_argument("--kernel", default=None, help="kernel to time for the roofline (profiler name)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -304,6 +378,13 @@ def main():
                   "target": "32L d4096 32q/8kv hd128 ffn14336 V128256", "draft": "16L d2048 32q/8kv hd64 ffn8192",
                   "batch": 1, "context": 2048, "k": 5, "temperature": args.temperature}
         bound = "hbm"
+    elif args.workload == "8b-serving":
+        info = bench_serving(args)
+        config = {"workload": "8b-shaped target / 1b-shaped drafter serving 64 sequences, contexts log-uniform "
+                              "[512, 4096] in 16-token pages, k per sequence in {3,5,7}",
+                  "batch": 64, "mean_context": info["mean_ctx"], "rows_per_verify": info["rows_per_verify"],
+                  "temperature": args.temperature}
+        bound = "mfma"
     else:
         info = bench_vocab(args)
         config = {"workload": "vocab-stress: decision pass alone, 256 seqs x 8 rows x 128256",
@@ -312,13 +393,21 @@ def main():
     steps = args.steps
     value = info["tokens"] / info["wall_s"]
     per_launch_ms = info["k_ms"] / max(1, info["k_n"])
-    achieved = (info["k_bytes"] / max(1, info["k_n"])) / (per_launch_ms / 1e3) / 1e9 if info["k_n"] else None
-    roofline = {"bound": bound, "kernel": info["kernel"], "achieved": achieved, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": (achieved / HBM_PEAK_GBS) if achieved else None, "traffic": None,
+    if bound == "mfma":
+        achieved = (info["k_flops"] / max(1, info["k_n"])) / (per_launch_ms / 1e3) / 1e12 if info["k_n"] else None
+        peak, unit = BF16_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        achieved = (info["k_bytes"] / max(1, info["k_n"])) / (per_launch_ms / 1e3) / 1e9 if info["k_n"] else None
+        peak, unit = HBM_PEAK_GBS, "GB/s"
+    roofline = {"bound": bound, "kernel": info["kernel"], "achieved": achieved, "peak": peak,
+                "unit": unit, "frac": (achieved / peak) if achieved else None, "traffic": None,
                 "launches": info["k_n"], "avg_launch_us": per_launch_ms * 1e3,
-                "bytes_per_launch": info["k_bytes"] / max(1, info["k_n"])}
-    if info["k_flops"] and info["k_n"]:
+                "bytes_per_launch": info["k_bytes"] / max(1, info["k_n"]),
+                "flops_per_launch": info["k_flops"] / max(1, info["k_n"])}
+    if bound == "hbm" and info["k_flops"] and info["k_n"]:
         roofline["tflops"] = info["k_flops"] / (info["k_ms"] / 1e3) / 1e12
+    if bound == "mfma" and info["k_n"]:
+        roofline["gbs"] = info["k_bytes"] / (info["k_ms"] / 1e3) / 1e9
     line = {
         "metric": "verified tokens/sec + verify-step latency (ms) at 1 MI355X; % MFMA/HBM peak",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
@@ -334,7 +423,17 @@ def main():
         mean_tok = info["tokens"] / steps
         model, threads, aff = cpu_info()
         log("timing the oracle on a bounded sample")
-        cb = cpu_baseline_8b(mean_tok) if args.workload == "8b-shaped" else cpu_baseline_vocab(mean_tok)
+        if args.workload == "8b-shaped":
+            cb = cpu_baseline_8b(mean_tok)
+        elif args.workload == "8b-serving":
+            # the oracle runs sequences one at a time: a serving step costs the
+            # batch-1 step estimate once per sequence
+            cb = cpu_baseline_8b(1.0)
+            cb["step_s"] *= 64
+            cb["value"] = mean_tok / cb["step_s"]
+            cb["sample"] += "; multiplied by the 64 sequences of the batch (the oracle runs them one by one)"
+        else:
+            cb = cpu_baseline_vocab(mean_tok)
         line["cpu_baseline"] = {"value": cb["value"], "unit": "tokens/s", "cores": threads, "kind": "oracle",
                                 "sample": cb["sample"], "sample_s": cb["sample_s"],
                                 "est_step_s": cb["step_s"], "cpu": model, "affinity": aff}

@@ -22,9 +22,13 @@ enum { SPEC_EPI_STORE_F32 = 0, SPEC_EPI_ADD_F32 = 1, SPEC_EPI_SWIGLU = 2 };
  *   SPEC_EPI_STORE_F32: Y fp32 [R, N] = X W^T
  *   SPEC_EPI_ADD_F32:   Y fp32 [R, N] += X W^T   (residual add)
  *   SPEC_EPI_SWIGLU:    Y dtype [R, N] = silu(X Wg^T) * (X Wu^T)
- * bf16 needs K % 128 == 0 (else SPEC_E_UNSUPPORTED). */
+ * bf16 needs K % 128 == 0 (else SPEC_E_UNSUPPORTED).  workspace (device,
+ * optional, NULL allowed): fp32 split-K partials for R > 64 when the output
+ * grid is small; size it with spec_op_gemm_workspace_bytes(R, N_w). */
+SPEC_API size_t spec_op_gemm_workspace_bytes(int32_t R, int32_t Nw);
 SPEC_API spec_status spec_op_gemm(int32_t dtype, int32_t R, int32_t N, int32_t K, const void* X,
-                                  const void* W, void* Y, int32_t epilogue, void* stream);
+                                  const void* W, void* Y, int32_t epilogue, void* workspace,
+                                  size_t workspace_bytes, void* stream);
 
 /* RMSNorm: y[r] (dtype) = h[r] / sqrt(mean(h[r]^2) + eps) * w, h fp32 [R, d]. */
 SPEC_API spec_status spec_op_rmsnorm(int32_t dtype, int32_t R, int32_t d, const float* h,

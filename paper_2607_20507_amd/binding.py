@@ -82,7 +82,8 @@ SIGNATURES = {
     "spec_sample_draft": (c_int32, [c_int32, _P, c_int32, _F32P, _I64P, _I32P, c_uint64, _P, _P,
                                     c_size_t, _P]),
     "spec_philox_uniform": (c_int32, [c_uint64, c_int64, c_int32, c_int32, c_int32, _P, _P]),
-    "spec_op_gemm": (c_int32, [c_int32, c_int32, c_int32, c_int32, _P, _P, _P, c_int32, _P]),
+    "spec_op_gemm_workspace_bytes": (c_size_t, [c_int32, c_int32]),
+    "spec_op_gemm": (c_int32, [c_int32, c_int32, c_int32, c_int32, _P, _P, _P, c_int32, _P, c_size_t, _P]),
     "spec_op_rmsnorm": (c_int32, [c_int32, c_int32, c_int32, _P, _P, c_float, _P, _P]),
     "spec_op_rope_kv": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_float, _P, _P, _P,
                                   _P, _P, _P, _P]),
@@ -281,8 +282,14 @@ def spec_philox_uniform(seed: int, seq_id: int, pos: int, purpose: int, n: int, 
     check(lib().spec_philox_uniform(seed, int(seq_id), pos, purpose, n, dptr(out), stream_ptr(stream)))
 
 
-def spec_op_gemm(dtype: int, R: int, N: int, K: int, X, W, Y, epilogue: int, stream=None):
-    check(lib().spec_op_gemm(dtype, R, N, K, dptr(X), dptr(W), dptr(Y), epilogue, stream_ptr(stream)))
+def spec_op_gemm_workspace_bytes(R: int, Nw: int) -> int:
+    return lib().spec_op_gemm_workspace_bytes(R, Nw)
+
+
+def spec_op_gemm(dtype: int, R: int, N: int, K: int, X, W, Y, epilogue: int, workspace=None, stream=None):
+    wb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    check(lib().spec_op_gemm(dtype, R, N, K, dptr(X), dptr(W), dptr(Y), epilogue, dptr(workspace), wb,
+                             stream_ptr(stream)))
 
 
 def spec_op_rmsnorm(dtype: int, R: int, d: int, h, w, eps: float, y, stream=None):

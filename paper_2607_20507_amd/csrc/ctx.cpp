@@ -75,6 +75,7 @@ struct Seq {
 struct Ws {
   size_t h = 0, y = 0, qkv = 0, q = 0, o = 0, u = 0, logits = 0, dq = 0, dtok = 0, rowtok = 0;
   size_t part_o = 0, part_ml = 0, vocab = 0, draft = 0, nacc = 0, otok = 0, meta = 0;
+  size_t splitk = 0, splitk_bytes = 0;
   size_t meta_cap = 0, total = 0;
 };
 
@@ -195,6 +196,8 @@ void compute_ws(spec_ctx* c) {
   w.draft = take(draft_ws_bytes(draft_plan(c->max_seqs, c->V)));
   w.nacc = take(c->max_seqs * 4);
   w.otok = take(vr * 4);
+  w.splitk_bytes = gemm_splitk_bytes(c->R_max, std::max(c->qkv_max, 2 * c->ffn_max));
+  w.splitk = take(w.splitk_bytes);
   // metadata bound for one call
   size_t mc = 0;
   mc += 6 * align_up(R * 4);
@@ -288,7 +291,8 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
                   const int32_t* rm) -> hipError_t {
     const bool timed = tm.wants(gemm_kernel_name(dt, rows, epi));
     if (timed) tm.begin(st);
-    const hipError_t e = launch_gemm(dt, rows, N, K, X, W, Y, epi, st, rm);
+    const hipError_t e = launch_gemm(dt, rows, N, K, X, W, Y, epi, st, rm, wsptr<float>(ctx, ctx->ws.splitk),
+                                     ctx->ws.splitk_bytes);
     if (timed) {
       const double nw = epi == kEpiSwiGLU ? 2.0 * N : N;
       const double ob = epi == kEpiStoreF32 ? 4.0 : (epi == kEpiAddF32 ? 8.0 : esz);

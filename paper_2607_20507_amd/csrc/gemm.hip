@@ -12,8 +12,9 @@
 //    features (gate+up pairs for SwiGLU); its waves split K and reduce through
 //    LDS in a fixed order (deterministic, no atomics).  M is padded to 16 per
 //    tile; MFMA throughput is ~10x what the weight stream needs.
-//  * tiled (R > 64): 128x128 workgroup tiles, BK = 64, LDS double buffering
-//    with an XOR swizzle of 16-byte chunks, 2x2 waves of 64x64.
+//  * mfma (R > 64): 128x256 workgroup tiles, BK = 64, LDS double buffering
+//    with an XOR swizzle of 16-byte chunks, 4 waves of 64x128, split-K with
+//    a fixed-order reduction when the grid is small.
 //  * fp32 (the fp32 configuration): a plain LDS-tiled FMA kernel; no
 //    reduced-precision arithmetic.
 
@@ -126,128 +127,140 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 }
 
 // ---------------------------------------------------------------------------
-// tiled bf16: BM = BN = 128, BK = 64, 256 threads (2x2 waves of 64x64)
+// MFMA bf16 for R > 64: 128 x 256 workgroup tile (256 W rows; 128 gate + 128
+// up rows for SwiGLU), BK = 64, 4 waves of 64 x 128.  A 64 x 128 wave tile
+// halves the LDS bytes per flop of a 64 x 64 one (operand bytes / flop =
+// (64 + 128) / (64 * 128)).  Global loads of tile k+1 run while tile k is
+// multiplied, staged in registers into an LDS double buffer (96 KB) of
+// XOR-swizzled 16-byte chunks; one barrier per k-step.
+// Split-K (blockIdx.z) writes raw fp32 partials by W row; a reduction pass
+// applies the epilogue in a fixed order.
 
-constexpr int kTM = 128, kTN = 128, kTK = 64;
+constexpr int kMM = 128, kMN = 256, kMK = 64;
 
 template <int EPI>
-__global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict__ X,
-                                                       const bf16_t* __restrict__ W,
-                                                       void* __restrict__ Y, int R, int N, int K,
-                                                       const int32_t* __restrict__ row_map) {
+__global__ __launch_bounds__(256) void gemm_mfma_bf16(const bf16_t* __restrict__ X,
+                                                      const bf16_t* __restrict__ W,
+                                                      void* __restrict__ Y, float* __restrict__ part,
+                                                      int R, int N, int K, int k_len,
+                                                      const int32_t* __restrict__ row_map) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
-  __shared__ uint4 As[2][kTM * 8];
-  __shared__ uint4 Bs[2][kTN * 8];
+  __shared__ u32x4 As[2][kMM * 8];
+  __shared__ u32x4 Bs[2][kMN * 8];
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1), wave = t / kWave;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave & 1, wn = wave >> 1;
   const int g = lane >> 4, l16 = lane & 15;
-  const int m0 = blockIdx.y * kTM;
-  const int ncols = SW ? kTN / 2 : kTN;  // output features per tile
-  const int f0 = blockIdx.x * ncols;
+  const int m0 = blockIdx.y * kMM;
+  const int f0 = blockIdx.x * (SW ? kMN / 2 : kMN);
+  const int kbeg = blockIdx.z * k_len;
+  const int nk = (min(K, kbeg + k_len) - kbeg) / kMK;
 
-  // global source rows for the 4 chunks each thread stages per operand
-  const uint4* asrc[4];
-  const uint4* bsrc[4];
-  bool av[4], bv[4];
-  int lds_off[4];
+  // staging: thread t moves chunk (t & 7) of tile rows (t >> 3) + 32 i.  Rows
+  // past R or N are clamped to the last valid row: read but never written back.
+  const int sr = t >> 3, sc = t & 7;
+  const int lds_st = sr * 8 + (sc ^ (sr & 7));
+  const bf16_t* xs = X + kbeg + sc * 8;
+  const bf16_t* ws = W + kbeg + sc * 8;
+  uint32_t aoff[4], boff[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int idx = t + 256 * i;
-    const int r = idx >> 3, c = idx & 7;
-    lds_off[i] = r * 8 + (c ^ (r & 7));
-    const int m = m0 + r;
-    av[i] = m < R;
-    asrc[i] = reinterpret_cast<const uint4*>(X + static_cast<size_t>(av[i] ? m : 0) * K) + c;
-    int wrow;
-    if (SW) {
-      const int f = f0 + (r & 63);
-      bv[i] = f < N;
-      wrow = (r < 64 ? 0 : N) + (bv[i] ? f : 0);
-    } else {
-      const int f = f0 + r;
-      bv[i] = f < N;
-      wrow = bv[i] ? f : 0;
-    }
-    bsrc[i] = reinterpret_cast<const uint4*>(W + static_cast<size_t>(wrow) * K) + c;
+  for (int i = 0; i < 4; ++i) aoff[i] = static_cast<uint32_t>(min(m0 + sr + 32 * i, R - 1));
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int br = sr + 32 * i;
+    if (SW)
+      boff[i] = static_cast<uint32_t>((br < 128 ? 0 : N) + min(f0 + (br & 127), N - 1));
+    else
+      boff[i] = static_cast<uint32_t>(min(f0 + br, N - 1));
   }
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  uint4 ra[4], rb[4];
-  auto gload = [&](int kt) {
-    const int co = kt * (kTK / 8);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = av[i] ? asrc[i][co] : zero;
-      rb[i] = bv[i] ? bsrc[i][co] : zero;
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      As[buf][lds_off[i]] = ra[i];
-      Bs[buf][lds_off[i]] = rb[i];
-    }
-  };
-  // B-tile row of the wave's n-subtile j
-  auto brow = [&](int j) -> int {
-    if (SW) return (j < 2) ? (32 * wn + 16 * j) : (64 + 32 * wn + 16 * (j - 2));
-    return 64 * wn + 16 * j;
-  };
+  // one register staging set: tile kt+1 loads while tile kt is multiplied
+  // (native vector types keep the staging values in registers)
+  u32x4 sa[4], sb[8];
+#define SPEC_MFMA_LOAD(KT)                                                                         \
+  do {                                                                                             \
+    const int ko_ = (KT) * kMK;                                                                    \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                  \
+        sa[i] = *reinterpret_cast<const u32x4*>(xs + static_cast<size_t>(aoff[i]) * K + ko_);      \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                                  \
+        sb[i] = *reinterpret_cast<const u32x4*>(ws + static_cast<size_t>(boff[i]) * K + ko_);      \
+  } while (0)
+#define SPEC_MFMA_STORE(AL, BL)                                                                    \
+  do {                                                                                             \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) AL[lds_st + 256 * i] = sa[i];                    \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) BL[lds_st + 256 * i] = sb[i];                    \
+  } while (0)
 
-  f32x4 acc[4][4];
+  f32x4 acc[4][8];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = K / kTK;
-  gload(0);
-  lstore(0);
+  const int sw = l16 & 7;  // row & 7 of every fragment row this lane reads
+#define SPEC_MFMA_COMPUTE(AL, BL)                                                                  \
+  _Pragma("unroll") for (int ks = 0; ks < 2; ++ks) {                                               \
+    const int c = (4 * ks + g) ^ sw;                                                               \
+    u32x4 a[4], b[8];                                                                              \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) a[i] = AL[(64 * wm + 16 * i + l16) * 8 + c];     \
+    _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                                \
+      const int r = SW ? ((j < 4) ? (64 * wn + 16 * j) : (128 + 64 * wn + 16 * (j - 4)))           \
+                       : (128 * wn + 16 * j);                                                      \
+      b[j] = BL[(r + l16) * 8 + c];                                                                \
+    }                                                                                              \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                  \
+        _Pragma("unroll") for (int j = 0; j < 8; ++j) acc[i][j] = mfma16x16x32v(a[i], b[j], acc[i][j]); \
+  }
+
+  if (nk > 0) {
+    SPEC_MFMA_LOAD(0);
+    SPEC_MFMA_STORE(As[0], Bs[0]);
+  }
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int c = 4 * ks + g;
-      uint4 a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 64 * wm + 16 * i + l16;
-        a[i] = As[buf][r * 8 + (c ^ (r & 7))];
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = brow(j) + l16;
-        b[j] = Bs[buf][r * 8 + (c ^ (r & 7))];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a[i], b[j], acc[i][j]);
-    }
-    if (kt + 1 < nk) lstore(buf ^ 1);
+    if (kt + 1 < nk) SPEC_MFMA_LOAD(kt + 1);
+    SPEC_MFMA_COMPUTE(As[buf], Bs[buf]);
+    if (kt + 1 < nk) SPEC_MFMA_STORE(As[buf ^ 1], Bs[buf ^ 1]);
     __syncthreads();
   }
-  // epilogue
+#undef SPEC_MFMA_COMPUTE
+#undef SPEC_MFMA_STORE
+#undef SPEC_MFMA_LOAD
+
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
       if (m >= R) continue;
+      if (part) {
+        float* pr = part + (static_cast<size_t>(blockIdx.z) * R + m) * (SW ? 2 * N : N);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          int n, wrow;
+          if (SW) {
+            n = f0 + 64 * wn + 16 * (j & 3) + l16;
+            wrow = (j < 4 ? 0 : N) + n;
+          } else {
+            n = f0 + 128 * wn + 16 * j + l16;
+            wrow = n;
+          }
+          if (n < N) pr[wrow] = acc[i][j][r];
+        }
+        continue;
+      }
       const size_t mo = static_cast<size_t>(row_map ? row_map[m] : m);
       if (SW) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int n = f0 + 32 * wn + 16 * j + l16;
+        for (int j = 0; j < 4; ++j) {
+          const int n = f0 + 64 * wn + 16 * j + l16;
           if (n < N)
-            static_cast<bf16_t*>(Y)[mo * N + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + 2][r]);
+            static_cast<bf16_t*>(Y)[mo * N + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + 4][r]);
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = f0 + 64 * wn + 16 * j + l16;
+        for (int j = 0; j < 8; ++j) {
+          const int n = f0 + 128 * wn + 16 * j + l16;
           if (n >= N) continue;
           float* y = static_cast<float*>(Y) + mo * N + n;
           if (EPI == kEpiStoreF32) *y = acc[i][j][r];
@@ -255,6 +268,29 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
         }
       }
     }
+}
+
+// Sum split-K partials [S][R][Nw] in split order and apply the epilogue.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part, int S, int R, int N,
+                                                     void* __restrict__ Y, const int32_t* __restrict__ row_map) {
+  constexpr bool SW = (EPI == kEpiSwiGLU);
+  const int Nw = SW ? 2 * N : N;
+  const size_t total = static_cast<size_t>(R) * N;
+  for (size_t e = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
+       e += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    const int m = static_cast<int>(e / N), n = static_cast<int>(e % N);
+    float v = 0.f, u = 0.f;
+    for (int s = 0; s < S; ++s) {
+      const float* pr = part + (static_cast<size_t>(s) * R + m) * Nw;
+      v += pr[n];
+      if (SW) u += pr[N + n];
+    }
+    const size_t o = static_cast<size_t>(row_map ? row_map[m] : m) * N + n;
+    if (EPI == kEpiStoreF32) static_cast<float*>(Y)[o] = v;
+    if (EPI == kEpiAddF32) static_cast<float*>(Y)[o] += v;
+    if (EPI == kEpiSwiGLU) static_cast<bf16_t*>(Y)[o] = f32_to_bf16(silu(v) * u);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -351,9 +387,44 @@ hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hi
   return hipGetLastError();
 }
 
+// Split-K factor for the MFMA kernel: enough workgroups to cover the 256 CUs
+// about twice, partials within the workspace, k-splits multiples of 64.
+template <int EPI>
+int mfma_splits(int R, int N, int K, size_t ws_bytes, int* k_len) {
+  const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
+  const int tiles = ((Nw + kMN - 1) / kMN) * ((R + kMM - 1) / kMM);
+  int S = 1;
+  if (ws_bytes && tiles < 256) {
+    S = std::min(8, (512 + tiles - 1) / tiles);
+    while (S > 1 && static_cast<size_t>(S) * R * Nw * sizeof(float) > ws_bytes) --S;
+  }
+  *k_len = ((K + S - 1) / S + kMK - 1) / kMK * kMK;
+  return (K + *k_len - 1) / *k_len;
+}
+
+template <int EPI>
+hipError_t mfma(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
+                const int32_t* rm, float* ws, size_t ws_bytes) {
+  int k_len = K;
+  const int S = mfma_splits<EPI>(R, N, K, ws ? ws_bytes : 0, &k_len);
+  const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
+  dim3 grid((Nw + kMN - 1) / kMN, (R + kMM - 1) / kMM, S);
+  const bf16_t* x = static_cast<const bf16_t*>(X);
+  const bf16_t* w = static_cast<const bf16_t*>(W);
+  if (S <= 1) {
+    gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, rm);
+    return hipGetLastError();
+  }
+  gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, rm);
+  const size_t total = static_cast<size_t>(R) * N;
+  const int blocks = static_cast<int>(std::min<size_t>(2048, (total + 255) / 256));
+  splitk_reduce<EPI><<<blocks, 256, 0, st>>>(ws, S, R, N, Y, rm);
+  return hipGetLastError();
+}
+
 template <int EPI>
 hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
-                    hipStream_t st, const int32_t* rm) {
+                    hipStream_t st, const int32_t* rm, float* ws, size_t ws_bytes) {
   if (dtype == 0) {
     const int ncols = (EPI == kEpiSwiGLU) ? 32 : 64;
     dim3 grid((N + ncols - 1) / ncols, (R + 63) / 64);
@@ -366,18 +437,22 @@ hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W
   if (R <= 32) return skinny<2, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 48) return skinny<3, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 64) return skinny<4, EPI>(R, N, K, X, W, Y, st, rm);
-  const int ncols = (EPI == kEpiSwiGLU) ? kTN / 2 : kTN;
-  dim3 grid((N + ncols - 1) / ncols, (R + kTM - 1) / kTM);
-  gemm_tiled_bf16<EPI><<<grid, 256, 0, st>>>(static_cast<const bf16_t*>(X),
-                                             static_cast<const bf16_t*>(W), Y, R, N, K, rm);
-  return hipGetLastError();
+  return mfma<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
 }
 
 }  // namespace
 
+size_t gemm_splitk_bytes(int R_max, int Nw_max) {
+  // only grids of fewer than 256 tiles split, into S <= ceil(512 / tiles)
+  // parts, so S * tiles < 768 and the partials S * R * Nw stay below
+  // 768 * kMM * kMN floats; smaller problems need less
+  const size_t tiles = static_cast<size_t>((Nw_max + kMN - 1) / kMN) * ((R_max + kMM - 1) / kMM);
+  return std::min<size_t>(768, 2 * tiles + 512) * kMM * kMN * sizeof(float);
+}
+
 const char* gemm_kernel_name(int dtype, int R, int epi) {
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
-  static const char* tiled[3] = {"gemm_tiled_bf16<0>", "gemm_tiled_bf16<1>", "gemm_tiled_bf16<2>"};
+  static const char* tiled[3] = {"gemm_mfma_bf16<0>", "gemm_mfma_bf16<1>", "gemm_mfma_bf16<2>"};
   static const char* skinny[4][3] = {
       {"gemm_skinny_bf16<1, 0>", "gemm_skinny_bf16<1, 1>", "gemm_skinny_bf16<1, 2>"},
       {"gemm_skinny_bf16<2, 0>", "gemm_skinny_bf16<2, 1>", "gemm_skinny_bf16<2, 2>"},
@@ -390,12 +465,16 @@ const char* gemm_kernel_name(int dtype, int R, int epi) {
 }
 
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
-                       int epi, hipStream_t st, const int32_t* row_map) {
+                       int epi, hipStream_t st, const int32_t* row_map, float* splitk_ws,
+                       size_t splitk_bytes) {
   if (R <= 0 || N <= 0) return hipSuccess;
   switch (epi) {
-    case kEpiStoreF32: return dispatch<kEpiStoreF32>(dtype, R, N, K, X, W, Y, st, row_map);
-    case kEpiAddF32: return dispatch<kEpiAddF32>(dtype, R, N, K, X, W, Y, st, row_map);
-    case kEpiSwiGLU: return dispatch<kEpiSwiGLU>(dtype, R, N, K, X, W, Y, st, row_map);
+    case kEpiStoreF32:
+      return dispatch<kEpiStoreF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes);
+    case kEpiAddF32:
+      return dispatch<kEpiAddF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes);
+    case kEpiSwiGLU:
+      return dispatch<kEpiSwiGLU>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes);
   }
   return hipErrorInvalidValue;
 }

@@ -147,14 +147,19 @@ spec_status spec_philox_uniform(uint64_t seed, int64_t seq_id, int32_t pos, int3
                                           static_cast<hipStream_t>(stream)));
 }
 
+size_t spec_op_gemm_workspace_bytes(int32_t R, int32_t Nw) {
+  return (R <= 0 || Nw <= 0) ? 0 : gemm_splitk_bytes(R, Nw);
+}
+
 spec_status spec_op_gemm(int32_t dtype, int32_t R, int32_t N, int32_t K, const void* X, const void* W,
-                         void* Y, int32_t epilogue, void* stream) {
+                         void* Y, int32_t epilogue, void* workspace, size_t workspace_bytes, void* stream) {
   if ((dtype != SPEC_F32 && dtype != SPEC_BF16) || R < 0 || N < 0 || K <= 0 || !X || !W || !Y)
     return SPEC_E_INVALID;
   if (epilogue < SPEC_EPI_STORE_F32 || epilogue > SPEC_EPI_SWIGLU) return SPEC_E_INVALID;
   if (dtype == SPEC_BF16 && K % 128 != 0) return SPEC_E_UNSUPPORTED;
   return hip_status(launch_gemm(dtype == SPEC_F32 ? 0 : 1, R, N, K, X, W, Y, epilogue,
-                                static_cast<hipStream_t>(stream)));
+                                static_cast<hipStream_t>(stream), nullptr, static_cast<float*>(workspace),
+                                workspace ? workspace_bytes : 0));
 }
 
 spec_status spec_op_rmsnorm(int32_t dtype, int32_t R, int32_t d, const float* h, const void* w, float eps,

@@ -45,7 +45,7 @@ def _rand_bf16(shape, std, gen_seed, dev):
     return (torch.randn(*shape, generator=g, device=dev) * std).to(torch.bfloat16)
 
 
-def _gemm_case(dt, R, N, K, epi, dev, seed=0, cols=None):
+def _gemm_case(dt, R, N, K, epi, dev, seed=0, cols=None, splitk=True):
     b = B()
     rows_w = 2 * N if epi == b.SPEC_EPI_SWIGLU else N
     if dt == b.SPEC_BF16:
@@ -63,8 +63,11 @@ def _gemm_case(dt, R, N, K, epi, dev, seed=0, cols=None):
     else:
         Y = torch.full((R, N), float("nan"), device=dev)
     Y0 = Y.float().cpu().numpy().astype(np.float64)
-    say("gemm", dt, R, N, K, epi)
-    b.spec_op_gemm(dt, R, N, K, X, W, Y, epi)
+    ws = None
+    if splitk:
+        ws = torch.empty(b.spec_op_gemm_workspace_bytes(R, rows_w), dtype=torch.uint8, device=dev)
+    say("gemm", dt, R, N, K, epi, "splitk" if splitk else "")
+    b.spec_op_gemm(dt, R, N, K, X, W, Y, epi, ws)
     torch.cuda.synchronize()
     if cols is None:
         cols = np.arange(N)
@@ -91,11 +94,12 @@ EPIS = [0, 1, 2]
 
 @pytest.mark.parametrize("R,N,K", [(1, 48, 128), (6, 200, 256), (16, 64, 384), (17, 100, 128), (33, 130, 256),
                                    (48, 96, 512), (64, 64, 128), (65, 300, 256), (130, 260, 384),
-                                   (384, 512, 512), (257, 136, 128)])
+                                   (384, 512, 512), (257, 136, 128), (364, 600, 1024), (129, 257, 640)])
 @pytest.mark.parametrize("epi", EPIS)
-def test_gemm_bf16_small(R, N, K, epi):
+@pytest.mark.parametrize("splitk", [True, False])
+def test_gemm_bf16_small(R, N, K, epi, splitk):
     dev = device()
-    got, ref = _gemm_case(B().SPEC_BF16, R, N, K, epi, dev, seed=R * 7 + N)
+    got, ref = _gemm_case(B().SPEC_BF16, R, N, K, epi, dev, seed=R * 7 + N, splitk=splitk)
     tol = 1e-2 if epi == 2 else 1e-5
     assert rel_err(got, ref) < tol
 
