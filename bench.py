@@ -42,6 +42,32 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def pmc_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` measured by the profiler's FETCH_SIZE and
+    WRITE_SIZE counters (scaled by a copy of known size), from the committed
+    summaries under profiles/; None unless the kernel's source is unchanged
+    since the counters were taken."""
+    import glob
+    import hashlib
+    for path in glob.glob(os.path.join(ROOT, "profiles", "pmc_*.txt")):
+        fields = {}
+        with open(path) as f:
+            for line in f:
+                if ": " in line and not line.startswith((" ", "#")):
+                    key, val = line.rstrip("\n").split(": ", 1)
+                    fields[key] = val
+        if fields.get("kernel") != kernel or fields.get("workload") != workload:
+            continue
+        try:
+            with open(os.path.join(ROOT, fields["source"]), "rb") as f:
+                if hashlib.sha256(f.read()).hexdigest() != fields["source_sha256"]:
+                    return None
+            return float(fields["traffic_bytes_per_launch"])
+        except (OSError, KeyError, ValueError):
+            return None
+    return None
+
+
 def cpu_info():
     model = "unknown"
     try:
@@ -360,6 +386,9 @@ def main():
     ap.add_argument("--temperature", type=float, default=0.8)
     ap.add_argument("--kernel", default=None, help="kernel to time for the roofline (profiler name)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-MiB device buffer --steps times (a plain copy kernel of known "
+                         "size, for scaling the profiler's FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -371,6 +400,18 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
+
+    if args.calibrate_copy:
+        nbytes = args.calibrate_copy << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "device copy", "bytes_read_per_copy": nbytes,
+                          "bytes_written_per_copy": nbytes, "copies": args.steps}), flush=True)
+        return
 
     if args.workload == "8b-shaped":
         info = bench_8b(args)
@@ -400,7 +441,8 @@ def main():
         achieved = (info["k_bytes"] / max(1, info["k_n"])) / (per_launch_ms / 1e3) / 1e9 if info["k_n"] else None
         peak, unit = HBM_PEAK_GBS, "GB/s"
     roofline = {"bound": bound, "kernel": info["kernel"], "achieved": achieved, "peak": peak,
-                "unit": unit, "frac": (achieved / peak) if achieved else None, "traffic": None,
+                "unit": unit, "frac": (achieved / peak) if achieved else None,
+                "traffic": pmc_traffic(info["kernel"], args.workload),
                 "launches": info["k_n"], "avg_launch_us": per_launch_ms * 1e3,
                 "bytes_per_launch": info["k_bytes"] / max(1, info["k_n"]),
                 "flops_per_launch": info["k_flops"] / max(1, info["k_n"])}

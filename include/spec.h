@@ -189,7 +189,7 @@ SPEC_API spec_status spec_last_logits(const spec_ctx* ctx, const float** logits,
 /* Kernel timing for roofline measurement.  While a kernel name is set, the
  * context records HIP events on the call's stream around every launch of that
  * kernel (names as the profiler reports them without namespaces and argument
- * lists, e.g. "gemm_skinny_bf16<1, 2>", "gemm_tiled_bf16<0>",
+ * lists, e.g. "gemm_skinny_bf16<1, 2>", "gemm_mfma_bf16<0>",
  * "attn_bf16_kernel<128, 2>", "stats_kernel<true>") and accumulates the
  * elapsed time, the launch count and each launch's algorithmic HBM bytes and
  * flops (weights, activations and KV actually required, each read once).
