@@ -12,9 +12,10 @@
 //    features (gate+up pairs for SwiGLU); its waves split K and reduce through
 //    LDS in a fixed order (deterministic, no atomics).  M is padded to 16 per
 //    tile; MFMA throughput is ~10x what the weight stream needs.
-//  * mfma (R > 64): 128x256 workgroup tiles, BK = 64, LDS double buffering
-//    with an XOR swizzle of 16-byte chunks, 4 waves of 64x128, split-K with
-//    a fixed-order reduction when the grid is small.
+//  * mfma (R > 64): 128x256 workgroup tiles, BK = 32, two workgroups per CU,
+//    loads two k-steps ahead, LDS double buffering with an XOR swizzle of
+//    16-byte chunks, 4 waves of 64x128, XCD-aware tile order, split-K with a
+//    fixed-order reduction when the grid is small.
 //  * fp32 (the fp32 configuration): a plain LDS-tiled FMA kernel; no
 //    reduced-precision arithmetic.
 
@@ -128,66 +129,76 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 
 // ---------------------------------------------------------------------------
 // MFMA bf16 for R > 64: 128 x 256 workgroup tile (256 W rows; 128 gate + 128
-// up rows for SwiGLU), BK = 64, 4 waves of 64 x 128.  A 64 x 128 wave tile
-// halves the LDS bytes per flop of a 64 x 64 one (operand bytes / flop =
-// (64 + 128) / (64 * 128)).  Global loads of tile k+1 run while tile k is
-// multiplied, staged in registers into an LDS double buffer (96 KB) of
-// XOR-swizzled 16-byte chunks; one barrier per k-step.
-// Split-K (blockIdx.z) writes raw fp32 partials by W row; a reduction pass
-// applies the epilogue in a fixed order.
+// up rows for SwiGLU), BK = 32, 4 waves of 64 x 128.  Two workgroups share a
+// CU (48 KB of LDS and at most 256 registers per lane each), so one
+// workgroup's MFMAs cover the other's barrier and load waits.  Global loads
+// run two k-steps ahead through two register staging sets: tile kt+2 is in
+// flight while tile kt is multiplied and tile kt+1 waits to be stored into the
+// LDS double buffer (XOR-swizzled 16-byte chunks, one barrier per k-step).
+// The 1-D grid is decoded XCD-aware: workgroups are dispatched round-robin
+// over the 8 XCDs, so consecutive tile ids are mapped to one XCD, and the row
+// tiles of a column tile are consecutive, sharing that XCD's L2 for the W tile.
+// Split-K writes raw fp32 partials by W row; a reduction pass applies the
+// epilogue in a fixed order.
 
-constexpr int kMM = 128, kMN = 256, kMK = 64;
+constexpr int kMM = 128, kMN = 256, kMK = 32;
+constexpr int kMCh = kMK / 8;           // 16-byte chunks per tile row per k-step
+constexpr int kMRows = 256 / kMCh;      // tile rows one staging pass covers
+constexpr int kMPA = kMM / kMRows, kMPB = kMN / kMRows;
 
 template <int EPI>
-__global__ __launch_bounds__(256) void gemm_mfma_bf16(const bf16_t* __restrict__ X,
-                                                      const bf16_t* __restrict__ W,
-                                                      void* __restrict__ Y, float* __restrict__ part,
-                                                      int R, int N, int K, int k_len,
-                                                      const int32_t* __restrict__ row_map) {
+__global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(const bf16_t* __restrict__ X,
+                                                         const bf16_t* __restrict__ W,
+                                                         void* __restrict__ Y, float* __restrict__ part,
+                                                         int R, int N, int K, int k_len, int MT, int NT,
+                                                         const int32_t* __restrict__ row_map) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
-  __shared__ u32x4 As[2][kMM * 8];
-  __shared__ u32x4 Bs[2][kMN * 8];
+  __shared__ u32x4 As[2][kMM * kMCh];
+  __shared__ u32x4 Bs[2][kMN * kMCh];
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1), wave = t / kWave;
   const int wm = wave & 1, wn = wave >> 1;
   const int g = lane >> 4, l16 = lane & 15;
-  const int m0 = blockIdx.y * kMM;
-  const int f0 = blockIdx.x * (SW ? kMN / 2 : kMN);
-  const int kbeg = blockIdx.z * k_len;
-  const int nk = (min(K, kbeg + k_len) - kbeg) / kMK;
+  const int total = gridDim.x, nid = blockIdx.x;
+  const int xcd = nid & 7, slot = nid >> 3, per = total >> 3, rem = total & 7;
+  const int tix = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+  const int mt = tix % MT, rest = tix / MT, sp = rest / NT, nt = rest % NT;
+  const int m0 = mt * kMM;
+  const int f0 = nt * (SW ? kMN / 2 : kMN);
+  const int kbeg = sp * k_len;
+  const int nk = (min(K, kbeg + k_len) - kbeg) / kMK;  // even: k_len and K - kbeg are multiples of 64
 
-  // staging: thread t moves chunk (t & 7) of tile rows (t >> 3) + 32 i.  Rows
-  // past R or N are clamped to the last valid row: read but never written back.
-  const int sr = t >> 3, sc = t & 7;
-  const int lds_st = sr * 8 + (sc ^ (sr & 7));
+  // staging: thread t moves chunk t % kMCh of tile rows t / kMCh + kMRows i.
+  // Rows past R or N are clamped to the last valid row: read, never written back.
+  const int sr = t / kMCh, sc = t % kMCh;
+  const int lds_st = sr * kMCh + (sc ^ (sr & (kMCh - 1)));
   const bf16_t* xs = X + kbeg + sc * 8;
   const bf16_t* ws = W + kbeg + sc * 8;
-  uint32_t aoff[4], boff[8];
+  uint32_t aoff[kMPA], boff[kMPB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) aoff[i] = static_cast<uint32_t>(min(m0 + sr + 32 * i, R - 1));
+  for (int i = 0; i < kMPA; ++i) aoff[i] = static_cast<uint32_t>(min(m0 + sr + kMRows * i, R - 1));
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int br = sr + 32 * i;
+  for (int i = 0; i < kMPB; ++i) {
+    const int br = sr + kMRows * i;
     if (SW)
       boff[i] = static_cast<uint32_t>((br < 128 ? 0 : N) + min(f0 + (br & 127), N - 1));
     else
       boff[i] = static_cast<uint32_t>(min(f0 + br, N - 1));
   }
-  // one register staging set: tile kt+1 loads while tile kt is multiplied
-  // (native vector types keep the staging values in registers)
-  u32x4 sa[4], sb[8];
-#define SPEC_MFMA_LOAD(KT)                                                                         \
+  // native vector types keep the staging values in registers
+  u32x4 sa[kMPA], sb[kMPB], ta[kMPA], tb[kMPB];
+#define SPEC_MFMA_LOAD(SA, SB, KT)                                                                 \
   do {                                                                                             \
     const int ko_ = (KT) * kMK;                                                                    \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                  \
-        sa[i] = *reinterpret_cast<const u32x4*>(xs + static_cast<size_t>(aoff[i]) * K + ko_);      \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                                  \
-        sb[i] = *reinterpret_cast<const u32x4*>(ws + static_cast<size_t>(boff[i]) * K + ko_);      \
+    _Pragma("unroll") for (int i = 0; i < kMPA; ++i)                                               \
+        SA[i] = *reinterpret_cast<const u32x4*>(xs + static_cast<size_t>(aoff[i]) * K + ko_);      \
+    _Pragma("unroll") for (int i = 0; i < kMPB; ++i)                                               \
+        SB[i] = *reinterpret_cast<const u32x4*>(ws + static_cast<size_t>(boff[i]) * K + ko_);      \
   } while (0)
-#define SPEC_MFMA_STORE(AL, BL)                                                                    \
+#define SPEC_MFMA_STORE(SA, SB, AL, BL)                                                            \
   do {                                                                                             \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) AL[lds_st + 256 * i] = sa[i];                    \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) BL[lds_st + 256 * i] = sb[i];                    \
+    _Pragma("unroll") for (int i = 0; i < kMPA; ++i) AL[lds_st + 256 * i] = SA[i];                 \
+    _Pragma("unroll") for (int i = 0; i < kMPB; ++i) BL[lds_st + 256 * i] = SB[i];                 \
   } while (0)
 
   f32x4 acc[4][8];
@@ -196,31 +207,38 @@ __global__ __launch_bounds__(256) void gemm_mfma_bf16(const bf16_t* __restrict__
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int sw = l16 & 7;  // row & 7 of every fragment row this lane reads
+  const int c = g ^ (l16 & (kMCh - 1));  // chunk of k-group g in a fragment row
 #define SPEC_MFMA_COMPUTE(AL, BL)                                                                  \
-  _Pragma("unroll") for (int ks = 0; ks < 2; ++ks) {                                               \
-    const int c = (4 * ks + g) ^ sw;                                                               \
+  {                                                                                                \
     u32x4 a[4], b[8];                                                                              \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) a[i] = AL[(64 * wm + 16 * i + l16) * 8 + c];     \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) a[i] = AL[(64 * wm + 16 * i + l16) * kMCh + c];  \
     _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                                \
       const int r = SW ? ((j < 4) ? (64 * wn + 16 * j) : (128 + 64 * wn + 16 * (j - 4)))           \
                        : (128 * wn + 16 * j);                                                      \
-      b[j] = BL[(r + l16) * 8 + c];                                                                \
+      b[j] = BL[(r + l16) * kMCh + c];                                                             \
     }                                                                                              \
     _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                  \
         _Pragma("unroll") for (int j = 0; j < 8; ++j) acc[i][j] = mfma16x16x32v(a[i], b[j], acc[i][j]); \
   }
 
+  // prefetches past the end are clamped, in-bounds reloads; the scheduling
+  // barriers keep each k-step's loads ahead of its MFMAs
   if (nk > 0) {
-    SPEC_MFMA_LOAD(0);
-    SPEC_MFMA_STORE(As[0], Bs[0]);
+    SPEC_MFMA_LOAD(sa, sb, 0);
+    SPEC_MFMA_STORE(sa, sb, As[0], Bs[0]);
+    SPEC_MFMA_LOAD(ta, tb, min(1, nk - 1));
   }
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) SPEC_MFMA_LOAD(kt + 1);
-    SPEC_MFMA_COMPUTE(As[buf], Bs[buf]);
-    if (kt + 1 < nk) SPEC_MFMA_STORE(As[buf ^ 1], Bs[buf ^ 1]);
+  for (int kt = 0; kt < nk; kt += 2) {
+    SPEC_MFMA_LOAD(sa, sb, min(kt + 2, nk - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    SPEC_MFMA_COMPUTE(As[0], Bs[0]);
+    SPEC_MFMA_STORE(ta, tb, As[1], Bs[1]);
+    __syncthreads();
+    SPEC_MFMA_LOAD(ta, tb, min(kt + 3, nk - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    SPEC_MFMA_COMPUTE(As[1], Bs[1]);
+    SPEC_MFMA_STORE(sa, sb, As[0], Bs[0]);
     __syncthreads();
   }
 #undef SPEC_MFMA_COMPUTE
@@ -234,7 +252,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_bf16(const bf16_t* __restrict__
       const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
       if (m >= R) continue;
       if (part) {
-        float* pr = part + (static_cast<size_t>(blockIdx.z) * R + m) * (SW ? 2 * N : N);
+        float* pr = part + (static_cast<size_t>(sp) * R + m) * (SW ? 2 * N : N);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           int n, wrow;
@@ -387,18 +405,20 @@ hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hi
   return hipGetLastError();
 }
 
-// Split-K factor for the MFMA kernel: enough workgroups to cover the 256 CUs
-// about twice, partials within the workspace, k-splits multiples of 64.
+// Split-K factor for the MFMA kernel: grids under 256 tiles are split so that
+// tiles x splits stays within one wave of the 256 CUs (measured at the
+// 364-row verify shapes: more splits lose to the partials' traffic and to
+// short k-loops), k-splits multiples of 64, partials within the workspace.
 template <int EPI>
 int mfma_splits(int R, int N, int K, size_t ws_bytes, int* k_len) {
   const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
   const int tiles = ((Nw + kMN - 1) / kMN) * ((R + kMM - 1) / kMM);
   int S = 1;
   if (ws_bytes && tiles < 256) {
-    S = std::min(8, (512 + tiles - 1) / tiles);
+    S = std::max(1, std::min(8, 256 / tiles));
     while (S > 1 && static_cast<size_t>(S) * R * Nw * sizeof(float) > ws_bytes) --S;
   }
-  *k_len = ((K + S - 1) / S + kMK - 1) / kMK * kMK;
+  *k_len = ((K + S - 1) / S + 2 * kMK - 1) / (2 * kMK) * (2 * kMK);
   return (K + *k_len - 1) / *k_len;
 }
 
@@ -408,14 +428,15 @@ hipError_t mfma(int R, int N, int K, const void* X, const void* W, void* Y, hipS
   int k_len = K;
   const int S = mfma_splits<EPI>(R, N, K, ws ? ws_bytes : 0, &k_len);
   const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
-  dim3 grid((Nw + kMN - 1) / kMN, (R + kMM - 1) / kMM, S);
+  const int MT = (R + kMM - 1) / kMM, NT = (Nw + kMN - 1) / kMN;
+  const int grid = MT * NT * S;
   const bf16_t* x = static_cast<const bf16_t*>(X);
   const bf16_t* w = static_cast<const bf16_t*>(W);
   if (S <= 1) {
-    gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, rm);
+    gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, MT, NT, rm);
     return hipGetLastError();
   }
-  gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, rm);
+  gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, MT, NT, rm);
   const size_t total = static_cast<size_t>(R) * N;
   const int blocks = static_cast<int>(std::min<size_t>(2048, (total + 255) / 256));
   splitk_reduce<EPI><<<blocks, 256, 0, st>>>(ws, S, R, N, Y, rm);
@@ -443,11 +464,11 @@ hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W
 }  // namespace
 
 size_t gemm_splitk_bytes(int R_max, int Nw_max) {
-  // only grids of fewer than 256 tiles split, into S <= ceil(512 / tiles)
-  // parts, so S * tiles < 768 and the partials S * R * Nw stay below
-  // 768 * kMM * kMN floats; smaller problems need less
+  // only grids of fewer than 256 tiles split, into S <= 256 / tiles parts, so
+  // the partials S * R * Nw stay below 256 * kMM * kMN floats; smaller
+  // problems need less
   const size_t tiles = static_cast<size_t>((Nw_max + kMN - 1) / kMN) * ((R_max + kMM - 1) / kMM);
-  return std::min<size_t>(768, 2 * tiles + 512) * kMM * kMN * sizeof(float);
+  return std::min<size_t>(256, 8 * tiles) * kMM * kMN * sizeof(float);
 }
 
 const char* gemm_kernel_name(int dtype, int R, int epi) {
