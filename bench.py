@@ -88,6 +88,19 @@ def cpu_info():
     return model, threads or aff, aff
 
 
+def roofline_pass(B, sess, kernel, step, args):
+    """Per-kernel timing: the timed steps replay captured graphs, in which a
+    single launch cannot be bracketed by events, so `roof_steps` further steps
+    of the same workload run with the library's kernel timer on (eager
+    launches) and HIP events around every launch of `kernel`."""
+    B.spec_timing_enable(sess.ctx, kernel)
+    for s in range(args.roof_steps):
+        step(args.warmup + args.steps + s, False)
+    out = B.spec_timing_read(sess.ctx)
+    B.spec_timing_enable(sess.ctx, None)
+    return out
+
+
 # ---------------------------------------------------------------------------
 # 8B-shaped pair, batch 1
 
@@ -105,7 +118,7 @@ def bench_8b(args):
     log("drawing weights on device")
     target = DeviceModel(cfg.target, None, dev, seed=cfg.seed)
     draft = DeviceModel(cfg.draft, None, dev, seed=cfg.seed + 1)
-    total_steps = args.warmup + args.steps
+    total_steps = args.warmup + args.steps + args.roof_steps
     max_len = ctx_len + total_steps * (k + 1) + 64
     pages = (max_len + 15) // 16
     sess = SpecSession(target, draft, max_seqs=1, k_max=k, max_pages_per_seq=pages, max_rows=2048)
@@ -134,7 +147,6 @@ def bench_8b(args):
     for s in range(args.warmup):
         step(s, False)
     kernel = args.kernel or "gemm_skinny_bf16<1, 2>"
-    B.spec_timing_enable(sess.ctx, kernel)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0 = torch.cuda.Event(enable_timing=True)
@@ -147,8 +159,7 @@ def bench_8b(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ev_ms = ev0.elapsed_time(ev1)
-    k_ms, k_n, k_bytes, k_flops = B.spec_timing_read(sess.ctx)
-    B.spec_timing_enable(sess.ctx, None)
+    k_ms, k_n, k_bytes, k_flops = roofline_pass(B, sess, kernel, step, args)
     lats = sorted(a.elapsed_time(b) for a, b in lat)
     info = {
         "tokens": tokens, "wall_s": wall, "event_ms": ev_ms, "acc_hist": acc_hist,
@@ -243,7 +254,7 @@ def bench_serving(args):
     log("drawing weights on device")
     target = DeviceModel(cfg.target, None, dev, seed=cfg.seed)
     draft = DeviceModel(cfg.draft, None, dev, seed=cfg.seed + 1)
-    total_steps = args.warmup + args.steps
+    total_steps = args.warmup + args.steps + args.roof_steps
     max_len = int(ctx.max()) + total_steps * (kmax + 1) + 64
     pages = (max_len + 15) // 16
     need = int(sum((int(c) + total_steps * (kmax + 1) + 64 + 15) // 16 for c in ctx))
@@ -274,7 +285,6 @@ def bench_serving(args):
     for s in range(args.warmup):
         step(s, False)
     kernel = args.kernel or "gemm_mfma_bf16<2>"
-    B.spec_timing_enable(sess.ctx, kernel)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0 = torch.cuda.Event(enable_timing=True)
@@ -286,8 +296,7 @@ def bench_serving(args):
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    k_ms, k_n, k_bytes, k_flops = B.spec_timing_read(sess.ctx)
-    B.spec_timing_enable(sess.ctx, None)
+    k_ms, k_n, k_bytes, k_flops = roofline_pass(B, sess, kernel, step, args)
     lats = sorted(a.elapsed_time(b) for a, b in lat)
     sess.close()
     return {"tokens": tokens, "wall_s": wall, "event_ms": ev0.elapsed_time(ev1), "acc_hist": acc_hist,
@@ -386,6 +395,8 @@ def main():
     ap.add_argument("--temperature", type=float, default=0.8)
     ap.add_argument("--kernel", default=None, help="kernel to time for the roofline (profiler name)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--roof-steps", type=int, default=4,
+                    help="steps after the timed region that run with per-kernel timing (eager launches)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-MiB device buffer --steps times (a plain copy kernel of known "
                          "size, for scaling the profiler's FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -444,6 +455,7 @@ def main():
                 "unit": unit, "frac": (achieved / peak) if achieved else None,
                 "traffic": pmc_traffic(info["kernel"], args.workload),
                 "launches": info["k_n"], "avg_launch_us": per_launch_ms * 1e3,
+                "timing": f"HIP events around each launch, {args.roof_steps} steps after the timed region",
                 "bytes_per_launch": info["k_bytes"] / max(1, info["k_n"]),
                 "flops_per_launch": info["k_flops"] / max(1, info["k_n"])}
     if bound == "hbm" and info["k_flops"] and info["k_n"]:

@@ -186,6 +186,16 @@ SPEC_API spec_status spec_seq_info(const spec_ctx* ctx, int64_t seq_id, int32_t*
  * call order (sequence i's k_i + 1 rows are contiguous), and the row count. */
 SPEC_API spec_status spec_last_logits(const spec_ctx* ctx, const float** logits, int32_t* rows);
 
+/* Graph replay of the draft step and the verify (on by default).  Their
+ * kernel sequence depends only on the batch shape (rows, sequences, attention
+ * work items), so the first call of a shape captures it into a HIP graph and
+ * later calls of that shape upload their metadata and replay the graph: one
+ * launch instead of ~10 per layer.  Up to 16 shapes are kept (least recently
+ * used replaced); a new workspace drops them.  Results are identical with and
+ * without graphs.  While kernel timing is on, calls run eagerly so that each
+ * launch can be timed.  enable = 0 turns replay off. */
+SPEC_API spec_status spec_set_graphs(spec_ctx* ctx, int32_t enable);
+
 /* Kernel timing for roofline measurement.  While a kernel name is set, the
  * context records HIP events on the call's stream around every launch of that
  * kernel (names as the profiler reports them without namespaces and argument

@@ -73,6 +73,7 @@ SIGNATURES = {
     "spec_seq_release": (c_int32, [_P, c_int64]),
     "spec_seq_info": (c_int32, [_P, c_int64, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, c_int32]),
     "spec_last_logits": (c_int32, [_P, POINTER(c_void_p), _I32P]),
+    "spec_set_graphs": (c_int32, [_P, c_int32]),
     "spec_timing_enable": (c_int32, [_P, ctypes.c_char_p]),
     "spec_timing_read": (c_int32, [_P, POINTER(ctypes.c_double), _I64P, POINTER(ctypes.c_double),
                                    POINTER(ctypes.c_double)]),
@@ -239,6 +240,10 @@ def spec_last_logits(ctx: int):
     r = c_int32()
     check(lib().spec_last_logits(ctx, ctypes.byref(p), ctypes.byref(r)), ctx)
     return p.value, r.value
+
+
+def spec_set_graphs(ctx: int, enable: bool) -> None:
+    check(lib().spec_set_graphs(ctx, 1 if enable else 0), ctx)
 
 
 def spec_timing_enable(ctx: int, kernel_name: Optional[str]):

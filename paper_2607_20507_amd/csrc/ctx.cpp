@@ -8,9 +8,13 @@
 // writes their K/V, and applies the speculative sampling rule.  Commit keeps
 // target positions <= n + a and draft positions < min(len_d, n + a + 1).
 //
-// One metadata block (rows, positions, KV slots, compact page tables,
-// attention work items, decision tables) is uploaded per call through a
+// One metadata block (rows, positions, KV slots, page tables, attention work
+// items, decision tables, the Philox seed) is uploaded per call through a
 // pinned ring; the decision outputs come back in one small copy per verify.
+// The kernel sequence of a draft step or a verify depends only on the batch
+// shape (rows, sequences, attention work items), so it is captured once per
+// shape into a HIP graph whose kernels read that call's metadata from a fixed
+// device area, and replayed: one launch instead of ~10 per layer.
 
 #include <hip/hip_runtime.h>
 
@@ -38,6 +42,7 @@ namespace {
 
 constexpr int kMaxParts = 1024;
 constexpr int kMetaRing = 4;
+constexpr int kGraphSlots = 16;
 
 struct Model {
   spec_model_desc d{};
@@ -74,7 +79,7 @@ struct Seq {
 
 struct Ws {
   size_t h = 0, y = 0, qkv = 0, q = 0, o = 0, u = 0, logits = 0, dq = 0, dtok = 0, rowtok = 0;
-  size_t part_o = 0, part_ml = 0, vocab = 0, draft = 0, nacc = 0, otok = 0, meta = 0;
+  size_t part_o = 0, part_ml = 0, vocab = 0, draft = 0, nacc = 0, otok = 0, meta = 0, gmeta = 0;
   size_t splitk = 0, splitk_bytes = 0;
   size_t meta_cap = 0, total = 0;
 };
@@ -146,6 +151,26 @@ struct spec_ctx {
   bool broken = false;
   int last_rows = 0;
   EventTimer timer;
+  // captured kernel sequences, one per batch shape (least recently used out)
+  struct Graph {
+    std::vector<int64_t> key;
+    hipGraphExec_t exec = nullptr;
+    uint64_t used = 0;
+  };
+  Graph graphs[kGraphSlots];
+  uint64_t graph_clock = 0;
+  // shapes seen recently but not captured: a shape is captured when it comes
+  // back, so batches whose shape changes every call (growing contexts across
+  // many sequences) run eagerly instead of paying a capture per call
+  std::vector<std::vector<int64_t>> seen;
+  bool use_graphs = true;
+  hipStream_t cap_stream = nullptr;  // capture only: nothing runs on it
+  void drop_graphs() {
+    for (auto& g : graphs) {
+      if (g.exec) (void)hipGraphExecDestroy(g.exec);
+      g = Graph{};
+    }
+  }
 };
 
 static thread_local std::string g_err;
@@ -211,6 +236,7 @@ void compute_ws(spec_ctx* c) {
   mc += 16 * 256;
   w.meta_cap = align_up(mc);
   w.meta = take(w.meta_cap * kMetaRing);
+  w.gmeta = take(w.meta_cap * kGraphSlots);
   w.total = off;
 }
 
@@ -333,9 +359,11 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   return SPEC_OK;
 }
 
-// Compact page table of the listed sequences (row i = sequence i).
-void build_ptab(const std::vector<const std::vector<int32_t>*>& tabs, Fwd& f) {
-  size_t w = 1;
+// Page table of the listed sequences (row i = sequence i), `stride` entries per
+// row (the per-sequence maximum, so that the layout depends on the batch shape
+// only).
+void build_ptab(const std::vector<const std::vector<int32_t>*>& tabs, Fwd& f, int stride) {
+  size_t w = static_cast<size_t>(std::max(1, stride));
   for (auto* t : tabs) w = std::max(w, t->size());
   f.ptab_stride = static_cast<int>(w);
   f.ptab.assign(tabs.size() * w, 0);
@@ -358,6 +386,80 @@ bool check_ids(spec_ctx* ctx, int32_t n, const int64_t* ids, bool must_exist) {
     }
   }
   return true;
+}
+
+// Run a call's kernels: eagerly through the metadata ring while kernel timing
+// is on or graphs are off, else by replaying the graph captured for `key`
+// (captured the second time the shape occurs; the metadata goes to that
+// graph's fixed area).
+spec_status run_kernels(spec_ctx* ctx, const std::vector<int64_t>& key, const MetaBlock& mb,
+                        hipStream_t st,
+                        const std::function<spec_status(const char*, hipStream_t)>& launches) {
+  if (!ctx->use_graphs || !ctx->timer.name.empty()) {
+    char* dev = nullptr;
+    spec_status s = upload_meta(ctx, mb, st, &dev);
+    if (s != SPEC_OK) return s;
+    return launches(dev, st);
+  }
+  if (mb.size() > ctx->ws.meta_cap) FAIL(SPEC_E_UNSUPPORTED, "call metadata exceeds its bound");
+  int slot = -1;
+  for (int i = 0; i < kGraphSlots && slot < 0; ++i)
+    if (ctx->graphs[i].exec && ctx->graphs[i].key == key) slot = i;
+  if (slot < 0) {
+    auto it = std::find(ctx->seen.begin(), ctx->seen.end(), key);
+    if (it == ctx->seen.end()) {
+      if (ctx->seen.size() >= 4 * kGraphSlots) ctx->seen.erase(ctx->seen.begin());
+      ctx->seen.push_back(key);
+      char* dev = nullptr;
+      spec_status s = upload_meta(ctx, mb, st, &dev);
+      if (s != SPEC_OK) return s;
+      return launches(dev, st);
+    }
+    ctx->seen.erase(it);
+    slot = 0;
+    for (int i = 1; i < kGraphSlots; ++i)
+      if (ctx->graphs[i].used < ctx->graphs[slot].used) slot = i;
+  }
+  auto& g = ctx->graphs[slot];
+  char* dev = ctx->wsp + ctx->ws.gmeta + static_cast<size_t>(slot) * ctx->ws.meta_cap;
+  HIPC(ctx->stager.upload(dev, mb.data(), mb.size(), st));
+  if (!g.exec || g.key != key) {
+    if (g.exec) {
+      // the slot's previous graph may still be queued on `st`: destroy it
+      // after everything enqueued so far has run
+      HIPC(hipStreamSynchronize(st));
+      HIPC(hipGraphExecDestroy(g.exec));
+      g = spec_ctx::Graph{};
+    }
+    if (!ctx->cap_stream) HIPC(hipStreamCreateWithFlags(&ctx->cap_stream, hipStreamNonBlocking));
+    HIPC(hipStreamBeginCapture(ctx->cap_stream, hipStreamCaptureModeThreadLocal));
+    spec_status s = launches(dev, ctx->cap_stream);
+    hipGraph_t graph = nullptr;
+    const hipError_t e = hipStreamEndCapture(ctx->cap_stream, &graph);
+    if (s != SPEC_OK) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return s;
+    }
+    HIPC(e);
+    const hipError_t ei = hipGraphInstantiate(&g.exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    HIPC(ei);
+    g.key = key;
+  }
+  g.used = ++ctx->graph_clock;
+  HIPC(hipGraphLaunch(g.exec, st));
+  return SPEC_OK;
+}
+
+// Shape key of a forward: everything its grids and metadata layout depend on.
+void key_forward(std::vector<int64_t>& k, const FwdOff& o) {
+  const int64_t v[] = {o.R, o.n_items, o.n_groups, o.nt, o.n_lm, o.lm_map, o.ptab_stride,
+                       static_cast<int64_t>(o.tok), static_cast<int64_t>(o.pos),
+                       static_cast<int64_t>(o.slot), static_cast<int64_t>(o.seqi),
+                       static_cast<int64_t>(o.pt), static_cast<int64_t>(o.items),
+                       static_cast<int64_t>(o.groups), static_cast<int64_t>(o.lmr),
+                       static_cast<int64_t>(o.lmm)};
+  k.insert(k.end(), std::begin(v), std::end(v));
 }
 
 spec_status launch_clears(spec_ctx* ctx, const std::vector<int32_t>& ct, const std::vector<int32_t>& cd,
@@ -450,6 +552,9 @@ spec_status spec_ctx_create(const spec_model_desc* target, const spec_model_desc
 
 void spec_ctx_destroy(spec_ctx* ctx) {
   if (!ctx) return;
+  (void)hipDeviceSynchronize();  // queued copies and graph launches still use ctx resources
+  ctx->drop_graphs();
+  if (ctx->cap_stream) (void)hipStreamDestroy(ctx->cap_stream);
   ctx->stager.release();
   if (ctx->h_out) (void)hipHostFree(ctx->h_out);
   if (ctx->out_ev) (void)hipEventDestroy(ctx->out_ev);
@@ -464,6 +569,11 @@ spec_status spec_set_workspace(spec_ctx* ctx, void* dev_ptr, size_t bytes) {
   if (!ctx) return SPEC_E_INVALID;
   if (!dev_ptr || bytes < ctx->ws.total || (reinterpret_cast<uintptr_t>(dev_ptr) & 255))
     FAIL(SPEC_E_INVALID, "workspace null, too small or not 256-byte aligned");
+  if (ctx->wsp != dev_ptr) {
+    // captured graphs hold workspace addresses
+    if (ctx->wsp) (void)hipDeviceSynchronize();
+    ctx->drop_graphs();
+  }
   ctx->wsp = static_cast<char*>(dev_ptr);
   ctx->ws_bytes = bytes;
   return SPEC_OK;
@@ -552,7 +662,7 @@ spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const
           f.seqi.push_back(static_cast<int32_t>(c));
         }
       }
-      build_ptab(tabs, f);
+      build_ptab(tabs, f, 1);
       MetaBlock mb;
       FwdOff o = add_forward(ctx, M, f, mb);
       char* dev = nullptr;
@@ -618,17 +728,22 @@ spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
     d.out = qidx;
     dr.push_back(d);
   }
-  build_ptab(tabs, f);
+  build_ptab(tabs, f, ctx->max_pages);
   MetaBlock mb;
   FwdOff o = add_forward(ctx, D, f, mb);
   const size_t odr = mb.add(dr);
-  char* dev = nullptr;
-  spec_status s = upload_meta(ctx, mb, st, &dev);
+  const size_t osd = mb.add(&seed, 1);
+  std::vector<int64_t> key = {1, n, static_cast<int64_t>(odr), static_cast<int64_t>(osd)};
+  key_forward(key, o);
+  spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
+    spec_status r = launch_forward(ctx, D, o, dev, dq, ls);
+    if (r != SPEC_OK) return r;
+    HIPC(launch_draft_sample(draft_plan(n, ctx->V), reinterpret_cast<const DRow*>(dev + odr), seed,
+                             wsptr<int32_t>(ctx, ctx->ws.dtok), ctx->wsp + ctx->ws.draft, ls,
+                             reinterpret_cast<const uint64_t*>(dev + osd)));
+    return SPEC_OK;
+  });
   if (s != SPEC_OK) return s;
-  s = launch_forward(ctx, D, o, dev, dq, st);
-  if (s != SPEC_OK) return s;
-  HIPC(launch_draft_sample(draft_plan(n, ctx->V), reinterpret_cast<const DRow*>(dev + odr), seed,
-                           wsptr<int32_t>(ctx, ctx->ws.dtok), ctx->wsp + ctx->ws.draft, st));
   for (int i = 0; i < n; ++i) {
     Seq& q = ctx->seqs[seq_ids[i]];
     const int c = q.k == 0 ? q.n() + 1 - q.len_d : 1;
@@ -722,21 +837,27 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   for (auto& q : vs) q.q_row += R;
   std::vector<VRow> rows = prow;
   rows.insert(rows.end(), qrow.begin(), qrow.end());
-  build_ptab(tabs, f);
+  build_ptab(tabs, f, ctx->max_pages);
   MetaBlock mb;
   FwdOff o = add_forward(ctx, T, f, mb);
   const size_t orow = mb.add(rows), oseq = mb.add(vs);
-  char* dev = nullptr;
-  spec_status s = upload_meta(ctx, mb, st, &dev);
-  if (s != SPEC_OK) return s;
-  s = launch_forward(ctx, T, o, dev, logits, st);
-  if (s != SPEC_OK) return s;
+  const size_t osd = mb.add(&seed, 1);
   int32_t* d_nacc = wsptr<int32_t>(ctx, ctx->ws.nacc);
   int32_t* d_otok = wsptr<int32_t>(ctx, ctx->ws.otok);
   const VocabPlan vp = vocab_plan(n, static_cast<int>(rows.size()), ctx->V);
-  HIPC(launch_vocab_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
-                         reinterpret_cast<const VSeq*>(dev + oseq), wsptr<int32_t>(ctx, ctx->ws.rowtok),
-                         seed, ctx->k_max, d_nacc, d_otok, ctx->wsp + ctx->ws.vocab, st, &ctx->timer));
+  std::vector<int64_t> key = {0, n, static_cast<int64_t>(rows.size()), static_cast<int64_t>(orow),
+                              static_cast<int64_t>(oseq), static_cast<int64_t>(osd)};
+  key_forward(key, o);
+  spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
+    spec_status r = launch_forward(ctx, T, o, dev, logits, ls);
+    if (r != SPEC_OK) return r;
+    HIPC(launch_vocab_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
+                           reinterpret_cast<const VSeq*>(dev + oseq), wsptr<int32_t>(ctx, ctx->ws.rowtok),
+                           seed, ctx->k_max, d_nacc, d_otok, ctx->wsp + ctx->ws.vocab, ls, &ctx->timer,
+                           reinterpret_cast<const uint64_t*>(dev + osd)));
+    return SPEC_OK;
+  });
+  if (s != SPEC_OK) return s;
   const int W = ctx->k_max + 1;
   HIPC(hipMemcpyAsync(ctx->h_out, d_nacc, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
   HIPC(hipMemcpyAsync(ctx->h_out + ctx->max_seqs, d_otok, sizeof(int32_t) * n * W, hipMemcpyDeviceToHost, st));
@@ -752,6 +873,12 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   }
   ctx->last_rows = R;
   ctx->timer.flush();
+  return SPEC_OK;
+}
+
+spec_status spec_set_graphs(spec_ctx* ctx, int32_t enable) {
+  if (!ctx) return SPEC_E_INVALID;
+  ctx->use_graphs = enable != 0;
   return SPEC_OK;
 }
 

@@ -104,7 +104,7 @@ class MetaBlock {
   }
   template <typename T>
   size_t add(const std::vector<T>& v) { return add(v.data(), v.size()); }
-  size_t size() const { return align_up(buf_.size()); }
+  size_t size() const { return buf_.size(); }
   const char* data() const { return buf_.data(); }
   void clear() { buf_.clear(); }
 

@@ -51,10 +51,12 @@ VocabPlan vocab_plan(int B, int n_rows, int V);
 size_t vocab_ws_bytes(const VocabPlan& p);
 
 // Full decision pass.  Outputs n_acc[B], out_tok[B * (kmax + 1)] (device).
+// d_seed (optional, device): read the Philox seed there instead of `seed`, so
+// that a captured graph of the pass takes a new seed with each replay.
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax,
                              int32_t* d_n_acc, int32_t* d_out_tok, void* d_ws, hipStream_t st,
-                             KernelTimer* timer = nullptr);
+                             KernelTimer* timer = nullptr, const uint64_t* d_seed = nullptr);
 
 struct DraftPlan {
   int n = 0, V = 0, chunk = 0, n_chunks = 0;
@@ -62,7 +64,8 @@ struct DraftPlan {
 DraftPlan draft_plan(int n, int V);
 size_t draft_ws_bytes(const DraftPlan& p);
 hipError_t launch_draft_sample(const DraftPlan& p, const DRow* d_rows, uint64_t seed,
-                               int32_t* d_tokens, void* d_ws, hipStream_t st);
+                               int32_t* d_tokens, void* d_ws, hipStream_t st,
+                               const uint64_t* d_seed = nullptr);
 
 hipError_t launch_philox_uniform(uint64_t seed, uint64_t seq_id, int32_t pos, int32_t purpose,
                                  int32_t n, float* out, hipStream_t st);

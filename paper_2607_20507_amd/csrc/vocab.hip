@@ -168,13 +168,14 @@ template <bool VEC>
 __global__ __launch_bounds__(kThreads) void decide_kernel(
     const VRow* __restrict__ rows, const VSeq* __restrict__ seqs,
     const int32_t* __restrict__ draft_tok, const VStat* __restrict__ stats, int n_chunks1, int V,
-    int chunk2, int n_chunks2, uint64_t seed, VPick* __restrict__ picks, VDec* __restrict__ decs) {
+    int chunk2, int n_chunks2, uint64_t seed, const uint64_t* __restrict__ seed_ptr,
+    VPick* __restrict__ picks, VDec* __restrict__ decs) {
   const int b = blockIdx.y, c = blockIdx.x;
   const VSeq sq = seqs[b];
   const bool greedy = !(sq.t > 0.f);
   const float it = greedy ? 0.f : 1.f / sq.t;
   const uint64_t seq_id = (static_cast<uint64_t>(sq.seq_hi) << 32) | sq.seq_lo;
-  const PhiloxKey key = philox_key(seed);
+  const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
 
   __shared__ int s_a, s_tok;
   __shared__ float s_mp, s_sp, s_mq, s_sq;
@@ -313,6 +314,7 @@ __global__ void final_kernel(const VSeq* __restrict__ seqs, const int32_t* __res
 template <bool VEC>
 __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __restrict__ rows, int chunk,
                                                          int n_chunks, uint64_t seed,
+                                                         const uint64_t* __restrict__ seed_ptr,
                                                          VPick* __restrict__ picks) {
   const int r = blockIdx.y, c = blockIdx.x;
   const DRow row = rows[r];
@@ -321,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
   const float it = greedy ? 0.f : 1.f / row.t;
   const uint64_t seq_id = (static_cast<uint64_t>(row.seq_hi) << 32) | row.seq_lo;
   const StreamId sid = stream_id(seq_id, row.pos, 0 /*DRAFT*/);
-  const PhiloxKey key = philox_key(seed);
+  const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
   const int beg = c * chunk, end = min(V, beg + chunk);
   float best = -INFINITY;
   int bi = INT_MAX;
@@ -421,7 +423,8 @@ size_t vocab_ws_bytes(const VocabPlan& p) {
 
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax, int32_t* d_n_acc,
-                             int32_t* d_out_tok, void* d_ws, hipStream_t st, KernelTimer* timer) {
+                             int32_t* d_out_tok, void* d_ws, hipStream_t st, KernelTimer* timer,
+                             const uint64_t* d_seed) {
   if (p.B == 0) return hipSuccess;
   char* ws = static_cast<char*>(d_ws);
   VStat* stats = reinterpret_cast<VStat*>(ws);
@@ -441,10 +444,10 @@ hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq*
   dim3 g2(p.n_chunks2, p.B);
   if (vec)
     decide_kernel<true><<<g2, kThreads, 0, st>>>(d_rows, d_seqs, d_draft_tok, stats, p.n_chunks1,
-                                                 p.V, p.chunk2, p.n_chunks2, seed, picks, decs);
+                                                 p.V, p.chunk2, p.n_chunks2, seed, d_seed, picks, decs);
   else
     decide_kernel<false><<<g2, kThreads, 0, st>>>(d_rows, d_seqs, d_draft_tok, stats, p.n_chunks1,
-                                                  p.V, p.chunk2, p.n_chunks2, seed, picks, decs);
+                                                  p.V, p.chunk2, p.n_chunks2, seed, d_seed, picks, decs);
   final_kernel<<<(p.B + 63) / 64, 64, 0, st>>>(d_seqs, d_draft_tok, decs, picks, p.n_chunks2, p.B,
                                                kmax, d_n_acc, d_out_tok);
   return hipGetLastError();
@@ -463,14 +466,14 @@ size_t draft_ws_bytes(const DraftPlan& p) {
 }
 
 hipError_t launch_draft_sample(const DraftPlan& p, const DRow* d_rows, uint64_t seed,
-                               int32_t* d_tokens, void* d_ws, hipStream_t st) {
+                               int32_t* d_tokens, void* d_ws, hipStream_t st, const uint64_t* d_seed) {
   if (p.n == 0) return hipSuccess;
   VPick* picks = static_cast<VPick*>(d_ws);
   dim3 g(p.n_chunks, p.n);
   if (p.V % 4 == 0)
-    draft_kernel<true><<<g, kThreads, 0, st>>>(p.V, d_rows, p.chunk, p.n_chunks, seed, picks);
+    draft_kernel<true><<<g, kThreads, 0, st>>>(p.V, d_rows, p.chunk, p.n_chunks, seed, d_seed, picks);
   else
-    draft_kernel<false><<<g, kThreads, 0, st>>>(p.V, d_rows, p.chunk, p.n_chunks, seed, picks);
+    draft_kernel<false><<<g, kThreads, 0, st>>>(p.V, d_rows, p.chunk, p.n_chunks, seed, d_seed, picks);
   draft_final_kernel<<<(p.n + 63) / 64, 64, 0, st>>>(d_rows, picks, p.n_chunks, p.n, d_tokens);
   return hipGetLastError();
 }

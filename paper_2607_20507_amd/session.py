@@ -94,7 +94,7 @@ class SpecSession:
 
     def __init__(self, target: DeviceModel, draft: DeviceModel, *, max_seqs: int, k_max: int,
                  max_pages_per_seq: int, num_pages_target: Optional[int] = None,
-                 num_pages_draft: Optional[int] = None, max_rows: int = 2048):
+                 num_pages_draft: Optional[int] = None, max_rows: int = 2048, graphs: bool = True):
         self.target, self.draft = target, draft
         self.k_max = k_max
         dev = target.device
@@ -110,6 +110,7 @@ class SpecSession:
         off = (-self.workspace.data_ptr()) % 256
         self.ws_view = self.workspace[off:off + nbytes]
         B.spec_set_workspace(self.ctx, self.ws_view)
+        B.spec_set_graphs(self.ctx, graphs)
 
     def close(self):
         if self.ctx:
@@ -124,6 +125,9 @@ class SpecSession:
 
     def prefill(self, seq_ids, prompts, stream=None):
         B.spec_prefill(self.ctx, seq_ids, prompts, stream)
+
+    def set_graphs(self, enable: bool):
+        B.spec_set_graphs(self.ctx, enable)
 
     def draft_step(self, seq_ids, temps, seed: int, stream=None):
         B.spec_draft_step(self.ctx, seq_ids, temps, seed, stream)
