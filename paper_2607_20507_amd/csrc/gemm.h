@@ -24,7 +24,7 @@ hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void
 // Bytes of split-K workspace that cover every launch shape.
 size_t gemm_splitk_bytes(int R_max, int Nw_max);
 
-// Profiler name of the kernel launch_gemm uses for (dtype, R, epi).
-const char* gemm_kernel_name(int dtype, int R, int epi);
+// Profiler name of the kernel launch_gemm uses for (dtype, R, N, K, epi).
+const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi);
 
 }  // namespace spec

@@ -8,7 +8,8 @@
 // four consecutive MFMAs, so a W row's 256-byte block is read by four lanes
 // with 16-byte loads straight from HBM.
 //
-//  * skinny (R <= 64): weight streaming, HBM-bound.  A workgroup owns 16 output
+//  * skinny (R <= 64, except where use_mfma picks the MFMA kernel): weight
+//    streaming, HBM-bound.  A workgroup owns 16 output
 //    features (gate+up pairs for SwiGLU); its waves split K and reduce through
 //    LDS in a fixed order (deterministic, no atomics).  M is padded to 16 per
 //    tile; MFMA throughput is ~10x what the weight stream needs.
@@ -443,6 +444,16 @@ hipError_t mfma(int R, int N, int K, const void* X, const void* W, void* Y, hipS
   return hipGetLastError();
 }
 
+// Skinny (weight streaming, X re-read per workgroup) or MFMA tiles (X staged
+// once per 128 rows): measured at 8..64 rows on the 1B-shaped projections, the
+// MFMA kernel wins for the 128256-row LM head above 8 rows and for the large
+// projections (>= 16M weights) above 40 rows.
+bool use_mfma(int R, int Nw, int K) {
+  if (R > 64) return true;
+  if (R > 8 && Nw >= 65536) return true;
+  return R > 40 && static_cast<double>(Nw) * K >= 16.0 * (1 << 20);
+}
+
 template <int EPI>
 hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
                     hipStream_t st, const int32_t* rm, float* ws, size_t ws_bytes) {
@@ -454,6 +465,7 @@ hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W
     return hipGetLastError();
   }
   if (K % 128 != 0) return hipErrorInvalidValue;
+  if (use_mfma(R, EPI == kEpiSwiGLU ? 2 * N : N, K)) return mfma<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
   if (R <= 16) return skinny<1, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 32) return skinny<2, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 48) return skinny<3, EPI>(R, N, K, X, W, Y, st, rm);
@@ -471,7 +483,7 @@ size_t gemm_splitk_bytes(int R_max, int Nw_max) {
   return std::min<size_t>(256, 8 * tiles) * kMM * kMN * sizeof(float);
 }
 
-const char* gemm_kernel_name(int dtype, int R, int epi) {
+const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi) {
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
   static const char* tiled[3] = {"gemm_mfma_bf16<0>", "gemm_mfma_bf16<1>", "gemm_mfma_bf16<2>"};
   static const char* skinny[4][3] = {
@@ -481,8 +493,8 @@ const char* gemm_kernel_name(int dtype, int R, int epi) {
       {"gemm_skinny_bf16<4, 0>", "gemm_skinny_bf16<4, 1>", "gemm_skinny_bf16<4, 2>"}};
   if (epi < 0 || epi > 2) return "";
   if (dtype == 0) return f32[epi];
-  if (R <= 64) return skinny[(std::max(R, 1) - 1) / 16][epi];
-  return tiled[epi];
+  if (use_mfma(R, epi == kEpiSwiGLU ? 2 * N : N, K)) return tiled[epi];
+  return skinny[(std::max(R, 1) - 1) / 16][epi];
 }
 
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,

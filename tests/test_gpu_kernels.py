@@ -119,6 +119,7 @@ FULL = [
     (6, 6144, 4096, 0), (6, 4096, 4096, 1), (6, 14336, 4096, 2), (6, 4096, 14336, 1), (6, 128256, 4096, 0),
     (384, 6144, 4096, 0), (384, 14336, 4096, 2), (384, 4096, 14336, 1), (384, 128256, 4096, 0),
     (1, 3072, 2048, 0), (1, 8192, 2048, 2), (1, 2048, 8192, 1), (64, 128256, 2048, 0),
+    (21, 128256, 2048, 0), (48, 8192, 2048, 2), (43, 2048, 8192, 1), (9, 70000, 256, 0),
 ]
 
 
