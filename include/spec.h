@@ -186,6 +186,17 @@ SPEC_API spec_status spec_seq_info(const spec_ctx* ctx, int64_t seq_id, int32_t*
  * call order (sequence i's k_i + 1 rows are contiguous), and the row count. */
 SPEC_API spec_status spec_last_logits(const spec_ctx* ctx, const float** logits, int32_t* rows);
 
+/* Device address of the draft logits row (fp32 [vocab]) from which draft j
+ * (0-based) of the sequence's current drafts was drawn (for spec_set_drafts
+ * drafts: the caller's row).  Valid until the sequence's next commit,
+ * rollback or release. */
+SPEC_API spec_status spec_draft_logits(const spec_ctx* ctx, int64_t seq_id, int32_t j, const float** row);
+
+/* The sequence's current drafts, copied to the host: tokens[0 .. *k - 1]
+ * (room for k_max entries), *k = their count.  Waits for `stream`. */
+SPEC_API spec_status spec_draft_tokens(spec_ctx* ctx, int64_t seq_id, int32_t* tokens, int32_t* k,
+                                       void* stream);
+
 /* Graph replay of the draft step and the verify (on by default).  Their
  * kernel sequence depends only on the batch shape (rows, sequences, attention
  * work items), so the first call of a shape captures it into a HIP graph and

@@ -74,6 +74,8 @@ SIGNATURES = {
     "spec_seq_info": (c_int32, [_P, c_int64, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, c_int32]),
     "spec_last_logits": (c_int32, [_P, POINTER(c_void_p), _I32P]),
     "spec_set_graphs": (c_int32, [_P, c_int32]),
+    "spec_draft_logits": (c_int32, [_P, c_int64, c_int32, _P]),
+    "spec_draft_tokens": (c_int32, [_P, c_int64, _P, _P, _P]),
     "spec_timing_enable": (c_int32, [_P, ctypes.c_char_p]),
     "spec_timing_read": (c_int32, [_P, POINTER(ctypes.c_double), _I64P, POINTER(ctypes.c_double),
                                    POINTER(ctypes.c_double)]),
@@ -240,6 +242,21 @@ def spec_last_logits(ctx: int):
     r = c_int32()
     check(lib().spec_last_logits(ctx, ctypes.byref(p), ctypes.byref(r)), ctx)
     return p.value, r.value
+
+
+def spec_draft_logits(ctx: int, seq_id: int, j: int) -> int:
+    """Device address of the draft logits row that drew draft j of seq_id."""
+    p = c_void_p()
+    check(lib().spec_draft_logits(ctx, seq_id, j, ctypes.byref(p)), ctx)
+    return p.value
+
+
+def spec_draft_tokens(ctx: int, seq_id: int, k_max: int, stream=None) -> np.ndarray:
+    """The sequence's current draft tokens (host int32 [k])."""
+    out = np.zeros(max(1, k_max), dtype=np.int32)
+    k = c_int32()
+    check(lib().spec_draft_tokens(ctx, seq_id, out.ctypes.data, ctypes.byref(k), stream_ptr(stream)), ctx)
+    return out[:k.value].copy()
 
 
 def spec_set_graphs(ctx: int, enable: bool) -> None:

@@ -80,7 +80,7 @@ struct Seq {
 struct Ws {
   size_t h = 0, y = 0, qkv = 0, q = 0, o = 0, u = 0, logits = 0, dq = 0, dtok = 0, rowtok = 0;
   size_t part_o = 0, part_ml = 0, vocab = 0, draft = 0, nacc = 0, otok = 0, meta = 0, gmeta = 0;
-  size_t splitk = 0, splitk_bytes = 0;
+  size_t splitk = 0, splitk_bytes = 0, ss = 0;
   size_t meta_cap = 0, total = 0;
 };
 
@@ -214,6 +214,7 @@ void compute_ws(spec_ctx* c) {
   w.dq = take(nq * c->V * 4);
   w.dtok = take(nq * 4);
   w.rowtok = take(R * 4);
+  w.ss = take(R * (c->d_max / 16 + 1) * 4);
   w.part_o = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * c->hd_max * 4);
   w.part_ml = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * 2 * 4);
   const int vrows = c->max_seqs * (2 * c->k_max + 1);
@@ -296,8 +297,16 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   void* q = ctx->wsp + ctx->ws.q;
   void* ob = ctx->wsp + ctx->ws.o;
   void* u = ctx->wsp + ctx->ws.u;
+  // Up to 8 rows (batch-1 verify and draft steps) RMSNorm and RoPE / KV
+  // append run inside the GEMMs (launch_gemm_fused): each residual-add GEMM
+  // (and the embedding) also writes bf16(h (.) w_next) into y and per-16-column
+  // sums of squares into ss; the next GEMM reads y and scales its output rows
+  // by 1/rms; the QKV GEMM applies RoPE and writes q and the KV cache itself.
+  const bool fused = dt == 1 && R <= 8 && d.head_dim % 16 == 0 && d.d_model % 16 == 0;
+  float* ss = wsptr<float>(ctx, ctx->ws.ss);
   HIPC(launch_embed(dt, R, d.d_model, I(o.tok), wsptr<int32_t>(ctx, ctx->ws.dtok), d.embed, h,
-                    wsptr<int32_t>(ctx, ctx->ws.rowtok), st));
+                    wsptr<int32_t>(ctx, ctx->ws.rowtok), st, fused ? y : nullptr,
+                    fused ? M.layers[0].attn_norm : nullptr, fused ? ss : nullptr));
   AttnArgs a;
   a.dtype = dt;
   a.Hq = d.n_heads;
@@ -314,11 +323,13 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   // GEMM launch, timed when selected: algorithmic bytes = weights + inputs +
   // outputs (read-modify-write for the residual add), flops = 2 R N_w K.
   auto gemm = [&](int rows, int N, int K, const void* X, const void* W, void* Y, int epi,
-                  const int32_t* rm) -> hipError_t {
-    const bool timed = tm.wants(gemm_kernel_name(dt, rows, N, K, epi));
+                  const int32_t* rm, const GemmFuse* f = nullptr) -> hipError_t {
+    const bool timed = tm.wants(gemm_kernel_name(dt, rows, N, K, epi, f != nullptr));
     if (timed) tm.begin(st);
-    const hipError_t e = launch_gemm(dt, rows, N, K, X, W, Y, epi, st, rm, wsptr<float>(ctx, ctx->ws.splitk),
-                                     ctx->ws.splitk_bytes);
+    const hipError_t e =
+        f ? launch_gemm_fused(rows, N, K, X, W, Y, epi, *f, st, rm)
+          : launch_gemm(dt, rows, N, K, X, W, Y, epi, st, rm, wsptr<float>(ctx, ctx->ws.splitk),
+                        ctx->ws.splitk_bytes);
     if (timed) {
       const double nw = epi == kEpiSwiGLU ? 2.0 * N : N;
       const double ob = epi == kEpiStoreF32 ? 4.0 : (epi == kEpiAddF32 ? 8.0 : esz);
@@ -328,10 +339,26 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   };
   for (int l = 0; l < d.n_layers; ++l) {
     const auto& L = M.layers[l];
-    HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
-    HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr));
-    HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, qkv, I(o.pos),
-                        I(o.slot), q, M.kl(l), M.vl(l), st));
+    if (fused) {
+      GemmFuse fq;
+      fq.ss = ss;
+      fq.eps = d.rms_eps;
+      fq.Hq = d.n_heads;
+      fq.Hkv = d.n_kv_heads;
+      fq.hd = d.head_dim;
+      fq.theta = d.rope_theta;
+      fq.pos = I(o.pos);
+      fq.slot = I(o.slot);
+      fq.qout = q;
+      fq.kpool = M.kl(l);
+      fq.vpool = M.vl(l);
+      HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, nullptr, kEpiQKVRope, nullptr, &fq));
+    } else {
+      HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
+      HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr));
+      HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, qkv, I(o.pos),
+                          I(o.slot), q, M.kl(l), M.vl(l), st));
+    }
     a.kpool = M.kl(l);
     a.vpool = M.vl(l);
     if (dt == 1) {
@@ -347,14 +374,40 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
     } else {
       HIPC(launch_attention_f32(a, R, I(o.seqi), I(o.pos), st));
     }
-    HIPC(gemm(R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, nullptr));
-    HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.mlp_norm, d.rms_eps, y, st));
-    HIPC(gemm(R, d.ffn_dim, d.d_model, y, L.w_gate_up, u, kEpiSwiGLU, nullptr));
-    HIPC(gemm(R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, nullptr));
+    if (fused) {
+      GemmFuse fo;
+      fo.hb = y;
+      fo.wn = L.mlp_norm;
+      fo.ss_out = ss;
+      HIPC(gemm(R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, nullptr, &fo));
+      GemmFuse fg;
+      fg.ss = ss;
+      fg.eps = d.rms_eps;
+      HIPC(gemm(R, d.ffn_dim, d.d_model, y, L.w_gate_up, u, kEpiSwiGLU, nullptr, &fg));
+      GemmFuse fd;
+      fd.hb = y;
+      fd.wn = l + 1 < d.n_layers ? M.layers[l + 1].attn_norm : d.final_norm;
+      fd.ss_out = ss;
+      HIPC(gemm(R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, nullptr, &fd));
+    } else {
+      HIPC(gemm(R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, nullptr));
+      HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.mlp_norm, d.rms_eps, y, st));
+      HIPC(gemm(R, d.ffn_dim, d.d_model, y, L.w_gate_up, u, kEpiSwiGLU, nullptr));
+      HIPC(gemm(R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, nullptr));
+    }
   }
   if (o.n_lm > 0) {
-    HIPC(launch_rmsnorm(dt, o.n_lm, d.d_model, h, I(o.lmr), d.final_norm, d.rms_eps, y, st));
-    HIPC(gemm(o.n_lm, d.vocab, d.d_model, y, d.lm_head, logits, kEpiStoreF32, o.lm_map ? I(o.lmm) : nullptr));
+    if (fused) {
+      GemmFuse fl;
+      fl.ss = ss;
+      fl.xrow = I(o.lmr);
+      fl.eps = d.rms_eps;
+      HIPC(gemm(o.n_lm, d.vocab, d.d_model, y, d.lm_head, logits, kEpiStoreF32, o.lm_map ? I(o.lmm) : nullptr,
+                &fl));
+    } else {
+      HIPC(launch_rmsnorm(dt, o.n_lm, d.d_model, h, I(o.lmr), d.final_norm, d.rms_eps, y, st));
+      HIPC(gemm(o.n_lm, d.vocab, d.d_model, y, d.lm_head, logits, kEpiStoreF32, o.lm_map ? I(o.lmm) : nullptr));
+    }
   }
   return SPEC_OK;
 }
@@ -873,6 +926,33 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   }
   ctx->last_rows = R;
   ctx->timer.flush();
+  return SPEC_OK;
+}
+
+spec_status spec_draft_logits(const spec_ctx* ctx, int64_t seq_id, int32_t j, const float** row) {
+  if (!ctx || !row) return SPEC_E_INVALID;
+  auto it = ctx->seqs.find(seq_id);
+  if (it == ctx->seqs.end() || j < 0 || j >= it->second.k) return SPEC_E_INVALID;
+  *row = it->second.qrow[j];
+  return SPEC_OK;
+}
+
+spec_status spec_draft_tokens(spec_ctx* ctx, int64_t seq_id, int32_t* tokens, int32_t* k, void* stream) {
+  CHECK_READY();
+  if (!tokens || !k) FAIL(SPEC_E_INVALID, "bad arguments");
+  auto it = ctx->seqs.find(seq_id);
+  if (it == ctx->seqs.end()) FAIL(SPEC_E_INVALID, "unknown seq_id");
+  const Seq& s = it->second;
+  HIPC(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+  const int32_t* pool = wsptr<int32_t>(ctx, ctx->ws.dtok);
+  for (int j = 0; j < s.k; ++j) {
+    if (s.dsrc[j] >= 0) {
+      tokens[j] = s.dsrc[j];
+    } else {
+      HIPC(hipMemcpy(tokens + j, pool + (-1 - s.dsrc[j]), sizeof(int32_t), hipMemcpyDeviceToHost));
+    }
+  }
+  *k = s.k;
   return SPEC_OK;
 }
 

@@ -14,14 +14,30 @@ template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(int d, const int32_t* __restrict__ tok_src,
                                                     const int32_t* __restrict__ tok_pool,
                                                     const T* __restrict__ E, float* __restrict__ h,
-                                                    int32_t* __restrict__ row_tok) {
+                                                    int32_t* __restrict__ row_tok, T* __restrict__ hb,
+                                                    const T* __restrict__ wn, float* __restrict__ ss) {
   const int r = blockIdx.x;
   const int s = tok_src[r];
   const int tok = s >= 0 ? s : tok_pool[-1 - s];
   if (threadIdx.x == 0) row_tok[r] = tok;
   const T* e = E + static_cast<size_t>(tok) * d;
   float* o = h + static_cast<size_t>(r) * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) o[i] = Elem<T>::to_f32(e[i]);
+  // whole waves run every iteration: 16 consecutive lanes hold the 16
+  // columns whose sum of squares is one entry of ss
+  for (int i0 = 0; i0 < d; i0 += blockDim.x) {
+    const int i = i0 + threadIdx.x;
+    const float x = i < d ? Elem<T>::to_f32(e[i]) : 0.f;
+    if (i < d) {
+      o[i] = x;
+      if (hb) hb[static_cast<size_t>(r) * d + i] = Elem<T>::from_f32(x * Elem<T>::to_f32(wn[i]));
+    }
+    if (ss) {
+      float sq = x * x;
+#pragma unroll
+      for (int k = 1; k < 16; k <<= 1) sq += __shfl_xor(sq, k, kWave);
+      if ((threadIdx.x & 15) == 0 && i < d) ss[static_cast<size_t>(r) * (d / 16) + i / 16] = sq;
+    }
+  }
 }
 
 template <typename T>
@@ -105,12 +121,16 @@ __global__ __launch_bounds__(256) void kv_clear_kernel(const int32_t* __restrict
 }  // namespace
 
 hipError_t launch_embed(int dtype, int R, int d, const int32_t* tok_src, const int32_t* tok_pool,
-                        const void* E, float* h, int32_t* row_tok, hipStream_t st) {
+                        const void* E, float* h, int32_t* row_tok, hipStream_t st, void* hb, const void* wn,
+                        float* ss) {
   if (R <= 0) return hipSuccess;
+  if (ss && d % 16 != 0) return hipErrorInvalidValue;
   if (dtype == 0)
-    embed_kernel<float><<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const float*>(E), h, row_tok);
+    embed_kernel<float><<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const float*>(E), h, row_tok,
+                                           static_cast<float*>(hb), static_cast<const float*>(wn), ss);
   else
-    embed_kernel<bf16_t><<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const bf16_t*>(E), h, row_tok);
+    embed_kernel<bf16_t><<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const bf16_t*>(E), h, row_tok,
+                                            static_cast<bf16_t*>(hb), static_cast<const bf16_t*>(wn), ss);
   return hipGetLastError();
 }
 

@@ -9,8 +9,41 @@ namespace spec {
 enum GemmEpi {
   kEpiStoreF32 = 0,  // Y fp32 [R, N] = X W^T
   kEpiAddF32 = 1,    // Y fp32 [R, N] += X W^T (residual stream)
-  kEpiSwiGLU = 2     // W has 2N rows (gate then up); Y (element type) [R, N] = silu(g) * u
+  kEpiSwiGLU = 2,    // W has 2N rows (gate then up); Y (element type) [R, N] = silu(g) * u
+  kEpiQKVRope = 3    // fused path only: RoPE on q and k, q out, k and v into the paged cache
 };
+
+// Extras of the fused skinny GEMM (bf16, R <= 16), which folds the RMSNorm
+// and the RoPE / KV append of the decoder into the GEMMs around them.
+struct GemmFuse {
+  // Consumer side of RMSNorm: X holds rows bf16(h (.) w) written by the
+  // producer, and output row m is scaled by 1/sqrt(mean(h[m]^2) + eps), the
+  // mean taken from `ss`, the producer's sums of squares per 16 columns
+  // ([rows][K / 16]).  xrow (optional): X and ss row of output row m.
+  const float* ss = nullptr;
+  const int32_t* xrow = nullptr;
+  float eps = 0.f;
+  // Producer side (kEpiAddF32): with the new residual h also write
+  // hb = bf16(h (.) wn) [R][N] and its sums of squares ss_out [R][N / 16].
+  void* hb = nullptr;
+  const void* wn = nullptr;
+  float* ss_out = nullptr;
+  // kEpiQKVRope: W is the [(Hq + 2 Hkv) hd, K] QKV projection; rotate-half
+  // RoPE (angle pos[m] * theta^(-2i/hd), evaluated in fp64) on the q and k
+  // heads; q to qout [R][Hq][hd], k and v to K [page][Hkv][16][hd] and
+  // V^T [page][Hkv][hd][16] at slot[m] = page * 16 + offset.
+  int Hq = 0, Hkv = 0, hd = 0;
+  float theta = 0.f;
+  const int32_t* pos = nullptr;
+  const int32_t* slot = nullptr;
+  void* qout = nullptr;
+  void* kpool = nullptr;
+  void* vpool = nullptr;
+};
+
+// Fused skinny GEMM (bf16, R <= 16, K % 128 == 0); epi as above.
+hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, void* Y, int epi,
+                             const GemmFuse& f, hipStream_t st, const int32_t* row_map = nullptr);
 
 // dtype: 0 = fp32 (X, W, SwiGLU output fp32), 1 = bf16 (X, W, SwiGLU output bf16).
 // bf16 requires K % 128 == 0 (returns hipErrorInvalidValue otherwise).
@@ -24,7 +57,8 @@ hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void
 // Bytes of split-K workspace that cover every launch shape.
 size_t gemm_splitk_bytes(int R_max, int Nw_max);
 
-// Profiler name of the kernel launch_gemm uses for (dtype, R, N, K, epi).
-const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi);
+// Profiler name of the kernel launch_gemm uses for (dtype, R, N, K, epi), or
+// launch_gemm_fused when fused.
+const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused = false);
 
 }  // namespace spec

@@ -35,20 +35,42 @@ __device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); 
 
 constexpr int kSkinnyMaxWaves = 8;
 
-template <int MT, int EPI>
+// Tiles of the fused QKV epilogue: the q and k heads come first, each as
+// hd / 16 tiles of 8 rotary pairs (i, i + hd / 2), so that a pair meets in one
+// workgroup (lanes l and l ^ 8 of a 16-lane group); the v heads follow in
+// plain order.
+__device__ __forceinline__ int qkv_tile_row(const GemmFuse& f, int tile, int l16, int* head, int* dim) {
+  const int per_head = f.hd / 16;
+  *head = tile / per_head;
+  const int i = 8 * (tile % per_head) + (l16 & 7);
+  *dim = i + (l16 >> 3) * (f.hd / 2);
+  return *head * f.hd + *dim;
+}
+
+template <int MT, int EPI, bool FUSE>
 __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, void* __restrict__ Y, int R, int N,
-    int K, int kb_per_wave, const int32_t* __restrict__ row_map) {
+    int K, int kb_per_wave, const int32_t* __restrict__ row_map, const GemmFuse fu) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
+  constexpr bool QKV = (EPI == kEpiQKVRope);
   constexpr int NACC = MT * (SW ? 2 : 1);
+  static_assert(!FUSE || MT == 1, "the fused path covers up to 16 rows");
+  static_assert(FUSE || !QKV, "the QKV epilogue is fused only");
   __shared__ float red[kSkinnyMaxWaves * NACC * 256];
+  __shared__ float s_rs[16];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int nw = blockDim.x / kWave;
   const int row = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * 16;
-  const int nrow = min(n0 + row, N - 1);
+  const int qk_tiles = QKV ? (fu.Hq + fu.Hkv) * fu.hd / 16 : 0;
+  int feat = n0 + row;
+  if (QKV && static_cast<int>(blockIdx.x) < qk_tiles) {
+    int hh, dd;
+    feat = qkv_tile_row(fu, blockIdx.x, row, &hh, &dd);
+  }
+  const int nrow = min(feat, N - 1);
   // lane group g, step s carries k = 32 s + 8 g .. +7 of each 128-wide block:
   // the four lanes of a row read one contiguous 64-byte run per load
   const bf16_t* wg = W + static_cast<size_t>(nrow) * K + g * 8;
@@ -59,7 +81,24 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
   for (int mt = 0; mt < MT; ++mt) {
     const int m = mt * 16 + row;
     xv[mt] = m < R;
-    xr[mt] = X + static_cast<size_t>(xv[mt] ? m : 0) * K + g * 8;
+    const int src = !xv[mt] ? 0 : ((FUSE && fu.xrow) ? fu.xrow[m] : m);
+    xr[mt] = X + static_cast<size_t>(src) * K + g * 8;
+  }
+  if (FUSE && fu.ss) {
+    // 1 / rms of each X row from the producer's sums of squares per 16
+    // columns: 32 lanes per row, fixed order (strided sums, then a tree)
+    const int np = K / 16;
+    for (int base = 0; base < 16; base += blockDim.x / 32) {
+      const int rr = base + static_cast<int>(threadIdx.x) / 32, sub = threadIdx.x & 31;
+      float a = 0.f;
+      if (rr < R) {
+        const float* sp = fu.ss + static_cast<size_t>(fu.xrow ? fu.xrow[rr] : rr) * np;
+        for (int p = sub; p < np; p += 32) a += sp[p];
+      }
+#pragma unroll
+      for (int o = 16; o > 0; o >>= 1) a += __shfl_xor(a, o, kWave);
+      if (sub == 0 && rr < 16) s_rs[rr] = 1.f / sqrtf(a / static_cast<float>(K) + fu.eps);
+    }
   }
   f32x4 acc[MT], accu[MT];
 #pragma unroll
@@ -110,6 +149,74 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
       if (SW) red[((wave * NACC + MT + mt) * 4 + r) * kWave + lane] = accu[mt][r];
     }
   __syncthreads();
+  if (FUSE) {
+    // one element per thread of waves 0..3; whole waves take part in the
+    // 16-lane exchanges below (lanes of a group hold the 16 columns of a row)
+    if (threadIdx.x >= 256) return;
+    const int e = threadIdx.x, r = (e / kWave) & 3, ln = e & (kWave - 1);
+    const int m = 4 * (ln >> 4) + r, l16 = ln & 15;
+    const int n = n0 + l16;
+    float v = 0.f, vu = 0.f;
+    for (int wv = 0; wv < nw; ++wv) {
+      v += red[((wv * NACC) * 4 + r) * kWave + ln];
+      if (SW) vu += red[((wv * NACC + 1) * 4 + r) * kWave + ln];
+    }
+    if (fu.ss) {
+      const float rs = s_rs[m];
+      v *= rs;
+      vu *= rs;
+    }
+    const bool ok = m < R && n < N;
+    if (EPI == kEpiAddF32) {
+      float hn = 0.f;
+      if (ok) {
+        float* y = static_cast<float*>(Y) + static_cast<size_t>(m) * N + n;
+        hn = *y + v;
+        *y = hn;
+        if (fu.hb)
+          static_cast<bf16_t*>(fu.hb)[static_cast<size_t>(m) * N + n] =
+              f32_to_bf16(hn * bf16_to_f32(static_cast<const bf16_t*>(fu.wn)[n]));
+      }
+      if (fu.ss_out) {
+        float sq = hn * hn;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o, kWave);
+        if (l16 == 0 && m < R) fu.ss_out[static_cast<size_t>(m) * (N / 16) + n0 / 16] = sq;
+      }
+    } else if (QKV) {
+      const float partner = __shfl_xor(v, 8, kWave);
+      if (m < R) {
+        const int sl = fu.slot[m];
+        const int page = sl >> 4, off = sl & 15;
+        if (static_cast<int>(blockIdx.x) < qk_tiles) {
+          int head, dim;
+          qkv_tile_row(fu, blockIdx.x, l16, &head, &dim);
+          const int i = dim % (fu.hd / 2);
+          double sn, cs;
+          sincos(static_cast<double>(fu.pos[m]) * exp(-(2.0 * i / fu.hd) * log(static_cast<double>(fu.theta))),
+                 &sn, &cs);
+          const float c = static_cast<float>(cs), sv = static_cast<float>(sn);
+          // first half: a cos - b sin; second half: b cos + a sin (a, b = pair)
+          const float o = (l16 < 8) ? v * c - partner * sv : v * c + partner * sv;
+          if (head < fu.Hq)
+            static_cast<bf16_t*>(fu.qout)[(static_cast<size_t>(m) * fu.Hq + head) * fu.hd + dim] = f32_to_bf16(o);
+          else
+            static_cast<bf16_t*>(fu.kpool)[((static_cast<size_t>(page) * fu.Hkv + (head - fu.Hq)) * 16 + off) * fu.hd + dim] =
+                f32_to_bf16(o);
+        } else if (n < N) {
+          const int vi = n - (fu.Hq + fu.Hkv) * fu.hd;
+          const int kh = vi / fu.hd, dd = vi % fu.hd;
+          static_cast<bf16_t*>(fu.vpool)[((static_cast<size_t>(page) * fu.Hkv + kh) * fu.hd + dd) * 16 + off] =
+              f32_to_bf16(v);
+        }
+      }
+    } else if (ok) {
+      const size_t o = static_cast<size_t>(row_map ? row_map[m] : m) * N + n;
+      if (EPI == kEpiStoreF32) static_cast<float*>(Y)[o] = v;
+      if (EPI == kEpiSwiGLU) static_cast<bf16_t*>(Y)[o] = f32_to_bf16(silu(v) * vu);
+    }
+    return;
+  }
   for (int e = threadIdx.x; e < MT * 256; e += blockDim.x) {
     const int mt = e / 256, r = (e / kWave) & 3, ln = e & (kWave - 1);
     const int m = mt * 16 + 4 * (ln >> 4) + r;
@@ -390,19 +497,19 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X,
   }
 }
 
-template <int MT, int EPI>
+template <int MT, int EPI, bool FUSE = false>
 hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
-                  const int32_t* row_map) {
+                  const int32_t* row_map, const GemmFuse& fu = GemmFuse{}) {
   const int tiles = (N + 15) / 16;
   const int nb = K / 128;
   // waves per workgroup split K: 8 when there are few feature tiles (and K is
   // not long enough to keep 4 waves busy), else 4 (measured at the verify and
   // draft shapes of the 8B/1B-shaped pair)
   int nw = (tiles <= 256 && K < 12288) ? 8 : 4;
-  nw = std::max(1, std::min(nw, nb));
+  nw = std::max(FUSE ? 4 : 1, std::min(nw, nb));
   const int kbpw = (nb + nw - 1) / nw;
-  gemm_skinny_bf16<MT, EPI><<<tiles, nw * kWave, 0, st>>>(
-      static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map);
+  gemm_skinny_bf16<MT, EPI, FUSE><<<tiles, nw * kWave, 0, st>>>(
+      static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map, fu);
   return hipGetLastError();
 }
 
@@ -483,14 +590,31 @@ size_t gemm_splitk_bytes(int R_max, int Nw_max) {
   return std::min<size_t>(256, 8 * tiles) * kMM * kMN * sizeof(float);
 }
 
-const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi) {
+hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, void* Y, int epi,
+                             const GemmFuse& f, hipStream_t st, const int32_t* row_map) {
+  if (R <= 0 || N <= 0) return hipSuccess;
+  if (R > 16 || K % 128 != 0 || N % 16 != 0) return hipErrorInvalidValue;
+  if (epi == kEpiQKVRope && (f.hd % 16 != 0 || N != (f.Hq + 2 * f.Hkv) * f.hd)) return hipErrorInvalidValue;
+  switch (epi) {
+    case kEpiStoreF32: return skinny<1, kEpiStoreF32, true>(R, N, K, X, W, Y, st, row_map, f);
+    case kEpiAddF32: return skinny<1, kEpiAddF32, true>(R, N, K, X, W, Y, st, nullptr, f);
+    case kEpiSwiGLU: return skinny<1, kEpiSwiGLU, true>(R, N, K, X, W, Y, st, row_map, f);
+    case kEpiQKVRope: return skinny<1, kEpiQKVRope, true>(R, N, K, X, W, Y, st, nullptr, f);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused) {
+  static const char* fz[4] = {"gemm_skinny_bf16<1, 0, true>", "gemm_skinny_bf16<1, 1, true>",
+                              "gemm_skinny_bf16<1, 2, true>", "gemm_skinny_bf16<1, 3, true>"};
+  if (fused) return (epi >= 0 && epi <= 3) ? fz[epi] : "";
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
   static const char* tiled[3] = {"gemm_mfma_bf16<0>", "gemm_mfma_bf16<1>", "gemm_mfma_bf16<2>"};
   static const char* skinny[4][3] = {
-      {"gemm_skinny_bf16<1, 0>", "gemm_skinny_bf16<1, 1>", "gemm_skinny_bf16<1, 2>"},
-      {"gemm_skinny_bf16<2, 0>", "gemm_skinny_bf16<2, 1>", "gemm_skinny_bf16<2, 2>"},
-      {"gemm_skinny_bf16<3, 0>", "gemm_skinny_bf16<3, 1>", "gemm_skinny_bf16<3, 2>"},
-      {"gemm_skinny_bf16<4, 0>", "gemm_skinny_bf16<4, 1>", "gemm_skinny_bf16<4, 2>"}};
+      {"gemm_skinny_bf16<1, 0, false>", "gemm_skinny_bf16<1, 1, false>", "gemm_skinny_bf16<1, 2, false>"},
+      {"gemm_skinny_bf16<2, 0, false>", "gemm_skinny_bf16<2, 1, false>", "gemm_skinny_bf16<2, 2, false>"},
+      {"gemm_skinny_bf16<3, 0, false>", "gemm_skinny_bf16<3, 1, false>", "gemm_skinny_bf16<3, 2, false>"},
+      {"gemm_skinny_bf16<4, 0, false>", "gemm_skinny_bf16<4, 1, false>", "gemm_skinny_bf16<4, 2, false>"}};
   if (epi < 0 || epi > 2) return "";
   if (dtype == 0) return f32[epi];
   if (use_mfma(R, epi == kEpiSwiGLU ? 2 * N : N, K)) return tiled[epi];

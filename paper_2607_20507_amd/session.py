@@ -150,6 +150,18 @@ class SpecSession:
     def seq_info(self, seq_id: int):
         return B.spec_seq_info(self.ctx, seq_id)
 
+    def draft_tokens(self, seq_id: int, stream=None):
+        """The sequence's current draft tokens (list of int)."""
+        return [int(x) for x in B.spec_draft_tokens(self.ctx, seq_id, self.k_max, stream)]
+
+    def draft_logits(self, seq_id: int, j: int) -> torch.Tensor:
+        """Copy of the draft logits row [V] (fp32) behind draft j of seq_id
+        (drafts made by draft_step live in this session's workspace)."""
+        ptr = B.spec_draft_logits(self.ctx, seq_id, j)
+        V = self.target.shape.vocab
+        off = ptr - self.ws_view.data_ptr()
+        return self.ws_view[off:off + V * 4].view(torch.float32).clone()
+
     def last_logits(self) -> torch.Tensor:
         """Copy of the last verify's target logits [rows, V] (fp32)."""
         ptr, rows = B.spec_last_logits(self.ctx)

@@ -164,3 +164,57 @@ def test_small_bf16_verify_logits():
         assert 0 <= int(na[i]) <= k
     gpu.commit(ids, na)
     gpu.close()
+
+
+def _bf16_pair_hd128():
+    """A small bf16 pair with the 8B-shaped head layout (head_dim 128, GQA 2:1)."""
+    from dataclasses import replace
+    from workloads.configs import ModelShape
+    t = ModelShape("tiny-bf16-hd128", n_layers=2, d_model=256, n_heads=2, n_kv_heads=1, head_dim=128,
+                   ffn_dim=512, vocab=1024, rope_theta=5e5, dtype="bf16")
+    return replace(SMALL_BF16, name="tiny-bf16-hd128", target=t, draft=replace(t, n_layers=1), k=(4,))
+
+
+@pytest.mark.parametrize("which", ["hd128", "small-2L"])
+def test_fused_small_rows_teacher_forced(which):
+    """Batch-1 rows (<= 8: RMSNorm and RoPE / KV append fused into the GEMMs):
+    every draft logits row and every verify logits row of three rounds against
+    the oracle's no-cache forward over the same tokens, within 2e-2."""
+    from paper_2607_20507_amd.session import DeviceModel, SpecSession
+    if which == "hd128":
+        cfg, lt, ld = _bf16_pair_hd128(), None, None
+    else:
+        cfg, lt, ld = SMALL_BF16, 2, 1
+    k = cfg.k[0]
+    dev = device()
+    tw = model_weights(cfg.target, cfg.seed, lt)
+    dw = model_weights(cfg.draft, cfg.seed + 1, ld)
+    gpu = SpecSession(DeviceModel(cfg.target, tw, dev, n_layers=lt), DeviceModel(cfg.draft, dw, dev, n_layers=ld),
+                      max_seqs=1, k_max=k, max_pages_per_seq=16, max_rows=256)
+    tgt, drf = Decoder(cfg.target, tw), Decoder(cfg.draft, dw)
+    sid = 77
+    hist = [int(x) for x in uniform_prompts(cfg.seed, [45], cfg.target.vocab)[0]]
+    say("fused rows teacher-forced", which)
+    gpu.prefill([sid], [np.array(hist, dtype=np.int32)])
+    for rnd in range(3):
+        for _ in range(k):
+            gpu.draft_step([sid], [0.8], 31 + rnd)
+        drafts = gpu.draft_tokens(sid)
+        na, ot = gpu.verify([sid], [0.8], 31 + rnd)
+        zp_gpu = gpu.last_logits().cpu().numpy()
+        zq_gpu = np.stack([gpu.draft_logits(sid, j).cpu().numpy() for j in range(k)])
+        fed = hist + drafts
+        zt = tgt.full_logits(fed)
+        zd = drf.full_logits(fed[:-1])
+        n = len(hist) - 1
+        for j in range(k):
+            e = rel_err(zq_gpu[j], zd[n + j])
+            assert e < 2e-2, f"round {rnd} draft row {j}: {e}"
+        for r in range(k + 1):
+            e = rel_err(zp_gpu[r], zt[n + r])
+            assert e < 2e-2, f"round {rnd} verify row {r}: {e}"
+        a = int(na[0])
+        gpu.commit([sid], na)
+        hist += [int(x) for x in ot[0, :a + 1]]
+    gpu.close()
+
