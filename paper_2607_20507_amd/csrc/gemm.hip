@@ -8,6 +8,7 @@
 // four consecutive MFMAs, so a W row's 256-byte block is read by four lanes
 // with 16-byte loads straight from HBM.
 //
+//  * gemv (R <= 2): vector-FMA weight streaming with 256-byte row runs.
 //  * skinny (R <= 64, except where use_mfma picks the MFMA kernel): weight
 //    streaming, HBM-bound.  A workgroup owns 16 output
 //    features (gate+up pairs for SwiGLU); its waves split K and reduce through
@@ -47,6 +48,86 @@ __device__ __forceinline__ int qkv_tile_row(const GemmFuse& f, int tile, int l16
   return *head * f.hd + *dim;
 }
 
+// 1 / rms of each X row (R <= 16) from the producer's sums of squares per 16
+// columns, into s_rs: 32 lanes per row, fixed order (strided sums, then a
+// tree).  Run by the whole workgroup.
+__device__ __forceinline__ void row_rscale(const GemmFuse& fu, int R, int K, float* s_rs) {
+  const int np = K / 16;
+  for (int base = 0; base < 16; base += blockDim.x / 32) {
+    const int rr = base + static_cast<int>(threadIdx.x) / 32, sub = threadIdx.x & 31;
+    float a = 0.f;
+    if (rr < R) {
+      const float* sp = fu.ss + static_cast<size_t>(fu.xrow ? fu.xrow[rr] : rr) * np;
+      for (int p = sub; p < np; p += 32) a += sp[p];
+    }
+#pragma unroll
+    for (int o = 16; o > 0; o >>= 1) a += __shfl_xor(a, o, kWave);
+    if (sub == 0 && rr < 16) s_rs[rr] = 1.f / sqrtf(a / static_cast<float>(K) + fu.eps);
+  }
+}
+
+// Epilogue of the fused GEMMs for output row m (< 16) and tile column l16 of
+// the 16-feature tile at n0, given the (row-scaled) dot products v (and vu,
+// the up rows of SwiGLU).  Run by whole waves: threads 0..255 with
+// m = 4 (lane / 16) + r, so the 16 lanes of a group hold the 16 columns of a
+// row and exchange values with shuffles.
+template <int EPI>
+__device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l16, int n0, int R, int N,
+                                               float v, float vu, void* __restrict__ Y,
+                                               const int32_t* __restrict__ row_map, int qk_tiles) {
+  constexpr bool QKV = (EPI == kEpiQKVRope);
+  const int n = n0 + l16;
+  const bool ok = m < R && n < N;
+  if (EPI == kEpiAddF32) {
+    float hn = 0.f;
+    if (ok) {
+      float* y = static_cast<float*>(Y) + static_cast<size_t>(m) * N + n;
+      hn = *y + v;
+      *y = hn;
+      if (fu.hb)
+        static_cast<bf16_t*>(fu.hb)[static_cast<size_t>(m) * N + n] =
+            f32_to_bf16(hn * bf16_to_f32(static_cast<const bf16_t*>(fu.wn)[n]));
+    }
+    if (fu.ss_out) {
+      float sq = hn * hn;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o, kWave);
+      if (l16 == 0 && m < R) fu.ss_out[static_cast<size_t>(m) * (N / 16) + n0 / 16] = sq;
+    }
+  } else if (QKV) {
+    const float partner = __shfl_xor(v, 8, kWave);
+    if (m < R) {
+      const int sl = fu.slot[m];
+      const int page = sl >> 4, off = sl & 15;
+      if (static_cast<int>(blockIdx.x) < qk_tiles) {
+        int head, dim;
+        qkv_tile_row(fu, blockIdx.x, l16, &head, &dim);
+        const int i = dim % (fu.hd / 2);
+        double sn, cs;
+        sincos(static_cast<double>(fu.pos[m]) * exp(-(2.0 * i / fu.hd) * log(static_cast<double>(fu.theta))),
+               &sn, &cs);
+        const float c = static_cast<float>(cs), sv = static_cast<float>(sn);
+        // first half: a cos - b sin; second half: b cos + a sin (a, b = pair)
+        const float o = (l16 < 8) ? v * c - partner * sv : v * c + partner * sv;
+        if (head < fu.Hq)
+          static_cast<bf16_t*>(fu.qout)[(static_cast<size_t>(m) * fu.Hq + head) * fu.hd + dim] = f32_to_bf16(o);
+        else
+          static_cast<bf16_t*>(fu.kpool)[((static_cast<size_t>(page) * fu.Hkv + (head - fu.Hq)) * 16 + off) * fu.hd + dim] =
+              f32_to_bf16(o);
+      } else if (n < N) {
+        const int vi = n - (fu.Hq + fu.Hkv) * fu.hd;
+        const int kh = vi / fu.hd, dd = vi % fu.hd;
+        static_cast<bf16_t*>(fu.vpool)[((static_cast<size_t>(page) * fu.Hkv + kh) * fu.hd + dd) * 16 + off] =
+            f32_to_bf16(v);
+      }
+    }
+  } else if (ok) {
+    const size_t o = static_cast<size_t>(row_map ? row_map[m] : m) * N + n;
+    if (EPI == kEpiStoreF32) static_cast<float*>(Y)[o] = v;
+    if (EPI == kEpiSwiGLU) static_cast<bf16_t*>(Y)[o] = f32_to_bf16(silu(v) * vu);
+  }
+}
+
 template <int MT, int EPI, bool FUSE>
 __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, void* __restrict__ Y, int R, int N,
@@ -84,22 +165,7 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     const int src = !xv[mt] ? 0 : ((FUSE && fu.xrow) ? fu.xrow[m] : m);
     xr[mt] = X + static_cast<size_t>(src) * K + g * 8;
   }
-  if (FUSE && fu.ss) {
-    // 1 / rms of each X row from the producer's sums of squares per 16
-    // columns: 32 lanes per row, fixed order (strided sums, then a tree)
-    const int np = K / 16;
-    for (int base = 0; base < 16; base += blockDim.x / 32) {
-      const int rr = base + static_cast<int>(threadIdx.x) / 32, sub = threadIdx.x & 31;
-      float a = 0.f;
-      if (rr < R) {
-        const float* sp = fu.ss + static_cast<size_t>(fu.xrow ? fu.xrow[rr] : rr) * np;
-        for (int p = sub; p < np; p += 32) a += sp[p];
-      }
-#pragma unroll
-      for (int o = 16; o > 0; o >>= 1) a += __shfl_xor(a, o, kWave);
-      if (sub == 0 && rr < 16) s_rs[rr] = 1.f / sqrtf(a / static_cast<float>(K) + fu.eps);
-    }
-  }
+  if (FUSE && fu.ss) row_rscale(fu, R, K, s_rs);
   f32x4 acc[MT], accu[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
@@ -155,7 +221,6 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     if (threadIdx.x >= 256) return;
     const int e = threadIdx.x, r = (e / kWave) & 3, ln = e & (kWave - 1);
     const int m = 4 * (ln >> 4) + r, l16 = ln & 15;
-    const int n = n0 + l16;
     float v = 0.f, vu = 0.f;
     for (int wv = 0; wv < nw; ++wv) {
       v += red[((wv * NACC) * 4 + r) * kWave + ln];
@@ -166,55 +231,7 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
       v *= rs;
       vu *= rs;
     }
-    const bool ok = m < R && n < N;
-    if (EPI == kEpiAddF32) {
-      float hn = 0.f;
-      if (ok) {
-        float* y = static_cast<float*>(Y) + static_cast<size_t>(m) * N + n;
-        hn = *y + v;
-        *y = hn;
-        if (fu.hb)
-          static_cast<bf16_t*>(fu.hb)[static_cast<size_t>(m) * N + n] =
-              f32_to_bf16(hn * bf16_to_f32(static_cast<const bf16_t*>(fu.wn)[n]));
-      }
-      if (fu.ss_out) {
-        float sq = hn * hn;
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o, kWave);
-        if (l16 == 0 && m < R) fu.ss_out[static_cast<size_t>(m) * (N / 16) + n0 / 16] = sq;
-      }
-    } else if (QKV) {
-      const float partner = __shfl_xor(v, 8, kWave);
-      if (m < R) {
-        const int sl = fu.slot[m];
-        const int page = sl >> 4, off = sl & 15;
-        if (static_cast<int>(blockIdx.x) < qk_tiles) {
-          int head, dim;
-          qkv_tile_row(fu, blockIdx.x, l16, &head, &dim);
-          const int i = dim % (fu.hd / 2);
-          double sn, cs;
-          sincos(static_cast<double>(fu.pos[m]) * exp(-(2.0 * i / fu.hd) * log(static_cast<double>(fu.theta))),
-                 &sn, &cs);
-          const float c = static_cast<float>(cs), sv = static_cast<float>(sn);
-          // first half: a cos - b sin; second half: b cos + a sin (a, b = pair)
-          const float o = (l16 < 8) ? v * c - partner * sv : v * c + partner * sv;
-          if (head < fu.Hq)
-            static_cast<bf16_t*>(fu.qout)[(static_cast<size_t>(m) * fu.Hq + head) * fu.hd + dim] = f32_to_bf16(o);
-          else
-            static_cast<bf16_t*>(fu.kpool)[((static_cast<size_t>(page) * fu.Hkv + (head - fu.Hq)) * 16 + off) * fu.hd + dim] =
-                f32_to_bf16(o);
-        } else if (n < N) {
-          const int vi = n - (fu.Hq + fu.Hkv) * fu.hd;
-          const int kh = vi / fu.hd, dd = vi % fu.hd;
-          static_cast<bf16_t*>(fu.vpool)[((static_cast<size_t>(page) * fu.Hkv + kh) * fu.hd + dd) * 16 + off] =
-              f32_to_bf16(v);
-        }
-      }
-    } else if (ok) {
-      const size_t o = static_cast<size_t>(row_map ? row_map[m] : m) * N + n;
-      if (EPI == kEpiStoreF32) static_cast<float*>(Y)[o] = v;
-      if (EPI == kEpiSwiGLU) static_cast<bf16_t*>(Y)[o] = f32_to_bf16(silu(v) * vu);
-    }
+    fused_epilogue<EPI>(fu, m, l16, n0, R, N, v, vu, Y, row_map, qk_tiles);
     return;
   }
   for (int e = threadIdx.x; e < MT * 256; e += blockDim.x) {
@@ -233,6 +250,110 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
       if (EPI == kEpiSwiGLU) static_cast<bf16_t*>(Y)[o] = f32_to_bf16(silu(v) * vu);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 GEMV for 1-2 rows (a single sequence's draft step): vector FMAs, no
+// MFMA.  A workgroup owns 16 features (for SwiGLU their 16 gate and 16 up
+// rows); each wave reads 4 weight rows, 16 lanes per row with 16-byte loads,
+// so every load instruction covers 256 contiguous bytes of each of its rows
+// (the MFMA operand layout can only give 64).  Waves split K in two halves
+// (SwiGLU: gate and up instead); lanes of a row reduce with shuffles, halves
+// through LDS, then the fused epilogue.
+
+constexpr int kGemvRows = 2;  // measured: the MFMA skinny kernel wins from 3 rows on
+
+__device__ __forceinline__ float dot8(const u32x4& w, const u32x4& x) {
+  float a = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    a = fmaf(__uint_as_float(w[j] << 16), __uint_as_float(x[j] << 16), a);
+    a = fmaf(__uint_as_float(w[j] & 0xFFFF0000u), __uint_as_float(x[j] & 0xFFFF0000u), a);
+  }
+  return a;
+}
+
+template <int EPI, int RM>
+__global__ __launch_bounds__(512) void gemv_bf16(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W,
+                                                 void* __restrict__ Y, int R, int N, int K,
+                                                 const int32_t* __restrict__ row_map, const GemmFuse fu) {
+  constexpr bool SW = (EPI == kEpiSwiGLU);
+  constexpr bool QKV = (EPI == kEpiQKVRope);
+  constexpr int KB = 8;  // 128-wide chunks per batch: 8 weight loads in flight per lane
+  __shared__ float part[2][RM][16];  // [K half or gate/up][row][tile column]
+  __shared__ float s_rs[16];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int c = lane & 15, trow = 4 * (wave & 3) + (lane >> 4);
+  const int half = wave >> 2;  // K half, or (SwiGLU) 0 gate / 1 up
+  const int n0 = blockIdx.x * 16;
+  const int qk_tiles = QKV ? (fu.Hq + fu.Hkv) * fu.hd / 16 : 0;
+  int feat = n0 + trow;
+  if (QKV && static_cast<int>(blockIdx.x) < qk_tiles) {
+    int hh, dd;
+    feat = qkv_tile_row(fu, blockIdx.x, trow, &hh, &dd);
+  }
+  const int wrow = (SW && half ? N : 0) + min(feat, N - 1);
+  const bf16_t* wp = W + static_cast<size_t>(wrow) * K + c * 8;
+  const bf16_t* xp[RM];
+#pragma unroll
+  for (int m = 0; m < RM; ++m)
+    xp[m] = X + static_cast<size_t>(m < R ? (fu.xrow ? fu.xrow[m] : m) : 0) * K + c * 8;
+  const int chunks = K / 128;
+  const int per = SW ? chunks : (chunks + 1) / 2;
+  const int c0 = SW ? 0 : half * per, c1 = min(chunks, c0 + per);
+  float a[RM];
+#pragma unroll
+  for (int m = 0; m < RM; ++m) a[m] = 0.f;
+  for (int ch = c0; ch < c1; ch += KB) {
+    u32x4 w[KB], x[KB][RM];
+#pragma unroll
+    for (int b = 0; b < KB; ++b) {
+      const int o = min(ch + b, c1 - 1) * 128;
+      w[b] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wp + o));
+#pragma unroll
+      for (int m = 0; m < RM; ++m)
+        if (m < R) x[b][m] = *reinterpret_cast<const u32x4*>(xp[m] + o);
+    }
+#pragma unroll
+    for (int b = 0; b < KB; ++b) {
+      if (ch + b >= c1) break;
+#pragma unroll
+      for (int m = 0; m < RM; ++m)
+        if (m < R) a[m] += dot8(w[b], x[b][m]);
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < RM; ++m) {
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) a[m] += __shfl_xor(a[m], o, kWave);
+    if (c == 0) part[half][m][trow] = a[m];
+  }
+  if (fu.ss) row_rscale(fu, R, K, s_rs);
+  __syncthreads();
+  if (threadIdx.x >= 256) return;
+  const int e = threadIdx.x, r = (e / kWave) & 3, ln = e & (kWave - 1);
+  const int m = 4 * (ln >> 4) + r, l16 = ln & 15;
+  float v = 0.f, vu = 0.f;
+  if (m < R) {
+    v = SW ? part[0][m][l16] : part[0][m][l16] + part[1][m][l16];
+    if (SW) vu = part[1][m][l16];
+    if (fu.ss) {
+      v *= s_rs[m];
+      vu *= s_rs[m];
+    }
+  }
+  fused_epilogue<EPI>(fu, m, l16, n0, R, N, v, vu, Y, row_map, qk_tiles);
+}
+
+template <int EPI>
+hipError_t gemv(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
+                const int32_t* row_map, const GemmFuse& fu) {
+  const dim3 grid((N + 15) / 16);
+  const bf16_t* x = static_cast<const bf16_t*>(X);
+  const bf16_t* w = static_cast<const bf16_t*>(W);
+  if (R > kGemvRows) return hipErrorInvalidValue;
+  gemv_bf16<EPI, kGemvRows><<<grid, 512, 0, st>>>(x, w, Y, R, N, K, row_map, fu);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -572,6 +693,7 @@ hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W
     return hipGetLastError();
   }
   if (K % 128 != 0) return hipErrorInvalidValue;
+  if (R <= kGemvRows) return gemv<EPI>(R, N, K, X, W, Y, st, rm, GemmFuse{});
   if (use_mfma(R, EPI == kEpiSwiGLU ? 2 * N : N, K)) return mfma<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
   if (R <= 16) return skinny<1, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 32) return skinny<2, EPI>(R, N, K, X, W, Y, st, rm);
@@ -595,6 +717,15 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
   if (R <= 0 || N <= 0) return hipSuccess;
   if (R > 16 || K % 128 != 0 || N % 16 != 0) return hipErrorInvalidValue;
   if (epi == kEpiQKVRope && (f.hd % 16 != 0 || N != (f.Hq + 2 * f.Hkv) * f.hd)) return hipErrorInvalidValue;
+  if (R <= kGemvRows) {
+    switch (epi) {
+      case kEpiStoreF32: return gemv<kEpiStoreF32>(R, N, K, X, W, Y, st, row_map, f);
+      case kEpiAddF32: return gemv<kEpiAddF32>(R, N, K, X, W, Y, st, nullptr, f);
+      case kEpiSwiGLU: return gemv<kEpiSwiGLU>(R, N, K, X, W, Y, st, row_map, f);
+      case kEpiQKVRope: return gemv<kEpiQKVRope>(R, N, K, X, W, Y, st, nullptr, f);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (epi) {
     case kEpiStoreF32: return skinny<1, kEpiStoreF32, true>(R, N, K, X, W, Y, st, row_map, f);
     case kEpiAddF32: return skinny<1, kEpiAddF32, true>(R, N, K, X, W, Y, st, nullptr, f);
@@ -607,6 +738,8 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
 const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused) {
   static const char* fz[4] = {"gemm_skinny_bf16<1, 0, true>", "gemm_skinny_bf16<1, 1, true>",
                               "gemm_skinny_bf16<1, 2, true>", "gemm_skinny_bf16<1, 3, true>"};
+  static const char* gv[4] = {"gemv_bf16<0, 2>", "gemv_bf16<1, 2>", "gemv_bf16<2, 2>", "gemv_bf16<3, 2>"};
+  if (dtype == 1 && R <= kGemvRows) return (epi >= 0 && epi <= 3) ? gv[epi] : "";
   if (fused) return (epi >= 0 && epi <= 3) ? fz[epi] : "";
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
   static const char* tiled[3] = {"gemm_mfma_bf16<0>", "gemm_mfma_bf16<1>", "gemm_mfma_bf16<2>"};

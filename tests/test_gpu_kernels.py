@@ -95,7 +95,8 @@ EPIS = [0, 1, 2]
 @pytest.mark.parametrize("R,N,K", [(1, 48, 128), (6, 200, 256), (16, 64, 384), (17, 100, 128), (33, 130, 256),
                                    (48, 96, 512), (64, 64, 128), (65, 300, 256), (130, 260, 384),
                                    (384, 512, 512), (257, 136, 128), (364, 600, 1024), (129, 257, 640),
-                                   (1, 48, 1024), (6, 200, 2048), (33, 130, 1024), (64, 64, 768)])
+                                   (1, 48, 1024), (6, 200, 2048), (33, 130, 1024), (64, 64, 768),
+                                   (2, 100, 256), (2, 48, 1152)])
 @pytest.mark.parametrize("epi", EPIS)
 @pytest.mark.parametrize("splitk", [True, False])
 def test_gemm_bf16_small(R, N, K, epi, splitk):
