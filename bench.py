@@ -240,7 +240,7 @@ def bench_serving(args):
     import torch
     from paper_2607_20507_amd import binding as B
     from paper_2607_20507_amd.session import DeviceModel, SpecSession
-    from workloads import (SERVING_8B, context_lengths_loguniform, draft_lengths, seq_ids_for,
+    from workloads import (SERVING_8B, context_lengths_loguniform, draft_lengths, mix_draws, seq_ids_for,
                            uniform_prompts)
 
     cfg = SERVING_8B
@@ -265,25 +265,52 @@ def bench_serving(args):
     sess.prefill(ids, prompts)
     stream = torch.cuda.current_stream()
     temps = [T] * n
-    acc_hist, lat = [], []
+    acc_hist, lat, on_clock = [], [], []
+    pend = {ids[i]: int(ctx[i]) - 1 for i in range(n)}  # pending-token position n of each sequence
+    mix = cfg.mix_rate > 0 and not args.no_mix
+    V = cfg.target.vocab
 
     def step(s, record):
+        # Draft mixing (off the clock): before drafting position n + j the
+        # target's top-1 token there comes from the target forward over the
+        # pending token and the drafts so far; with probability mix_rate
+        # (seeded per sequence and position) the draft is guided to it.  Only
+        # the draft steps, the verify and the commit are timed, on the GPU
+        # clock between events.
+        spans = []
         for j in range(1, kmax + 1):
             live = [ids[i] for i in range(n) if ks[i] >= j]
-            sess.draft_step(live, [T] * len(live), cfg.seed + s)
+            if mix:
+                sess.target_forward(live)
+                z = sess.last_logits()
+                top1 = torch.argmax(z.view(len(live), j, V)[:, j - 1, :], dim=1).to(torch.int32).cpu().numpy()
+                pos = [pend[sid] + j for sid in live]
+                guide = np.where(mix_draws(cfg.seed + s, live, pos, cfg.mix_rate), top1, -1).astype(np.int32)
+                torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            if mix:
+                sess.draft_step_guided(live, [T] * len(live), cfg.seed + s, guide, cfg.mix_boost)
+            else:
+                sess.draft_step(live, [T] * len(live), cfg.seed + s)
+            b.record(stream)
+            spans.append((a, b))
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         na, _ = sess.verify(ids, temps, cfg.seed + s)
         sess.commit(ids, na)
         e1.record(stream)
+        spans.append((e0, e1))
+        for i, sid in enumerate(ids):
+            pend[sid] += int(na[i]) + 1
         if record:
             acc_hist.extend(int(x) for x in na)
             lat.append((e0, e1))
+            on_clock.append(spans)
         return int(na.sum()) + n
 
-    for s in range(args.warmup):
-        step(s, False)
     kernel = args.kernel or "gemm_mfma_bf16<2>"
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -296,10 +323,14 @@ def bench_serving(args):
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    event_ms = ev0.elapsed_time(ev1)
+    clock_ms = sum(a.elapsed_time(b) for spans in on_clock for a, b in spans)
     k_ms, k_n, k_bytes, k_flops = roofline_pass(B, sess, kernel, step, args)
     lats = sorted(a.elapsed_time(b) for a, b in lat)
     sess.close()
-    return {"tokens": tokens, "wall_s": wall, "event_ms": ev0.elapsed_time(ev1), "acc_hist": acc_hist,
+    # with mixing, the timed work is the on-clock spans only
+    return {"tokens": tokens, "wall_s": (clock_ms / 1e3) if mix else wall, "event_ms": event_ms,
+            "acc_hist": acc_hist, "mix": mix, "offclock_ms": event_ms - clock_ms if mix else 0.0,
             "verify_ms_median": float(np.median(lats)), "verify_ms_p90": float(np.percentile(lats, 90)),
             "kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops,
             "mean_ctx": float(ctx.mean()), "rows_per_verify": int((ks + 1).sum())}
@@ -392,15 +423,21 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="8b-shaped", choices=["8b-shaped", "8b-serving", "vocab-stress"])
-    ap.add_argument("--temperature", type=float, default=0.8)
+    ap.add_argument("--temperature", type=float, default=None,
+                    help="sampling temperature (default 0.8; 0, greedy, for the serving workload, whose draft "
+                         "mixing fixes top-1 agreement, i.e. the greedy acceptance test)")
     ap.add_argument("--kernel", default=None, help="kernel to time for the roofline (profiler name)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-mix", action="store_true",
+                    help="serving workload without draft mixing (natural acceptance of the random-init pair)")
     ap.add_argument("--roof-steps", type=int, default=4,
                     help="steps after the timed region that run with per-kernel timing (eager launches)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-MiB device buffer --steps times (a plain copy kernel of known "
                          "size, for scaling the profiler's FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
+    if args.temperature is None:
+        args.temperature = 0.0 if args.workload == "8b-serving" else 0.8
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs on one GPU only: sequences shard by data parallelism "
@@ -433,9 +470,11 @@ def main():
     elif args.workload == "8b-serving":
         info = bench_serving(args)
         config = {"workload": "8b-shaped target / 1b-shaped drafter serving 64 sequences, contexts log-uniform "
-                              "[512, 4096] in 16-token pages, k per sequence in {3,5,7}",
+                              "[512, 4096] in 16-token pages, k per sequence in {3,5,7}"
+                              + (", drafts mixed toward the target's top-1 at rate 0.7 (boost 2.0), off the clock"
+                                 if info["mix"] else ", no draft mixing"),
                   "batch": 64, "mean_context": info["mean_ctx"], "rows_per_verify": info["rows_per_verify"],
-                  "temperature": args.temperature}
+                  "temperature": args.temperature, "draft_mixing": info["mix"]}
         bound = "mfma"
     else:
         info = bench_vocab(args)
@@ -471,6 +510,7 @@ def main():
         "verify_ms_median": info["verify_ms_median"], "verify_ms_p90": info["verify_ms_p90"],
         "event_ms_per_step": info["event_ms"] / steps,
         "mean_accepted": float(np.mean(info["acc_hist"])) if info["acc_hist"] else None,
+        "offclock_ms_per_step": info.get("offclock_ms", 0.0) / steps,
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

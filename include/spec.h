@@ -141,6 +141,23 @@ SPEC_API spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_i
 SPEC_API spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
                                      const float* temperature, uint64_t seed, void* stream);
 
+/* spec_draft_step with draft guidance, a workload-shaping hook: for each
+ * sequence i with guide[i] >= 0 (host int32 [n]; -1 = none), the guide
+ * token's draft logit is raised to the row maximum + boost (>= 0) before the
+ * draw, and the raised row is kept as that draft's proposal q (so the rule
+ * stays exact).  Used to give random-init drafters a target-like acceptance
+ * rate: the caller passes the target's top-1 token at that position for a
+ * seeded fraction of the drafts. */
+SPEC_API spec_status spec_draft_step_guided(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
+                                            const float* temperature, uint64_t seed,
+                                            const int32_t* guide, float boost, void* stream);
+
+/* The verify's target forward alone: rows x_n, x~_1..x~_k at positions n..n+k
+ * of each listed sequence (their K/V are written, as the verify that follows
+ * writes them), fp32 logits where spec_last_logits points, no decision pass.
+ * Committed state is unchanged; the drafts stay pending.  Asynchronous. */
+SPEC_API spec_status spec_target_forward(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, void* stream);
+
 /* Replace a sequence's drafts by externally supplied ones: k tokens (host) and
  * their draft logits rows (device fp32 [k, vocab], which must stay alive until
  * the verify has run). */

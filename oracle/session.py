@@ -71,9 +71,13 @@ class Session:
             self.seqs[sid] = st
 
     def draft_step(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int,
-                   margins: rule.Margins = rule.Margins()) -> List[int]:
+                   margins: rule.Margins = rule.Margins(), guide: Sequence[int] = None,
+                   boost: float = 0.0) -> List[int]:
+        """One draft token per sequence.  With guide[i] >= 0 the guide token's
+        logit is first raised to the row maximum + boost (workload shaping: the
+        raised row is the proposal q that the draw and the rule use)."""
         out = []
-        for sid, T in zip(seq_ids, temps):
+        for i, (sid, T) in enumerate(zip(seq_ids, temps)):
             st = self.seqs[int(sid)]
             if st.drafts:
                 toks = [st.drafts[-1]]
@@ -82,6 +86,9 @@ class Session:
             start = st.kv_d.length
             self.pool_d.ensure(int(sid), start + len(toks))
             z = self.draft.forward(st.kv_d, toks, start + np.arange(len(toks)))[-1]
+            if guide is not None and guide[i] >= 0:
+                z = z.copy()
+                z[int(guide[i])] = z.max() + boost
             pos = st.n + len(st.drafts) + 1
             x, bad = rule.sample_draft(z, float(T), seed, int(sid), pos, margins)
             st.drafts.append(x)

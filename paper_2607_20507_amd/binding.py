@@ -74,6 +74,8 @@ SIGNATURES = {
     "spec_seq_info": (c_int32, [_P, c_int64, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, _I32P, c_int32]),
     "spec_last_logits": (c_int32, [_P, POINTER(c_void_p), _I32P]),
     "spec_set_graphs": (c_int32, [_P, c_int32]),
+    "spec_draft_step_guided": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, c_float, _P]),
+    "spec_target_forward": (c_int32, [_P, c_int32, _I64P, _P]),
     "spec_draft_logits": (c_int32, [_P, c_int64, c_int32, _P]),
     "spec_draft_tokens": (c_int32, [_P, c_int64, _P, _P, _P]),
     "spec_timing_enable": (c_int32, [_P, ctypes.c_char_p]),
@@ -192,6 +194,19 @@ def spec_draft_step(ctx: int, seq_ids, temperature, seed: int, stream=None):
     t = _f32(temperature)
     check(lib().spec_draft_step(ctx, len(ids), _ptr(ids, _I64P), _ptr(t, _F32P), seed,
                                 stream_ptr(stream)), ctx)
+
+
+def spec_draft_step_guided(ctx: int, seq_ids, temperature, seed: int, guide, boost: float, stream=None):
+    ids = _i64(seq_ids)
+    t = _f32(temperature)
+    g = np.ascontiguousarray(np.asarray(guide, dtype=np.int32))
+    check(lib().spec_draft_step_guided(ctx, len(ids), _ptr(ids, _I64P), _ptr(t, _F32P), seed, _ptr(g, _I32P),
+                                       float(boost), stream_ptr(stream)), ctx)
+
+
+def spec_target_forward(ctx: int, seq_ids, stream=None):
+    ids = _i64(seq_ids)
+    check(lib().spec_target_forward(ctx, len(ids), _ptr(ids, _I64P), stream_ptr(stream)), ctx)
 
 
 def spec_set_drafts(ctx: int, seq_id: int, tokens, q_logits, stream=None):

@@ -730,8 +730,10 @@ spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const
   return SPEC_OK;
 }
 
-spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
-                            uint64_t seed, void* stream) {
+namespace {
+
+spec_status draft_step_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                            uint64_t seed, const int32_t* guide, float boost, void* stream) {
   CHECK_READY();
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (n < 0 || (n > 0 && (!seq_ids || !temperature))) FAIL(SPEC_E_INVALID, "bad arguments");
@@ -779,6 +781,7 @@ spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
     d.seq_lo = static_cast<uint32_t>(static_cast<uint64_t>(s.id));
     d.seq_hi = static_cast<uint32_t>(static_cast<uint64_t>(s.id) >> 32);
     d.out = qidx;
+    d.guide = guide ? guide[i] : -1;
     dr.push_back(d);
   }
   build_ptab(tabs, f, ctx->max_pages);
@@ -786,11 +789,15 @@ spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
   FwdOff o = add_forward(ctx, D, f, mb);
   const size_t odr = mb.add(dr);
   const size_t osd = mb.add(&seed, 1);
-  std::vector<int64_t> key = {1, n, static_cast<int64_t>(odr), static_cast<int64_t>(osd)};
+  uint32_t boost_bits = 0;
+  std::memcpy(&boost_bits, &boost, sizeof(boost_bits));
+  std::vector<int64_t> key = {1, n, static_cast<int64_t>(odr), static_cast<int64_t>(osd), guide ? 1 : 0,
+                              static_cast<int64_t>(boost_bits)};
   key_forward(key, o);
   spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
     spec_status r = launch_forward(ctx, D, o, dev, dq, ls);
     if (r != SPEC_OK) return r;
+    if (guide) HIPC(launch_draft_guide(n, ctx->V, reinterpret_cast<const DRow*>(dev + odr), boost, ls));
     HIPC(launch_draft_sample(draft_plan(n, ctx->V), reinterpret_cast<const DRow*>(dev + odr), seed,
                              wsptr<int32_t>(ctx, ctx->ws.dtok), ctx->wsp + ctx->ws.draft, ls,
                              reinterpret_cast<const uint64_t*>(dev + osd)));
@@ -807,6 +814,20 @@ spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
     q.k += 1;
   }
   return SPEC_OK;
+}
+
+}  // namespace
+
+spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                            uint64_t seed, void* stream) {
+  return draft_step_impl(ctx, n, seq_ids, temperature, seed, nullptr, 0.f, stream);
+}
+
+spec_status spec_draft_step_guided(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                                   uint64_t seed, const int32_t* guide, float boost, void* stream) {
+  if (ctx && n > 0 && !guide) FAIL(SPEC_E_INVALID, "guide tokens missing");
+  if (ctx && !(boost >= 0.f)) FAIL(SPEC_E_INVALID, "boost must be >= 0");
+  return draft_step_impl(ctx, n, seq_ids, temperature, seed, guide, boost, stream);
 }
 
 spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k, const int32_t* tokens,
@@ -832,11 +853,15 @@ spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k, const int3
   return SPEC_OK;
 }
 
-spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
-                        uint64_t seed, int32_t* n_accepted, int32_t* out_tokens, void* stream) {
+namespace {
+
+// The verify's target forward; with `decide` also the decision pass and the
+// outputs' copy to the host (the verify), else logits only.
+spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                        uint64_t seed, int32_t* n_accepted, int32_t* out_tokens, bool decide, void* stream) {
   CHECK_READY();
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (n < 0 || (n > 0 && (!seq_ids || !temperature || !n_accepted || !out_tokens)))
+  if (n < 0 || (n > 0 && (!seq_ids || (decide && (!temperature || !n_accepted || !out_tokens)))))
     FAIL(SPEC_E_INVALID, "bad arguments");
   if (n == 0) return SPEC_OK;
   if (!check_ids(ctx, n, seq_ids, true)) return SPEC_E_INVALID;
@@ -844,7 +869,7 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   int need = 0;
   for (int i = 0; i < n; ++i) {
     Seq& s = ctx->seqs[seq_ids[i]];
-    if (!(temperature[i] >= 0.f)) FAIL(SPEC_E_INVALID, "temperature must be >= 0");
+    if (decide && !(temperature[i] >= 0.f)) FAIL(SPEC_E_INVALID, "temperature must be >= 0");
     if (s.verified) FAIL(SPEC_E_STATE, "verify twice without commit");
     if (T.pool.pages_for(s.n() + s.k + 1) > ctx->max_pages) FAIL(SPEC_E_INVALID, "sequence exceeds max_pages_per_seq");
     need += T.pool.need(s.pages_t, s.n() + s.k + 1);
@@ -862,7 +887,7 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
     tabs.push_back(&s.pages_t);
     const int row0 = static_cast<int>(f.tok_src.size());
     f.segs.push_back(AttnSegment{i, row0, s.k + 1, nn});
-    const float t = temperature[i];
+    const float t = decide ? temperature[i] : 1.f;
     const float it = t > 0.f ? 1.f / t : 0.f;
     VSeq q{};
     q.k = s.k;
@@ -898,12 +923,12 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   int32_t* d_nacc = wsptr<int32_t>(ctx, ctx->ws.nacc);
   int32_t* d_otok = wsptr<int32_t>(ctx, ctx->ws.otok);
   const VocabPlan vp = vocab_plan(n, static_cast<int>(rows.size()), ctx->V);
-  std::vector<int64_t> key = {0, n, static_cast<int64_t>(rows.size()), static_cast<int64_t>(orow),
+  std::vector<int64_t> key = {decide ? 0 : 2, n, static_cast<int64_t>(rows.size()), static_cast<int64_t>(orow),
                               static_cast<int64_t>(oseq), static_cast<int64_t>(osd)};
   key_forward(key, o);
   spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
     spec_status r = launch_forward(ctx, T, o, dev, logits, ls);
-    if (r != SPEC_OK) return r;
+    if (r != SPEC_OK || !decide) return r;
     HIPC(launch_vocab_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
                            reinterpret_cast<const VSeq*>(dev + oseq), wsptr<int32_t>(ctx, ctx->ws.rowtok),
                            seed, ctx->k_max, d_nacc, d_otok, ctx->wsp + ctx->ws.vocab, ls, &ctx->timer,
@@ -911,6 +936,8 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
     return SPEC_OK;
   });
   if (s != SPEC_OK) return s;
+  ctx->last_rows = R;
+  if (!decide) return SPEC_OK;
   const int W = ctx->k_max + 1;
   HIPC(hipMemcpyAsync(ctx->h_out, d_nacc, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
   HIPC(hipMemcpyAsync(ctx->h_out + ctx->max_seqs, d_otok, sizeof(int32_t) * n * W, hipMemcpyDeviceToHost, st));
@@ -924,9 +951,19 @@ spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
     q.a_ver = n_accepted[i];
     q.emitted.assign(out_tokens + i * W, out_tokens + i * W + q.a_ver + 1);
   }
-  ctx->last_rows = R;
   ctx->timer.flush();
   return SPEC_OK;
+}
+
+}  // namespace
+
+spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                        uint64_t seed, int32_t* n_accepted, int32_t* out_tokens, void* stream) {
+  return verify_impl(ctx, n, seq_ids, temperature, seed, n_accepted, out_tokens, true, stream);
+}
+
+spec_status spec_target_forward(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, void* stream) {
+  return verify_impl(ctx, n, seq_ids, nullptr, 0, nullptr, nullptr, false, stream);
 }
 
 spec_status spec_draft_logits(const spec_ctx* ctx, int64_t seq_id, int32_t j, const float** row) {

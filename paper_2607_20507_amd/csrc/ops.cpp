@@ -130,6 +130,7 @@ spec_status spec_sample_draft(int32_t n, const float* logits, int32_t V, const f
     d.seq_lo = static_cast<uint32_t>(static_cast<uint64_t>(seq_ids[i]));
     d.seq_hi = static_cast<uint32_t>(static_cast<uint64_t>(seq_ids[i]) >> 32);
     d.out = i;
+    d.guide = -1;
     rows[i] = d;
   }
   char* ws = static_cast<char*>(workspace);

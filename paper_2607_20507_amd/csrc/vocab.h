@@ -31,14 +31,15 @@ struct VSeq {
 };
 
 // One row of the draft sampler: its logits, temperature, the absolute position
-// of the token being drawn, the sequence id and where the token is written.
+// of the token being drawn, the sequence id, where the token is written and
+// an optional guide token (-1: none; see launch_draft_guide).
 struct DRow {
   const float* ptr;
   float t;
   int32_t pos;
   uint32_t seq_lo, seq_hi;
   int32_t out;
-  int32_t pad;
+  int32_t guide;
 };
 
 struct VocabPlan {
@@ -63,6 +64,11 @@ struct DraftPlan {
 };
 DraftPlan draft_plan(int n, int V);
 size_t draft_ws_bytes(const DraftPlan& p);
+// Draft guidance (workload shaping, before launch_draft_sample): in each row
+// with guide >= 0 the guide token's logit becomes the row maximum + boost, in
+// place, so the stored row is the proposal the token is drawn from.
+hipError_t launch_draft_guide(int n, int V, const DRow* d_rows, float boost, hipStream_t st);
+
 hipError_t launch_draft_sample(const DraftPlan& p, const DRow* d_rows, uint64_t seed,
                                int32_t* d_tokens, void* d_ws, hipStream_t st,
                                const uint64_t* d_seed = nullptr);

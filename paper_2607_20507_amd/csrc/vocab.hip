@@ -373,6 +373,25 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
   }
 }
 
+// One workgroup per row: row maximum, then the guide token's logit becomes
+// maximum + boost (all reads of the row finish before the write).
+__global__ __launch_bounds__(kThreads) void draft_guide_kernel(int V, const DRow* __restrict__ rows, float boost) {
+  const DRow row = rows[blockIdx.x];
+  if (row.guide < 0 || row.guide >= V) return;
+  const float* z = row.ptr;
+  float mx = -INFINITY;
+  for (int i = threadIdx.x; i < V; i += kThreads) mx = fmaxf(mx, z[i]);
+  mx = wave_max(mx);
+  __shared__ float part[kThreads / kWave];
+  if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float m = part[0];
+    for (int w = 1; w < kThreads / kWave; ++w) m = fmaxf(m, part[w]);
+    const_cast<float*>(z)[row.guide] = m + boost;
+  }
+}
+
 __global__ void draft_final_kernel(const DRow* __restrict__ rows, const VPick* __restrict__ picks,
                                    int n_chunks, int n, int32_t* __restrict__ tokens) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
@@ -475,6 +494,12 @@ hipError_t launch_draft_sample(const DraftPlan& p, const DRow* d_rows, uint64_t 
   else
     draft_kernel<false><<<g, kThreads, 0, st>>>(p.V, d_rows, p.chunk, p.n_chunks, seed, d_seed, picks);
   draft_final_kernel<<<(p.n + 63) / 64, 64, 0, st>>>(d_rows, picks, p.n_chunks, p.n, d_tokens);
+  return hipGetLastError();
+}
+
+hipError_t launch_draft_guide(int n, int V, const DRow* d_rows, float boost, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  draft_guide_kernel<<<n, kThreads, 0, st>>>(V, d_rows, boost);
   return hipGetLastError();
 }
 

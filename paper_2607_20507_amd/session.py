@@ -132,6 +132,12 @@ class SpecSession:
     def draft_step(self, seq_ids, temps, seed: int, stream=None):
         B.spec_draft_step(self.ctx, seq_ids, temps, seed, stream)
 
+    def draft_step_guided(self, seq_ids, temps, seed: int, guide, boost: float, stream=None):
+        B.spec_draft_step_guided(self.ctx, seq_ids, temps, seed, guide, boost, stream)
+
+    def target_forward(self, seq_ids, stream=None):
+        B.spec_target_forward(self.ctx, seq_ids, stream)
+
     def set_drafts(self, seq_id: int, tokens, q_logits, stream=None):
         B.spec_set_drafts(self.ctx, seq_id, tokens, q_logits, stream)
 

@@ -48,7 +48,7 @@ def _compare_state(gpu, ora, sid):
     assert info["pending_pos"] == len(ora.seqs[sid].history) - 1
 
 
-def run_tiny(temps, steps, seed, n_seqs=1, rollback_at=None):
+def run_tiny(temps, steps, seed, n_seqs=1, rollback_at=None, guided=False):
     cfg = TINY_FP32
     k = cfg.k[0]
     gpu, ora = _sessions(cfg, max_seqs=max(2, n_seqs), pages=40)
@@ -67,10 +67,23 @@ def run_tiny(temps, steps, seed, n_seqs=1, rollback_at=None):
         if not live:
             break
         tl = [temps[ids.index(s) % len(temps)] for s in live]
-        for _ in range(k):
-            gpu.draft_step(live, tl, seed + step)
-            ora.draft_step(live, tl, seed + step, margins)
+        for j in range(k):
+            if guided:
+                # seeded guide tokens, half of the drafts guided
+                g = np.random.default_rng([seed, step, j]).integers(0, cfg.target.vocab, size=len(live))
+                g[::2] = -1
+                gpu.draft_step_guided(live, tl, seed + step, g, 2.0)
+                ora.draft_step(live, tl, seed + step, margins, guide=g, boost=2.0)
+            else:
+                gpu.draft_step(live, tl, seed + step)
+                ora.draft_step(live, tl, seed + step, margins)
+        if guided:
+            gpu.target_forward(live)
+            z_pre = gpu.last_logits().cpu().numpy()
         na, ot = gpu.verify(live, tl, seed + step)
+        if guided:
+            assert np.array_equal(z_pre, gpu.last_logits().cpu().numpy()), "target_forward != verify logits"
+
         outs = ora.verify(live, tl, seed + step, margins)
         zg = gpu.last_logits().cpu().numpy()
         r0 = 0
@@ -107,6 +120,14 @@ def run_tiny(temps, steps, seed, n_seqs=1, rollback_at=None):
 def test_tiny_fp32_end_to_end(T):
     st = run_tiny([T], TINY_FP32.steps, seed=2024)
     assert st["steps"] >= 8 and st["excluded"] <= 1
+
+
+def test_tiny_fp32_guided_drafts():
+    """Draft guidance (guide token raised to max + 2 before the draw) on a mixed
+    batch: accepted counts and tokens bit-exact with the oracle, and the target
+    forward alone gives the verify's logits bit for bit."""
+    st = run_tiny([1.0, 0.0, 0.7], 10, seed=99, n_seqs=3, guided=True)
+    assert st["steps"] >= 6
 
 
 def test_tiny_fp32_batch_mixed_with_rollback():

@@ -69,3 +69,29 @@ def test_session_lengths_pages_and_history():
     assert sess.seqs[1].history == [1, 2, 3]
     used = sum(len(v) for v in sess.pool_t.tables.values())
     assert used + len(sess.pool_t.free) == 32
+
+
+def test_guided_draft_row_and_draw():
+    """Draft guidance raises the guide token to max + boost in the kept q row;
+    with a large boost the draw is the guide token, with guide -1 nothing changes."""
+    import numpy as np
+    from oracle.decoder import Decoder
+    from oracle.session import Session
+    from workloads import TINY_FP32, model_weights, uniform_prompts
+    cfg = TINY_FP32
+    tw = model_weights(cfg.target, cfg.seed, 1)
+    dw = model_weights(cfg.draft, cfg.seed, 1)
+    a = Session(Decoder(cfg.target, tw), Decoder(cfg.draft, dw), 64, 64)
+    b = Session(Decoder(cfg.target, tw), Decoder(cfg.draft, dw), 64, 64)
+    prompt = uniform_prompts(3, [20], cfg.target.vocab)[0]
+    a.prefill([1], [prompt])
+    b.prefill([1], [prompt])
+    x_a = a.draft_step([1], [1.0], 5, guide=[17], boost=50.0)
+    x_b = b.draft_step([1], [1.0], 5)
+    assert x_a == [17]
+    za, zb = a.seqs[1].zq[0], b.seqs[1].zq[0]
+    assert za[17] == zb.max() + 50.0
+    assert np.array_equal(np.delete(za, 17), np.delete(zb, 17))
+    c = Session(Decoder(cfg.target, tw), Decoder(cfg.draft, dw), 64, 64)
+    c.prefill([1], [prompt])
+    assert c.draft_step([1], [1.0], 5, guide=[-1], boost=50.0) == x_b

@@ -13,7 +13,7 @@ from .configs import (ModelShape, PairConfig, VocabPassConfig, CONFIGS,
 from .gen import (bf16_round_u16, bf16_u16_to_f32, model_weights,
                   layer_weights, uniform_prompts, prompt_lengths_uniform,
                   context_lengths_loguniform, draft_lengths, vocab_logits,
-                  vocab_temperatures, base_positions, seq_ids_for)
+                  vocab_temperatures, base_positions, seq_ids_for, mix_draws)
 
 __all__ = [
     "ModelShape", "PairConfig", "VocabPassConfig", "CONFIGS", "TINY_FP32",
@@ -21,5 +21,5 @@ __all__ = [
     "bf16_round_u16", "bf16_u16_to_f32", "model_weights", "layer_weights",
     "uniform_prompts", "prompt_lengths_uniform", "context_lengths_loguniform",
     "draft_lengths", "vocab_logits", "vocab_temperatures", "base_positions",
-    "seq_ids_for",
+    "seq_ids_for", "mix_draws",
 ]

@@ -91,6 +91,10 @@ class PairConfig:
     steps: int
     seed: int = 1234
     page_size: int = 16
+    # draft mixing (workload shaping for random-init pairs): the fraction of
+    # drafts guided to the target's top-1 token, and the logit boost
+    mix_rate: float = 0.0
+    mix_boost: float = 2.0
 
 
 @dataclass(frozen=True)
@@ -124,7 +128,7 @@ LLAMA8B_SHAPED = PairConfig("8b-shaped", L8B_TARGET, L1B_DRAFT, batch=1,
                             temperatures=(0.0, 0.8), steps=64)
 SERVING_8B = PairConfig("8b-serving", L8B_TARGET, L1B_DRAFT, batch=64,
                         context=("loguniform", 512, 4096), k=(3, 5, 7),
-                        temperatures=(0.8,), steps=256)
+                        temperatures=(0.8,), steps=256, mix_rate=0.7, mix_boost=2.0)
 VOCAB_STRESS = VocabPassConfig("vocab-stress", batch=256, k=7, vocab=128256,
                                temperatures=(0.3, 1.0, 1.5))
 

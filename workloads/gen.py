@@ -149,3 +149,10 @@ def vocab_temperatures(batch: int, temps: Sequence[float]) -> np.ndarray:
 def base_positions(seed: int, batch: int, lo: int, hi: int) -> np.ndarray:
     """Seeded absolute position n_s of each sequence's pending token, in [lo, hi)."""
     return rng_for(seed, "base-pos").integers(lo, hi, size=batch).astype(np.int32)
+
+
+def mix_draws(seed: int, seq_ids, positions, rate: float) -> np.ndarray:
+    """Bernoulli(rate) per (sequence, drafted position): whether draft mixing
+    guides that draft to the target's top-1 token (workload shaping)."""
+    return np.array([rng_for(seed, "mix", int(s), int(p)).random() < rate
+                     for s, p in zip(seq_ids, positions)], dtype=bool)
