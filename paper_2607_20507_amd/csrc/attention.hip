@@ -27,6 +27,7 @@ namespace spec {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kAttnStagedPages = 256;  // page ids of one work item kept in LDS (4096 keys)
 
 __device__ __forceinline__ uint32_t mask_pair(uint32_t w, int valid) {
   // keep the first `valid` (0, 1, 2) bf16 halves of a 32-bit word
@@ -47,6 +48,17 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
   const bf16_t* kp = static_cast<const bf16_t*>(a.kpool);
   const bf16_t* vp = static_cast<const bf16_t*>(a.vpool);
   const int32_t* pt = a.page_table + static_cast<size_t>(it.seq) * a.max_pages;
+  // the item's page ids, staged once in LDS so that no chunk waits on a
+  // page-table load before its K / V loads can go out (items spanning more
+  // pages than the stage holds read the table directly)
+  __shared__ int32_t s_pt[kAttnStagedPages];
+  const int p0 = it.t0 >> 4;
+  const int np = it.t1 > it.t0 ? ((it.t1 - 1) >> 4) - p0 + 1 : 0;
+  const bool staged = np <= kAttnStagedPages;
+  if (staged)
+    for (int i = lane; i < np; i += kWave) s_pt[i] = pt[p0 + i];
+  __syncthreads();
+  auto page = [&](int t) { return staged ? s_pt[(t >> 4) - p0] : pt[t >> 4]; };
 
   uint4 qf[NT][DS];
   int vpos[NT];
@@ -81,12 +93,12 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
     for (int hh = 0; hh < 2; ++hh) {
       const int t = min(c0 + 8 * (l16 >> 2) + 4 * hh + (l16 & 3), it.t1 - 1);
       const bf16_t* kb =
-          kp + (static_cast<size_t>(pt[t >> 4] * a.Hkv + gkv) * 16 + (t & 15)) * HD + g * 8;
+          kp + (static_cast<size_t>(page(t) * a.Hkv + gkv) * 16 + (t & 15)) * HD + g * 8;
 #pragma unroll
       for (int s = 0; s < DS; ++s) kf[hh][s] = ld_stream(reinterpret_cast<const uint4*>(kb) + 4 * s);
     }
     const int tvc = min(c0 + 8 * g, it.t1 - 1);
-    const bf16_t* vb = vp + static_cast<size_t>(pt[tvc >> 4] * a.Hkv + gkv) * HD * 16 + (tvc & 8);
+    const bf16_t* vb = vp + static_cast<size_t>(page(tvc) * a.Hkv + gkv) * HD * 16 + (tvc & 8);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) vf[dt] = ld_stream(reinterpret_cast<const uint4*>(vb + (16 * dt + l16) * 16));
   };
