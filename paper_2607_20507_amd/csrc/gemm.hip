@@ -22,6 +22,8 @@
 //    reduced-precision arithmetic.
 
 #include <algorithm>
+#include <cstdio>
+#include <mutex>
 
 #include "common.h"
 #include "gemm.h"
@@ -67,14 +69,15 @@ __device__ __forceinline__ void row_rscale(const GemmFuse& fu, int R, int K, flo
 }
 
 // Epilogue of the fused GEMMs for output row m (< 16) and tile column l16 of
-// the 16-feature tile at n0, given the (row-scaled) dot products v (and vu,
+// 16-feature tile `tile`, given the (row-scaled) dot products v (and vu,
 // the up rows of SwiGLU).  Run by whole waves: threads 0..255 with
 // m = 4 (lane / 16) + r, so the 16 lanes of a group hold the 16 columns of a
 // row and exchange values with shuffles.
 template <int EPI>
-__device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l16, int n0, int R, int N,
+__device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l16, int tile, int R, int N,
                                                float v, float vu, void* __restrict__ Y,
                                                const int32_t* __restrict__ row_map, int qk_tiles) {
+  const int n0 = tile * 16;
   constexpr bool QKV = (EPI == kEpiQKVRope);
   const int n = n0 + l16;
   const bool ok = m < R && n < N;
@@ -92,16 +95,16 @@ __device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l1
       float sq = hn * hn;
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o, kWave);
-      if (l16 == 0 && m < R) fu.ss_out[static_cast<size_t>(m) * (N / 16) + n0 / 16] = sq;
+      if (l16 == 0 && m < R && n0 < N) fu.ss_out[static_cast<size_t>(m) * (N / 16) + n0 / 16] = sq;
     }
   } else if (QKV) {
     const float partner = __shfl_xor(v, 8, kWave);
     if (m < R) {
       const int sl = fu.slot[m];
       const int page = sl >> 4, off = sl & 15;
-      if (static_cast<int>(blockIdx.x) < qk_tiles) {
+      if (tile < qk_tiles) {
         int head, dim;
-        qkv_tile_row(fu, blockIdx.x, l16, &head, &dim);
+        qkv_tile_row(fu, tile, l16, &head, &dim);
         const int i = dim % (fu.hd / 2);
         double sn, cs;
         sincos(static_cast<double>(fu.pos[m]) * exp(-(2.0 * i / fu.hd) * log(static_cast<double>(fu.theta))),
@@ -128,34 +131,39 @@ __device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l1
   }
 }
 
-template <int MT, int EPI, bool FUSE>
+template <int MT, int NT, int EPI, bool FUSE>
 __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, void* __restrict__ Y, int R, int N,
     int K, int kb_per_wave, const int32_t* __restrict__ row_map, const GemmFuse fu) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
   constexpr bool QKV = (EPI == kEpiQKVRope);
-  constexpr int NACC = MT * (SW ? 2 : 1);
+  constexpr int NS = SW ? 2 : 1;  // weight streams: gate and up rows for SwiGLU
+  constexpr int NACC = MT * NT * NS;
   static_assert(!FUSE || MT == 1, "the fused path covers up to 16 rows");
   static_assert(FUSE || !QKV, "the QKV epilogue is fused only");
-  __shared__ float red[kSkinnyMaxWaves * NACC * 256];
+  extern __shared__ float red[];  // [waves][NACC][4][64]
   __shared__ float s_rs[16];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int nw = blockDim.x / kWave;
   const int row = lane & 15, g = lane >> 4;
-  const int n0 = blockIdx.x * 16;
+  const int tile0 = blockIdx.x * NT;
   const int qk_tiles = QKV ? (fu.Hq + fu.Hkv) * fu.hd / 16 : 0;
-  int feat = n0 + row;
-  if (QKV && static_cast<int>(blockIdx.x) < qk_tiles) {
-    int hh, dd;
-    feat = qkv_tile_row(fu, blockIdx.x, row, &hh, &dd);
-  }
-  const int nrow = min(feat, N - 1);
   // lane group g, step s carries k = 32 s + 8 g .. +7 of each 128-wide block:
   // the four lanes of a row read one contiguous 64-byte run per load
-  const bf16_t* wg = W + static_cast<size_t>(nrow) * K + g * 8;
-  const bf16_t* wu = SW ? W + static_cast<size_t>(N + nrow) * K + g * 8 : nullptr;
+  const bf16_t* wp[NT][NS];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    int feat = (tile0 + j) * 16 + row;
+    if (QKV && tile0 + j < qk_tiles) {
+      int hh, dd;
+      feat = qkv_tile_row(fu, tile0 + j, row, &hh, &dd);
+    }
+    const int nrow = min(feat, N - 1);
+    wp[j][0] = W + static_cast<size_t>(nrow) * K + g * 8;
+    if (SW) wp[j][NS - 1] = W + static_cast<size_t>(N + nrow) * K + g * 8;
+  }
   const bf16_t* xr[MT];
   bool xv[MT];
 #pragma unroll
@@ -166,28 +174,30 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     xr[mt] = X + static_cast<size_t>(src) * K + g * 8;
   }
   if (FUSE && fu.ss) row_rscale(fu, R, K, s_rs);
-  f32x4 acc[MT], accu[MT];
+  f32x4 acc[MT][NT][NS];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    accu[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int h = 0; h < NS; ++h) acc[mt][j][h] = f32x4{0.f, 0.f, 0.f, 0.f};
   // KB 128-wide blocks per iteration, every load of the iteration issued
-  // before its first MFMA (fewer blocks for larger M to bound registers)
-  constexpr int KB = MT == 1 ? 4 : (MT == 2 ? 2 : 1);
+  // before its first MFMA; each X fragment feeds NT x NS weight tiles
+  constexpr int KB = (NT * NS * MT >= 4) ? 1 : ((NT * NS * MT >= 2) ? 2 : 4);
   const int nb = K / 128;
   const int kb0 = wave * kb_per_wave;
   const int kb1 = min(nb, kb0 + kb_per_wave);
   for (int kb = kb0; kb < kb1; kb += KB) {
-    uint4 w[KB][4], u[KB][4], x[KB][MT][4];
+    uint4 w[KB][NT][NS][4], x[KB][MT][4];
 #pragma unroll
     for (int b = 0; b < KB; ++b) {
       const int ko = (kb + b < kb1 ? kb + b : kb) * 128;
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        w[b][s] = ld_stream(reinterpret_cast<const uint4*>(wg + ko) + 4 * s);
-        if (SW) u[b][s] = ld_stream(reinterpret_cast<const uint4*>(wu + ko) + 4 * s);
-      }
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int h = 0; h < NS; ++h)
+#pragma unroll
+          for (int s = 0; s < 4; ++s) w[b][j][h][s] = ld_stream(reinterpret_cast<const uint4*>(wp[j][h] + ko) + 4 * s);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -200,49 +210,46 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          acc[mt] = mfma16x16x32(x[b][mt][s], w[b][s], acc[mt]);
-          if (SW) accu[mt] = mfma16x16x32(x[b][mt][s], u[b][s], accu[mt]);
-        }
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int h = 0; h < NS; ++h) acc[mt][j][h] = mfma16x16x32(x[b][mt][s], w[b][j][h][s], acc[mt][j][h]);
     }
   }
-  // red[wave][a][r][lane]
+  // red[wave][(mt, j, h)][r][lane]
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      red[((wave * NACC + mt) * 4 + r) * kWave + lane] = acc[mt][r];
-      if (SW) red[((wave * NACC + MT + mt) * 4 + r) * kWave + lane] = accu[mt][r];
-    }
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int h = 0; h < NS; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          red[((wave * NACC + (mt * NT + j) * NS + h) * 4 + r) * kWave + lane] = acc[mt][j][h][r];
   __syncthreads();
-  if (FUSE) {
-    // one element per thread of waves 0..3; whole waves take part in the
-    // 16-lane exchanges below (lanes of a group hold the 16 columns of a row)
-    if (threadIdx.x >= 256) return;
-    const int e = threadIdx.x, r = (e / kWave) & 3, ln = e & (kWave - 1);
-    const int m = 4 * (ln >> 4) + r, l16 = ln & 15;
+  // element e: accumulator set e / 256 = (mt, j), output row m = 16 mt +
+  // 4 (lane / 16) + r, column l16 of tile tile0 + j.  Whole waves take the
+  // same (mt, j), as the fused epilogue's 16-lane exchanges need.
+  for (int e = threadIdx.x; e < MT * NT * 256; e += blockDim.x) {
+    const int set = e / 256, r = (e / kWave) & 3, ln = e & (kWave - 1);
+    const int mt = set / NT, j = set % NT;
+    const int m = mt * 16 + 4 * (ln >> 4) + r, l16 = ln & 15;
     float v = 0.f, vu = 0.f;
     for (int wv = 0; wv < nw; ++wv) {
-      v += red[((wv * NACC) * 4 + r) * kWave + ln];
-      if (SW) vu += red[((wv * NACC + 1) * 4 + r) * kWave + ln];
+      v += red[((wv * NACC + set * NS) * 4 + r) * kWave + ln];
+      if (SW) vu += red[((wv * NACC + set * NS + 1) * 4 + r) * kWave + ln];
     }
-    if (fu.ss) {
-      const float rs = s_rs[m];
-      v *= rs;
-      vu *= rs;
+    if (FUSE) {
+      if (fu.ss) {
+        const float rs = s_rs[m];
+        v *= rs;
+        vu *= rs;
+      }
+      fused_epilogue<EPI>(fu, m, l16, tile0 + j, R, N, v, vu, Y, row_map, qk_tiles);
+      continue;
     }
-    fused_epilogue<EPI>(fu, m, l16, n0, R, N, v, vu, Y, row_map, qk_tiles);
-    return;
-  }
-  for (int e = threadIdx.x; e < MT * 256; e += blockDim.x) {
-    const int mt = e / 256, r = (e / kWave) & 3, ln = e & (kWave - 1);
-    const int m = mt * 16 + 4 * (ln >> 4) + r;
-    const int n = n0 + (ln & 15);
-    float v = 0.f, vu = 0.f;
-    for (int wv = 0; wv < nw; ++wv) {
-      v += red[((wv * NACC + mt) * 4 + r) * kWave + ln];
-      if (SW) vu += red[((wv * NACC + MT + mt) * 4 + r) * kWave + ln];
-    }
+    const int n = (tile0 + j) * 16 + l16;
     if (m < R && n < N) {
       const size_t o = static_cast<size_t>(row_map ? row_map[m] : m) * N + n;
       if (EPI == kEpiStoreF32) static_cast<float*>(Y)[o] = v;
@@ -342,7 +349,7 @@ __global__ __launch_bounds__(512) void gemv_bf16(const bf16_t* __restrict__ X, c
       vu *= s_rs[m];
     }
   }
-  fused_epilogue<EPI>(fu, m, l16, n0, R, N, v, vu, Y, row_map, qk_tiles);
+  fused_epilogue<EPI>(fu, m, l16, blockIdx.x, R, N, v, vu, Y, row_map, qk_tiles);
 }
 
 template <int EPI>
@@ -618,20 +625,46 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X,
   }
 }
 
+template <int MT, int NT, int EPI, bool FUSE>
+hipError_t skinny_nt(int nw, int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
+                     const int32_t* row_map, const GemmFuse& fu) {
+  constexpr int NACC = MT * NT * (EPI == kEpiSwiGLU ? 2 : 1);
+  const int groups = ((N + 15) / 16 + NT - 1) / NT;
+  const int nb = K / 128;
+  nw = std::max(FUSE ? 4 : 1, std::min(nw, nb));
+  if (FUSE && nw < 4) return hipErrorInvalidValue;  // the fused epilogue needs 256 threads
+  const int kbpw = (nb + nw - 1) / nw;
+  const size_t lds = static_cast<size_t>(nw) * NACC * 256 * sizeof(float);
+  gemm_skinny_bf16<MT, NT, EPI, FUSE><<<groups, nw * kWave, lds, st>>>(
+      static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map, fu);
+  return hipGetLastError();
+}
+
+// Feature tiles per workgroup and waves per workgroup of the skinny kernel,
+// measured at 6..64 rows on the projections of the 8B/1B-shaped pair: several
+// tiles per workgroup share each X fragment load (the L2 traffic of X limits
+// the wide LM head and gate/up), but cost parallelism on narrow projections;
+// 8 waves split K when there are few workgroups and K is mid-sized.
+int skinny_tiles_per_wg(int MT, int N, bool sw) {
+  const int tiles = (N + 15) / 16;
+  int nt = sw ? (tiles >= 768 ? 4 : 1) : (tiles >= 2048 ? 4 : (tiles >= 384 ? 2 : 1));
+  while (nt > 1 && MT * nt * (sw ? 2 : 1) > 8) nt /= 2;  // bounds registers
+  return nt;
+}
+
+int skinny_waves(int groups, int K) { return (groups <= 256 && K >= 4096 && K < 12288) ? 8 : 4; }
+
 template <int MT, int EPI, bool FUSE = false>
 hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
                   const int32_t* row_map, const GemmFuse& fu = GemmFuse{}) {
-  const int tiles = (N + 15) / 16;
-  const int nb = K / 128;
-  // waves per workgroup split K: 8 when there are few feature tiles (and K is
-  // not long enough to keep 4 waves busy), else 4 (measured at the verify and
-  // draft shapes of the 8B/1B-shaped pair)
-  int nw = (tiles <= 256 && K < 12288) ? 8 : 4;
-  nw = std::max(FUSE ? 4 : 1, std::min(nw, nb));
-  const int kbpw = (nb + nw - 1) / nw;
-  gemm_skinny_bf16<MT, EPI, FUSE><<<tiles, nw * kWave, 0, st>>>(
-      static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map, fu);
-  return hipGetLastError();
+  constexpr bool SW = (EPI == kEpiSwiGLU);
+  const int nt = skinny_tiles_per_wg(MT, N, SW);
+  const int nw = skinny_waves(((N + 15) / 16 + nt - 1) / nt, K);
+  if (nt == 4 && MT * 4 * (SW ? 2 : 1) <= 8)
+    return skinny_nt<MT, (MT * 4 * (SW ? 2 : 1) <= 8 ? 4 : 1), EPI, FUSE>(nw, R, N, K, X, W, Y, st, row_map, fu);
+  if (nt == 2 && MT * 2 * (SW ? 2 : 1) <= 8)
+    return skinny_nt<MT, (MT * 2 * (SW ? 2 : 1) <= 8 ? 2 : 1), EPI, FUSE>(nw, R, N, K, X, W, Y, st, row_map, fu);
+  return skinny_nt<MT, 1, EPI, FUSE>(nw, R, N, K, X, W, Y, st, row_map, fu);
 }
 
 // Split-K factor for the MFMA kernel: grids under 256 tiles are split so that
@@ -736,22 +769,31 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
 }
 
 const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused) {
-  static const char* fz[4] = {"gemm_skinny_bf16<1, 0, true>", "gemm_skinny_bf16<1, 1, true>",
-                              "gemm_skinny_bf16<1, 2, true>", "gemm_skinny_bf16<1, 3, true>"};
   static const char* gv[4] = {"gemv_bf16<0, 2>", "gemv_bf16<1, 2>", "gemv_bf16<2, 2>", "gemv_bf16<3, 2>"};
   if (dtype == 1 && R <= kGemvRows) return (epi >= 0 && epi <= 3) ? gv[epi] : "";
-  if (fused) return (epi >= 0 && epi <= 3) ? fz[epi] : "";
+  // skinny names [MT - 1][log2 NT][epi][fused]
+  static char names[4][3][4][2][48];
+  static std::once_flag once;
+  std::call_once(once, [] {
+    for (int mt = 0; mt < 4; ++mt)
+      for (int t = 0; t < 3; ++t)
+        for (int e = 0; e < 4; ++e)
+          for (int f = 0; f < 2; ++f)
+            snprintf(names[mt][t][e][f], sizeof(names[mt][t][e][f]), "gemm_skinny_bf16<%d, %d, %d, %s>", mt + 1,
+                     1 << t, e, f ? "true" : "false");
+  });
+  auto skinny_name = [&](int MT, bool f) {
+    const int nt = skinny_tiles_per_wg(MT, N, epi == kEpiSwiGLU);
+    return names[MT - 1][nt == 4 ? 2 : (nt == 2 ? 1 : 0)][epi][f ? 1 : 0];
+  };
+  if (epi < 0 || epi > 3) return "";
+  if (fused) return skinny_name(1, true);
+  if (epi > 2) return "";
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
   static const char* tiled[3] = {"gemm_mfma_bf16<0>", "gemm_mfma_bf16<1>", "gemm_mfma_bf16<2>"};
-  static const char* skinny[4][3] = {
-      {"gemm_skinny_bf16<1, 0, false>", "gemm_skinny_bf16<1, 1, false>", "gemm_skinny_bf16<1, 2, false>"},
-      {"gemm_skinny_bf16<2, 0, false>", "gemm_skinny_bf16<2, 1, false>", "gemm_skinny_bf16<2, 2, false>"},
-      {"gemm_skinny_bf16<3, 0, false>", "gemm_skinny_bf16<3, 1, false>", "gemm_skinny_bf16<3, 2, false>"},
-      {"gemm_skinny_bf16<4, 0, false>", "gemm_skinny_bf16<4, 1, false>", "gemm_skinny_bf16<4, 2, false>"}};
-  if (epi < 0 || epi > 2) return "";
   if (dtype == 0) return f32[epi];
   if (use_mfma(R, epi == kEpiSwiGLU ? 2 * N : N, K)) return tiled[epi];
-  return skinny[(std::max(R, 1) - 1) / 16][epi];
+  return skinny_name((std::max(R, 1) - 1) / 16 + 1, false);
 }
 
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
