@@ -146,7 +146,7 @@ def bench_8b(args):
 
     for s in range(args.warmup):
         step(s, False)
-    kernel = args.kernel or "gemm_skinny_bf16<1, 4, 2, true>"
+    kernel = args.kernel or "gemm_skinny_bf16<1, 2, true>"
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0 = torch.cuda.Event(enable_timing=True)

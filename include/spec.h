@@ -58,10 +58,13 @@ enum {
 };
 
 enum { SPEC_F32 = 0, SPEC_BF16 = 1 };
+enum { SPEC_LAYOUT_ROWMAJOR = 0, SPEC_LAYOUT_TILED = 1 };
 enum { SPEC_DRAFT = 0, SPEC_ACCEPT = 1, SPEC_RESAMPLE = 2, SPEC_BONUS = 3 };
 
 /* One decoder layer's weights (device pointers, element type = model dtype,
- * row-major with the reduction dimension innermost):
+ * reduction dimension innermost; the projections wqkv, wo, w_gate_up and
+ * w_down are row-major for fp32 models and in the tiled layout of
+ * spec_pack_model for bf16 models, the norms are plain vectors):
  *   attn_norm, mlp_norm  [d]
  *   wqkv       [(Hq + 2*Hkv) * hd, d]   rows: q heads, then k heads, then v heads
  *   wo         [d, Hq * hd]
@@ -85,9 +88,27 @@ typedef struct spec_model_desc {
   float rope_theta, rms_eps;
   const void* embed;      /* device [vocab, d] */
   const void* final_norm; /* device [d] */
-  const void* lm_head;    /* device [vocab, d] */
+  const void* lm_head;    /* device [vocab, d] (a projection: tiled for bf16) */
   const spec_layer_weights* layers; /* host array [n_layers]; copied by spec_ctx_create */
+  int32_t weight_layout;  /* SPEC_LAYOUT_ROWMAJOR (fp32 models) or SPEC_LAYOUT_TILED
+                             (bf16 models, set by spec_pack_model); checked by spec_ctx_create */
 } spec_model_desc;
+
+/* Convert the projection weights of a bf16 model in place from row-major to
+ * the tiled layout that the bf16 kernels stream, and set m->weight_layout to
+ * SPEC_LAYOUT_TILED.  Requires m->weight_layout == SPEC_LAYOUT_ROWMAJOR
+ * (SPEC_E_STATE otherwise: converting twice would scramble the weights) and
+ * d_model, ffn_dim and n_heads * head_dim multiples of 128, head_dim % 16 == 0
+ * (SPEC_E_UNSUPPORTED).  Weights shared by two descriptors are converted
+ * once.  The layout, per matrix W [N, K]: in every complete group of 16 rows
+ * and block of 128 columns, the 16 x 16 matrix of 16-byte chunks is
+ * transposed (chunk j of row r moves to row j, chunk position r); a trailing
+ * group of fewer than 16 rows stays row-major; wqkv's q and k heads are first
+ * reordered inside each head so that rows 8t..8t+7 and hd/2+8t..hd/2+8t+7
+ * (rotary pairs) form tile t; w_gate_up is converted as two [ffn, d]
+ * matrices.  Asynchronous on `stream`; fp32 models are left unchanged
+ * (SPEC_OK, layout stays row-major). */
+SPEC_API spec_status spec_pack_model(spec_model_desc* m, void* stream);
 
 /* Paged KV cache.  Each pool holds, per layer, K pages [page][Hkv][16][hd] and
  * V pages stored transposed [page][Hkv][hd][16], element type = model dtype;

@@ -16,9 +16,19 @@ extern "C" {
 
 enum { SPEC_EPI_STORE_F32 = 0, SPEC_EPI_ADD_F32 = 1, SPEC_EPI_SWIGLU = 2 };
 
+/* One bf16 weight [rows, K] (device) from row-major to the tiled layout, in
+ * place (the per-matrix step of spec_pack_model; K % 128 == 0, else
+ * SPEC_E_UNSUPPORTED).  rot_rows > 0 marks the first rot_rows rows as rotary
+ * heads of head_dim rows (head_dim % 16 == 0, rot_rows % head_dim == 0),
+ * reordered as wqkv's q and k heads are.  Asynchronous. */
+SPEC_API spec_status spec_pack_weight(void* w, int32_t rows, int32_t K, int32_t rot_rows,
+                                      int32_t head_dim, void* stream);
+
 /* Decoder projection Y = X W^T (the QKV, O, gate/up, down and LM-head
- * products of the Llama layer).  X device [R, K], W device [N, K] (SwiGLU: [2N, K],
- * gate rows then up rows), element type dtype; fp32 accumulation.
+ * products of the Llama layer).  X device [R, K] row-major, W device [N, K]
+ * (SwiGLU: [2N, K], gate rows then up rows), element type dtype; fp32
+ * accumulation.  fp32 W is row-major; bf16 W is in the tiled layout
+ * (spec_pack_weight; for SwiGLU the gate and up halves packed separately).
  *   SPEC_EPI_STORE_F32: Y fp32 [R, N] = X W^T
  *   SPEC_EPI_ADD_F32:   Y fp32 [R, N] += X W^T   (residual add)
  *   SPEC_EPI_SWIGLU:    Y dtype [R, N] = silu(X Wg^T) * (X Wu^T)

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libspecverify.so")
 
 SPEC_OK, SPEC_E_INVALID, SPEC_E_NOPAGES, SPEC_E_HIP, SPEC_E_STATE, SPEC_E_UNSUPPORTED = range(6)
 SPEC_F32, SPEC_BF16 = 0, 1
+SPEC_LAYOUT_ROWMAJOR, SPEC_LAYOUT_TILED = 0, 1
 SPEC_DRAFT, SPEC_ACCEPT, SPEC_RESAMPLE, SPEC_BONUS = range(4)
 SPEC_EPI_STORE_F32, SPEC_EPI_ADD_F32, SPEC_EPI_SWIGLU = range(3)
 
@@ -41,7 +42,8 @@ class spec_model_desc(ctypes.Structure):
                 ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
                 ("vocab", c_int32), ("dtype", c_int32), ("rope_theta", c_float),
                 ("rms_eps", c_float), ("embed", c_void_p), ("final_norm", c_void_p),
-                ("lm_head", c_void_p), ("layers", POINTER(spec_layer_weights))]
+                ("lm_head", c_void_p), ("layers", POINTER(spec_layer_weights)),
+                ("weight_layout", c_int32)]
 
 
 class spec_cache_desc(ctypes.Structure):
@@ -87,6 +89,8 @@ SIGNATURES = {
     "spec_sample_draft": (c_int32, [c_int32, _P, c_int32, _F32P, _I64P, _I32P, c_uint64, _P, _P,
                                     c_size_t, _P]),
     "spec_philox_uniform": (c_int32, [c_uint64, c_int64, c_int32, c_int32, c_int32, _P, _P]),
+    "spec_pack_model": (c_int32, [POINTER(spec_model_desc), _P]),
+    "spec_pack_weight": (c_int32, [_P, c_int32, c_int32, c_int32, c_int32, _P]),
     "spec_op_gemm_workspace_bytes": (c_size_t, [c_int32, c_int32]),
     "spec_op_gemm": (c_int32, [c_int32, c_int32, c_int32, c_int32, _P, _P, _P, c_int32, _P, c_size_t, _P]),
     "spec_op_rmsnorm": (c_int32, [c_int32, c_int32, c_int32, _P, _P, c_float, _P, _P]),
@@ -317,6 +321,14 @@ def spec_sample_draft(logits, V: int, temperature, seq_ids, pos, seed: int, toke
 
 def spec_philox_uniform(seed: int, seq_id: int, pos: int, purpose: int, n: int, out, stream=None):
     check(lib().spec_philox_uniform(seed, int(seq_id), pos, purpose, n, dptr(out), stream_ptr(stream)))
+
+
+def spec_pack_model(desc: spec_model_desc, stream=None) -> None:
+    check(lib().spec_pack_model(ctypes.byref(desc), stream_ptr(stream)))
+
+
+def spec_pack_weight(w, rows: int, K: int, rot_rows: int = 0, head_dim: int = 0, stream=None) -> None:
+    check(lib().spec_pack_weight(dptr(w), rows, K, rot_rows, head_dim, stream_ptr(stream)))
 
 
 def spec_op_gemm_workspace_bytes(R: int, Nw: int) -> int:

@@ -110,6 +110,11 @@ bool valid_model(const spec_model_desc* m, std::string& why) {
       m->head_dim <= 0 || m->ffn_dim <= 0 || m->vocab <= 0) { why = "non-positive model size"; return false; }
   if (m->n_heads % m->n_kv_heads != 0) { why = "n_heads must be a multiple of n_kv_heads"; return false; }
   if (m->dtype != SPEC_F32 && m->dtype != SPEC_BF16) { why = "dtype must be SPEC_F32 or SPEC_BF16"; return false; }
+  if (m->weight_layout != (m->dtype == SPEC_BF16 ? SPEC_LAYOUT_TILED : SPEC_LAYOUT_ROWMAJOR)) {
+    why = m->dtype == SPEC_BF16 ? "bf16 weights must be in the tiled layout (spec_pack_model)"
+                                : "fp32 weights must be row-major";
+    return false;
+  }
   if (!m->embed || !m->final_norm || !m->lm_head || !m->layers) { why = "null weight pointer"; return false; }
   for (int l = 0; l < m->n_layers; ++l) {
     const auto& L = m->layers[l];
@@ -357,7 +362,7 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
       HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
       HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr));
       HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, qkv, I(o.pos),
-                          I(o.slot), q, M.kl(l), M.vl(l), st));
+                          I(o.slot), q, M.kl(l), M.vl(l), st, dt == 1));
     }
     a.kpool = M.kl(l);
     a.vpool = M.vl(l);

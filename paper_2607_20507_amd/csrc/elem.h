@@ -21,9 +21,13 @@ hipError_t launch_rmsnorm(int dtype, int R, int d, const float* h, const int32_t
 // From qkv fp32 [R, (Hq + 2 Hkv) hd]: q <- RoPE(q) [R, Hq, hd]; K page slot
 // slot[r] <- RoPE(k); V^T page slot <- v.  Rotate-half pairs (i, i + hd/2)
 // at angle pos[r] * theta^(-2i/hd), angles and sin/cos evaluated in fp64.
+// rot_tiled: the q and k head columns of qkv are in the rotary tile order of
+// the tiled QKV weight (what the bf16 GEMMs produce from it): position
+// 16 (i / 8) + i % 8 holds dim i, and the position 8 further holds dim
+// i + hd / 2 (i < hd / 2); v columns are in plain order.
 hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta, const float* qkv,
                           const int32_t* pos, const int32_t* slot, void* q, void* kpool,
-                          void* vpool, hipStream_t st);
+                          void* vpool, hipStream_t st, bool rot_tiled = false);
 
 // Zero the K and V entries of `n` flat slots in every layer of a pool whose
 // layer l holds K at kv + l * layer_stride and V at + v_off (elements).

@@ -68,7 +68,7 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
                                                       const int32_t* __restrict__ pos,
                                                       const int32_t* __restrict__ slot,
                                                       T* __restrict__ q, T* __restrict__ kpool,
-                                                      T* __restrict__ vpool) {
+                                                      T* __restrict__ vpool, bool rot_tiled) {
   const int r = blockIdx.x;
   const int half = hd / 2;
   const int width = (Hq + 2 * Hkv) * hd;
@@ -82,8 +82,12 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
     double sn, cs;
     sincos(p * exp(-(2.0 * i / hd) * lt), &sn, &cs);
     const float c = static_cast<float>(cs), s = static_cast<float>(sn);
+    // rot_tiled: the q and k columns of each head are in the rotary tile
+    // order of the tiled QKV weight (rows 8t..8t+7, then hd/2+8t.. of tile t)
     const float* src = x + head * hd;
-    const float a = src[i], b = src[i + half];
+    const int ia = rot_tiled ? 16 * (i / 8) + (i % 8) : i;
+    const int ib = rot_tiled ? ia + 8 : i + half;
+    const float a = src[ia], b = src[ib];
     const float ra = a * c - b * s, rb = b * c + a * s;
     if (head < Hq) {
       T* o = q + (static_cast<size_t>(r) * Hq + head) * hd;
@@ -148,15 +152,16 @@ hipError_t launch_rmsnorm(int dtype, int R, int d, const float* h, const int32_t
 
 hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta, const float* qkv,
                           const int32_t* pos, const int32_t* slot, void* q, void* kpool,
-                          void* vpool, hipStream_t st) {
+                          void* vpool, hipStream_t st, bool rot_tiled) {
   if (R <= 0) return hipSuccess;
-  if (hd % 2 != 0) return hipErrorInvalidValue;
+  if (hd % 2 != 0 || (rot_tiled && hd % 16 != 0)) return hipErrorInvalidValue;
   if (dtype == 0)
     rope_kv_kernel<float><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
-                                             static_cast<float*>(kpool), static_cast<float*>(vpool));
+                                             static_cast<float*>(kpool), static_cast<float*>(vpool), rot_tiled);
   else
     rope_kv_kernel<bf16_t><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
-                                              static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool));
+                                              static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool),
+                                              rot_tiled);
   return hipGetLastError();
 }
 

@@ -1,4 +1,5 @@
-// Decoder GEMMs: Y = X W^T with W stored [N, K] (reduction dim innermost).
+// Decoder GEMMs: Y = X W^T with W [N, K] (reduction dim innermost): row-major
+// for fp32, in the tiled layout of launch_pack_weight for bf16.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -53,6 +54,15 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
                        int epi, hipStream_t st, const int32_t* row_map = nullptr,
                        float* splitk_ws = nullptr, size_t splitk_bytes = 0);
+
+// In place: bf16 row-major [rows, K] -> the tiled layout every bf16 GEMM
+// reads (K % 128 == 0).  In each complete group of 16 rows and 128-column
+// block the 16 x 16 matrix of 16-byte chunks is transposed; a trailing group
+// of fewer than 16 rows stays row-major.  rot_rows > 0 (the QKV weight's q
+// and k heads, head dim hd, hd % 16 == 0): those rows are first reordered in
+// each head to the rotary tile order, rows 8t..8t+7 then hd/2+8t..hd/2+8t+7
+// forming tile t, so that GEMM output column 16 t + j is that row.
+hipError_t launch_pack_weight(void* W, int rows, int K, int rot_rows, int hd, hipStream_t st);
 
 // Bytes of split-K workspace that cover every launch shape.
 size_t gemm_splitk_bytes(int R_max, int Nw_max);

@@ -1,25 +1,32 @@
-// Decoder GEMMs on gfx950: Y = X W^T, X [R, K], W [N, K] (both K-contiguous).
+// Decoder GEMMs on gfx950: Y = X W^T, X [R, K] (row-major), W [N, K].
+//
+// bf16 weights are stored in the tiled layout (pack_weight below): in every
+// complete group of 16 rows and block of 128 columns the 16 x 16 matrix of
+// 16-byte chunks is transposed, so chunk j (columns 8j..8j+7) of row r of the
+// group sits in row j of the group at chunk position r.  A trailing group of
+// fewer than 16 rows stays row-major.  With this layout every load the
+// kernels issue for a 16-feature tile covers whole 256-byte runs of memory
+// rows; row-major MFMA operand loads only give 64-byte runs of 16 rows.
 //
 // bf16 paths use v_mfma_f32_16x16x32_bf16 with fp32 accumulation.  Operand
 // fragments: lane l supplies A[l % 16][kgroup(l / 16)] and B[kgroup(l / 16)][l % 16],
-// and receives D[4 (l / 16) + r][l % 16], r = 0..3.  Because the reduction only
-// needs A and B to agree on which k each (lane group, element) carries, each
-// lane reads one contiguous 64-byte run of its X row and W row and feeds it to
-// four consecutive MFMAs, so a W row's 256-byte block is read by four lanes
-// with 16-byte loads straight from HBM.
+// and receives D[4 (l / 16) + r][l % 16], r = 0..3.  The reduction only needs
+// A and B to agree on which k each (lane group, element) carries: lane group
+// g of step s carries k = 32 s + 8 g .. +7 of a 128-wide block, which in the
+// tiled layout is row 4 s + g of the tile.
 //
-//  * gemv (R <= 2): vector-FMA weight streaming with 256-byte row runs.
+//  * gemv (R <= 2): vector-FMA weight streaming, one tile per workgroup.
 //  * skinny (R <= 64, except where use_mfma picks the MFMA kernel): weight
-//    streaming, HBM-bound.  A workgroup owns 16 output
-//    features (gate+up pairs for SwiGLU); its waves split K and reduce through
-//    LDS in a fixed order (deterministic, no atomics).  M is padded to 16 per
+//    streaming, HBM-bound.  A workgroup owns one 16-feature tile (for SwiGLU
+//    the gate tile and its up tile); its waves split K and reduce through LDS
+//    in a fixed order (deterministic, no atomics).  M is padded to 16 per
 //    tile; MFMA throughput is ~10x what the weight stream needs.
 //  * mfma (R > 64): 128x256 workgroup tiles, BK = 32, two workgroups per CU,
 //    loads two k-steps ahead, LDS double buffering with an XOR swizzle of
 //    16-byte chunks, 4 waves of 64x128, XCD-aware tile order, split-K with a
 //    fixed-order reduction when the grid is small.
-//  * fp32 (the fp32 configuration): a plain LDS-tiled FMA kernel; no
-//    reduced-precision arithmetic.
+//  * fp32 (the fp32 configuration): a plain LDS-tiled FMA kernel on row-major
+//    weights; no reduced-precision arithmetic.
 
 #include <algorithm>
 #include <cstdio>
@@ -34,19 +41,71 @@ namespace {
 __device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
 
 // ---------------------------------------------------------------------------
+// tiled weight layout
+
+// Element offset of 16-byte chunk `ch` (columns 8 ch .. 8 ch + 7) of row n of
+// a tiled [N, K] weight, as base + (ch % 16) * s1 + (ch / 16) * 128.
+struct ChunkAddr {
+  size_t base;
+  int s1;
+};
+__device__ __forceinline__ ChunkAddr chunk_addr(int n, int N, int K) {
+  if (n < (N & ~15)) return {static_cast<size_t>(n & ~15) * K + (n & 15) * 8, K};
+  return {static_cast<size_t>(n) * K, 8};
+}
+
+// Position, inside its head, of rotary row `dim` in the QKV weight's tiled
+// row order: the q and k heads are laid out as hd / 16 tiles of 8 rotary
+// pairs (i, i + hd / 2), rows 8t..8t+7 then hd/2+8t..hd/2+8t+7 in tile t, so
+// that the two halves of a pair meet in one 16-feature tile (lanes l and
+// l ^ 8 of a 16-lane group).
+__host__ __device__ __forceinline__ int rot_tile_pos(int dim, int hd) {
+  const int half = hd / 2, i = dim % half;
+  return 16 * (i / 8) + (dim >= half ? 8 : 0) + (i % 8);
+}
+__host__ __device__ __forceinline__ int rot_tile_dim(int p, int hd) {
+  const int t = p / 16, i = p % 16;
+  return (i < 8 ? 0 : hd / 2) + 8 * t + (i & 7);
+}
+
+// In place: row-major [rows, K] -> tiled.  Rows [0, rot_rows) form rotary
+// heads of hd rows, first reordered by rot_tile_dim.  One workgroup per (row
+// group, 128-column block) reads the block (hd or 16 rows x 256 bytes) into
+// LDS and writes it back transformed; blocks are disjoint, so in place is safe.
+__global__ __launch_bounds__(256) void pack_weight_kernel(bf16_t* __restrict__ W, int rows, int K,
+                                                          int rot_rows, int hd) {
+  extern __shared__ u32x4 blk[];  // [G rows][16 chunks]
+  const int nb = K / 128;
+  const int kb = blockIdx.x % nb, grp = blockIdx.x / nb;
+  const int n_rot = rot_rows > 0 ? rot_rows / hd : 0;
+  const bool rot = grp < n_rot;
+  const int G = rot ? hd : 16;
+  const int r0 = rot ? grp * hd : rot_rows + (grp - n_rot) * 16;
+  if (r0 + G > rows) return;  // a trailing partial group stays row-major
+  bf16_t* base = W + static_cast<size_t>(r0) * K + kb * 128;
+  for (int e = threadIdx.x; e < G * 16; e += blockDim.x)
+    blk[e] = *reinterpret_cast<const u32x4*>(base + static_cast<size_t>(e / 16) * K + (e % 16) * 8);
+  __syncthreads();
+  for (int e = threadIdx.x; e < G * 16; e += blockDim.x) {
+    const int p = e / 16, c = e % 16;  // destination row of the group, chunk position
+    const int pos = (p & ~15) + c;     // feature (in tile order) whose chunk p % 16 lands here
+    const int src = rot ? rot_tile_dim(pos, G) : pos;
+    *reinterpret_cast<u32x4*>(base + static_cast<size_t>(p) * K + c * 8) = blk[src * 16 + (p & 15)];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // skinny bf16
 
 constexpr int kSkinnyMaxWaves = 8;
 
-// Tiles of the fused QKV epilogue: the q and k heads come first, each as
-// hd / 16 tiles of 8 rotary pairs (i, i + hd / 2), so that a pair meets in one
-// workgroup (lanes l and l ^ 8 of a 16-lane group); the v heads follow in
-// plain order.
+// Output (head, dim) of column l16 of tile `tile` of the QKV projection,
+// whose q and k heads are in rotary tile order; the v heads follow in plain
+// order.  Returns the natural row head * hd + dim.
 __device__ __forceinline__ int qkv_tile_row(const GemmFuse& f, int tile, int l16, int* head, int* dim) {
   const int per_head = f.hd / 16;
   *head = tile / per_head;
-  const int i = 8 * (tile % per_head) + (l16 & 7);
-  *dim = i + (l16 >> 3) * (f.hd / 2);
+  *dim = rot_tile_dim(16 * (tile % per_head) + l16, f.hd);
   return *head * f.hd + *dim;
 }
 
@@ -131,14 +190,14 @@ __device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l1
   }
 }
 
-template <int MT, int NT, int EPI, bool FUSE>
+template <int MT, int EPI, bool FUSE>
 __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, void* __restrict__ Y, int R, int N,
     int K, int kb_per_wave, const int32_t* __restrict__ row_map, const GemmFuse fu) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
   constexpr bool QKV = (EPI == kEpiQKVRope);
-  constexpr int NS = SW ? 2 : 1;  // weight streams: gate and up rows for SwiGLU
-  constexpr int NACC = MT * NT * NS;
+  constexpr int NS = SW ? 2 : 1;  // weight streams: gate and up tiles for SwiGLU
+  constexpr int NACC = MT * NS;
   static_assert(!FUSE || MT == 1, "the fused path covers up to 16 rows");
   static_assert(FUSE || !QKV, "the QKV epilogue is fused only");
   extern __shared__ float red[];  // [waves][NACC][4][64]
@@ -148,21 +207,21 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
   const int wave = threadIdx.x / kWave;
   const int nw = blockDim.x / kWave;
   const int row = lane & 15, g = lane >> 4;
-  const int tile0 = blockIdx.x * NT;
+  const int tile = blockIdx.x;
   const int qk_tiles = QKV ? (fu.Hq + fu.Hkv) * fu.hd / 16 : 0;
-  // lane group g, step s carries k = 32 s + 8 g .. +7 of each 128-wide block:
-  // the four lanes of a row read one contiguous 64-byte run per load
-  const bf16_t* wp[NT][NS];
+  // Step s of lane group g reads row 4 s + g of the tile at chunk position
+  // `row` (tiled layout): 16 bytes of W[tile * 16 + row][32 s + 8 g ..].  A
+  // trailing partial tile is row-major, read at clamped rows.
+  const bf16_t* wp[NS];
+  int ws;  // element stride between steps
+  {
+    const bool full = (tile + 1) * 16 <= N;
+    ws = full ? 4 * K : 32;
 #pragma unroll
-  for (int j = 0; j < NT; ++j) {
-    int feat = (tile0 + j) * 16 + row;
-    if (QKV && tile0 + j < qk_tiles) {
-      int hh, dd;
-      feat = qkv_tile_row(fu, tile0 + j, row, &hh, &dd);
-    }
-    const int nrow = min(feat, N - 1);
-    wp[j][0] = W + static_cast<size_t>(nrow) * K + g * 8;
-    if (SW) wp[j][NS - 1] = W + static_cast<size_t>(N + nrow) * K + g * 8;
+    for (int h = 0; h < NS; ++h)
+      wp[h] = W + static_cast<size_t>(h) * N * K +
+              (full ? static_cast<size_t>(tile * 16 + g) * K + row * 8
+                    : static_cast<size_t>(min(tile * 16 + row, N - 1)) * K + g * 8);
   }
   const bf16_t* xr[MT];
   bool xv[MT];
@@ -174,30 +233,26 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     xr[mt] = X + static_cast<size_t>(src) * K + g * 8;
   }
   if (FUSE && fu.ss) row_rscale(fu, R, K, s_rs);
-  f32x4 acc[MT][NT][NS];
+  f32x4 acc[MT][NS];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int j = 0; j < NT; ++j)
-#pragma unroll
-      for (int h = 0; h < NS; ++h) acc[mt][j][h] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // KB 128-wide blocks per iteration, every load of the iteration issued
-  // before its first MFMA; each X fragment feeds NT x NS weight tiles
-  constexpr int KB = (NT * NS * MT >= 4) ? 1 : ((NT * NS * MT >= 2) ? 2 : 4);
+    for (int h = 0; h < NS; ++h) acc[mt][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // KB 128-wide blocks per iteration (8 weight loads per lane in flight),
+  // every load of the iteration issued before its first MFMA
+  constexpr int KB = (NS * MT >= 2) ? 1 : 2;
   const int nb = K / 128;
   const int kb0 = wave * kb_per_wave;
   const int kb1 = min(nb, kb0 + kb_per_wave);
   for (int kb = kb0; kb < kb1; kb += KB) {
-    uint4 w[KB][NT][NS][4], x[KB][MT][4];
+    uint4 w[KB][NS][4], x[KB][MT][4];
 #pragma unroll
     for (int b = 0; b < KB; ++b) {
       const int ko = (kb + b < kb1 ? kb + b : kb) * 128;
 #pragma unroll
-      for (int j = 0; j < NT; ++j)
+      for (int h = 0; h < NS; ++h)
 #pragma unroll
-        for (int h = 0; h < NS; ++h)
-#pragma unroll
-          for (int s = 0; s < 4; ++s) w[b][j][h][s] = ld_stream(reinterpret_cast<const uint4*>(wp[j][h] + ko) + 4 * s);
+        for (int s = 0; s < 4; ++s) w[b][h][s] = ld_stream(reinterpret_cast<const uint4*>(wp[h] + ko + s * ws));
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -212,33 +267,27 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int j = 0; j < NT; ++j)
-#pragma unroll
-            for (int h = 0; h < NS; ++h) acc[mt][j][h] = mfma16x16x32(x[b][mt][s], w[b][j][h][s], acc[mt][j][h]);
+          for (int h = 0; h < NS; ++h) acc[mt][h] = mfma16x16x32(x[b][mt][s], w[b][h][s], acc[mt][h]);
     }
   }
-  // red[wave][(mt, j, h)][r][lane]
+  // red[wave][(mt, h)][r][lane]
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int j = 0; j < NT; ++j)
+    for (int h = 0; h < NS; ++h)
 #pragma unroll
-      for (int h = 0; h < NS; ++h)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          red[((wave * NACC + (mt * NT + j) * NS + h) * 4 + r) * kWave + lane] = acc[mt][j][h][r];
+      for (int r = 0; r < 4; ++r) red[((wave * NACC + mt * NS + h) * 4 + r) * kWave + lane] = acc[mt][h][r];
   __syncthreads();
-  // element e: accumulator set e / 256 = (mt, j), output row m = 16 mt +
-  // 4 (lane / 16) + r, column l16 of tile tile0 + j.  Whole waves take the
-  // same (mt, j), as the fused epilogue's 16-lane exchanges need.
-  for (int e = threadIdx.x; e < MT * NT * 256; e += blockDim.x) {
-    const int set = e / 256, r = (e / kWave) & 3, ln = e & (kWave - 1);
-    const int mt = set / NT, j = set % NT;
+  // element e: row block mt = e / 256, output row m = 16 mt + 4 (lane / 16) + r,
+  // column l16.  Whole waves take the same mt, as the fused epilogue's 16-lane
+  // exchanges need.
+  for (int e = threadIdx.x; e < MT * 256; e += blockDim.x) {
+    const int mt = e / 256, r = (e / kWave) & 3, ln = e & (kWave - 1);
     const int m = mt * 16 + 4 * (ln >> 4) + r, l16 = ln & 15;
     float v = 0.f, vu = 0.f;
     for (int wv = 0; wv < nw; ++wv) {
-      v += red[((wv * NACC + set * NS) * 4 + r) * kWave + ln];
-      if (SW) vu += red[((wv * NACC + set * NS + 1) * 4 + r) * kWave + ln];
+      v += red[((wv * NACC + mt * NS) * 4 + r) * kWave + ln];
+      if (SW) vu += red[((wv * NACC + mt * NS + 1) * 4 + r) * kWave + ln];
     }
     if (FUSE) {
       if (fu.ss) {
@@ -246,10 +295,10 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
         v *= rs;
         vu *= rs;
       }
-      fused_epilogue<EPI>(fu, m, l16, tile0 + j, R, N, v, vu, Y, row_map, qk_tiles);
+      fused_epilogue<EPI>(fu, m, l16, tile, R, N, v, vu, Y, row_map, qk_tiles);
       continue;
     }
-    const int n = (tile0 + j) * 16 + l16;
+    const int n = tile * 16 + l16;
     if (m < R && n < N) {
       const size_t o = static_cast<size_t>(row_map ? row_map[m] : m) * N + n;
       if (EPI == kEpiStoreF32) static_cast<float*>(Y)[o] = v;
@@ -261,12 +310,12 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 
 // ---------------------------------------------------------------------------
 // bf16 GEMV for 1-2 rows (a single sequence's draft step): vector FMAs, no
-// MFMA.  A workgroup owns 16 features (for SwiGLU their 16 gate and 16 up
-// rows); each wave reads 4 weight rows, 16 lanes per row with 16-byte loads,
-// so every load instruction covers 256 contiguous bytes of each of its rows
-// (the MFMA operand layout can only give 64).  Waves split K in two halves
-// (SwiGLU: gate and up instead); lanes of a row reduce with shuffles, halves
-// through LDS, then the fused epilogue.
+// MFMA.  A workgroup owns one 16-feature tile (for SwiGLU its gate tile and
+// its up tile).  Per 128-wide block a wave reads the tile's 16 rows in four
+// loads of 4 rows x 256 bytes: lane (r = lane / 16, c = lane % 16) gets
+// 16 bytes of feature c, chunk 4 q + r.  Waves split K (SwiGLU: waves 0-3 gate,
+// 4-7 up); lanes of a feature reduce with shuffles, waves through LDS, then
+// the fused epilogue.
 
 constexpr int kGemvRows = 2;  // measured: the MFMA skinny kernel wins from 3 rows on
 
@@ -286,70 +335,82 @@ __global__ __launch_bounds__(512) void gemv_bf16(const bf16_t* __restrict__ X, c
                                                  const int32_t* __restrict__ row_map, const GemmFuse fu) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
   constexpr bool QKV = (EPI == kEpiQKVRope);
-  constexpr int KB = 8;  // 128-wide chunks per batch: 8 weight loads in flight per lane
-  __shared__ float part[2][RM][16];  // [K half or gate/up][row][tile column]
+  constexpr int KB = 2;  // 128-wide blocks per iteration: 8 weight loads in flight per lane
+  __shared__ float part[8][RM][16];  // [wave][row][feature]
   __shared__ float s_rs[16];
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int c = lane & 15, trow = 4 * (wave & 3) + (lane >> 4);
-  const int half = wave >> 2;  // K half, or (SwiGLU) 0 gate / 1 up
-  const int n0 = blockIdx.x * 16;
+  const int c = lane & 15, r = lane >> 4;
+  const int tile = blockIdx.x;
   const int qk_tiles = QKV ? (fu.Hq + fu.Hkv) * fu.hd / 16 : 0;
-  int feat = n0 + trow;
-  if (QKV && static_cast<int>(blockIdx.x) < qk_tiles) {
-    int hh, dd;
-    feat = qkv_tile_row(fu, blockIdx.x, trow, &hh, &dd);
-  }
-  const int wrow = (SW && half ? N : 0) + min(feat, N - 1);
-  const bf16_t* wp = W + static_cast<size_t>(wrow) * K + c * 8;
+  const int grp = SW ? (wave >> 2) : 0;  // SwiGLU: gate (0) or up (1) tile
+  const int gw = SW ? (wave & 3) : wave, ngw = SW ? 4 : 8;
+  const bf16_t* wh = W + (grp ? static_cast<size_t>(N) * K : 0);
+  // load q of block kb: wp + q * qs + kb * 128 (tiled: rows 4 q + r at
+  // position c; a trailing partial tile is row-major at clamped rows)
+  const bool full = (tile + 1) * 16 <= N;
+  const bf16_t* wp = wh + (full ? static_cast<size_t>(tile * 16 + r) * K + c * 8
+                                : static_cast<size_t>(min(tile * 16 + c, N - 1)) * K + r * 8);
+  const int qs = full ? 4 * K : 32;
   const bf16_t* xp[RM];
 #pragma unroll
   for (int m = 0; m < RM; ++m)
-    xp[m] = X + static_cast<size_t>(m < R ? (fu.xrow ? fu.xrow[m] : m) : 0) * K + c * 8;
-  const int chunks = K / 128;
-  const int per = SW ? chunks : (chunks + 1) / 2;
-  const int c0 = SW ? 0 : half * per, c1 = min(chunks, c0 + per);
+    xp[m] = X + static_cast<size_t>(m < R ? (fu.xrow ? fu.xrow[m] : m) : 0) * K + r * 8;
+  const int nb = K / 128;
+  const int per = (nb + ngw - 1) / ngw;
+  const int kb0 = gw * per, kb1 = min(nb, kb0 + per);
   float a[RM];
 #pragma unroll
   for (int m = 0; m < RM; ++m) a[m] = 0.f;
-  for (int ch = c0; ch < c1; ch += KB) {
-    u32x4 w[KB], x[KB][RM];
+  for (int kb = kb0; kb < kb1; kb += KB) {
+    u32x4 w[KB][4], x[KB][RM][4];
 #pragma unroll
     for (int b = 0; b < KB; ++b) {
-      const int o = min(ch + b, c1 - 1) * 128;
-      w[b] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wp + o));
+      const int o = min(kb + b, kb1 - 1) * 128;
 #pragma unroll
-      for (int m = 0; m < RM; ++m)
-        if (m < R) x[b][m] = *reinterpret_cast<const u32x4*>(xp[m] + o);
+      for (int q = 0; q < 4; ++q) {
+        w[b][q] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wp + o + q * qs));
+#pragma unroll
+        for (int m = 0; m < RM; ++m)
+          if (m < R) x[b][m][q] = *reinterpret_cast<const u32x4*>(xp[m] + o + 32 * q);
+      }
     }
 #pragma unroll
     for (int b = 0; b < KB; ++b) {
-      if (ch + b >= c1) break;
+      if (kb + b >= kb1) break;
 #pragma unroll
-      for (int m = 0; m < RM; ++m)
-        if (m < R) a[m] += dot8(w[b], x[b][m]);
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int m = 0; m < RM; ++m)
+          if (m < R) a[m] += dot8(w[b][q], x[b][m][q]);
     }
   }
 #pragma unroll
   for (int m = 0; m < RM; ++m) {
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) a[m] += __shfl_xor(a[m], o, kWave);
-    if (c == 0) part[half][m][trow] = a[m];
+    a[m] += __shfl_xor(a[m], 16, kWave);
+    a[m] += __shfl_xor(a[m], 32, kWave);
+    if (lane < 16) part[wave][m][c] = a[m];
   }
   if (fu.ss) row_rscale(fu, R, K, s_rs);
   __syncthreads();
   if (threadIdx.x >= 256) return;
-  const int e = threadIdx.x, r = (e / kWave) & 3, ln = e & (kWave - 1);
-  const int m = 4 * (ln >> 4) + r, l16 = ln & 15;
+  const int e = threadIdx.x, rr = (e / kWave) & 3, ln = e & (kWave - 1);
+  const int m = 4 * (ln >> 4) + rr, l16 = ln & 15;
   float v = 0.f, vu = 0.f;
   if (m < R) {
-    v = SW ? part[0][m][l16] : part[0][m][l16] + part[1][m][l16];
-    if (SW) vu = part[1][m][l16];
+    if (SW) {
+      for (int wv = 0; wv < 4; ++wv) {
+        v += part[wv][m][l16];
+        vu += part[4 + wv][m][l16];
+      }
+    } else {
+      for (int wv = 0; wv < 8; ++wv) v += part[wv][m][l16];
+    }
     if (fu.ss) {
       v *= s_rs[m];
       vu *= s_rs[m];
     }
   }
-  fused_epilogue<EPI>(fu, m, l16, blockIdx.x, R, N, v, vu, Y, row_map, qk_tiles);
+  fused_epilogue<EPI>(fu, m, l16, tile, R, N, v, vu, Y, row_map, qk_tiles);
 }
 
 template <int EPI>
@@ -409,18 +470,21 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(const bf16_t* __restric
   const int sr = t / kMCh, sc = t % kMCh;
   const int lds_st = sr * kMCh + (sc ^ (sr & (kMCh - 1)));
   const bf16_t* xs = X + kbeg + sc * 8;
-  const bf16_t* ws = W + kbeg + sc * 8;
-  uint32_t aoff[kMPA], boff[kMPB];
+  uint32_t aoff[kMPA];
 #pragma unroll
   for (int i = 0; i < kMPA; ++i) aoff[i] = static_cast<uint32_t>(min(m0 + sr + kMRows * i, R - 1));
+  // W rows in the tiled layout: chunk ch of row n at bb + (ch % 16) * s1 + (ch / 16) * 128
+  size_t bb[kMPB];
+  int bs1[kMPB];
 #pragma unroll
   for (int i = 0; i < kMPB; ++i) {
     const int br = sr + kMRows * i;
-    if (SW)
-      boff[i] = static_cast<uint32_t>((br < 128 ? 0 : N) + min(f0 + (br & 127), N - 1));
-    else
-      boff[i] = static_cast<uint32_t>(min(f0 + br, N - 1));
+    const int n = SW ? min(f0 + (br & 127), N - 1) : min(f0 + br, N - 1);
+    const ChunkAddr ca = chunk_addr(n, N, K);
+    bb[i] = ca.base + ((SW && br >= 128) ? static_cast<size_t>(N) * K : 0);
+    bs1[i] = ca.s1;
   }
+  const int ch0 = kbeg / 8 + sc;  // chunk of k-step 0
   // native vector types keep the staging values in registers
   u32x4 sa[kMPA], sb[kMPB], ta[kMPA], tb[kMPB];
 #define SPEC_MFMA_LOAD(SA, SB, KT)                                                                 \
@@ -428,8 +492,9 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(const bf16_t* __restric
     const int ko_ = (KT) * kMK;                                                                    \
     _Pragma("unroll") for (int i = 0; i < kMPA; ++i)                                               \
         SA[i] = *reinterpret_cast<const u32x4*>(xs + static_cast<size_t>(aoff[i]) * K + ko_);      \
+    const int ch_ = ch0 + (KT) * kMCh;                                                             \
     _Pragma("unroll") for (int i = 0; i < kMPB; ++i)                                               \
-        SB[i] = *reinterpret_cast<const u32x4*>(ws + static_cast<size_t>(boff[i]) * K + ko_);      \
+        SB[i] = *reinterpret_cast<const u32x4*>(W + bb[i] + (ch_ & 15) * bs1[i] + (ch_ >> 4) * 128); \
   } while (0)
 #define SPEC_MFMA_STORE(SA, SB, AL, BL)                                                            \
   do {                                                                                             \
@@ -625,46 +690,23 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X,
   }
 }
 
-template <int MT, int NT, int EPI, bool FUSE>
-hipError_t skinny_nt(int nw, int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
-                     const int32_t* row_map, const GemmFuse& fu) {
-  constexpr int NACC = MT * NT * (EPI == kEpiSwiGLU ? 2 : 1);
-  const int groups = ((N + 15) / 16 + NT - 1) / NT;
-  const int nb = K / 128;
-  nw = std::max(FUSE ? 4 : 1, std::min(nw, nb));
-  if (FUSE && nw < 4) return hipErrorInvalidValue;  // the fused epilogue needs 256 threads
-  const int kbpw = (nb + nw - 1) / nw;
-  const size_t lds = static_cast<size_t>(nw) * NACC * 256 * sizeof(float);
-  gemm_skinny_bf16<MT, NT, EPI, FUSE><<<groups, nw * kWave, lds, st>>>(
-      static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map, fu);
-  return hipGetLastError();
-}
-
-// Feature tiles per workgroup and waves per workgroup of the skinny kernel,
-// measured at 6..64 rows on the projections of the 8B/1B-shaped pair: several
-// tiles per workgroup share each X fragment load (the L2 traffic of X limits
-// the wide LM head and gate/up), but cost parallelism on narrow projections;
-// 8 waves split K when there are few workgroups and K is mid-sized.
-int skinny_tiles_per_wg(int MT, int N, bool sw) {
-  const int tiles = (N + 15) / 16;
-  int nt = sw ? (tiles >= 768 ? 4 : 1) : (tiles >= 2048 ? 4 : (tiles >= 384 ? 2 : 1));
-  while (nt > 1 && MT * nt * (sw ? 2 : 1) > 8) nt /= 2;  // bounds registers
-  return nt;
-}
-
-int skinny_waves(int groups, int K) { return (groups <= 256 && K >= 4096 && K < 12288) ? 8 : 4; }
+// Waves per workgroup of the skinny kernel: 8 split K when there are few
+// tiles, else 4 (measured on the 8B/1B-shaped projections at 6 rows).
+int skinny_waves(int tiles, int K) { return (tiles <= 512 && K >= 2048) ? 8 : 4; }
 
 template <int MT, int EPI, bool FUSE = false>
 hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
                   const int32_t* row_map, const GemmFuse& fu = GemmFuse{}) {
-  constexpr bool SW = (EPI == kEpiSwiGLU);
-  const int nt = skinny_tiles_per_wg(MT, N, SW);
-  const int nw = skinny_waves(((N + 15) / 16 + nt - 1) / nt, K);
-  if (nt == 4 && MT * 4 * (SW ? 2 : 1) <= 8)
-    return skinny_nt<MT, (MT * 4 * (SW ? 2 : 1) <= 8 ? 4 : 1), EPI, FUSE>(nw, R, N, K, X, W, Y, st, row_map, fu);
-  if (nt == 2 && MT * 2 * (SW ? 2 : 1) <= 8)
-    return skinny_nt<MT, (MT * 2 * (SW ? 2 : 1) <= 8 ? 2 : 1), EPI, FUSE>(nw, R, N, K, X, W, Y, st, row_map, fu);
-  return skinny_nt<MT, 1, EPI, FUSE>(nw, R, N, K, X, W, Y, st, row_map, fu);
+  constexpr int NACC = MT * (EPI == kEpiSwiGLU ? 2 : 1);
+  const int tiles = (N + 15) / 16;
+  const int nb = K / 128;
+  int nw = std::max(FUSE ? 4 : 1, std::min(skinny_waves(tiles, K), nb));
+  if (FUSE && nw < 4) return hipErrorInvalidValue;  // the fused epilogue needs 256 threads
+  const int kbpw = (nb + nw - 1) / nw;
+  const size_t lds = static_cast<size_t>(nw) * NACC * 256 * sizeof(float);
+  gemm_skinny_bf16<MT, EPI, FUSE><<<tiles, nw * kWave, lds, st>>>(
+      static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map, fu);
+  return hipGetLastError();
 }
 
 // Split-K factor for the MFMA kernel: grids under 256 tiles are split so that
@@ -737,6 +779,18 @@ hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W
 
 }  // namespace
 
+hipError_t launch_pack_weight(void* W, int rows, int K, int rot_rows, int hd, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  if (K <= 0 || K % 128 != 0 || rot_rows < 0 || rot_rows > rows) return hipErrorInvalidValue;
+  if (rot_rows > 0 && (hd <= 0 || hd % 16 != 0 || hd > 256 || rot_rows % hd != 0)) return hipErrorInvalidValue;
+  const int n_rot = rot_rows > 0 ? rot_rows / hd : 0;
+  const int groups = n_rot + (rows - rot_rows + 15) / 16;
+  const int G = std::max(16, rot_rows > 0 ? hd : 16);
+  const size_t lds = static_cast<size_t>(G) * 16 * sizeof(u32x4);
+  pack_weight_kernel<<<groups * (K / 128), 256, lds, st>>>(static_cast<bf16_t*>(W), rows, K, rot_rows, hd);
+  return hipGetLastError();
+}
+
 size_t gemm_splitk_bytes(int R_max, int Nw_max) {
   // only grids of fewer than 256 tiles split, into S <= 256 / tiles parts, so
   // the partials S * R * Nw stay below 256 * kMM * kMN floats; smaller
@@ -771,29 +825,24 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
 const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused) {
   static const char* gv[4] = {"gemv_bf16<0, 2>", "gemv_bf16<1, 2>", "gemv_bf16<2, 2>", "gemv_bf16<3, 2>"};
   if (dtype == 1 && R <= kGemvRows) return (epi >= 0 && epi <= 3) ? gv[epi] : "";
-  // skinny names [MT - 1][log2 NT][epi][fused]
-  static char names[4][3][4][2][48];
+  // skinny names [MT - 1][epi][fused]
+  static char names[4][4][2][40];
   static std::once_flag once;
   std::call_once(once, [] {
     for (int mt = 0; mt < 4; ++mt)
-      for (int t = 0; t < 3; ++t)
-        for (int e = 0; e < 4; ++e)
-          for (int f = 0; f < 2; ++f)
-            snprintf(names[mt][t][e][f], sizeof(names[mt][t][e][f]), "gemm_skinny_bf16<%d, %d, %d, %s>", mt + 1,
-                     1 << t, e, f ? "true" : "false");
+      for (int e = 0; e < 4; ++e)
+        for (int f = 0; f < 2; ++f)
+          snprintf(names[mt][e][f], sizeof(names[mt][e][f]), "gemm_skinny_bf16<%d, %d, %s>", mt + 1, e,
+                   f ? "true" : "false");
   });
-  auto skinny_name = [&](int MT, bool f) {
-    const int nt = skinny_tiles_per_wg(MT, N, epi == kEpiSwiGLU);
-    return names[MT - 1][nt == 4 ? 2 : (nt == 2 ? 1 : 0)][epi][f ? 1 : 0];
-  };
   if (epi < 0 || epi > 3) return "";
-  if (fused) return skinny_name(1, true);
+  if (fused) return names[0][epi][1];
   if (epi > 2) return "";
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
   static const char* tiled[3] = {"gemm_mfma_bf16<0>", "gemm_mfma_bf16<1>", "gemm_mfma_bf16<2>"};
   if (dtype == 0) return f32[epi];
   if (use_mfma(R, epi == kEpiSwiGLU ? 2 * N : N, K)) return tiled[epi];
-  return skinny_name((std::max(R, 1) - 1) / 16 + 1, false);
+  return names[(std::max(R, 1) - 1) / 16][epi][0];
 }
 
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,

@@ -152,6 +152,56 @@ size_t spec_op_gemm_workspace_bytes(int32_t R, int32_t Nw) {
   return (R <= 0 || Nw <= 0) ? 0 : gemm_splitk_bytes(R, Nw);
 }
 
+spec_status spec_pack_weight(void* w, int32_t rows, int32_t K, int32_t rot_rows, int32_t head_dim,
+                             void* stream) {
+  if (!w || rows < 0 || K <= 0 || rot_rows < 0 || rot_rows > rows) return SPEC_E_INVALID;
+  if (K % 128 != 0) return SPEC_E_UNSUPPORTED;
+  if (rot_rows > 0 && (head_dim <= 0 || head_dim % 16 != 0 || head_dim > 256 || rot_rows % head_dim != 0))
+    return SPEC_E_UNSUPPORTED;
+  return hip_status(launch_pack_weight(w, rows, K, rot_rows, head_dim, static_cast<hipStream_t>(stream)));
+}
+
+spec_status spec_pack_model(spec_model_desc* m, void* stream) {
+  if (!m || !m->layers || !m->lm_head) return SPEC_E_INVALID;
+  if (m->weight_layout != SPEC_LAYOUT_ROWMAJOR) return SPEC_E_STATE;
+  if (m->dtype == SPEC_F32) return SPEC_OK;
+  if (m->dtype != SPEC_BF16 || m->n_layers <= 0 || m->d_model <= 0 || m->ffn_dim <= 0 || m->n_heads <= 0 ||
+      m->n_kv_heads <= 0 || m->head_dim <= 0 || m->vocab <= 0)
+    return SPEC_E_INVALID;
+  const int d = m->d_model, f = m->ffn_dim, hd = m->head_dim, qd = m->n_heads * hd;
+  if (d % 128 || f % 128 || qd % 128 || hd % 16) return SPEC_E_UNSUPPORTED;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int qkv_rows = (m->n_heads + 2 * m->n_kv_heads) * hd, rot = (m->n_heads + m->n_kv_heads) * hd;
+  const size_t esz = 2;
+  std::vector<const void*> done;  // matrices shared between layers are converted once
+  auto once = [&](const void* p) {
+    if (std::find(done.begin(), done.end(), p) != done.end()) return false;
+    done.push_back(p);
+    return true;
+  };
+  auto pack = [&](const void* p, int rows, int K, int rr) -> hipError_t {
+    if (!p || !once(p)) return hipSuccess;
+    return launch_pack_weight(const_cast<void*>(p), rows, K, rr, hd, st);
+  };
+  for (int l = 0; l < m->n_layers; ++l) {
+    const spec_layer_weights& L = m->layers[l];
+    hipError_t e = pack(L.wqkv, qkv_rows, d, rot);
+    if (e == hipSuccess) e = pack(L.wo, d, qd, 0);
+    if (e == hipSuccess && L.w_gate_up && once(L.w_gate_up)) {
+      e = launch_pack_weight(const_cast<void*>(L.w_gate_up), f, d, 0, hd, st);
+      if (e == hipSuccess)
+        e = launch_pack_weight(static_cast<char*>(const_cast<void*>(L.w_gate_up)) + static_cast<size_t>(f) * d * esz,
+                               f, d, 0, hd, st);
+    }
+    if (e == hipSuccess) e = pack(L.w_down, d, f, 0);
+    if (e != hipSuccess) return hip_status(e);
+  }
+  const hipError_t e = pack(m->lm_head, m->vocab, d, 0);
+  if (e != hipSuccess) return hip_status(e);
+  m->weight_layout = SPEC_LAYOUT_TILED;
+  return SPEC_OK;
+}
+
 spec_status spec_op_gemm(int32_t dtype, int32_t R, int32_t N, int32_t K, const void* X, const void* W,
                          void* Y, int32_t epilogue, void* workspace, size_t workspace_bytes, void* stream) {
   if ((dtype != SPEC_F32 && dtype != SPEC_BF16) || R < 0 || N < 0 || K <= 0 || !X || !W || !Y)

@@ -29,7 +29,8 @@ def to_device(a: np.ndarray, device) -> torch.Tensor:
 class DeviceModel:
     """A decoder's weights on the GPU and its spec_model_desc.
 
-    weights: the dict of ``workloads.gen.model_weights`` (numpy), uploaded as is;
+    weights: the dict of ``workloads.gen.model_weights`` (numpy), uploaded and,
+    for bf16, converted in place to the library's tiled weight layout;
     or None with ``seed`` to draw N(0, std^2) weights on the device (torch's
     generator; used for the large random-init models where host generation and
     upload would dominate set-up time)."""
@@ -58,7 +59,10 @@ class DeviceModel:
                                       sh.vocab, _SPEC_DTYPE[sh.dtype], sh.rope_theta, sh.rms_eps,
                                       self.t["embed"].data_ptr(), self.t["final_norm"].data_ptr(),
                                       self.t["lm_head"].data_ptr(),
-                                      ctypes.cast(self._layers, ctypes.POINTER(B.spec_layer_weights)))
+                                      ctypes.cast(self._layers, ctypes.POINTER(B.spec_layer_weights)),
+                                      B.SPEC_LAYOUT_ROWMAJOR)
+        # bf16 projections go to the tiled layout the kernels stream (in place)
+        B.spec_pack_model(self.desc)
 
     def _draw(self, seed: int, L: int):
         sh = self.shape

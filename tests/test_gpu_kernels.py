@@ -63,11 +63,16 @@ def _gemm_case(dt, R, N, K, epi, dev, seed=0, cols=None, splitk=True):
     else:
         Y = torch.full((R, N), float("nan"), device=dev)
     Y0 = Y.float().cpu().numpy().astype(np.float64)
+    Wk = W
+    if dt == b.SPEC_BF16:  # the bf16 kernels read the tiled layout (gate and up halves packed separately)
+        Wk = W.clone()
+        for h in range(rows_w // N):
+            b.spec_pack_weight(Wk[h * N:(h + 1) * N], N, K)
     ws = None
     if splitk:
         ws = torch.empty(b.spec_op_gemm_workspace_bytes(R, rows_w), dtype=torch.uint8, device=dev)
     say("gemm", dt, R, N, K, epi, "splitk" if splitk else "")
-    b.spec_op_gemm(dt, R, N, K, X, W, Y, epi, ws)
+    b.spec_op_gemm(dt, R, N, K, X, Wk, Y, epi, ws)
     torch.cuda.synchronize()
     if cols is None:
         cols = np.arange(N)
@@ -90,6 +95,35 @@ def _gemm_case(dt, R, N, K, epi, dev, seed=0, cols=None, splitk=True):
 
 
 EPIS = [0, 1, 2]
+
+
+def tiled_layout_ref(w, rot_rows=0, hd=0):
+    """The tiled weight layout written out on the CPU from its definition:
+    rotary heads reordered (tile t = rows 8t..8t+7, hd/2+8t..hd/2+8t+7), then
+    in every full 16-row group and 128-column block the 16 x 16 matrix of
+    8-element chunks transposed; a trailing partial group stays as is."""
+    rows, K = w.shape
+    src = w.copy()
+    for h0 in range(0, rot_rows, hd or 1):
+        order = [(0 if i < 8 else hd // 2) + 8 * t + (i % 8) for t in range(hd // 16) for i in range(16)]
+        src[h0:h0 + hd] = w[h0 + np.array(order)]
+    out = src.copy()
+    for g0 in range(0, rows - rows % 16, 16):
+        blk = src[g0:g0 + 16].reshape(16, K // 128, 16, 8)  # [row, block, chunk, 8]
+        out[g0:g0 + 16] = blk.transpose(2, 1, 0, 3).reshape(16, K)
+    return out
+
+
+@pytest.mark.parametrize("rows,K,rot_rows,hd", [(32, 256, 0, 0), (40, 384, 0, 0), (7, 128, 0, 0),
+                                               (6 * 64 + 24, 256, 4 * 64, 64), (3 * 128, 128, 2 * 128, 128)])
+def test_pack_weight_layout(rows, K, rot_rows, hd):
+    dev = device()
+    w = _rand_bf16((rows, K), 1.0, rows + K, dev)
+    ref = tiled_layout_ref(bf16_bits(w), rot_rows, hd)
+    say("pack", rows, K, rot_rows, hd)
+    B().spec_pack_weight(w, rows, K, rot_rows, hd)
+    torch.cuda.synchronize()
+    assert np.array_equal(bf16_bits(w), ref)
 
 
 @pytest.mark.parametrize("R,N,K", [(1, 48, 128), (6, 200, 256), (16, 64, 384), (17, 100, 128), (33, 130, 256),
