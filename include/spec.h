@@ -110,9 +110,15 @@ typedef struct spec_model_desc {
  * (SPEC_OK, layout stays row-major). */
 SPEC_API spec_status spec_pack_model(spec_model_desc* m, void* stream);
 
-/* Paged KV cache.  Each pool holds, per layer, K pages [page][Hkv][16][hd] and
- * V pages stored transposed [page][Hkv][hd][16], element type = model dtype;
- * size it with spec_kv_pool_bytes(). */
+/* Paged KV cache.  Each pool holds, per layer, K pages [page][Hkv][16 x hd] and
+ * V pages [page][Hkv][16 x hd], element type = model dtype; size it with
+ * spec_kv_pool_bytes().  Inside a (page, kv head) block, fp32 stores K as
+ * [16 tokens][hd] and V transposed as [hd][16 tokens]; bf16 orders the block
+ * for the attention kernel's operand loads: token k, dim d of K at
+ * 8 * (((s * 2 + h) * 4 + g) * 8 + j) + d % 8 with c = d / 8, s = c / 4,
+ * g = c % 4, h = (k / 4) % 2, j = k % 4 + 4 * (k / 8); of V at
+ * 8 * (((d / 16) * 2 + k / 8) * 16 + d % 16) + k % 8.  The library alone
+ * writes the pools. */
 typedef struct spec_cache_desc {
   int32_t page_size;          /* must be 16 */
   int32_t num_pages_target;

@@ -33,16 +33,18 @@ struct AttnArgs {
 };
 
 // bf16: items/groups as above, nt = 16-wide query-vector tiles per item
-// (query vectors per item = nrows * Hq / Hkv <= 16 * nt, nt in {1, 2, 4}).
+// (query vectors per item = nrows * Hq / Hkv <= 16 * nt, nt in {1, 2, 4}),
+// w = waves per workgroup sharing an item's key range (1, 2, 4; at most 2
+// for nt = 4).
 hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int n_items,
-                                 const AttnGroup* d_groups, int n_groups, int nt, hipStream_t st);
+                                 const AttnGroup* d_groups, int n_groups, int nt, int w, hipStream_t st);
 
 // fp32: one wave per (row, head); row r of sequence slot row_seq[r] at
 // position row_pos[r] attends keys 0..row_pos[r].
 hipError_t launch_attention_f32(const AttnArgs& a, int R, const int32_t* d_row_seq,
                                 const int32_t* d_row_pos, hipStream_t st);
 
-// Profiler name of the bf16 attention kernel for (hd, nt).
-const char* attn_kernel_name(int hd, int nt);
+// Profiler name of the bf16 attention kernel for (hd, nt, w).
+const char* attn_kernel_name(int hd, int nt, int w);
 
 }  // namespace spec

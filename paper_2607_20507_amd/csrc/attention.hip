@@ -5,19 +5,22 @@
 // kernel runs, so drafts see each other causally).  Query head h reads kv head
 // h / (Hq / Hkv).  Scale 1/sqrt(hd).
 //
-// KV pages hold 16 tokens: K as [page][Hkv][16][hd] and V transposed as
-// [page][Hkv][hd][16].  The bf16 kernel assigns one wave per (rows of one
-// sequence, kv head, key range) and runs both products on MFMA:
+// KV pages hold 16 tokens per (page, kv head) block, in the operand order of
+// kv_layout.h for bf16 (K as [16][hd] and V transposed as [hd][16] for fp32).
+// The bf16 kernel gives each workgroup of W waves one (rows of one sequence,
+// kv head, key range) work item and runs both products on MFMA:
 //   S^T = K Q^T : A = 16 keys x 32 dims of K, B = 32 dims x 16 query vectors.
 //   O^T = V^T P^T: A = 16 dims x 32 keys of V^T, B = P^T.
 // Keys inside each 32-key chunk are permuted (A row i of key tile h reads key
 // 8 (i / 4) + 4 h + i % 4) so that the S^T accumulators a lane ends up with are
 // exactly the 8 consecutive keys it must supply as the P^T operand, and the
 // softmax statistics of query vector (l % 16) stay lane-local: no shuffles of
-// P, no LDS.  Every K and V^T operand is one contiguous 16-byte load.  Long
-// contexts are split into key ranges (multiples of 32) whose unnormalised
-// partials a combine kernel merges.
+// P, no LDS in the loop.  With the page layout of kv_layout.h every K and V^T
+// operand load of a wave reads two contiguous 512-byte runs.  Long contexts
+// are split into key ranges (multiples of 32) whose unnormalised partials a
+// combine kernel merges.
 
+#include <algorithm>
 #include <cmath>
 
 #include "attention.h"
@@ -34,14 +37,17 @@ __device__ __forceinline__ uint32_t mask_pair(uint32_t w, int valid) {
   return valid >= 2 ? w : (valid == 1 ? (w & 0xFFFFu) : 0u);
 }
 
-template <int HD, int NT>
-__global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
+// W waves per workgroup share one work item: wave w takes the 32-key chunks
+// w, w + W, ... of the item's key range, and the waves' softmax states are
+// merged through LDS at the end (exact rescaling by exp2(m_w - m)).
+template <int HD, int NT, int W>
+__global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
   constexpr int DS = HD / 32;   // MFMA k-steps over the head dim
-  constexpr int DPL = HD / 4;   // contiguous dims per lane group
   constexpr int DT = HD / 16;   // 16-dim output tiles
   const AttnItem it = items[blockIdx.x];
   const int gkv = blockIdx.y;
-  const int lane = threadIdx.x, g = lane >> 4, l16 = lane & 15;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int g = lane >> 4, l16 = lane & 15;
   const int G = a.Hq / a.Hkv;
   const int M = it.nrows * G;
   const bf16_t* q = static_cast<const bf16_t*>(a.q);
@@ -56,7 +62,7 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
   const int np = it.t1 > it.t0 ? ((it.t1 - 1) >> 4) - p0 + 1 : 0;
   const bool staged = np <= kAttnStagedPages;
   if (staged)
-    for (int i = lane; i < np; i += kWave) s_pt[i] = pt[p0 + i];
+    for (int i = threadIdx.x; i < np; i += kWave * W) s_pt[i] = pt[p0 + i];
   __syncthreads();
   auto page = [&](int t) { return staged ? s_pt[(t >> 4) - p0] : pt[t >> 4]; };
 
@@ -89,24 +95,28 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
   // K and V^T operands of one 32-key chunk (keys past t1 are clamped to a
   // valid address; their scores are masked and their V entries zeroed)
   auto load_chunk = [&](int c0, uint4 (&kf)[2][DS], uint4 (&vf)[DT]) {
+    // lanes 0-7 / 8-15 of a group read the chunk's first / second page:
+    // unit ((s * 2 + hh) * 4 + g) * 8 + l16 % 8 of the page's K block holds
+    // dims 32 s + 8 g .. of key 8 (l16 / 4) + 4 hh + l16 % 4 (kv_layout.h)
+    const int tk = min(c0 + 16 * (l16 >> 3), it.t1 - 1);
+    const uint4* kb = reinterpret_cast<const uint4*>(kp + static_cast<size_t>(page(tk) * a.Hkv + gkv) * 16 * HD);
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int t = min(c0 + 8 * (l16 >> 2) + 4 * hh + (l16 & 3), it.t1 - 1);
-      const bf16_t* kb =
-          kp + (static_cast<size_t>(page(t) * a.Hkv + gkv) * 16 + (t & 15)) * HD + g * 8;
+    for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-      for (int s = 0; s < DS; ++s) kf[hh][s] = ld_stream(reinterpret_cast<const uint4*>(kb) + 4 * s);
-    }
+      for (int s = 0; s < DS; ++s) kf[hh][s] = ld_stream(kb + ((s * 2 + hh) * 4 + g) * 8 + (l16 & 7));
+    // V^T: unit (dt * 2 + g % 2) * 16 + l16 holds keys 8 (g % 2) .. + 7 of
+    // dim 16 dt + l16 of page (c0 + 8 g) / 16
     const int tvc = min(c0 + 8 * g, it.t1 - 1);
-    const bf16_t* vb = vp + static_cast<size_t>(page(tvc) * a.Hkv + gkv) * HD * 16 + (tvc & 8);
+    const uint4* vb = reinterpret_cast<const uint4*>(vp + static_cast<size_t>(page(tvc) * a.Hkv + gkv) * HD * 16);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vf[dt] = ld_stream(reinterpret_cast<const uint4*>(vb + (16 * dt + l16) * 16));
+    for (int dt = 0; dt < DT; ++dt) vf[dt] = ld_stream(vb + (dt * 2 + (g & 1)) * 16 + l16);
   };
   uint4 kf[2][DS], vf[DT], kn[2][DS], vn[DT];
-  load_chunk(it.t0, kf, vf);
-  for (int c0 = it.t0; c0 < it.t1; c0 += 32) {
-    const bool more = c0 + 32 < it.t1;
-    if (more) load_chunk(c0 + 32, kn, vn);
+  const int cfirst = it.t0 + 32 * wave;
+  if (cfirst < it.t1) load_chunk(cfirst, kf, vf);
+  for (int c0 = cfirst; c0 < it.t1; c0 += 32 * W) {
+    const bool more = c0 + 32 * W < it.t1;
+    if (more) load_chunk(c0 + 32 * W, kn, vn);
     const int tv = c0 + 8 * g;
     const int nvalid = min(max(it.t1 - tv, 0), 8);
 
@@ -175,11 +185,56 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
     }
   }
 
+  float ltot[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float lt = lrun[nt];
     lt += __shfl_xor(lt, 16, kWave);
     lt += __shfl_xor(lt, 32, kWave);
+    ltot[nt] = lt;
+  }
+  if (W > 1) {
+    // waves 1..W-1 hand their state to wave 0 (same lane layout in every wave)
+    __shared__ float s_acc[W > 1 ? W - 1 : 1][NT][DT][4][kWave];
+    __shared__ float s_ml[W > 1 ? W - 1 : 1][NT][2][kWave];
+    if (wave > 0) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        s_ml[wave - 1][nt][0][lane] = mrun[nt];
+        s_ml[wave - 1][nt][1][lane] = ltot[nt];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) s_acc[wave - 1][nt][dt][r][lane] = acc[dt][nt][r];
+      }
+    }
+    __syncthreads();
+    if (wave > 0) return;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      float mm = mrun[nt];
+      for (int w = 0; w < W - 1; ++w) mm = fmaxf(mm, s_ml[w][nt][0][lane]);
+      if (mm == -INFINITY) continue;  // no key of the item for this query vector
+      const float e0 = (mrun[nt] == -INFINITY) ? 0.f : exp2f(mrun[nt] - mm);
+      float lt = ltot[nt] * e0;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) acc[dt][nt] *= e0;
+      for (int w = 0; w < W - 1; ++w) {
+        const float mw = s_ml[w][nt][0][lane];
+        const float ew = (mw == -INFINITY) ? 0.f : exp2f(mw - mm);
+        lt += ew * s_ml[w][nt][1][lane];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[dt][nt][r] += ew * s_acc[w][nt][dt][r][lane];
+      }
+      mrun[nt] = mm;
+      ltot[nt] = lt;
+    }
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const float lt = ltot[nt];
     const int m = 16 * nt + l16;
     if (m >= M) continue;
     if (it.part < 0) {
@@ -207,29 +262,50 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnArgs a, const AttnIte
   }
 }
 
-// One workgroup per (group, kv head, query vector), one thread per head dim:
-// the partials' loads are independent across parts and coalesced across dims.
+// One workgroup per (group, kv head, 4 query vectors), one thread per (query
+// vector, head dim).  Two passes over the parts (maximum, then weighted
+// sums), each issuing its loads in batches of 8 independent loads before
+// using them, coalesced across dims.
+constexpr int kCombineQv = 4;
+
 template <int HD>
-__global__ __launch_bounds__(HD) void attn_combine_kernel(AttnArgs a, const AttnGroup* __restrict__ groups) {
+__global__ __launch_bounds__(HD * kCombineQv) void attn_combine_kernel(AttnArgs a,
+                                                                        const AttnGroup* __restrict__ groups) {
+  constexpr int B = 8;
   const AttnGroup gr = groups[blockIdx.x];
-  const int gkv = blockIdx.y, m = blockIdx.z;
+  const int gkv = blockIdx.y;
+  const int m = blockIdx.z * kCombineQv + static_cast<int>(threadIdx.x) / HD;
   const int G = a.Hq / a.Hkv;
   if (m >= gr.nrows * G) return;
-  const int d = threadIdx.x;
+  const int d = threadIdx.x % HD;
+  const int n = gr.nparts;
   const size_t base = static_cast<size_t>(gr.part0 * a.Hkv + gkv) * 64 + m;
   const size_t stride = static_cast<size_t>(a.Hkv) * 64;
   float mx = -INFINITY;
-#pragma unroll 8
-  for (int c = 0; c < gr.nparts; ++c) mx = fmaxf(mx, a.part_ml[(base + c * stride) * 2]);
+  for (int c0 = 0; c0 < n; c0 += B) {
+    float mc[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) mc[j] = a.part_ml[(base + min(c0 + j, n - 1) * stride) * 2];
+#pragma unroll
+    for (int j = 0; j < B; ++j) mx = fmaxf(mx, mc[j]);
+  }
   float num = 0.f, den = 0.f;
   if (mx != -INFINITY) {
-#pragma unroll 8
-    for (int c = 0; c < gr.nparts; ++c) {
-      const size_t pm = base + c * stride;
-      const float mc = a.part_ml[pm * 2];
-      const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - mx);
-      num += w * a.part_o[pm * HD + d];
-      den += w * a.part_ml[pm * 2 + 1];
+    for (int c0 = 0; c0 < n; c0 += B) {
+      float mc[B], lc[B], oc[B];
+#pragma unroll
+      for (int j = 0; j < B; ++j) {
+        const size_t pm = base + min(c0 + j, n - 1) * stride;
+        mc[j] = a.part_ml[pm * 2];
+        lc[j] = a.part_ml[pm * 2 + 1];
+        oc[j] = a.part_o[pm * HD + d];
+      }
+#pragma unroll
+      for (int j = 0; j < B; ++j) {
+        const float w = (c0 + j < n && mc[j] != -INFINITY) ? exp2f(mc[j] - mx) : 0.f;
+        num += w * oc[j];
+        den += w * lc[j];
+      }
     }
   }
   const size_t o = (static_cast<size_t>(gr.row0 + m / G) * a.Hq + gkv * G + m % G) * HD + d;
@@ -292,33 +368,48 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, const int32_t*
   }
 }
 
+template <int HD, int NT>
+void launch_item_kernel(const AttnArgs& a, const AttnItem* items, dim3 grid, int w, hipStream_t st) {
+  if (w >= 4) attn_bf16_kernel<HD, NT, 4><<<grid, 4 * kWave, 0, st>>>(a, items);
+  else if (w == 2) attn_bf16_kernel<HD, NT, 2><<<grid, 2 * kWave, 0, st>>>(a, items);
+  else attn_bf16_kernel<HD, NT, 1><<<grid, kWave, 0, st>>>(a, items);
+}
+
 template <int HD>
 hipError_t launch_bf16_hd(const AttnArgs& a, const AttnItem* items, int n_items,
-                          const AttnGroup* groups, int n_groups, int nt, hipStream_t st) {
+                          const AttnGroup* groups, int n_groups, int nt, int w, hipStream_t st) {
   dim3 grid(n_items, a.Hkv);
   if (n_items > 0) {
-    if (nt <= 1) attn_bf16_kernel<HD, 1><<<grid, 64, 0, st>>>(a, items);
-    else if (nt == 2) attn_bf16_kernel<HD, 2><<<grid, 64, 0, st>>>(a, items);
-    else attn_bf16_kernel<HD, 4><<<grid, 64, 0, st>>>(a, items);
+    if (nt <= 1) launch_item_kernel<HD, 1>(a, items, grid, w, st);
+    else if (nt == 2) launch_item_kernel<HD, 2>(a, items, grid, w, st);
+    else launch_item_kernel<HD, 4>(a, items, grid, std::min(w, 2), st);
   }
-  if (n_groups > 0) attn_combine_kernel<HD><<<dim3(n_groups, a.Hkv, 16 * nt), HD, 0, st>>>(a, groups);
+  if (n_groups > 0)
+    attn_combine_kernel<HD><<<dim3(n_groups, a.Hkv, 16 * nt / kCombineQv), HD * kCombineQv, 0, st>>>(a, groups);
   return hipGetLastError();
 }
 
 }  // namespace
 
-const char* attn_kernel_name(int hd, int nt) {
-  static const char* n128[3] = {"attn_bf16_kernel<128, 1>", "attn_bf16_kernel<128, 2>", "attn_bf16_kernel<128, 4>"};
-  static const char* n64[3] = {"attn_bf16_kernel<64, 1>", "attn_bf16_kernel<64, 2>", "attn_bf16_kernel<64, 4>"};
+const char* attn_kernel_name(int hd, int nt, int w) {
+  // [hd 64 / 128][nt 1 / 2 / 4][w 1 / 2 / 4]
+  static const char* names[2][3][3] = {
+      {{"attn_bf16_kernel<64, 1, 1>", "attn_bf16_kernel<64, 1, 2>", "attn_bf16_kernel<64, 1, 4>"},
+       {"attn_bf16_kernel<64, 2, 1>", "attn_bf16_kernel<64, 2, 2>", "attn_bf16_kernel<64, 2, 4>"},
+       {"attn_bf16_kernel<64, 4, 1>", "attn_bf16_kernel<64, 4, 2>", "attn_bf16_kernel<64, 4, 2>"}},
+      {{"attn_bf16_kernel<128, 1, 1>", "attn_bf16_kernel<128, 1, 2>", "attn_bf16_kernel<128, 1, 4>"},
+       {"attn_bf16_kernel<128, 2, 1>", "attn_bf16_kernel<128, 2, 2>", "attn_bf16_kernel<128, 2, 4>"},
+       {"attn_bf16_kernel<128, 4, 1>", "attn_bf16_kernel<128, 4, 2>", "attn_bf16_kernel<128, 4, 2>"}}};
   const int i = nt <= 1 ? 0 : (nt == 2 ? 1 : 2);
-  return hd == 128 ? n128[i] : n64[i];
+  const int j = w <= 1 ? 0 : (w == 2 ? 1 : 2);
+  return names[hd == 128 ? 1 : 0][i][j];
 }
 
 hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int n_items,
-                                 const AttnGroup* d_groups, int n_groups, int nt, hipStream_t st) {
-  if (nt > 4) return hipErrorInvalidValue;
-  if (a.hd == 128) return launch_bf16_hd<128>(a, d_items, n_items, d_groups, n_groups, nt, st);
-  if (a.hd == 64) return launch_bf16_hd<64>(a, d_items, n_items, d_groups, n_groups, nt, st);
+                                 const AttnGroup* d_groups, int n_groups, int nt, int w, hipStream_t st) {
+  if (nt > 4 || w > 4) return hipErrorInvalidValue;
+  if (a.hd == 128) return launch_bf16_hd<128>(a, d_items, n_items, d_groups, n_groups, nt, w, st);
+  if (a.hd == 64) return launch_bf16_hd<64>(a, d_items, n_items, d_groups, n_groups, nt, w, st);
   return hipErrorInvalidValue;
 }
 

@@ -6,9 +6,22 @@
 
 #include "common.h"
 #include "elem.h"
+#include "kv_layout.h"
 
 namespace spec {
 namespace {
+
+// Index of (token k of the page, dim d) in a (page, kv head) block: the bf16
+// cache uses the operand order of the attention kernel (kv_layout.h), the
+// fp32 cache K [16][hd] and V^T [hd][16].
+template <typename T>
+__device__ __forceinline__ int k_index(int k, int d, int hd) {
+  return sizeof(T) == 2 ? kv_k_off(k, d) : k * hd + d;
+}
+template <typename T>
+__device__ __forceinline__ int v_index(int k, int d) {
+  return sizeof(T) == 2 ? kv_v_off(k, d) : d * 16 + k;
+}
 
 template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(int d, const int32_t* __restrict__ tok_src,
@@ -94,16 +107,15 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
       o[i] = Elem<T>::from_f32(ra);
       o[i + half] = Elem<T>::from_f32(rb);
     } else {
-      const int kh = head - Hq;
-      T* o = kpool + ((static_cast<size_t>(page) * Hkv + kh) * 16 + off) * hd;
-      o[i] = Elem<T>::from_f32(ra);
-      o[i + half] = Elem<T>::from_f32(rb);
+      T* o = kpool + (static_cast<size_t>(page) * Hkv + (head - Hq)) * 16 * hd;
+      o[k_index<T>(off, i, hd)] = Elem<T>::from_f32(ra);
+      o[k_index<T>(off, i + half, hd)] = Elem<T>::from_f32(rb);
     }
   }
   const float* v = x + (Hq + Hkv) * hd;
   for (int e = threadIdx.x; e < Hkv * hd; e += blockDim.x) {
     const int kh = e / hd, dd = e % hd;
-    vpool[((static_cast<size_t>(page) * Hkv + kh) * hd + dd) * 16 + off] = Elem<T>::from_f32(v[e]);
+    vpool[(static_cast<size_t>(page) * Hkv + kh) * hd * 16 + v_index<T>(off, dd)] = Elem<T>::from_f32(v[e]);
   }
 }
 
@@ -117,8 +129,9 @@ __global__ __launch_bounds__(256) void kv_clear_kernel(const int32_t* __restrict
   T* V = K + v_off;
   for (int e = threadIdx.x; e < Hkv * hd; e += blockDim.x) {
     const int h = e / hd, dd = e % hd;
-    K[((static_cast<size_t>(page) * Hkv + h) * 16 + off) * hd + dd] = T(0);
-    V[((static_cast<size_t>(page) * Hkv + h) * hd + dd) * 16 + off] = T(0);
+    const size_t blk = (static_cast<size_t>(page) * Hkv + h) * 16 * hd;
+    K[blk + k_index<T>(off, dd, hd)] = T(0);
+    V[blk + v_index<T>(off, dd)] = T(0);
   }
 }
 

@@ -34,6 +34,7 @@
 
 #include "common.h"
 #include "gemm.h"
+#include "kv_layout.h"
 
 namespace spec {
 namespace {
@@ -174,12 +175,12 @@ __device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l1
         if (head < fu.Hq)
           static_cast<bf16_t*>(fu.qout)[(static_cast<size_t>(m) * fu.Hq + head) * fu.hd + dim] = f32_to_bf16(o);
         else
-          static_cast<bf16_t*>(fu.kpool)[((static_cast<size_t>(page) * fu.Hkv + (head - fu.Hq)) * 16 + off) * fu.hd + dim] =
-              f32_to_bf16(o);
+          static_cast<bf16_t*>(fu.kpool)[(static_cast<size_t>(page) * fu.Hkv + (head - fu.Hq)) * 16 * fu.hd +
+                                         kv_k_off(off, dim)] = f32_to_bf16(o);
       } else if (n < N) {
         const int vi = n - (fu.Hq + fu.Hkv) * fu.hd;
         const int kh = vi / fu.hd, dd = vi % fu.hd;
-        static_cast<bf16_t*>(fu.vpool)[((static_cast<size_t>(page) * fu.Hkv + kh) * fu.hd + dd) * 16 + off] =
+        static_cast<bf16_t*>(fu.vpool)[(static_cast<size_t>(page) * fu.Hkv + kh) * fu.hd * 16 + kv_v_off(off, dd)] =
             f32_to_bf16(v);
       }
     }

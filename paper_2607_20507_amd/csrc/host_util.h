@@ -164,20 +164,25 @@ class Stager {
 
 // Attention work for rows of one sequence: rows [row0, row0 + nrows) at
 // positions pos0.., page table row `seq` of the launch's compact table.
+// Workgroups an attention launch aims for (measured on the 8B/1B-shaped
+// verify and draft steps and the 64-sequence serving batch).
+constexpr int kAttnTargetWgs = 1024;
+
 struct AttnSegment {
   int32_t seq, row0, nrows, pos0;
 };
 
 struct AttnPlan {
   int nt = 1;
+  int w = 1;  // waves per workgroup
   std::vector<AttnItem> items;
   std::vector<AttnGroup> groups;
   int n_parts = 0;
 };
 
 // Tile rows into query tiles of (16 nt / G) rows and split key ranges so that
-// the launch has about `target_waves` waves; at most `max_parts` partials.
+// the launch has about `target_wgs` workgroups; at most `max_parts` partials.
 AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, int max_parts,
-                        int target_waves = 2048);
+                        int target_wgs = kAttnTargetWgs);
 
 }  // namespace spec

@@ -301,7 +301,7 @@ spec_status spec_op_attention(int32_t dtype, int32_t n_seqs, const int32_t* rows
     return hip_status(launch_attention_bf16(a, reinterpret_cast<const AttnItem*>(ws + oit),
                                             static_cast<int>(plan.items.size()),
                                             reinterpret_cast<const AttnGroup*>(ws + ogr),
-                                            static_cast<int>(plan.groups.size()), plan.nt, st));
+                                            static_cast<int>(plan.groups.size()), plan.nt, plan.w, st));
   return hip_status(launch_attention_f32(a, R, reinterpret_cast<const int32_t*>(ws + ors),
                                          reinterpret_cast<const int32_t*>(ws + orp), st));
 }

@@ -7,13 +7,14 @@
 namespace spec {
 
 AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, int max_parts,
-                        int target_waves) {
+                        int target_wgs) {
   AttnPlan p;
   int max_rows = 1;
   for (const auto& s : segs) max_rows = std::max(max_rows, s.nrows);
   // query vectors per tile: rows * G <= 16 * nt, nt in {1, 2, 4}
   const int want = std::min(max_rows * G, 64);
   p.nt = want <= 16 ? 1 : (want <= 32 ? 2 : 4);
+  p.w = p.nt >= 4 ? 2 : 4;  // waves per workgroup (LDS of the merge bounds it at nt = 4)
   const int qt = std::max(1, 16 * p.nt / G);
 
   struct Tile {
@@ -29,8 +30,10 @@ AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, in
       total_keys += kend;
     }
   }
-  long long split = (total_keys * Hkv + target_waves - 1) / std::max(1, target_waves);
-  split = std::max<long long>(64, (split + 31) / 32 * 32);
+  // key range per work item: about target_wgs workgroups over all (tile, kv
+  // head) pairs, at least one 32-key chunk per wave
+  long long split = (total_keys * Hkv + target_wgs - 1) / std::max(1, target_wgs);
+  split = std::max<long long>(32 * p.w, (split + 31) / 32 * 32);
   auto parts_for = [&](long long sp) {
     long long n = 0;
     for (const auto& t : tiles) {

@@ -114,6 +114,27 @@ def tiled_layout_ref(w, rot_rows=0, hd=0):
     return out
 
 
+def kv_block_index(hd):
+    """Position of (token k, dim d) inside one (page, kv head) block of the
+    bf16 KV cache, from the layout's definition: K unit
+    ((s*2 + h)*4 + g)*8 + j with c = d // 8, s = c // 4, g = c % 4,
+    h = (k // 4) % 2, j = k % 4 + 4 (k // 8); V unit ((d // 16)*2 + k // 8)*16
+    + d % 16; 8 elements per unit.  Returns (ik, iv), int64 [16, hd]."""
+    k = np.arange(16)[:, None]
+    d = np.arange(hd)[None, :]
+    c = d // 8
+    ik = ((((c // 4) * 2 + (k // 4) % 2) * 4 + c % 4) * 8 + (k % 4 + 4 * (k // 8))) * 8 + d % 8
+    iv = (((d // 16) * 2 + k // 8) * 16 + d % 16) * 8 + k % 8
+    return ik.astype(np.int64), iv.astype(np.int64)
+
+
+def test_kv_block_index_is_a_permutation():
+    for hd in (64, 128):
+        ik, iv = kv_block_index(hd)
+        assert np.array_equal(np.sort(ik.ravel()), np.arange(16 * hd))
+        assert np.array_equal(np.sort(iv.ravel()), np.arange(16 * hd))
+
+
 @pytest.mark.parametrize("rows,K,rot_rows,hd", [(32, 256, 0, 0), (40, 384, 0, 0), (7, 128, 0, 0),
                                                (6 * 64 + 24, 256, 4 * 64, 64), (3 * 128, 128, 2 * 128, 128)])
 def test_pack_weight_layout(rows, K, rot_rows, hd):
@@ -213,10 +234,16 @@ def test_rope_kv_append(dt, Hq, Hkv, hd, theta):
     tol = 1e-5 if dt == 0 else 8e-3
     assert rel_err(q.float().cpu().numpy(), qr) < tol
     kpn, vpn = kp.float().cpu().numpy(), vp.float().cpu().numpy()
+    ik, iv = kv_block_index(hd)
     for r in range(R):
         pg, off = divmod(int(slots[r]), 16)
-        assert rel_err(kpn[pg, :, off, :], kr[r]) < tol
-        assert rel_err(vpn[pg, :, :, off], vr[r]) < tol
+        if dt == 0:
+            kg, vg = kpn[pg, :, off, :], vpn[pg, :, :, off]
+        else:  # bf16 blocks are in the attention operand order
+            kg = kpn[pg].reshape(Hkv, 16 * hd)[:, ik[off]]
+            vg = vpn[pg].reshape(Hkv, 16 * hd)[:, iv[off]]
+        assert rel_err(kg, kr[r]) < tol
+        assert rel_err(vg, vr[r]) < tol
 
 
 # ---------------------------------------------------------------------------
@@ -251,6 +278,14 @@ def _attn_case(dt, rows, pos0, Hq, Hkv, hd, seed, check_seqs=None):
         t = torch.arange(ctx[i], device=dev)
         kpool[pg[t // 16], :, t % 16, :] = K
         vpool.permute(0, 3, 1, 2)[pg[t // 16], t % 16, :, :] = V
+    if dt == 1:  # bf16 blocks in the attention operand order
+        ik, iv = (torch.from_numpy(a).to(dev) for a in kv_block_index(hd))
+        P = kpool.shape[0]
+        kt = torch.empty(P, Hkv, 16 * hd, device=dev)
+        vt = torch.empty(P, Hkv, 16 * hd, device=dev)
+        kt[:, :, ik.reshape(-1)] = kpool.reshape(P, Hkv, 16 * hd)
+        vt[:, :, iv.reshape(-1)] = vpool.permute(0, 1, 3, 2).reshape(P, Hkv, 16 * hd)
+        kpool, vpool = kt.reshape(P, Hkv, 16, hd), vt.reshape(P, Hkv, hd, 16)
     kpool, vpool = kpool.to(et), vpool.to(et)
     R = sum(rows)
     g = torch.Generator(device=dev)
