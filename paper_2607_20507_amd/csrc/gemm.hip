@@ -21,10 +21,11 @@
 //    the gate tile and its up tile); its waves split K and reduce through LDS
 //    in a fixed order (deterministic, no atomics).  M is padded to 16 per
 //    tile; MFMA throughput is ~10x what the weight stream needs.
-//  * mfma (R > 64): 128x256 workgroup tiles, BK = 32, two workgroups per CU,
-//    loads two k-steps ahead, LDS double buffering with an XOR swizzle of
-//    16-byte chunks, 4 waves of 64x128, XCD-aware tile order, split-K with a
-//    fixed-order reduction when the grid is small.
+//  * mfma2 (R > 64, and the LM head / large projections above 8 / 40 rows):
+//    (32 MTW) x 256 workgroup tiles, one workgroup per CU, accumulators in
+//    AGPRs, X and W brought into LDS by direct-to-LDS loads four k-steps
+//    ahead, XCD-aware tile order, split-K with a fixed-order reduction when
+//    the grid is small.
 //  * fp32 (the fp32 configuration): a plain LDS-tiled FMA kernel on row-major
 //    weights; no reduced-precision arithmetic.
 
@@ -426,33 +427,79 @@ hipError_t gemv(int R, int N, int K, const void* X, const void* W, void* Y, hipS
 }
 
 // ---------------------------------------------------------------------------
-// MFMA bf16 for R > 64: 128 x 256 workgroup tile (256 W rows; 128 gate + 128
-// up rows for SwiGLU), BK = 32, 4 waves of 64 x 128.  Two workgroups share a
-// CU (48 KB of LDS and at most 256 registers per lane each), so one
-// workgroup's MFMAs cover the other's barrier and load waits.  Global loads
-// run two k-steps ahead through two register staging sets: tile kt+2 is in
-// flight while tile kt is multiplied and tile kt+1 waits to be stored into the
-// LDS double buffer (XOR-swizzled 16-byte chunks, one barrier per k-step).
-// The 1-D grid is decoded XCD-aware: workgroups are dispatched round-robin
-// over the 8 XCDs, so consecutive tile ids are mapped to one XCD, and the row
-// tiles of a column tile are consecutive, sharing that XCD's L2 for the W tile.
-// Split-K writes raw fp32 partials by W row; a reduction pass applies the
-// epilogue in a fixed order.
+// MFMA bf16, large tiles fed by direct-to-LDS loads: workgroup tile (32 MTW)
+// rows x 256 W rows (128 gate + 128 up rows for SwiGLU), 4 waves as 2 (M) x
+// 2 (N) of (16 MTW) x 128, one workgroup per CU (the accumulators, MTW x 8
+// MFMA blocks, sit in the AGPR half of the register file).  Every k-step
+// (BK = 32) of X and W is brought into LDS by global_load_lds_dwordx4, which
+// writes each lane's 16 bytes in lane order with no register staging; four
+// LDS stages, k-steps k + 1 .. k + 4 in flight while step k is multiplied.
+// X: one load covers 16 rows x 64 bytes (chunks XOR-swizzled across banks).
+// W (tiled layout): one load is one 16 x 32 MFMA fragment of a tile (4 memory
+// rows x 256 bytes), so LDS holds the fragments in lane order and each lane
+// reads back its own 16 bytes.  The fragments of step k + 1 are read from LDS
+// while the MFMAs of step k run from registers; one barrier per k-step
+// publishes the next stage.  Stages are separate LDS arrays.  The 1-D grid
+// is decoded XCD-aware: workgroups are dispatched round-robin over the 8
+// XCDs, so consecutive tile ids go to one XCD and the row tiles of a W tile
+// share that XCD's L2.  Split-K writes raw fp32 partials by W row, which
+// splitk_reduce sums in a fixed order; k-splits are multiples of 128
+// (K % 128 == 0), so the step count is a multiple of 4 and the k-loop
+// unrolls by 4 without remainders.
 
-constexpr int kMM = 128, kMN = 256, kMK = 32;
-constexpr int kMCh = kMK / 8;           // 16-byte chunks per tile row per k-step
-constexpr int kMRows = 256 / kMCh;      // tile rows one staging pass covers
-constexpr int kMPA = kMM / kMRows, kMPB = kMN / kMRows;
+typedef __attribute__((address_space(3))) void* lptr_t;
 
-template <int EPI>
-__global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(const bf16_t* __restrict__ X,
-                                                         const bf16_t* __restrict__ W,
-                                                         void* __restrict__ Y, float* __restrict__ part,
-                                                         int R, int N, int K, int k_len, int MT, int NT,
-                                                         const int32_t* __restrict__ row_map) {
+// One global_load_lds_dwordx4: lane i's 16 bytes at base + off_bytes land in
+// LDS at byte lds + 16 i (M0 holds the LDS address; one wait state separates
+// the M0 write from the load).  Issued as inline asm so that the compiler's
+// own wait insertion (which cannot tell the LDS stages apart and would wait
+// for every load in flight before each LDS read) leaves these loads to the
+// explicit per-stage waits of the kernel.
+__device__ __forceinline__ void load_lds16(const void* base, uint32_t off_bytes, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1" ::"v"(off_bytes),
+      "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory", "m0");
+}
+// MFMA accumulating in place, as inline asm: each accumulator stays in one
+// AGPR tuple across the k-loop.  Compiler-generated MFMAs in this loop rotate
+// the loop-carried accumulators through spare AGPRs, with four copies and a
+// wait state per MFMA (measured in a register-only loop of 6 x 8 blocks:
+// 1.5 PFLOP/s compiler-generated, 2.15 PFLOP/s in place).  The s_nop covers a
+// VALU write of an operand or accumulator right before the MFMA; after the
+// loop the kernel passes every accumulator through one compiler-generated
+// MFMA, so that the reads of the epilogue follow an MFMA the compiler's
+// hazard checks know about.
+__device__ __forceinline__ void mfma_acc(f32x4& acc, const u32x4& a, const u32x4& b) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lptr_t)(p)));
+}
+
+// s_waitcnt for at most n outstanding vector-memory operations (vmcnt bits
+// [3:0] and [15:14]) and no outstanding LDS operation (lgkmcnt 0); expcnt is
+// left at its maximum.
+#define SPEC_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4))
+
+template <int EPI, int MTW>
+__global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restrict__ X,
+                                                          const bf16_t* __restrict__ W,
+                                                          void* __restrict__ Y, float* __restrict__ part,
+                                                          int R, int N, int K, int k_len, int MT, int NT,
+                                                          const int32_t* __restrict__ row_map) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
-  __shared__ u32x4 As[2][kMM * kMCh];
-  __shared__ u32x4 Bs[2][kMN * kMCh];
+  constexpr int TM = 32 * MTW;
+  constexpr int LA = TM / 64;       // X loads per wave per k-step (16 rows each)
+  constexpr int LB = 4;             // W fragment loads per wave per k-step
+  constexpr int NL = LA + LB;       // loads per wave per stage
+  constexpr int SAU = TM * 4;       // 16-byte units of X per stage
+  constexpr int STU = SAU + 256 * 4;
+  static_assert(MTW % 2 == 0, "MTW even");
+  __shared__ u32x4 st0[STU], st1[STU], st2[STU], st3[STU];
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1), wave = t / kWave;
   const int wm = wave & 1, wn = wave >> 1;
@@ -461,97 +508,132 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(const bf16_t* __restric
   const int xcd = nid & 7, slot = nid >> 3, per = total >> 3, rem = total & 7;
   const int tix = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
   const int mt = tix % MT, rest = tix / MT, sp = rest / NT, nt = rest % NT;
-  const int m0 = mt * kMM;
-  const int f0 = nt * (SW ? kMN / 2 : kMN);
+  const int m0 = mt * TM;
+  const int f0 = nt * (SW ? 128 : 256);
   const int kbeg = sp * k_len;
-  const int nk = (min(K, kbeg + k_len) - kbeg) / kMK;  // even: k_len and K - kbeg are multiples of 64
+  const int nk = (min(K, kbeg + k_len) - kbeg) / 32;  // multiple of 4
 
-  // staging: thread t moves chunk t % kMCh of tile rows t / kMCh + kMRows i.
-  // Rows past R or N are clamped to the last valid row: read, never written back.
-  const int sr = t / kMCh, sc = t % kMCh;
-  const int lds_st = sr * kMCh + (sc ^ (sr & (kMCh - 1)));
-  const bf16_t* xs = X + kbeg + sc * 8;
-  uint32_t aoff[kMPA];
+  // X load q of this wave: row group wave * LA + q.  LDS unit u of a group
+  // holds row u / 4, chunk (u % 4) ^ (u / 16): the XOR spreads the 16 rows a
+  // fragment read touches over all 64 banks.  Lane l of a load writes unit l,
+  // so it fetches that chunk.  Rows past R clamped (read, never written back).
+  uint32_t xo[LA];
 #pragma unroll
-  for (int i = 0; i < kMPA; ++i) aoff[i] = static_cast<uint32_t>(min(m0 + sr + kMRows * i, R - 1));
-  // W rows in the tiled layout: chunk ch of row n at bb + (ch % 16) * s1 + (ch / 16) * 128
-  size_t bb[kMPB];
-  int bs1[kMPB];
+  for (int q = 0; q < LA; ++q)
+    xo[q] = static_cast<uint32_t>(min(m0 + (wave * LA + q) * 16 + (lane >> 2), R - 1)) * K +
+            ((lane & 3) ^ (lane >> 4)) * 8;
+  // W load q of this wave: tile slot ts = wave * 4 + q (SwiGLU: slots 0-7 gate
+  // tiles f0 / 16 + ts, 8-15 the same up tiles); lane (l16, g) of k-step e
+  // reads, in a full tile, memory row tile * 16 + 4 ((e / 32) % 4) + g at
+  // chunk position l16 of block e / 128; a trailing partial tile is row-major
+  // (row clamped to N - 1); tiles past N clamp to the last one.  Element
+  // offsets fit 32 bits (checked by the launcher).
+  const int ntiles = (N + 15) / 16;
+  uint32_t wo[LB];
+  uint32_t wfull = 0;
 #pragma unroll
-  for (int i = 0; i < kMPB; ++i) {
-    const int br = sr + kMRows * i;
-    const int n = SW ? min(f0 + (br & 127), N - 1) : min(f0 + br, N - 1);
-    const ChunkAddr ca = chunk_addr(n, N, K);
-    bb[i] = ca.base + ((SW && br >= 128) ? static_cast<size_t>(N) * K : 0);
-    bs1[i] = ca.s1;
+  for (int q = 0; q < LB; ++q) {
+    const int ts = wave * 4 + q;
+    const int tile = min(SW ? (f0 / 16 + (ts & 7)) : (f0 / 16 + ts), ntiles - 1);
+    const uint32_t half = (SW && ts >= 8) ? static_cast<uint32_t>(N) * K : 0u;
+    const bool full = (tile + 1) * 16 <= N;
+    wfull |= full ? (1u << q) : 0u;
+    wo[q] = half + (full ? static_cast<uint32_t>(tile * 16 + g) * K + l16 * 8
+                         : static_cast<uint32_t>(min(tile * 16 + l16, N - 1)) * K + g * 8);
   }
-  const int ch0 = kbeg / 8 + sc;  // chunk of k-step 0
-  // native vector types keep the staging values in registers
-  u32x4 sa[kMPA], sb[kMPB], ta[kMPA], tb[kMPB];
-#define SPEC_MFMA_LOAD(SA, SB, KT)                                                                 \
-  do {                                                                                             \
-    const int ko_ = (KT) * kMK;                                                                    \
-    _Pragma("unroll") for (int i = 0; i < kMPA; ++i)                                               \
-        SA[i] = *reinterpret_cast<const u32x4*>(xs + static_cast<size_t>(aoff[i]) * K + ko_);      \
-    const int ch_ = ch0 + (KT) * kMCh;                                                             \
-    _Pragma("unroll") for (int i = 0; i < kMPB; ++i)                                               \
-        SB[i] = *reinterpret_cast<const u32x4*>(W + bb[i] + (ch_ & 15) * bs1[i] + (ch_ >> 4) * 128); \
-  } while (0)
-#define SPEC_MFMA_STORE(SA, SB, AL, BL)                                                            \
-  do {                                                                                             \
-    _Pragma("unroll") for (int i = 0; i < kMPA; ++i) AL[lds_st + 256 * i] = SA[i];                 \
-    _Pragma("unroll") for (int i = 0; i < kMPB; ++i) BL[lds_st + 256 * i] = SB[i];                 \
-  } while (0)
-
-  f32x4 acc[4][8];
+  auto issue = [&](u32x4* stage, int kt) {
+    const uint32_t e = kbeg + 32 * kt;
+    const uint32_t sb = lds_addr(stage);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int q = 0; q < LA; ++q) load_lds16(X, (xo[q] + e) * 2, sb + (wave * LA + q) * 1024);
+    const uint32_t of = ((e >> 5) & 3) * 4 * K + (e >> 7) * 128;
+#pragma unroll
+    for (int q = 0; q < LB; ++q)
+      load_lds16(W, (wo[q] + (((wfull >> q) & 1) ? of : e)) * 2, sb + (SAU + (wave * 4 + q) * 64) * 16);
+  };
+
+  f32x4 acc[MTW][8];
+#pragma unroll
+  for (int i = 0; i < MTW; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int c = g ^ (l16 & (kMCh - 1));  // chunk of k-group g in a fragment row
-#define SPEC_MFMA_COMPUTE(AL, BL)                                                                  \
+  // fragment reads: A row block i of the wave is row group MTW wm + i, lane
+  // (l16, g) at unit l16 * 4 + (g ^ l16 / 4); B fragment j is tile slot
+  // 8 wn + j (SwiGLU: gate slots 4 wn + j for j < 4, up slots 8 + 4 wn + j - 4),
+  // each lane at its own unit
+  auto read_frags = [&](const u32x4* stage, u32x4 (&fa)[MTW], u32x4 (&fb)[8]) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ts = SW ? ((j < 4 ? 0 : 8) + 4 * wn + (j & 3)) : (8 * wn + j);
+      fb[j] = stage[SAU + ts * 64 + lane];
+    }
+#pragma unroll
+    for (int i = 0; i < MTW; ++i) fa[i] = stage[(MTW * wm + i) * 64 + l16 * 4 + (g ^ (l16 >> 2))];
+  };
+  auto mma = [&](const u32x4 (&fa)[MTW], const u32x4 (&fb)[8]) {
+#pragma unroll
+    for (int i = 0; i < MTW; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) mfma_acc(acc[i][j], fa[i], fb[j]);
+  };
+  // Step k (fragments of k-step k already in registers): wait for this
+  // wave's loads of stage k + 1 (later stages stay in flight) and its LDS
+  // reads of stage k; a bare s_barrier publishes stage k + 1 to every wave and
+  // ends all reads of stage k, whose buffer is refilled with k-step k + 4;
+  // then the MFMAs of step k run while the fragments of step k + 1 are read.
+  // (A __syncthreads would wait for every outstanding load: its workgroup
+  // fence has to cover the LDS writes of the loads in flight.)  The signal
+  // fences keep the compiler from moving LDS accesses across the barrier.
+#define SPEC_M2_STEP(K_, SR, SN, FA, FB, GA, GB)                                                   \
   {                                                                                                \
-    u32x4 a[4], b[8];                                                                              \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) a[i] = AL[(64 * wm + 16 * i + l16) * kMCh + c];  \
-    _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                                \
-      const int r = SW ? ((j < 4) ? (64 * wn + 16 * j) : (128 + 64 * wn + 16 * (j - 4)))           \
-                       : (128 * wn + 16 * j);                                                      \
-      b[j] = BL[(r + l16) * kMCh + c];                                                             \
+    const int k_ = (K_);                                                                           \
+    if (k_ + 3 < nk) {                                                                             \
+      SPEC_WAIT_VM_LDS(2 * NL);                                                                    \
+    } else if (k_ + 2 < nk) {                                                                      \
+      SPEC_WAIT_VM_LDS(NL);                                                                        \
+    } else {                                                                                       \
+      SPEC_WAIT_VM_LDS(0);                                                                         \
     }                                                                                              \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                  \
-        _Pragma("unroll") for (int j = 0; j < 8; ++j) acc[i][j] = mfma16x16x32v(a[i], b[j], acc[i][j]); \
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);                                                       \
+    __builtin_amdgcn_s_barrier();                                                                  \
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);                                                       \
+    if (k_ + 4 < nk) issue(SR, k_ + 4);                                                            \
+    if (k_ + 1 < nk) read_frags(SN, GA, GB);                                                       \
+    mma(FA, FB);                                                                                   \
   }
-
-  // prefetches past the end are clamped, in-bounds reloads; the scheduling
-  // barriers keep each k-step's loads ahead of its MFMAs
+  u32x4 fa0[MTW], fb0[8], fa1[MTW], fb1[8];
   if (nk > 0) {
-    SPEC_MFMA_LOAD(sa, sb, 0);
-    SPEC_MFMA_STORE(sa, sb, As[0], Bs[0]);
-    SPEC_MFMA_LOAD(ta, tb, min(1, nk - 1));
+    issue(st0, 0);
+    issue(st1, 1);
+    issue(st2, 2);
+    issue(st3, 3);
+    SPEC_WAIT_VM_LDS(3 * NL);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    read_frags(st0, fa0, fb0);
   }
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    SPEC_MFMA_LOAD(sa, sb, min(kt + 2, nk - 1));
-    __builtin_amdgcn_sched_barrier(0);
-    SPEC_MFMA_COMPUTE(As[0], Bs[0]);
-    SPEC_MFMA_STORE(ta, tb, As[1], Bs[1]);
-    __syncthreads();
-    SPEC_MFMA_LOAD(ta, tb, min(kt + 3, nk - 1));
-    __builtin_amdgcn_sched_barrier(0);
-    SPEC_MFMA_COMPUTE(As[1], Bs[1]);
-    SPEC_MFMA_STORE(sa, sb, As[0], Bs[0]);
-    __syncthreads();
+  for (int kt = 0; kt < nk; kt += 4) {
+    SPEC_M2_STEP(kt, st0, st1, fa0, fb0, fa1, fb1);
+    SPEC_M2_STEP(kt + 1, st1, st2, fa1, fb1, fa0, fb0);
+    SPEC_M2_STEP(kt + 2, st2, st3, fa0, fb0, fa1, fb1);
+    SPEC_M2_STEP(kt + 3, st3, st0, fa1, fb1, fa0, fb0);
   }
-#undef SPEC_MFMA_COMPUTE
-#undef SPEC_MFMA_STORE
-#undef SPEC_MFMA_LOAD
+#undef SPEC_M2_STEP
+  {  // acc + 0 * 0 (exact), by MFMAs the compiler sees
+    const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < MTW; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = mfma16x16x32v(z, z, acc[i][j]);
+  }
 
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MTW; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
+      const int m = m0 + 16 * MTW * wm + 16 * i + 4 * g + r;
       if (m >= R) continue;
       if (part) {
         float* pr = part + (static_cast<size_t>(sp) * R + m) * (SW ? 2 * N : N);
@@ -710,42 +792,58 @@ hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hi
   return hipGetLastError();
 }
 
-// Split-K factor for the MFMA kernel: grids under 256 tiles are split so that
-// tiles x splits stays within one wave of the 256 CUs (measured at the
-// 364-row verify shapes: more splits lose to the partials' traffic and to
-// short k-loops), k-splits multiples of 64, partials within the workspace.
-template <int EPI>
-int mfma_splits(int R, int N, int K, size_t ws_bytes, int* k_len) {
-  const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
-  const int tiles = ((Nw + kMN - 1) / kMN) * ((R + kMM - 1) / kMM);
-  int S = 1;
-  if (ws_bytes && tiles < 256) {
-    S = std::max(1, std::min(8, 256 / tiles));
-    while (S > 1 && static_cast<size_t>(S) * R * Nw * sizeof(float) > ws_bytes) --S;
+// Rows per workgroup tile of gemm_mfma2_bf16 (32 MTW): the candidate
+// (128, 192, 256) that pads R least, the larger on a tie.
+int mfma2_mtw(int R) {
+  int best = 8, pad = (R + 255) / 256 * 256 - R;
+  for (int mtw : {6, 4}) {
+    const int tm = 32 * mtw, p = (R + tm - 1) / tm * tm - R;
+    if (p < pad) {
+      pad = p;
+      best = mtw;
+    }
   }
-  *k_len = ((K + S - 1) / S + 2 * kMK - 1) / (2 * kMK) * (2 * kMK);
-  return (K + *k_len - 1) / *k_len;
+  return best;
 }
 
-template <int EPI>
-hipError_t mfma(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
-                const int32_t* rm, float* ws, size_t ws_bytes) {
-  int k_len = K;
-  const int S = mfma_splits<EPI>(R, N, K, ws ? ws_bytes : 0, &k_len);
+template <int EPI, int MTW>
+hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st,
+                   const int32_t* rm, float* ws, size_t ws_bytes) {
   const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
-  const int MT = (R + kMM - 1) / kMM, NT = (Nw + kMN - 1) / kMN;
+  if (static_cast<double>(Nw) * K >= 2147483648.0 || static_cast<double>(R) * K >= 2147483648.0 || K % 128)
+    return hipErrorInvalidValue;  // 32-bit byte offsets; whole 128-wide blocks
+  const int MT = (R + 32 * MTW - 1) / (32 * MTW), NT = (Nw + 255) / 256;
+  // split K so that tiles x splits fills the 256 CUs about once (k-splits
+  // multiples of 64, partials within the workspace)
+  int S = 1;
+  if (ws && MT * NT < 192) {
+    S = std::max(1, std::min(8, 256 / (MT * NT)));
+    while (S > 1 && static_cast<size_t>(S) * R * Nw * sizeof(float) > ws_bytes) --S;
+  }
+  const int k_len = ((K + S - 1) / S + 127) / 128 * 128;
+  S = (K + k_len - 1) / k_len;
   const int grid = MT * NT * S;
-  const bf16_t* x = static_cast<const bf16_t*>(X);
-  const bf16_t* w = static_cast<const bf16_t*>(W);
   if (S <= 1) {
-    gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, MT, NT, rm);
+    gemm_mfma2_bf16<EPI, MTW><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, MT, NT, rm);
     return hipGetLastError();
   }
-  gemm_mfma_bf16<EPI><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, MT, NT, rm);
+  gemm_mfma2_bf16<EPI, MTW><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, MT, NT, rm);
   const size_t total = static_cast<size_t>(R) * N;
   const int blocks = static_cast<int>(std::min<size_t>(2048, (total + 255) / 256));
   splitk_reduce<EPI><<<blocks, 256, 0, st>>>(ws, S, R, N, Y, rm);
   return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t mfma2(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
+                 const int32_t* rm, float* ws, size_t ws_bytes) {
+  const bf16_t* x = static_cast<const bf16_t*>(X);
+  const bf16_t* w = static_cast<const bf16_t*>(W);
+  switch (mfma2_mtw(R)) {
+    case 4: return mfma2_t<EPI, 4>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    case 6: return mfma2_t<EPI, 6>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    default: return mfma2_t<EPI, 8>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+  }
 }
 
 // Skinny (weight streaming, X re-read per workgroup) or MFMA tiles (X staged
@@ -770,12 +868,12 @@ hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W
   }
   if (K % 128 != 0) return hipErrorInvalidValue;
   if (R <= kGemvRows) return gemv<EPI>(R, N, K, X, W, Y, st, rm, GemmFuse{});
-  if (use_mfma(R, EPI == kEpiSwiGLU ? 2 * N : N, K)) return mfma<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
+  if (use_mfma(R, EPI == kEpiSwiGLU ? 2 * N : N, K)) return mfma2<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
   if (R <= 16) return skinny<1, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 32) return skinny<2, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 48) return skinny<3, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 64) return skinny<4, EPI>(R, N, K, X, W, Y, st, rm);
-  return mfma<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
+  return mfma2<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
 }
 
 }  // namespace
@@ -793,11 +891,11 @@ hipError_t launch_pack_weight(void* W, int rows, int K, int rot_rows, int hd, hi
 }
 
 size_t gemm_splitk_bytes(int R_max, int Nw_max) {
-  // only grids of fewer than 256 tiles split, into S <= 256 / tiles parts, so
-  // the partials S * R * Nw stay below 256 * kMM * kMN floats; smaller
-  // problems need less
-  const size_t tiles = static_cast<size_t>((Nw_max + kMN - 1) / kMN) * ((R_max + kMM - 1) / kMM);
-  return std::min<size_t>(256, 8 * tiles) * kMM * kMN * sizeof(float);
+  // only grids of fewer than 192 tiles split, into S <= min(8, 256 / tiles)
+  // parts; tiles >= R Nw / (256 * 256), so the partials S R Nw stay below
+  // 256 * 256 * 256 floats (and below 8 R Nw)
+  const double cap = std::min(8.0 * R_max * Nw_max, 256.0 * 256.0 * 256.0);
+  return static_cast<size_t>(cap) * sizeof(float);
 }
 
 hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, void* Y, int epi,
@@ -840,9 +938,12 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
   if (fused) return names[0][epi][1];
   if (epi > 2) return "";
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
-  static const char* tiled[3] = {"gemm_mfma_bf16<0>", "gemm_mfma_bf16<1>", "gemm_mfma_bf16<2>"};
+  static const char* tiled[3][3] = {
+      {"gemm_mfma2_bf16<0, 4>", "gemm_mfma2_bf16<0, 6>", "gemm_mfma2_bf16<0, 8>"},
+      {"gemm_mfma2_bf16<1, 4>", "gemm_mfma2_bf16<1, 6>", "gemm_mfma2_bf16<1, 8>"},
+      {"gemm_mfma2_bf16<2, 4>", "gemm_mfma2_bf16<2, 6>", "gemm_mfma2_bf16<2, 8>"}};
   if (dtype == 0) return f32[epi];
-  if (use_mfma(R, epi == kEpiSwiGLU ? 2 * N : N, K)) return tiled[epi];
+  if (use_mfma(R, epi == kEpiSwiGLU ? 2 * N : N, K)) return tiled[epi][mfma2_mtw(R) / 2 - 2];
   return names[(std::max(R, 1) - 1) / 16][epi][0];
 }
 
