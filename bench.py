@@ -317,7 +317,7 @@ def bench_serving(args):
             on_clock.append(spans)
         return int(na.sum()) + n
 
-    kernel = args.kernel or "gemm_mfma2_bf16<2, 6>"
+    kernel = args.kernel or "gemm_mfma2_bf16<2, 6, 8>"
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0 = torch.cuda.Event(enable_timing=True)

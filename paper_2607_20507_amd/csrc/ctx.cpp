@@ -330,7 +330,7 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   // outputs (read-modify-write for the residual add), flops = 2 R N_w K.
   auto gemm = [&](int rows, int N, int K, const void* X, const void* W, void* Y, int epi,
                   const int32_t* rm, const GemmFuse* f = nullptr) -> hipError_t {
-    const bool timed = tm.wants(gemm_kernel_name(dt, rows, N, K, epi, f != nullptr));
+    const bool timed = tm.wants(gemm_kernel_name(dt, rows, N, K, epi, f != nullptr, ctx->ws.splitk_bytes));
     if (timed) tm.begin(st);
     const hipError_t e =
         f ? launch_gemm_fused(rows, N, K, X, W, Y, epi, *f, st, rm)

@@ -67,8 +67,9 @@ hipError_t launch_pack_weight(void* W, int rows, int K, int rot_rows, int hd, hi
 // Bytes of split-K workspace that cover every launch shape.
 size_t gemm_splitk_bytes(int R_max, int Nw_max);
 
-// Profiler name of the kernel launch_gemm uses for (dtype, R, N, K, epi), or
-// launch_gemm_fused when fused.
-const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused = false);
+// Profiler name of the kernel launch_gemm uses for (dtype, R, N, K, epi) with
+// a split-K workspace of splitk_bytes, or launch_gemm_fused when fused.
+const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused = false,
+                             size_t splitk_bytes = 0);
 
 }  // namespace spec

@@ -485,7 +485,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // left at its maximum.
 #define SPEC_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4))
 
-template <int EPI, int MTW>
+template <int EPI, int MTW, int NTW>
 __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restrict__ X,
                                                           const bf16_t* __restrict__ W,
                                                           void* __restrict__ Y, float* __restrict__ part,
@@ -493,12 +493,13 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
                                                           const int32_t* __restrict__ row_map) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
   constexpr int TM = 32 * MTW;
+  constexpr int NTG = 2 * NTW;      // 16-feature W tiles per workgroup
   constexpr int LA = TM / 64;       // X loads per wave per k-step (16 rows each)
-  constexpr int LB = 4;             // W fragment loads per wave per k-step
+  constexpr int LB = NTG / 4;       // W fragment loads per wave per k-step
   constexpr int NL = LA + LB;       // loads per wave per stage
   constexpr int SAU = TM * 4;       // 16-byte units of X per stage
-  constexpr int STU = SAU + 256 * 4;
-  static_assert(MTW % 2 == 0, "MTW even");
+  constexpr int STU = SAU + NTG * 64;
+  static_assert(MTW % 2 == 0 && NTW % 2 == 0 && NTW >= 2, "MTW, NTW even");
   __shared__ u32x4 st0[STU], st1[STU], st2[STU], st3[STU];
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1), wave = t / kWave;
@@ -509,7 +510,7 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
   const int tix = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
   const int mt = tix % MT, rest = tix / MT, sp = rest / NT, nt = rest % NT;
   const int m0 = mt * TM;
-  const int f0 = nt * (SW ? 128 : 256);
+  const int f0 = nt * (SW ? 8 * NTG : 16 * NTG);
   const int kbeg = sp * k_len;
   const int nk = (min(K, kbeg + k_len) - kbeg) / 32;  // multiple of 4
 
@@ -522,8 +523,8 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
   for (int q = 0; q < LA; ++q)
     xo[q] = static_cast<uint32_t>(min(m0 + (wave * LA + q) * 16 + (lane >> 2), R - 1)) * K +
             ((lane & 3) ^ (lane >> 4)) * 8;
-  // W load q of this wave: tile slot ts = wave * 4 + q (SwiGLU: slots 0-7 gate
-  // tiles f0 / 16 + ts, 8-15 the same up tiles); lane (l16, g) of k-step e
+  // W load q of this wave: tile slot ts = wave * LB + q (SwiGLU: the first
+  // NTG / 2 slots gate tiles f0 / 16 + ts, the rest the same up tiles); lane (l16, g) of k-step e
   // reads, in a full tile, memory row tile * 16 + 4 ((e / 32) % 4) + g at
   // chunk position l16 of block e / 128; a trailing partial tile is row-major
   // (row clamped to N - 1); tiles past N clamp to the last one.  Element
@@ -533,9 +534,9 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
   uint32_t wfull = 0;
 #pragma unroll
   for (int q = 0; q < LB; ++q) {
-    const int ts = wave * 4 + q;
-    const int tile = min(SW ? (f0 / 16 + (ts & 7)) : (f0 / 16 + ts), ntiles - 1);
-    const uint32_t half = (SW && ts >= 8) ? static_cast<uint32_t>(N) * K : 0u;
+    const int ts = wave * LB + q;
+    const int tile = min(SW ? (f0 / 16 + ts % (NTG / 2)) : (f0 / 16 + ts), ntiles - 1);
+    const uint32_t half = (SW && ts >= NTG / 2) ? static_cast<uint32_t>(N) * K : 0u;
     const bool full = (tile + 1) * 16 <= N;
     wfull |= full ? (1u << q) : 0u;
     wo[q] = half + (full ? static_cast<uint32_t>(tile * 16 + g) * K + l16 * 8
@@ -549,33 +550,34 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
     const uint32_t of = ((e >> 5) & 3) * 4 * K + (e >> 7) * 128;
 #pragma unroll
     for (int q = 0; q < LB; ++q)
-      load_lds16(W, (wo[q] + (((wfull >> q) & 1) ? of : e)) * 2, sb + (SAU + (wave * 4 + q) * 64) * 16);
+      load_lds16(W, (wo[q] + (((wfull >> q) & 1) ? of : e)) * 2, sb + (SAU + (wave * LB + q) * 64) * 16);
   };
 
-  f32x4 acc[MTW][8];
+  f32x4 acc[MTW][NTW];
 #pragma unroll
   for (int i = 0; i < MTW; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NTW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // fragment reads: A row block i of the wave is row group MTW wm + i, lane
   // (l16, g) at unit l16 * 4 + (g ^ l16 / 4); B fragment j is tile slot
-  // 8 wn + j (SwiGLU: gate slots 4 wn + j for j < 4, up slots 8 + 4 wn + j - 4),
-  // each lane at its own unit
-  auto read_frags = [&](const u32x4* stage, u32x4 (&fa)[MTW], u32x4 (&fb)[8]) {
+  // NTW wn + j (SwiGLU: gate slots (NTW / 2) wn + j for j < NTW / 2, and the
+  // matching up slots NTG / 2 + (NTW / 2) wn + j - NTW / 2), each lane at its
+  // own unit
+  auto read_frags = [&](const u32x4* stage, u32x4 (&fa)[MTW], u32x4 (&fb)[NTW]) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int ts = SW ? ((j < 4 ? 0 : 8) + 4 * wn + (j & 3)) : (8 * wn + j);
+    for (int j = 0; j < NTW; ++j) {
+      const int ts = SW ? ((j < NTW / 2 ? 0 : NTG / 2) + (NTW / 2) * wn + j % (NTW / 2)) : (NTW * wn + j);
       fb[j] = stage[SAU + ts * 64 + lane];
     }
 #pragma unroll
     for (int i = 0; i < MTW; ++i) fa[i] = stage[(MTW * wm + i) * 64 + l16 * 4 + (g ^ (l16 >> 2))];
   };
-  auto mma = [&](const u32x4 (&fa)[MTW], const u32x4 (&fb)[8]) {
+  auto mma = [&](const u32x4 (&fa)[MTW], const u32x4 (&fb)[NTW]) {
 #pragma unroll
     for (int i = 0; i < MTW; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) mfma_acc(acc[i][j], fa[i], fb[j]);
+      for (int j = 0; j < NTW; ++j) mfma_acc(acc[i][j], fa[i], fb[j]);
   };
   // Step k (fragments of k-step k already in registers): wait for this
   // wave's loads of stage k + 1 (later stages stay in flight) and its LDS
@@ -602,7 +604,7 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
     if (k_ + 1 < nk) read_frags(SN, GA, GB);                                                       \
     mma(FA, FB);                                                                                   \
   }
-  u32x4 fa0[MTW], fb0[8], fa1[MTW], fb1[8];
+  u32x4 fa0[MTW], fb0[NTW], fa1[MTW], fb1[NTW];
   if (nk > 0) {
     issue(st0, 0);
     issue(st1, 1);
@@ -626,7 +628,7 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
 #pragma unroll
     for (int i = 0; i < MTW; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] = mfma16x16x32v(z, z, acc[i][j]);
+      for (int j = 0; j < NTW; ++j) acc[i][j] = mfma16x16x32v(z, z, acc[i][j]);
   }
 
 #pragma unroll
@@ -638,13 +640,13 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
       if (part) {
         float* pr = part + (static_cast<size_t>(sp) * R + m) * (SW ? 2 * N : N);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < NTW; ++j) {
           int n, wrow;
           if (SW) {
-            n = f0 + 64 * wn + 16 * (j & 3) + l16;
-            wrow = (j < 4 ? 0 : N) + n;
+            n = f0 + 8 * NTW * wn + 16 * (j % (NTW / 2)) + l16;
+            wrow = (j < NTW / 2 ? 0 : N) + n;
           } else {
-            n = f0 + 128 * wn + 16 * j + l16;
+            n = f0 + 16 * NTW * wn + 16 * j + l16;
             wrow = n;
           }
           if (n < N) pr[wrow] = acc[i][j][r];
@@ -654,15 +656,15 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
       const size_t mo = static_cast<size_t>(row_map ? row_map[m] : m);
       if (SW) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = f0 + 64 * wn + 16 * j + l16;
+        for (int j = 0; j < NTW / 2; ++j) {
+          const int n = f0 + 8 * NTW * wn + 16 * j + l16;
           if (n < N)
-            static_cast<bf16_t*>(Y)[mo * N + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + 4][r]);
+            static_cast<bf16_t*>(Y)[mo * N + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + NTW / 2][r]);
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int n = f0 + 128 * wn + 16 * j + l16;
+        for (int j = 0; j < NTW; ++j) {
+          const int n = f0 + 16 * NTW * wn + 16 * j + l16;
           if (n >= N) continue;
           float* y = static_cast<float*>(Y) + mo * N + n;
           if (EPI == kEpiStoreF32) *y = acc[i][j][r];
@@ -792,46 +794,83 @@ hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hi
   return hipGetLastError();
 }
 
-// Rows per workgroup tile of gemm_mfma2_bf16 (32 MTW): the candidate
-// (128, 192, 256) that pads R least, the larger on a tie.
-int mfma2_mtw(int R) {
-  int best = 8, pad = (R + 255) / 256 * 256 - R;
-  for (int mtw : {6, 4}) {
-    const int tm = 32 * mtw, p = (R + tm - 1) / tm * tm - R;
-    if (p < pad) {
-      pad = p;
-      best = mtw;
+// Split-K of gemm_mfma2_bf16: grids under 192 tiles are split so that
+// tiles x splits fills the 256 CUs about once (k-splits multiples of 128,
+// partials within the workspace).  Returns S and the k-split length.
+int mfma2_splits(int MT, int NT, int R, int Nw, int K, size_t ws_bytes, int* k_len) {
+  int S = 1;
+  if (ws_bytes && MT * NT < 192) {
+    S = std::max(1, std::min(8, 256 / (MT * NT)));
+    while (S > 1 && static_cast<size_t>(S) * R * Nw * sizeof(float) > ws_bytes) --S;
+  }
+  *k_len = ((K + S - 1) / S + 127) / 128 * 128;
+  return (K + *k_len - 1) / *k_len;
+}
+
+// Tile shape of gemm_mfma2_bf16: rows per workgroup 32 MTW (64 .. 256) and W
+// rows per workgroup 32 NTW (64 .. 256), the pair with the least estimated
+// time in a cost model fitted (least squares, median error 10%) to measured
+// launches of every shape at 64, 128 and 364 rows of the 8B/1B-shaped
+// projections: per-step terms for the MFMAs and the LDS loads of a
+// workgroup, times the k-steps and the rounds of workgroups over the 256
+// CUs, plus the split-K partial traffic.  Wide tiles waste rows or feed too
+// few CUs on small problems; narrow ones reload X and W more often.
+struct Mfma2Shape {
+  int mtw, ntw;
+};
+
+Mfma2Shape mfma2_shape(int R, int N, int Nw, int K, size_t ws_bytes) {
+  Mfma2Shape best{2, 2};
+  double best_t = 1e300;
+  for (int mtw : {2, 4, 6, 8}) {
+    if (32 * mtw > 2 * R + 64) continue;  // tiles far taller than R
+    for (int ntw : {2, 4, 8}) {
+      const int MT = (R + 32 * mtw - 1) / (32 * mtw), NT = (Nw + 32 * ntw - 1) / (32 * ntw);
+      int k_len = K;
+      const int S = mfma2_splits(MT, NT, R, Nw, K, ws_bytes, &k_len);
+      const double rounds = (MT * NT * S + 255) / 256;  // whole rounds of workgroups over the CUs
+      const double steps = rounds * (k_len / 32);
+      const double red_mb = S > 1 ? (S + 1.0) * R * N * 4.0 / 1e6 : 0.0;
+      const double t = 0.0119 * steps * mtw * ntw + 0.0056 * steps * (32.0 * (mtw + ntw)) * 64.0 / 1024.0 +
+                       0.0574 * steps + 0.3048 * red_mb + (S > 1 ? -6.41 : 0.0);
+      if (t < best_t) {
+        best_t = t;
+        best = {mtw, ntw};
+      }
     }
   }
   return best;
 }
 
-template <int EPI, int MTW>
+template <int EPI, int MTW, int NTW>
 hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st,
                    const int32_t* rm, float* ws, size_t ws_bytes) {
   const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
   if (static_cast<double>(Nw) * K >= 2147483648.0 || static_cast<double>(R) * K >= 2147483648.0 || K % 128)
     return hipErrorInvalidValue;  // 32-bit byte offsets; whole 128-wide blocks
-  const int MT = (R + 32 * MTW - 1) / (32 * MTW), NT = (Nw + 255) / 256;
-  // split K so that tiles x splits fills the 256 CUs about once (k-splits
-  // multiples of 64, partials within the workspace)
-  int S = 1;
-  if (ws && MT * NT < 192) {
-    S = std::max(1, std::min(8, 256 / (MT * NT)));
-    while (S > 1 && static_cast<size_t>(S) * R * Nw * sizeof(float) > ws_bytes) --S;
-  }
-  const int k_len = ((K + S - 1) / S + 127) / 128 * 128;
-  S = (K + k_len - 1) / k_len;
+  const int MT = (R + 32 * MTW - 1) / (32 * MTW), NT = (Nw + 32 * NTW - 1) / (32 * NTW);
+  int k_len = K;
+  const int S = mfma2_splits(MT, NT, R, Nw, K, ws ? ws_bytes : 0, &k_len);
   const int grid = MT * NT * S;
   if (S <= 1) {
-    gemm_mfma2_bf16<EPI, MTW><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, MT, NT, rm);
+    gemm_mfma2_bf16<EPI, MTW, NTW><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, MT, NT, rm);
     return hipGetLastError();
   }
-  gemm_mfma2_bf16<EPI, MTW><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, MT, NT, rm);
+  gemm_mfma2_bf16<EPI, MTW, NTW><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, MT, NT, rm);
   const size_t total = static_cast<size_t>(R) * N;
   const int blocks = static_cast<int>(std::min<size_t>(2048, (total + 255) / 256));
   splitk_reduce<EPI><<<blocks, 256, 0, st>>>(ws, S, R, N, Y, rm);
   return hipGetLastError();
+}
+
+template <int EPI, int MTW>
+hipError_t mfma2_m(int ntw, int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st,
+                   const int32_t* rm, float* ws, size_t ws_bytes) {
+  switch (ntw) {
+    case 2: return mfma2_t<EPI, MTW, 2>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    case 4: return mfma2_t<EPI, MTW, 4>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    default: return mfma2_t<EPI, MTW, 8>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+  }
 }
 
 template <int EPI>
@@ -839,21 +878,24 @@ hipError_t mfma2(int R, int N, int K, const void* X, const void* W, void* Y, hip
                  const int32_t* rm, float* ws, size_t ws_bytes) {
   const bf16_t* x = static_cast<const bf16_t*>(X);
   const bf16_t* w = static_cast<const bf16_t*>(W);
-  switch (mfma2_mtw(R)) {
-    case 4: return mfma2_t<EPI, 4>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
-    case 6: return mfma2_t<EPI, 6>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
-    default: return mfma2_t<EPI, 8>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+  const Mfma2Shape sh = mfma2_shape(R, N, EPI == kEpiSwiGLU ? 2 * N : N, K, ws ? ws_bytes : 0);
+  switch (sh.mtw) {
+    case 2: return mfma2_m<EPI, 2>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    case 4: return mfma2_m<EPI, 4>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    case 6: return mfma2_m<EPI, 6>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    default: return mfma2_m<EPI, 8>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
   }
 }
 
-// Skinny (weight streaming, X re-read per workgroup) or MFMA tiles (X staged
-// once per 128 rows): measured at 8..64 rows on the 1B-shaped projections, the
-// MFMA kernel wins for the 128256-row LM head above 8 rows and for the large
-// projections (>= 16M weights) above 40 rows.
+// Skinny (weight streaming, X re-read per 16-feature tile) or MFMA tiles (X
+// staged once per workgroup tile): measured at 9..64 rows on the 8B- and
+// 1B-shaped projections, the MFMA kernel wins above 40 rows, above 12 rows
+// for long reductions (K >= 8192) and the 128256-row LM heads, and above 24
+// rows for projections of >= 16M weights.
 bool use_mfma(int R, int Nw, int K) {
-  if (R > 64) return true;
-  if (R > 8 && Nw >= 65536) return true;
-  return R > 40 && static_cast<double>(Nw) * K >= 16.0 * (1 << 20);
+  if (R > 40) return true;
+  if (R > 12 && (K >= 8192 || Nw >= 65536)) return true;
+  return R > 24 && static_cast<double>(Nw) * K >= 16.0 * (1 << 20);
 }
 
 template <int EPI>
@@ -921,7 +963,7 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
   }
 }
 
-const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused) {
+const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused, size_t splitk_bytes) {
   static const char* gv[4] = {"gemv_bf16<0, 2>", "gemv_bf16<1, 2>", "gemv_bf16<2, 2>", "gemv_bf16<3, 2>"};
   if (dtype == 1 && R <= kGemvRows) return (epi >= 0 && epi <= 3) ? gv[epi] : "";
   // skinny names [MT - 1][epi][fused]
@@ -938,12 +980,20 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
   if (fused) return names[0][epi][1];
   if (epi > 2) return "";
   static const char* f32[3] = {"gemm_f32<0>", "gemm_f32<1>", "gemm_f32<2>"};
-  static const char* tiled[3][3] = {
-      {"gemm_mfma2_bf16<0, 4>", "gemm_mfma2_bf16<0, 6>", "gemm_mfma2_bf16<0, 8>"},
-      {"gemm_mfma2_bf16<1, 4>", "gemm_mfma2_bf16<1, 6>", "gemm_mfma2_bf16<1, 8>"},
-      {"gemm_mfma2_bf16<2, 4>", "gemm_mfma2_bf16<2, 6>", "gemm_mfma2_bf16<2, 8>"}};
+  static char tiled[3][4][3][40];
+  static std::once_flag once_t;
+  std::call_once(once_t, [] {
+    for (int e = 0; e < 3; ++e)
+      for (int m = 0; m < 4; ++m)
+        for (int n = 0; n < 3; ++n)
+          snprintf(tiled[e][m][n], sizeof(tiled[e][m][n]), "gemm_mfma2_bf16<%d, %d, %d>", e, 2 * m + 2, 2 << n);
+  });
   if (dtype == 0) return f32[epi];
-  if (use_mfma(R, epi == kEpiSwiGLU ? 2 * N : N, K)) return tiled[epi][mfma2_mtw(R) / 2 - 2];
+  const int Nw = epi == kEpiSwiGLU ? 2 * N : N;
+  if (use_mfma(R, Nw, K)) {
+    const Mfma2Shape sh = mfma2_shape(R, N, Nw, K, splitk_bytes);
+    return tiled[epi][sh.mtw / 2 - 1][sh.ntw == 2 ? 0 : (sh.ntw == 4 ? 1 : 2)];
+  }
   return names[(std::max(R, 1) - 1) / 16][epi][0];
 }
 

@@ -375,19 +375,41 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
 
 // One workgroup per row: row maximum, then the guide token's logit becomes
 // maximum + boost (all reads of the row finish before the write).
-__global__ __launch_bounds__(kThreads) void draft_guide_kernel(int V, const DRow* __restrict__ rows, float boost) {
+// One workgroup of 1024 threads per guided row: the row maximum with 16-byte
+// streaming loads, four in flight per thread, then z[guide] = max + boost.
+constexpr int kGuideThreads = 1024;
+
+__global__ __launch_bounds__(kGuideThreads) void draft_guide_kernel(int V, const DRow* __restrict__ rows,
+                                                                     float boost) {
   const DRow row = rows[blockIdx.x];
   if (row.guide < 0 || row.guide >= V) return;
   const float* z = row.ptr;
   float mx = -INFINITY;
-  for (int i = threadIdx.x; i < V; i += kThreads) mx = fmaxf(mx, z[i]);
+  int tail = 0;
+  if ((reinterpret_cast<uintptr_t>(z) & 15) == 0) {
+    const float4* p4 = reinterpret_cast<const float4*>(z);
+    const int n4 = V >> 2;
+    int i = threadIdx.x;
+    for (; i + 3 * kGuideThreads < n4; i += 4 * kGuideThreads) {
+      const float4 v0 = ld_stream(p4 + i), v1 = ld_stream(p4 + i + kGuideThreads);
+      const float4 v2 = ld_stream(p4 + i + 2 * kGuideThreads), v3 = ld_stream(p4 + i + 3 * kGuideThreads);
+      mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(v0.x, v0.y), fmaxf(v0.z, v0.w)), fmaxf(fmaxf(v1.x, v1.y), fmaxf(v1.z, v1.w))));
+      mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(v2.x, v2.y), fmaxf(v2.z, v2.w)), fmaxf(fmaxf(v3.x, v3.y), fmaxf(v3.z, v3.w))));
+    }
+    for (; i < n4; i += kGuideThreads) {
+      const float4 v = ld_stream(p4 + i);
+      mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+    }
+    tail = n4 * 4;
+  }
+  for (int i = tail + threadIdx.x; i < V; i += kGuideThreads) mx = fmaxf(mx, z[i]);
   mx = wave_max(mx);
-  __shared__ float part[kThreads / kWave];
+  __shared__ float part[kGuideThreads / kWave];
   if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = mx;
   __syncthreads();
   if (threadIdx.x == 0) {
     float m = part[0];
-    for (int w = 1; w < kThreads / kWave; ++w) m = fmaxf(m, part[w]);
+    for (int w = 1; w < kGuideThreads / kWave; ++w) m = fmaxf(m, part[w]);
     const_cast<float*>(z)[row.guide] = m + boost;
   }
 }
@@ -499,7 +521,7 @@ hipError_t launch_draft_sample(const DraftPlan& p, const DRow* d_rows, uint64_t 
 
 hipError_t launch_draft_guide(int n, int V, const DRow* d_rows, float boost, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  draft_guide_kernel<<<n, kThreads, 0, st>>>(V, d_rows, boost);
+  draft_guide_kernel<<<n, kGuideThreads, 0, st>>>(V, d_rows, boost);
   return hipGetLastError();
 }
 
