@@ -263,15 +263,17 @@ __global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const Att
 }
 
 // One workgroup per (group, kv head, 4 query vectors), one thread per (query
-// vector, head dim).  Two passes over the parts (maximum, then weighted
-// sums), each issuing its loads in batches of 8 independent loads before
-// using them, coalesced across dims.
+// vector, head dim).  Up to kCombineOnePass parts: every part's (max, sum)
+// and output element is loaded before the first is used (one round trip),
+// then the maximum and the weighted sums.  More parts: two passes (maximum,
+// then weighted sums), each issuing batches of 8 independent loads.  Both
+// sum the parts in index order.
 constexpr int kCombineQv = 4;
+constexpr int kCombineOnePass = 32;
 
 template <int HD>
 __global__ __launch_bounds__(HD * kCombineQv) void attn_combine_kernel(AttnArgs a,
                                                                         const AttnGroup* __restrict__ groups) {
-  constexpr int B = 8;
   const AttnGroup gr = groups[blockIdx.x];
   const int gkv = blockIdx.y;
   const int m = blockIdx.z * kCombineQv + static_cast<int>(threadIdx.x) / HD;
@@ -281,30 +283,57 @@ __global__ __launch_bounds__(HD * kCombineQv) void attn_combine_kernel(AttnArgs 
   const int n = gr.nparts;
   const size_t base = static_cast<size_t>(gr.part0 * a.Hkv + gkv) * 64 + m;
   const size_t stride = static_cast<size_t>(a.Hkv) * 64;
-  float mx = -INFINITY;
-  for (int c0 = 0; c0 < n; c0 += B) {
-    float mc[B];
-#pragma unroll
-    for (int j = 0; j < B; ++j) mc[j] = a.part_ml[(base + min(c0 + j, n - 1) * stride) * 2];
-#pragma unroll
-    for (int j = 0; j < B; ++j) mx = fmaxf(mx, mc[j]);
-  }
+  const float2* ml = reinterpret_cast<const float2*>(a.part_ml);
   float num = 0.f, den = 0.f;
-  if (mx != -INFINITY) {
-    for (int c0 = 0; c0 < n; c0 += B) {
-      float mc[B], lc[B], oc[B];
+  if (n <= kCombineOnePass) {
+    float2 mlc[kCombineOnePass];
+    float oc[kCombineOnePass];
 #pragma unroll
-      for (int j = 0; j < B; ++j) {
-        const size_t pm = base + min(c0 + j, n - 1) * stride;
-        mc[j] = a.part_ml[pm * 2];
-        lc[j] = a.part_ml[pm * 2 + 1];
+    for (int j = 0; j < kCombineOnePass; ++j)
+      if (j < n) {
+        const size_t pm = base + j * stride;
+        mlc[j] = ml[pm];
         oc[j] = a.part_o[pm * HD + d];
       }
+    float mx = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < B; ++j) {
-        const float w = (c0 + j < n && mc[j] != -INFINITY) ? exp2f(mc[j] - mx) : 0.f;
-        num += w * oc[j];
-        den += w * lc[j];
+    for (int j = 0; j < kCombineOnePass; ++j)
+      if (j < n) mx = fmaxf(mx, mlc[j].x);
+    if (mx != -INFINITY) {
+#pragma unroll
+      for (int j = 0; j < kCombineOnePass; ++j)
+        if (j < n) {
+          const float w = mlc[j].x != -INFINITY ? exp2f(mlc[j].x - mx) : 0.f;
+          num += w * oc[j];
+          den += w * mlc[j].y;
+        }
+    }
+  } else {
+    constexpr int B = 8;
+    float mx = -INFINITY;
+    for (int c0 = 0; c0 < n; c0 += B) {
+      float mc[B];
+#pragma unroll
+      for (int j = 0; j < B; ++j) mc[j] = ml[base + min(c0 + j, n - 1) * stride].x;
+#pragma unroll
+      for (int j = 0; j < B; ++j) mx = fmaxf(mx, mc[j]);
+    }
+    if (mx != -INFINITY) {
+      for (int c0 = 0; c0 < n; c0 += B) {
+        float2 mc[B];
+        float oc[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+          const size_t pm = base + min(c0 + j, n - 1) * stride;
+          mc[j] = ml[pm];
+          oc[j] = a.part_o[pm * HD + d];
+        }
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+          const float w = (c0 + j < n && mc[j].x != -INFINITY) ? exp2f(mc[j].x - mx) : 0.f;
+          num += w * oc[j];
+          den += w * mc[j].y;
+        }
       }
     }
   }

@@ -219,7 +219,7 @@ void compute_ws(spec_ctx* c) {
   w.dq = take(nq * c->V * 4);
   w.dtok = take(nq * 4);
   w.rowtok = take(R * 4);
-  w.ss = take(R * (c->d_max / 16 + 1) * 4);
+  w.ss = take(R * (c->d_max / 8 + 1) * 4);
   w.part_o = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * c->hd_max * 4);
   w.part_ml = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * 2 * 4);
   const int vrows = c->max_seqs * (2 * c->k_max + 1);

@@ -9,7 +9,7 @@ namespace spec {
 // h[r] = E[tok(r)] (fp32), tok(r) = tok_src[r] if >= 0 else tok_pool[-1 - tok_src[r]];
 // the resolved ids are written to row_tok[r].  Optional (for the fused GEMMs'
 // RMSNorm): hb[r] = h[r] (.) wn in the model dtype, and ss[r][j] = the sum of
-// squares of h[r][16 j .. 16 j + 15] (d % 16 == 0).
+// squares of h[r][8 j .. 8 j + 7] (d % 16 == 0).
 hipError_t launch_embed(int dtype, int R, int d, const int32_t* tok_src, const int32_t* tok_pool,
                         const void* E, float* h, int32_t* row_tok, hipStream_t st, void* hb = nullptr,
                         const void* wn = nullptr, float* ss = nullptr);

@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void embed_kernel(int d, const int32_t* __rest
   if (threadIdx.x == 0) row_tok[r] = tok;
   const T* e = E + static_cast<size_t>(tok) * d;
   float* o = h + static_cast<size_t>(r) * d;
-  // whole waves run every iteration: 16 consecutive lanes hold the 16
+  // whole waves run every iteration: 8 consecutive lanes hold the 8
   // columns whose sum of squares is one entry of ss
   for (int i0 = 0; i0 < d; i0 += blockDim.x) {
     const int i = i0 + threadIdx.x;
@@ -47,8 +47,8 @@ __global__ __launch_bounds__(256) void embed_kernel(int d, const int32_t* __rest
     if (ss) {
       float sq = x * x;
 #pragma unroll
-      for (int k = 1; k < 16; k <<= 1) sq += __shfl_xor(sq, k, kWave);
-      if ((threadIdx.x & 15) == 0 && i < d) ss[static_cast<size_t>(r) * (d / 16) + i / 16] = sq;
+      for (int k = 1; k < 8; k <<= 1) sq += __shfl_xor(sq, k, kWave);
+      if ((threadIdx.x & 7) == 0 && i < d) ss[static_cast<size_t>(r) * (d / 8) + i / 8] = sq;
     }
   }
 }

@@ -19,13 +19,13 @@ enum GemmEpi {
 struct GemmFuse {
   // Consumer side of RMSNorm: X holds rows bf16(h (.) w) written by the
   // producer, and output row m is scaled by 1/sqrt(mean(h[m]^2) + eps), the
-  // mean taken from `ss`, the producer's sums of squares per 16 columns
-  // ([rows][K / 16]).  xrow (optional): X and ss row of output row m.
+  // mean taken from `ss`, the producer's sums of squares per 8 columns
+  // ([rows][K / 8]).  xrow (optional): X and ss row of output row m.
   const float* ss = nullptr;
   const int32_t* xrow = nullptr;
   float eps = 0.f;
   // Producer side (kEpiAddF32): with the new residual h also write
-  // hb = bf16(h (.) wn) [R][N] and its sums of squares ss_out [R][N / 16].
+  // hb = bf16(h (.) wn) [R][N] and its sums of squares ss_out [R][N / 8].
   void* hb = nullptr;
   const void* wn = nullptr;
   float* ss_out = nullptr;

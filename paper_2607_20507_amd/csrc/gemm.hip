@@ -111,65 +111,96 @@ __device__ __forceinline__ int qkv_tile_row(const GemmFuse& f, int tile, int l16
   return *head * f.hd + *dim;
 }
 
-// 1 / rms of each X row (R <= 16) from the producer's sums of squares per 16
-// columns, into s_rs: 32 lanes per row, fixed order (strided sums, then a
-// tree).  Run by the whole workgroup.
+// 1 / rms of each X row (R <= 16) from the producer's sums of squares per 8
+// columns, into s_rs.  Wave w takes rows w, w + waves, ...; lane l sums
+// entries l, l + 64, ... of the row, eight loads issued together per round,
+// then a fixed-order shuffle tree.  Run by the whole workgroup.
 __device__ __forceinline__ void row_rscale(const GemmFuse& fu, int R, int K, float* s_rs) {
-  const int np = K / 16;
-  for (int base = 0; base < 16; base += blockDim.x / 32) {
-    const int rr = base + static_cast<int>(threadIdx.x) / 32, sub = threadIdx.x & 31;
+  const int np = K / 8;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave, nw = blockDim.x / kWave;
+  for (int rr = wave; rr < R; rr += nw) {
+    const float* sp = fu.ss + static_cast<size_t>(fu.xrow ? fu.xrow[rr] : rr) * np;
     float a = 0.f;
-    if (rr < R) {
-      const float* sp = fu.ss + static_cast<size_t>(fu.xrow ? fu.xrow[rr] : rr) * np;
-      for (int p = sub; p < np; p += 32) a += sp[p];
+    for (int p0 = 0; p0 < np; p0 += 8 * kWave) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int p = p0 + j * kWave + lane;
+        v[j] = p < np ? sp[p] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) a += v[j];
     }
 #pragma unroll
-    for (int o = 16; o > 0; o >>= 1) a += __shfl_xor(a, o, kWave);
-    if (sub == 0 && rr < 16) s_rs[rr] = 1.f / sqrtf(a / static_cast<float>(K) + fu.eps);
+    for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, kWave);
+    if (lane == 0) s_rs[rr] = 1.f / sqrtf(a / static_cast<float>(K) + fu.eps);
   }
+}
+
+// Operands of the fused epilogue that do not depend on the GEMM result, read
+// before the main loop so that their latency hides under the weight stream:
+// the residual and norm weight (kEpiAddF32), the slot and position
+// (kEpiQKVRope).
+struct EpiPre {
+  float h = 0.f, wn = 0.f;
+  int slot = 0, pos = 0;
+};
+
+template <int EPI>
+__device__ __forceinline__ EpiPre epi_prefetch(const GemmFuse& fu, int m, int l16, int tile, int R, int N,
+                                               const void* __restrict__ Y) {
+  EpiPre p;
+  const int n = tile * 16 + l16;
+  if (m >= R) return p;
+  if (EPI == kEpiAddF32 && n < N) {
+    p.h = static_cast<const float*>(Y)[static_cast<size_t>(m) * N + n];
+    if (fu.hb) p.wn = bf16_to_f32(static_cast<const bf16_t*>(fu.wn)[n]);
+  } else if (EPI == kEpiQKVRope) {
+    p.slot = fu.slot[m];
+    p.pos = fu.pos[m];
+  }
+  return p;
 }
 
 // Epilogue of the fused GEMMs for output row m (< 16) and tile column l16 of
 // 16-feature tile `tile`, given the (row-scaled) dot products v (and vu,
-// the up rows of SwiGLU).  Run by whole waves: threads 0..255 with
-// m = 4 (lane / 16) + r, so the 16 lanes of a group hold the 16 columns of a
-// row and exchange values with shuffles.
+// the up rows of SwiGLU) and the prefetched operands.  Run by whole waves:
+// threads 0..255 with m = 4 (lane / 16) + r, so the 16 lanes of a group hold
+// the 16 columns of a row and exchange values with shuffles.
 template <int EPI>
-__device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, int m, int l16, int tile, int R, int N,
-                                               float v, float vu, void* __restrict__ Y,
-                                               const int32_t* __restrict__ row_map, int qk_tiles) {
+__device__ __forceinline__ void fused_epilogue(const GemmFuse& fu, const EpiPre& p, int m, int l16, int tile,
+                                               int R, int N, float v, float vu, void* __restrict__ Y,
+                                               const int32_t* __restrict__ row_map, int qk_tiles,
+                                               int half = -1) {
   const int n0 = tile * 16;
   constexpr bool QKV = (EPI == kEpiQKVRope);
   const int n = n0 + l16;
-  const bool ok = m < R && n < N;
+  // half >= 0 (kEpiAddF32 only): the workgroup owns columns 8 half .. 8 half + 7 of the tile
+  const bool ok = m < R && n < N && (half < 0 || (l16 >> 3) == half);
   if (EPI == kEpiAddF32) {
     float hn = 0.f;
     if (ok) {
-      float* y = static_cast<float*>(Y) + static_cast<size_t>(m) * N + n;
-      hn = *y + v;
-      *y = hn;
-      if (fu.hb)
-        static_cast<bf16_t*>(fu.hb)[static_cast<size_t>(m) * N + n] =
-            f32_to_bf16(hn * bf16_to_f32(static_cast<const bf16_t*>(fu.wn)[n]));
+      hn = p.h + v;
+      static_cast<float*>(Y)[static_cast<size_t>(m) * N + n] = hn;
+      if (fu.hb) static_cast<bf16_t*>(fu.hb)[static_cast<size_t>(m) * N + n] = f32_to_bf16(hn * p.wn);
     }
     if (fu.ss_out) {
       float sq = hn * hn;
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o, kWave);
-      if (l16 == 0 && m < R && n0 < N) fu.ss_out[static_cast<size_t>(m) * (N / 16) + n0 / 16] = sq;
+      for (int o = 1; o < 8; o <<= 1) sq += __shfl_xor(sq, o, kWave);
+      if ((l16 & 7) == 0 && ok) fu.ss_out[static_cast<size_t>(m) * (N / 8) + n / 8] = sq;
     }
   } else if (QKV) {
     const float partner = __shfl_xor(v, 8, kWave);
     if (m < R) {
-      const int sl = fu.slot[m];
-      const int page = sl >> 4, off = sl & 15;
+      const int page = p.slot >> 4, off = p.slot & 15;
       if (tile < qk_tiles) {
         int head, dim;
         qkv_tile_row(fu, tile, l16, &head, &dim);
         const int i = dim % (fu.hd / 2);
         double sn, cs;
-        sincos(static_cast<double>(fu.pos[m]) * exp(-(2.0 * i / fu.hd) * log(static_cast<double>(fu.theta))),
-               &sn, &cs);
+        sincos(static_cast<double>(p.pos) * exp(-(2.0 * i / fu.hd) * log(static_cast<double>(fu.theta))), &sn,
+               &cs);
         const float c = static_cast<float>(cs), sv = static_cast<float>(sn);
         // first half: a cos - b sin; second half: b cos + a sin (a, b = pair)
         const float o = (l16 < 8) ? v * c - partner * sv : v * c + partner * sv;
@@ -234,7 +265,13 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
     const int src = !xv[mt] ? 0 : ((FUSE && fu.xrow) ? fu.xrow[m] : m);
     xr[mt] = X + static_cast<size_t>(src) * K + g * 8;
   }
+  // (measured: before the main loop here, after it in the GEMV)
   if (FUSE && fu.ss) row_rscale(fu, R, K, s_rs);
+  // the fused epilogue (MT = 1) is run by threads 0..255, one element each
+  EpiPre pre;
+  const int e_r = (threadIdx.x / kWave) & 3;
+  const int e_m = 4 * (lane >> 4) + e_r, e_l16 = lane & 15;
+  if (FUSE && threadIdx.x < 256) pre = epi_prefetch<EPI>(fu, e_m, e_l16, tile, R, N, Y);
   f32x4 acc[MT][NS];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -297,7 +334,7 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
         v *= rs;
         vu *= rs;
       }
-      fused_epilogue<EPI>(fu, m, l16, tile, R, N, v, vu, Y, row_map, qk_tiles);
+      fused_epilogue<EPI>(fu, pre, m, l16, tile, R, N, v, vu, Y, row_map, qk_tiles);
       continue;
     }
     const int n = tile * 16 + l16;
@@ -317,9 +354,18 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 // loads of 4 rows x 256 bytes: lane (r = lane / 16, c = lane % 16) gets
 // 16 bytes of feature c, chunk 4 q + r.  Waves split K (SwiGLU: waves 0-3 gate,
 // 4-7 up); lanes of a feature reduce with shuffles, waves through LDS, then
-// the fused epilogue.
+// the fused epilogue.  HALF (residual-add projections with fewer tiles than
+// compute units): two workgroups per tile, each owning 8 of its features and
+// reading 8 rows x 128 bytes per load (lane r = lane / 8, c = lane % 8:
+// feature 8 half + c, chunk 8 q + r), so that every compute unit streams
+// weights: one workgroup moves only about 28 GB/s, whatever its loads in
+// flight.
 
 constexpr int kGemvRows = 2;  // measured: the MFMA skinny kernel wins from 3 rows on
+
+// Half tiles for residual-add projections with fewer 16-feature tiles than
+// compute units.
+bool gemv_half(int epi, int N) { return epi == kEpiAddF32 && (N + 15) / 16 < 256; }
 
 __device__ __forceinline__ float dot8(const u32x4& w, const u32x4& x) {
   float a = 0.f;
@@ -331,32 +377,42 @@ __device__ __forceinline__ float dot8(const u32x4& w, const u32x4& x) {
   return a;
 }
 
-template <int EPI, int RM>
+template <int EPI, int RM, bool HALF>
 __global__ __launch_bounds__(512) void gemv_bf16(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W,
                                                  void* __restrict__ Y, int R, int N, int K,
                                                  const int32_t* __restrict__ row_map, const GemmFuse fu) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
   constexpr bool QKV = (EPI == kEpiQKVRope);
-  constexpr int KB = 2;  // 128-wide blocks per iteration: 8 weight loads in flight per lane
+  static_assert(!HALF || EPI == kEpiAddF32, "half tiles: residual-add projections");
+  constexpr int NQ = HALF ? 2 : 4;   // weight loads per 128-wide block
+  constexpr int KB = HALF ? 4 : 2;   // blocks per iteration: 8 weight loads in flight per lane
+  constexpr int XS = HALF ? 64 : 32;  // element step of X between the loads of a block
   __shared__ float part[8][RM][16];  // [wave][row][feature]
   __shared__ float s_rs[16];
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int c = lane & 15, r = lane >> 4;
-  const int tile = blockIdx.x;
+  const int tile = HALF ? static_cast<int>(blockIdx.x) >> 1 : blockIdx.x;
+  const int half = HALF ? static_cast<int>(blockIdx.x & 1) : -1;
+  const int c = HALF ? 8 * half + (lane & 7) : (lane & 15);  // feature within the tile
+  const int r = HALF ? lane >> 3 : lane >> 4;
   const int qk_tiles = QKV ? (fu.Hq + fu.Hkv) * fu.hd / 16 : 0;
   const int grp = SW ? (wave >> 2) : 0;  // SwiGLU: gate (0) or up (1) tile
   const int gw = SW ? (wave & 3) : wave, ngw = SW ? 4 : 8;
   const bf16_t* wh = W + (grp ? static_cast<size_t>(N) * K : 0);
-  // load q of block kb: wp + q * qs + kb * 128 (tiled: rows 4 q + r at
-  // position c; a trailing partial tile is row-major at clamped rows)
+  // load q of block kb: wp + q * qs + kb * 128 (tiled: memory row
+  // (16 / NQ) q + r at position c; a trailing partial tile is row-major at
+  // clamped rows)
   const bool full = (tile + 1) * 16 <= N;
   const bf16_t* wp = wh + (full ? static_cast<size_t>(tile * 16 + r) * K + c * 8
                                 : static_cast<size_t>(min(tile * 16 + c, N - 1)) * K + r * 8);
-  const int qs = full ? 4 * K : 32;
+  const int qs = full ? (16 / NQ) * K : XS;
   const bf16_t* xp[RM];
 #pragma unroll
   for (int m = 0; m < RM; ++m)
     xp[m] = X + static_cast<size_t>(m < R ? (fu.xrow ? fu.xrow[m] : m) : 0) * K + r * 8;
+  // threads 0..255 run the epilogue: output row m = 4 (lane / 16) + (wave % 4)
+  const int em = 4 * (lane >> 4) + (wave & 3);
+  EpiPre pre;
+  if (threadIdx.x < 256) pre = epi_prefetch<EPI>(fu, em, lane & 15, tile, R, N, Y);
   const int nb = K / 128;
   const int per = (nb + ngw - 1) / ngw;
   const int kb0 = gw * per, kb1 = min(nb, kb0 + per);
@@ -364,35 +420,36 @@ __global__ __launch_bounds__(512) void gemv_bf16(const bf16_t* __restrict__ X, c
 #pragma unroll
   for (int m = 0; m < RM; ++m) a[m] = 0.f;
   for (int kb = kb0; kb < kb1; kb += KB) {
-    u32x4 w[KB][4], x[KB][RM][4];
+    u32x4 w[KB][NQ], x[KB][RM][NQ];
 #pragma unroll
     for (int b = 0; b < KB; ++b) {
       const int o = min(kb + b, kb1 - 1) * 128;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < NQ; ++q) {
         w[b][q] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wp + o + q * qs));
 #pragma unroll
         for (int m = 0; m < RM; ++m)
-          if (m < R) x[b][m][q] = *reinterpret_cast<const u32x4*>(xp[m] + o + 32 * q);
+          if (m < R) x[b][m][q] = *reinterpret_cast<const u32x4*>(xp[m] + o + XS * q);
       }
     }
 #pragma unroll
     for (int b = 0; b < KB; ++b) {
       if (kb + b >= kb1) break;
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int m = 0; m < RM; ++m)
           if (m < R) a[m] += dot8(w[b][q], x[b][m][q]);
     }
   }
+  if (fu.ss) row_rscale(fu, R, K, s_rs);
 #pragma unroll
   for (int m = 0; m < RM; ++m) {
+    if (HALF) a[m] += __shfl_xor(a[m], 8, kWave);
     a[m] += __shfl_xor(a[m], 16, kWave);
     a[m] += __shfl_xor(a[m], 32, kWave);
-    if (lane < 16) part[wave][m][c] = a[m];
+    if (lane < (HALF ? 8 : 16)) part[wave][m][c] = a[m];
   }
-  if (fu.ss) row_rscale(fu, R, K, s_rs);
   __syncthreads();
   if (threadIdx.x >= 256) return;
   const int e = threadIdx.x, rr = (e / kWave) & 3, ln = e & (kWave - 1);
@@ -412,17 +469,25 @@ __global__ __launch_bounds__(512) void gemv_bf16(const bf16_t* __restrict__ X, c
       vu *= s_rs[m];
     }
   }
-  fused_epilogue<EPI>(fu, m, l16, tile, R, N, v, vu, Y, row_map, qk_tiles);
+  // (HALF: the other half's entries of part are not written; its lanes
+  // store nothing)
+  fused_epilogue<EPI>(fu, pre, m, l16, tile, R, N, v, vu, Y, row_map, qk_tiles, half);
 }
 
 template <int EPI>
 hipError_t gemv(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
                 const int32_t* row_map, const GemmFuse& fu) {
-  const dim3 grid((N + 15) / 16);
+  const int tiles = (N + 15) / 16;
   const bf16_t* x = static_cast<const bf16_t*>(X);
   const bf16_t* w = static_cast<const bf16_t*>(W);
   if (R > kGemvRows) return hipErrorInvalidValue;
-  gemv_bf16<EPI, kGemvRows><<<grid, 512, 0, st>>>(x, w, Y, R, N, K, row_map, fu);
+  if constexpr (EPI == kEpiAddF32) {
+    if (gemv_half(EPI, N)) {
+      gemv_bf16<EPI, kGemvRows, true><<<2 * tiles, 512, 0, st>>>(x, w, Y, R, N, K, row_map, fu);
+      return hipGetLastError();
+    }
+  }
+  gemv_bf16<EPI, kGemvRows, false><<<tiles, 512, 0, st>>>(x, w, Y, R, N, K, row_map, fu);
   return hipGetLastError();
 }
 
@@ -964,8 +1029,10 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
 }
 
 const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused, size_t splitk_bytes) {
-  static const char* gv[4] = {"gemv_bf16<0, 2>", "gemv_bf16<1, 2>", "gemv_bf16<2, 2>", "gemv_bf16<3, 2>"};
-  if (dtype == 1 && R <= kGemvRows) return (epi >= 0 && epi <= 3) ? gv[epi] : "";
+  static const char* gv[4] = {"gemv_bf16<0, 2, false>", "gemv_bf16<1, 2, false>", "gemv_bf16<2, 2, false>",
+                              "gemv_bf16<3, 2, false>"};
+  if (dtype == 1 && R <= kGemvRows)
+    return gemv_half(epi, N) ? "gemv_bf16<1, 2, true>" : ((epi >= 0 && epi <= 3) ? gv[epi] : "");
   // skinny names [MT - 1][epi][fused]
   static char names[4][4][2][40];
   static std::once_flag once;
