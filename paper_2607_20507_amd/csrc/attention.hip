@@ -41,7 +41,7 @@ __device__ __forceinline__ uint32_t mask_pair(uint32_t w, int valid) {
 // w, w + W, ... of the item's key range, and the waves' softmax states are
 // merged through LDS at the end (exact rescaling by exp2(m_w - m)).
 template <int HD, int NT, int W>
-__global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
+__global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
   constexpr int DS = HD / 32;   // MFMA k-steps over the head dim
   constexpr int DT = HD / 16;   // 16-dim output tiles
   const AttnItem it = items[blockIdx.x];
@@ -94,7 +94,7 @@ __global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const Att
 
   // K and V^T operands of one 32-key chunk (keys past t1 are clamped to a
   // valid address; their scores are masked and their V entries zeroed)
-  auto load_chunk = [&](int c0, uint4 (&kf)[2][DS], uint4 (&vf)[DT]) {
+  auto load_k = [&](int c0, uint4 (&kf)[2][DS]) {
     // lanes 0-7 / 8-15 of a group read the chunk's first / second page:
     // unit ((s * 2 + hh) * 4 + g) * 8 + l16 % 8 of the page's K block holds
     // dims 32 s + 8 g .. of key 8 (l16 / 4) + 4 hh + l16 % 4 (kv_layout.h)
@@ -104,6 +104,8 @@ __global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const Att
     for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
       for (int s = 0; s < DS; ++s) kf[hh][s] = ld_stream(kb + ((s * 2 + hh) * 4 + g) * 8 + (l16 & 7));
+  };
+  auto load_v = [&](int c0, uint4 (&vf)[DT]) {
     // V^T: unit (dt * 2 + g % 2) * 16 + l16 holds keys 8 (g % 2) .. + 7 of
     // dim 16 dt + l16 of page (c0 + 8 g) / 16
     const int tvc = min(c0 + 8 * g, it.t1 - 1);
@@ -111,16 +113,22 @@ __global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const Att
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) vf[dt] = ld_stream(vb + (dt * 2 + (g & 1)) * 16 + l16);
   };
-  uint4 kf[2][DS], vf[DT], kn[2][DS], vn[DT];
+  // One K and one V^T buffer: the next chunk's K is loaded once this chunk's
+  // scores are computed, its V^T once this chunk's output update is done
+  // (loads are unconditional, clamped past the end, so that the compiler's
+  // waits stay exact).
+  uint4 kf[2][DS], vf[DT];
   const int cfirst = it.t0 + 32 * wave;
-  if (cfirst < it.t1) load_chunk(cfirst, kf, vf);
+  if (cfirst < it.t1) {
+    load_k(cfirst, kf);
+    load_v(cfirst, vf);
+  }
   for (int c0 = cfirst; c0 < it.t1; c0 += 32 * W) {
-    const bool more = c0 + 32 * W < it.t1;
-    if (more) load_chunk(c0 + 32 * W, kn, vn);
+    const int cn = min(c0 + 32 * W, it.t1 - 1);
     const int tv = c0 + 8 * g;
     const int nvalid = min(max(it.t1 - tv, 0), 8);
 
-    uint4 pf[NT];
+    f32x4 sc[NT][2];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -129,11 +137,18 @@ __global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const Att
         s0 = mfma16x16x32(kf[0][s], qf[nt][s], s0);
         s1 = mfma16x16x32(kf[1][s], qf[nt][s], s1);
       }
+      sc[nt][0] = s0;
+      sc[nt][1] = s1;
+    }
+    load_k(cn, kf);
+    uint4 pf[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
       float sv[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int t = c0 + 8 * g + j;
-        const float raw = (j < 4) ? s0[j] : s1[j - 4];
+        const float raw = (j < 4) ? sc[nt][0][j] : sc[nt][1][j - 4];
         const bool ok = vval[nt] && t < it.t1 && t <= vpos[nt];
         sv[j] = ok ? raw * scale : -INFINITY;
       }
@@ -175,14 +190,7 @@ __global__ __launch_bounds__(64 * W) void attn_bf16_kernel(AttnArgs a, const Att
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[dt][nt] = mfma16x16x32(v, pf[nt], acc[dt][nt]);
     }
-    if (more) {
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int s = 0; s < DS; ++s) kf[hh][s] = kn[hh][s];
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) vf[dt] = vn[dt];
-    }
+    load_v(cn, vf);
   }
 
   float ltot[NT];
