@@ -46,7 +46,8 @@ SPEC_API spec_status spec_op_rmsnorm(int32_t dtype, int32_t R, int32_t d, const 
 
 /* Rotary embedding + paged KV append for one layer.  qkv device fp32
  * [R, (Hq + 2 Hkv) hd]; pos and slot device int32 [R] (slot = page * 16 + offset);
- * q_out device [R, Hq, hd]; k_pages [pages][Hkv][16][hd]; v_pages [pages][Hkv][hd][16]. */
+ * q_out device [R, Hq, hd]; k_pages [pages][Hkv][16][hd]; v_pages [pages][Hkv][hd][16].
+ * head_dim even and at most 256 (SPEC_E_INVALID otherwise). */
 SPEC_API spec_status spec_op_rope_kv(int32_t dtype, int32_t R, int32_t n_heads, int32_t n_kv_heads,
                                      int32_t head_dim, float theta, const float* qkv,
                                      const int32_t* pos, const int32_t* slot, void* q_out,

@@ -53,6 +53,14 @@ __global__ __launch_bounds__(256) void embed_kernel(int d, const int32_t* __rest
   }
 }
 
+// One workgroup per row.  Rows of up to 8192 columns (d % 4 == 0): thread t
+// holds 4-column chunks t, t + 256, ... of the row in registers (one round of
+// 16-byte loads, the norm weight's with them), so the row is read once and
+// written with 8- / 16-byte stores; wider rows take a strided two-pass loop.
+// The sum of squares is taken per thread in chunk order, then over the wave
+// and the waves in a fixed order.
+constexpr int kNormChunks = 8;  // 4-column chunks per thread held in registers
+
 template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(int d, const float* __restrict__ h,
                                                       const int32_t* __restrict__ row_idx,
@@ -61,20 +69,62 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int d, const float* __rest
   const int r = blockIdx.x;
   const int src = row_idx ? row_idx[r] : r;
   const float* x = h + static_cast<size_t>(src) * d;
+  T* o = y + static_cast<size_t>(r) * d;
+  __shared__ float part[256 / kWave];
+  auto total = [&](float ss) {
+    ss = wave_sum(ss);
+    if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = ss;
+    __syncthreads();
+    float tot = 0.f;
+    for (int k = 0; k < static_cast<int>(blockDim.x) / kWave; ++k) tot += part[k];
+    return 1.f / sqrtf(tot / static_cast<float>(d) + eps);
+  };
+  const int nch = d / 4;
+  if (d % 4 == 0 && nch <= kNormChunks * static_cast<int>(blockDim.x)) {
+    float4 xv[kNormChunks];
+    float wv[kNormChunks][4];
+#pragma unroll
+    for (int c = 0; c < kNormChunks; ++c) {
+      const int ch = threadIdx.x + c * blockDim.x;
+      if (ch < nch) {
+        xv[c] = reinterpret_cast<const float4*>(x)[ch];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) wv[c][e] = Elem<T>::to_f32(w[4 * ch + e]);
+      }
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < kNormChunks; ++c)
+      if (threadIdx.x + c * blockDim.x < nch) {
+        ss = fmaf(xv[c].x, xv[c].x, ss);
+        ss = fmaf(xv[c].y, xv[c].y, ss);
+        ss = fmaf(xv[c].z, xv[c].z, ss);
+        ss = fmaf(xv[c].w, xv[c].w, ss);
+      }
+    const float inv = total(ss);
+#pragma unroll
+    for (int c = 0; c < kNormChunks; ++c) {
+      const int ch = threadIdx.x + c * blockDim.x;
+      if (ch < nch) {
+        const float v0 = xv[c].x * inv * wv[c][0], v1 = xv[c].y * inv * wv[c][1];
+        const float v2 = xv[c].z * inv * wv[c][2], v3 = xv[c].w * inv * wv[c][3];
+        if constexpr (sizeof(T) == 2)
+          reinterpret_cast<uint2*>(o)[ch] = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+        else
+          reinterpret_cast<float4*>(o)[ch] = make_float4(v0, v1, v2, v3);
+      }
+    }
+    return;
+  }
   float ss = 0.f;
   for (int i = threadIdx.x; i < d; i += blockDim.x) ss = fmaf(x[i], x[i], ss);
-  ss = wave_sum(ss);
-  __shared__ float part[256 / kWave];
-  if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = ss;
-  __syncthreads();
-  float tot = 0.f;
-  for (int k = 0; k < static_cast<int>(blockDim.x) / kWave; ++k) tot += part[k];
-  const float inv = 1.f / sqrtf(tot / static_cast<float>(d) + eps);
-  T* o = y + static_cast<size_t>(r) * d;
+  const float inv = total(ss);
   for (int i = threadIdx.x; i < d; i += blockDim.x) o[i] = Elem<T>::from_f32(x[i] * inv * Elem<T>::to_f32(w[i]));
 }
 
 // One workgroup per row; thread (head, i) rotates the pair (i, i + hd/2).
+constexpr int kRopeMaxHalf = 128;  // head_dim <= 256
+
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, float theta,
                                                       const float* __restrict__ qkv,
@@ -90,11 +140,19 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
   const int sl = slot[r];
   const int page = sl >> 4, off = sl & 15;
   const double lt = log(static_cast<double>(theta));
-  for (int e = threadIdx.x; e < (Hq + Hkv) * half; e += blockDim.x) {
-    const int head = e / half, i = e % half;
+  // the row's rotation angles (they depend on the pair index only, not on
+  // the head), once per row in fp64
+  __shared__ float s_cos[kRopeMaxHalf], s_sin[kRopeMaxHalf];
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
     double sn, cs;
     sincos(p * exp(-(2.0 * i / hd) * lt), &sn, &cs);
-    const float c = static_cast<float>(cs), s = static_cast<float>(sn);
+    s_cos[i] = static_cast<float>(cs);
+    s_sin[i] = static_cast<float>(sn);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < (Hq + Hkv) * half; e += blockDim.x) {
+    const int head = e / half, i = e % half;
+    const float c = s_cos[i], s = s_sin[i];
     // rot_tiled: the q and k columns of each head are in the rotary tile
     // order of the tiled QKV weight (rows 8t..8t+7, then hd/2+8t.. of tile t)
     const float* src = x + head * hd;
@@ -167,7 +225,7 @@ hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta
                           const int32_t* pos, const int32_t* slot, void* q, void* kpool,
                           void* vpool, hipStream_t st, bool rot_tiled) {
   if (R <= 0) return hipSuccess;
-  if (hd % 2 != 0 || (rot_tiled && hd % 16 != 0)) return hipErrorInvalidValue;
+  if (hd % 2 != 0 || hd > 2 * kRopeMaxHalf || (rot_tiled && hd % 16 != 0)) return hipErrorInvalidValue;
   if (dtype == 0)
     rope_kv_kernel<float><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
                                              static_cast<float*>(kpool), static_cast<float*>(vpool), rot_tiled);

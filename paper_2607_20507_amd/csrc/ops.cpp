@@ -224,7 +224,7 @@ spec_status spec_op_rope_kv(int32_t dtype, int32_t R, int32_t n_heads, int32_t n
                             float theta, const float* qkv, const int32_t* pos, const int32_t* slot,
                             void* q_out, void* k_pages, void* v_pages, void* stream) {
   if ((dtype != SPEC_F32 && dtype != SPEC_BF16) || R < 0 || n_heads <= 0 || n_kv_heads <= 0 ||
-      head_dim <= 0 || head_dim % 2)
+      head_dim <= 0 || head_dim % 2 || head_dim > 256)
     return SPEC_E_INVALID;
   if (R == 0) return SPEC_OK;
   if (!qkv || !pos || !slot || !q_out || !k_pages || !v_pages) return SPEC_E_INVALID;
