@@ -166,7 +166,7 @@ class Stager {
 // positions pos0.., page table row `seq` of the launch's compact table.
 // Workgroups an attention launch aims for (measured on the 8B/1B-shaped
 // verify and draft steps and the 64-sequence serving batch).
-constexpr int kAttnTargetWgs = 1024;
+constexpr int kAttnTargetWgs = 512;
 
 struct AttnSegment {
   int32_t seq, row0, nrows, pos0;
