@@ -329,13 +329,13 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   // GEMM launch, timed when selected: algorithmic bytes = weights + inputs +
   // outputs (read-modify-write for the residual add), flops = 2 R N_w K.
   auto gemm = [&](int rows, int N, int K, const void* X, const void* W, void* Y, int epi,
-                  const int32_t* rm, const GemmFuse* f = nullptr) -> hipError_t {
+                  const int32_t* rm, const GemmFuse* f = nullptr, GemmNorm* nrm = nullptr) -> hipError_t {
     const bool timed = tm.wants(gemm_kernel_name(dt, rows, N, K, epi, f != nullptr, ctx->ws.splitk_bytes));
     if (timed) tm.begin(st);
     const hipError_t e =
         f ? launch_gemm_fused(rows, N, K, X, W, Y, epi, *f, st, rm)
           : launch_gemm(dt, rows, N, K, X, W, Y, epi, st, rm, wsptr<float>(ctx, ctx->ws.splitk),
-                        ctx->ws.splitk_bytes);
+                        ctx->ws.splitk_bytes, nrm);
     if (timed) {
       const double nw = epi == kEpiSwiGLU ? 2.0 * N : N;
       const double ob = epi == kEpiStoreF32 ? 4.0 : (epi == kEpiAddF32 ? 8.0 : esz);
@@ -343,6 +343,9 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
     }
     return e;
   };
+  // Above 8 rows each RMSNorm is its own kernel, unless the residual-add GEMM
+  // before it splits K: then the split-K reduction applies it (GemmNorm).
+  bool normed = false;  // y already holds the next RMSNorm's rows
   for (int l = 0; l < d.n_layers; ++l) {
     const auto& L = M.layers[l];
     if (fused) {
@@ -360,7 +363,7 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
       fq.vpool = M.vl(l);
       HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, nullptr, kEpiQKVRope, nullptr, &fq));
     } else {
-      HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
+      if (!normed) HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
       HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr));
       HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, qkv, I(o.pos),
                           I(o.slot), q, M.kl(l), M.vl(l), st, dt == 1));
@@ -396,10 +399,19 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
       fd.ss_out = ss;
       HIPC(gemm(R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, nullptr, &fd));
     } else {
-      HIPC(gemm(R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, nullptr));
-      HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.mlp_norm, d.rms_eps, y, st));
+      GemmNorm no;
+      no.w = L.mlp_norm;
+      no.eps = d.rms_eps;
+      no.y = y;
+      HIPC(gemm(R, d.d_model, M.qdim(), ob, L.wo, h, kEpiAddF32, nullptr, nullptr, &no));
+      if (!no.done) HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.mlp_norm, d.rms_eps, y, st));
       HIPC(gemm(R, d.ffn_dim, d.d_model, y, L.w_gate_up, u, kEpiSwiGLU, nullptr));
-      HIPC(gemm(R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, nullptr));
+      GemmNorm nd;  // the next layer's attention norm (the last layer's final norm is per LM row)
+      nd.w = l + 1 < d.n_layers ? M.layers[l + 1].attn_norm : nullptr;
+      nd.eps = d.rms_eps;
+      nd.y = y;
+      HIPC(gemm(R, d.d_model, d.ffn_dim, u, L.w_down, h, kEpiAddF32, nullptr, nullptr, nd.w ? &nd : nullptr));
+      normed = nd.done;
     }
   }
   if (o.n_lm > 0) {

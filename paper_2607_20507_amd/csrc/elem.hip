@@ -150,24 +150,69 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
     s_sin[i] = static_cast<float>(sn);
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < (Hq + Hkv) * half; e += blockDim.x) {
-    const int head = e / half, i = e % half;
-    const float c = s_cos[i], s = s_sin[i];
-    // rot_tiled: the q and k columns of each head are in the rotary tile
-    // order of the tiled QKV weight (rows 8t..8t+7, then hd/2+8t.. of tile t)
-    const float* src = x + head * hd;
-    const int ia = rot_tiled ? 16 * (i / 8) + (i % 8) : i;
-    const int ib = rot_tiled ? ia + 8 : i + half;
-    const float a = src[ia], b = src[ib];
-    const float ra = a * c - b * s, rb = b * c + a * s;
-    if (head < Hq) {
-      T* o = q + (static_cast<size_t>(r) * Hq + head) * hd;
-      o[i] = Elem<T>::from_f32(ra);
-      o[i + half] = Elem<T>::from_f32(rb);
+  // Groups of 8 consecutive pairs (half % 8 == 0): in both column orders
+  // their a and b values are 8 consecutive floats, and their outputs 8
+  // consecutive elements of q and of the K page (one 16-byte unit of the
+  // bf16 page layout), so one thread moves them with vector loads / stores.
+  auto put8 = [](T* dst, const float (&v)[8]) {
+    if constexpr (sizeof(T) == 2) {
+      *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                  pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
     } else {
-      T* o = kpool + (static_cast<size_t>(page) * Hkv + (head - Hq)) * 16 * hd;
-      o[k_index<T>(off, i, hd)] = Elem<T>::from_f32(ra);
-      o[k_index<T>(off, i + half, hd)] = Elem<T>::from_f32(rb);
+      reinterpret_cast<float4*>(dst)[0] = make_float4(v[0], v[1], v[2], v[3]);
+      reinterpret_cast<float4*>(dst)[1] = make_float4(v[4], v[5], v[6], v[7]);
+    }
+  };
+  if (half % 8 == 0) {
+    const int groups = half / 8;
+    for (int e = threadIdx.x; e < (Hq + Hkv) * groups; e += blockDim.x) {
+      const int head = e / groups, t = e % groups, i0 = 8 * t;
+      // rot_tiled: the q and k columns of each head are in the rotary tile
+      // order of the tiled QKV weight (rows 8t..8t+7, then hd/2+8t.. of tile t)
+      const float* src = x + head * hd;
+      const int ia = rot_tiled ? 16 * t : i0;
+      const int ib = rot_tiled ? ia + 8 : i0 + half;
+      const float4 a0 = reinterpret_cast<const float4*>(src + ia)[0], a1 = reinterpret_cast<const float4*>(src + ia)[1];
+      const float4 b0 = reinterpret_cast<const float4*>(src + ib)[0], b1 = reinterpret_cast<const float4*>(src + ib)[1];
+      const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+      float ra[8], rb[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float c = s_cos[i0 + j], sn = s_sin[i0 + j];
+        ra[j] = av[j] * c - bv[j] * sn;
+        rb[j] = bv[j] * c + av[j] * sn;
+      }
+      if (head < Hq) {
+        T* o = q + (static_cast<size_t>(r) * Hq + head) * hd;
+        put8(o + i0, ra);
+        put8(o + i0 + half, rb);
+      } else {
+        T* o = kpool + (static_cast<size_t>(page) * Hkv + (head - Hq)) * 16 * hd;
+        put8(o + k_index<T>(off, i0, hd), ra);
+        put8(o + k_index<T>(off, i0 + half, hd), rb);
+      }
+    }
+  } else {
+    for (int e = threadIdx.x; e < (Hq + Hkv) * half; e += blockDim.x) {
+      const int head = e / half, i = e % half;
+      const float c = s_cos[i], s = s_sin[i];
+      // rot_tiled: the q and k columns of each head are in the rotary tile
+      // order of the tiled QKV weight (rows 8t..8t+7, then hd/2+8t.. of tile t)
+      const float* src = x + head * hd;
+      const int ia = rot_tiled ? 16 * (i / 8) + (i % 8) : i;
+      const int ib = rot_tiled ? ia + 8 : i + half;
+      const float a = src[ia], b = src[ib];
+      const float ra = a * c - b * s, rb = b * c + a * s;
+      if (head < Hq) {
+        T* o = q + (static_cast<size_t>(r) * Hq + head) * hd;
+        o[i] = Elem<T>::from_f32(ra);
+        o[i + half] = Elem<T>::from_f32(rb);
+      } else {
+        T* o = kpool + (static_cast<size_t>(page) * Hkv + (head - Hq)) * 16 * hd;
+        o[k_index<T>(off, i, hd)] = Elem<T>::from_f32(ra);
+        o[k_index<T>(off, i + half, hd)] = Elem<T>::from_f32(rb);
+      }
     }
   }
   const float* v = x + (Hq + Hkv) * hd;

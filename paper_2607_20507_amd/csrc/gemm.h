@@ -46,14 +46,26 @@ struct GemmFuse {
 hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, void* Y, int epi,
                              const GemmFuse& f, hipStream_t st, const int32_t* row_map = nullptr);
 
+// RMSNorm of the residual-add GEMM's updated rows (kEpiAddF32, bf16 model):
+// y[m] = bf16(Y[m] / sqrt(mean(Y[m]^2) + eps) (.) w).  launch_gemm folds it
+// into the split-K reduction when the launch splits K and sets `done`; the
+// caller runs the separate RMSNorm otherwise.
+struct GemmNorm {
+  const void* w = nullptr;  // bf16 [N]
+  float eps = 0.f;
+  void* y = nullptr;        // bf16 [R][N]
+  bool done = false;
+};
+
 // dtype: 0 = fp32 (X, W, SwiGLU output fp32), 1 = bf16 (X, W, SwiGLU output bf16).
 // bf16 requires K % 128 == 0 (returns hipErrorInvalidValue otherwise).
 // row_map (device, optional): output row m goes to Y row row_map[m].
 // splitk_ws (device, optional): fp32 partials for split-K on small grids
 // (R > 64); without it the kernel does not split K.
+// norm (optional, kEpiAddF32 only): see GemmNorm.
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
                        int epi, hipStream_t st, const int32_t* row_map = nullptr,
-                       float* splitk_ws = nullptr, size_t splitk_bytes = 0);
+                       float* splitk_ws = nullptr, size_t splitk_bytes = 0, GemmNorm* norm = nullptr);
 
 // In place: bf16 row-major [rows, K] -> the tiled layout every bf16 GEMM
 // reads (K % 128 == 0).  In each complete group of 16 rows and 128-column

@@ -762,6 +762,64 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
   }
 }
 
+// Split-K sum of a residual-add GEMM fused with the RMSNorm after it, one
+// workgroup per row m (N % 4 == 0, N <= 4 * 256 * kNormRegChunks): thread t
+// holds 4-column chunks t, t + 256, ... of the row in registers, adds the
+// partials in split order to h (as splitk_reduce does), writes h, then
+// y[m] = bf16(h[m] / rms(h[m]) (.) w) with the sum of squares taken per
+// thread in chunk order, then over the wave and the waves in a fixed order.
+constexpr int kNormRegChunks = 8;
+
+__global__ __launch_bounds__(256) void splitk_reduce_norm(const float* __restrict__ part, int S, int R, int N,
+                                                          float* __restrict__ Y, const bf16_t* __restrict__ w,
+                                                          float eps, bf16_t* __restrict__ y) {
+  const int m = blockIdx.x;
+  const int nch = N / 4;
+  float4 hv[kNormRegChunks];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < kNormRegChunks; ++c) {
+    const int ch = threadIdx.x + c * 256;
+    if (ch >= nch) continue;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < S; ++s) {
+      const float4 p = reinterpret_cast<const float4*>(part + (static_cast<size_t>(s) * R + m) * N)[ch];
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+    float4* hp = reinterpret_cast<float4*>(Y + static_cast<size_t>(m) * N) + ch;
+    float4 h = *hp;
+    h.x += v.x;
+    h.y += v.y;
+    h.z += v.z;
+    h.w += v.w;
+    *hp = h;
+    hv[c] = h;
+    ss = fmaf(h.x, h.x, ss);
+    ss = fmaf(h.y, h.y, ss);
+    ss = fmaf(h.z, h.z, ss);
+    ss = fmaf(h.w, h.w, ss);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
+  __shared__ float s_part[4];
+  if ((threadIdx.x & (kWave - 1)) == 0) s_part[threadIdx.x / kWave] = ss;
+  __syncthreads();
+  const float tot = s_part[0] + s_part[1] + s_part[2] + s_part[3];
+  const float inv = 1.f / sqrtf(tot / static_cast<float>(N) + eps);
+#pragma unroll
+  for (int c = 0; c < kNormRegChunks; ++c) {
+    const int ch = threadIdx.x + c * 256;
+    if (ch >= nch) continue;
+    const float4 h = hv[c];
+    const float v0 = h.x * inv * bf16_to_f32(w[4 * ch]), v1 = h.y * inv * bf16_to_f32(w[4 * ch + 1]);
+    const float v2 = h.z * inv * bf16_to_f32(w[4 * ch + 2]), v3 = h.w * inv * bf16_to_f32(w[4 * ch + 3]);
+    reinterpret_cast<uint2*>(y + static_cast<size_t>(m) * N)[ch] = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+  }
+}
+
 // ---------------------------------------------------------------------------
 // fp32: 64x64 tiles (64x32 features + their up rows for SwiGLU), BK = 16
 
@@ -909,7 +967,7 @@ Mfma2Shape mfma2_shape(int R, int N, int Nw, int K, size_t ws_bytes) {
 
 template <int EPI, int MTW, int NTW>
 hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st,
-                   const int32_t* rm, float* ws, size_t ws_bytes) {
+                   const int32_t* rm, float* ws, size_t ws_bytes, GemmNorm* norm = nullptr) {
   const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
   if (static_cast<double>(Nw) * K >= 2147483648.0 || static_cast<double>(R) * K >= 2147483648.0 || K % 128)
     return hipErrorInvalidValue;  // 32-bit byte offsets; whole 128-wide blocks
@@ -922,6 +980,12 @@ hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* 
     return hipGetLastError();
   }
   gemm_mfma2_bf16<EPI, MTW, NTW><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, MT, NT, rm);
+  if (EPI == kEpiAddF32 && norm && !rm && N % 4 == 0 && N <= 4 * 256 * kNormRegChunks) {
+    splitk_reduce_norm<<<R, 256, 0, st>>>(ws, S, R, N, static_cast<float*>(Y), static_cast<const bf16_t*>(norm->w),
+                                          norm->eps, static_cast<bf16_t*>(norm->y));
+    norm->done = true;
+    return hipGetLastError();
+  }
   const size_t total = static_cast<size_t>(R) * N;
   const int blocks = static_cast<int>(std::min<size_t>(2048, (total + 255) / 256));
   splitk_reduce<EPI><<<blocks, 256, 0, st>>>(ws, S, R, N, Y, rm);
@@ -930,25 +994,25 @@ hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* 
 
 template <int EPI, int MTW>
 hipError_t mfma2_m(int ntw, int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st,
-                   const int32_t* rm, float* ws, size_t ws_bytes) {
+                   const int32_t* rm, float* ws, size_t ws_bytes, GemmNorm* norm = nullptr) {
   switch (ntw) {
-    case 2: return mfma2_t<EPI, MTW, 2>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
-    case 4: return mfma2_t<EPI, MTW, 4>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
-    default: return mfma2_t<EPI, MTW, 8>(R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    case 2: return mfma2_t<EPI, MTW, 2>(R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
+    case 4: return mfma2_t<EPI, MTW, 4>(R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
+    default: return mfma2_t<EPI, MTW, 8>(R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
   }
 }
 
 template <int EPI>
 hipError_t mfma2(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
-                 const int32_t* rm, float* ws, size_t ws_bytes) {
+                 const int32_t* rm, float* ws, size_t ws_bytes, GemmNorm* norm = nullptr) {
   const bf16_t* x = static_cast<const bf16_t*>(X);
   const bf16_t* w = static_cast<const bf16_t*>(W);
   const Mfma2Shape sh = mfma2_shape(R, N, EPI == kEpiSwiGLU ? 2 * N : N, K, ws ? ws_bytes : 0);
   switch (sh.mtw) {
-    case 2: return mfma2_m<EPI, 2>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
-    case 4: return mfma2_m<EPI, 4>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
-    case 6: return mfma2_m<EPI, 6>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
-    default: return mfma2_m<EPI, 8>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes);
+    case 2: return mfma2_m<EPI, 2>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
+    case 4: return mfma2_m<EPI, 4>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
+    case 6: return mfma2_m<EPI, 6>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
+    default: return mfma2_m<EPI, 8>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
   }
 }
 
@@ -965,7 +1029,7 @@ bool use_mfma(int R, int Nw, int K) {
 
 template <int EPI>
 hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
-                    hipStream_t st, const int32_t* rm, float* ws, size_t ws_bytes) {
+                    hipStream_t st, const int32_t* rm, float* ws, size_t ws_bytes, GemmNorm* norm = nullptr) {
   if (dtype == 0) {
     const int ncols = (EPI == kEpiSwiGLU) ? 32 : 64;
     dim3 grid((N + ncols - 1) / ncols, (R + 63) / 64);
@@ -975,12 +1039,12 @@ hipError_t dispatch(int dtype, int R, int N, int K, const void* X, const void* W
   }
   if (K % 128 != 0) return hipErrorInvalidValue;
   if (R <= kGemvRows) return gemv<EPI>(R, N, K, X, W, Y, st, rm, GemmFuse{});
-  if (use_mfma(R, EPI == kEpiSwiGLU ? 2 * N : N, K)) return mfma2<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
+  if (use_mfma(R, EPI == kEpiSwiGLU ? 2 * N : N, K)) return mfma2<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes, norm);
   if (R <= 16) return skinny<1, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 32) return skinny<2, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 48) return skinny<3, EPI>(R, N, K, X, W, Y, st, rm);
   if (R <= 64) return skinny<4, EPI>(R, N, K, X, W, Y, st, rm);
-  return mfma2<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes);
+  return mfma2<EPI>(R, N, K, X, W, Y, st, rm, ws, ws_bytes, norm);
 }
 
 }  // namespace
@@ -1066,13 +1130,15 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
 
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
                        int epi, hipStream_t st, const int32_t* row_map, float* splitk_ws,
-                       size_t splitk_bytes) {
+                       size_t splitk_bytes, GemmNorm* norm) {
+  if (norm) norm->done = false;
   if (R <= 0 || N <= 0) return hipSuccess;
   switch (epi) {
     case kEpiStoreF32:
       return dispatch<kEpiStoreF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes);
     case kEpiAddF32:
-      return dispatch<kEpiAddF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes);
+      return dispatch<kEpiAddF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes,
+                                  dtype == 1 ? norm : nullptr);
     case kEpiSwiGLU:
       return dispatch<kEpiSwiGLU>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes);
   }
