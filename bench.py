@@ -92,7 +92,8 @@ def roofline_pass(B, sess, kernel, step, args):
     """Per-kernel timing: the timed steps replay captured graphs, in which a
     single launch cannot be bracketed by events, so `roof_steps` further steps
     of the same workload run with the library's kernel timer on (eager
-    launches) and HIP events around every launch of `kernel`."""
+    launches), which records kernel-level start / end events on every launch
+    of `kernel`."""
     B.spec_timing_enable(sess.ctx, kernel)
     for s in range(args.roof_steps):
         step(args.warmup + args.steps + s, False)
@@ -505,7 +506,8 @@ def main():
                 "unit": unit, "frac": (achieved / peak) if achieved else None,
                 "traffic": pmc_traffic(info["kernel"], args.workload),
                 "launches": info["k_n"], "avg_launch_us": per_launch_ms * 1e3,
-                "timing": f"HIP events around each launch, {args.roof_steps} steps after the timed region"
+                "timing": f"kernel-level HIP events (start and end of each launch of the kernel), "
+                          f"{args.roof_steps} eager steps after the timed region"
                           + (" (verify launches only)" if args.workload == "8b-serving" else ""),
                 "bytes_per_launch": info["k_bytes"] / max(1, info["k_n"]),
                 "flops_per_launch": info["k_flops"] / max(1, info["k_n"])}

@@ -252,10 +252,12 @@ SPEC_API spec_status spec_draft_tokens(spec_ctx* ctx, int64_t seq_id, int32_t* t
 SPEC_API spec_status spec_set_graphs(spec_ctx* ctx, int32_t enable);
 
 /* Kernel timing for roofline measurement.  While a kernel name is set, the
- * context records HIP events on the call's stream around every launch of that
- * kernel (names as the profiler reports them without namespaces and argument
- * lists, e.g. "gemm_skinny_bf16<1, 2>", "gemm_mfma_bf16<0>",
- * "attn_bf16_kernel<128, 2>", "stats_kernel<true>") and accumulates the
+ * context times every launch of that kernel with HIP events that record the
+ * kernel's own start and end (the GEMM, attention and vocab-statistics
+ * kernels; other kernels: events on the call's stream around the launch).
+ * Names as the profiler reports them without namespaces and argument lists,
+ * e.g. "gemm_skinny_bf16<1, 2, true>", "gemm_mfma2_bf16<2, 6, 8>",
+ * "attn_bf16_kernel<128, 2, 4>", "stats_kernel<true>".  It accumulates the
  * elapsed time, the launch count and each launch's algorithmic HBM bytes and
  * flops (weights, activations and KV actually required, each read once).
  * name NULL or "" disables timing.  spec_timing_read waits for the recorded

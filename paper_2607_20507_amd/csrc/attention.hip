@@ -407,9 +407,9 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, const int32_t*
 
 template <int HD, int NT>
 void launch_item_kernel(const AttnArgs& a, const AttnItem* items, dim3 grid, int w, hipStream_t st) {
-  if (w >= 4) attn_bf16_kernel<HD, NT, 4><<<grid, 4 * kWave, 0, st>>>(a, items);
-  else if (w == 2) attn_bf16_kernel<HD, NT, 2><<<grid, 2 * kWave, 0, st>>>(a, items);
-  else attn_bf16_kernel<HD, NT, 1><<<grid, kWave, 0, st>>>(a, items);
+  if (w >= 4) launch_kernel(attn_bf16_kernel<HD, NT, 4>, grid, dim3(4 * kWave), 0, st, a, items);
+  else if (w == 2) launch_kernel(attn_bf16_kernel<HD, NT, 2>, grid, dim3(2 * kWave), 0, st, a, items);
+  else launch_kernel(attn_bf16_kernel<HD, NT, 1>, grid, dim3(kWave), 0, st, a, items);
 }
 
 template <int HD>

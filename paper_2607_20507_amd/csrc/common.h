@@ -2,10 +2,35 @@
 // MFMA operand types, wave64 reductions.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace spec {
+
+// Kernel-level timing: a timer arms a start / stop event pair for the next
+// launch made through launch_kernel, which then records the kernel's own
+// start and end (the interval a profiler reports), not the dispatch around
+// it.  Unarmed, launch_kernel is a plain launch (the only form used under
+// graph capture).
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+inline LaunchEvents& launch_events() {
+  static thread_local LaunchEvents e;
+  return e;
+}
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, size_t lds, hipStream_t st, Args... args) {
+  LaunchEvents& le = launch_events();
+  if (le.start) {
+    const LaunchEvents ev = le;
+    le = LaunchEvents{};
+    hipExtLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(lds), st, ev.start, ev.stop, 0u, args...);
+  } else {
+    kernel<<<grid, block, lds, st>>>(args...);
+  }
+}
 
 typedef uint16_t bf16_t;  // storage type: bf16 bit pattern
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

@@ -483,11 +483,11 @@ hipError_t gemv(int R, int N, int K, const void* X, const void* W, void* Y, hipS
   if (R > kGemvRows) return hipErrorInvalidValue;
   if constexpr (EPI == kEpiAddF32) {
     if (gemv_half(EPI, N)) {
-      gemv_bf16<EPI, kGemvRows, true><<<2 * tiles, 512, 0, st>>>(x, w, Y, R, N, K, row_map, fu);
+      launch_kernel(gemv_bf16<EPI, kGemvRows, true>, dim3(2 * tiles), dim3(512), 0, st, x, w, Y, R, N, K, row_map, fu);
       return hipGetLastError();
     }
   }
-  gemv_bf16<EPI, kGemvRows, false><<<tiles, 512, 0, st>>>(x, w, Y, R, N, K, row_map, fu);
+  launch_kernel(gemv_bf16<EPI, kGemvRows, false>, dim3(tiles), dim3(512), 0, st, x, w, Y, R, N, K, row_map, fu);
   return hipGetLastError();
 }
 
@@ -912,8 +912,8 @@ hipError_t skinny(int R, int N, int K, const void* X, const void* W, void* Y, hi
   if (FUSE && nw < 4) return hipErrorInvalidValue;  // the fused epilogue needs 256 threads
   const int kbpw = (nb + nw - 1) / nw;
   const size_t lds = static_cast<size_t>(nw) * NACC * 256 * sizeof(float);
-  gemm_skinny_bf16<MT, EPI, FUSE><<<tiles, nw * kWave, lds, st>>>(
-      static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map, fu);
+  launch_kernel(gemm_skinny_bf16<MT, EPI, FUSE>, dim3(tiles), dim3(nw * kWave), lds, st, static_cast<const bf16_t*>(X),
+                static_cast<const bf16_t*>(W), Y, R, N, K, kbpw, row_map, fu);
   return hipGetLastError();
 }
 
@@ -976,10 +976,12 @@ hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* 
   const int S = mfma2_splits(MT, NT, R, Nw, K, ws ? ws_bytes : 0, &k_len);
   const int grid = MT * NT * S;
   if (S <= 1) {
-    gemm_mfma2_bf16<EPI, MTW, NTW><<<grid, 256, 0, st>>>(x, w, Y, nullptr, R, N, K, K, MT, NT, rm);
+    launch_kernel(gemm_mfma2_bf16<EPI, MTW, NTW>, dim3(grid), dim3(256), 0, st, x, w, Y, static_cast<float*>(nullptr), R,
+                  N, K, K, MT, NT, rm);
     return hipGetLastError();
   }
-  gemm_mfma2_bf16<EPI, MTW, NTW><<<grid, 256, 0, st>>>(x, w, nullptr, ws, R, N, K, k_len, MT, NT, rm);
+  launch_kernel(gemm_mfma2_bf16<EPI, MTW, NTW>, dim3(grid), dim3(256), 0, st, x, w, static_cast<void*>(nullptr), ws, R,
+                N, K, k_len, MT, NT, rm);
   if (EPI == kEpiAddF32 && norm && !rm && N % 4 == 0 && N <= 4 * 256 * kNormRegChunks) {
     splitk_reduce_norm<<<R, 256, 0, st>>>(ws, S, R, N, static_cast<float*>(Y), static_cast<const bf16_t*>(norm->w),
                                           norm->eps, static_cast<bf16_t*>(norm->y));

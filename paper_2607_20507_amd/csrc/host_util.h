@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "attention.h"
+#include "common.h"
 
 namespace spec {
 
@@ -38,16 +39,34 @@ class EventTimer : public KernelTimer {
     for (hipEvent_t e : free_) (void)hipEventDestroy(e);
   }
   bool wants(const char* k) const override { return !name.empty() && name == k; }
+  // begin arms a kernel-level event pair for the next launch_kernel (the
+  // timed kernel's own start and end) and also records an event on the
+  // stream; end uses the kernel-level pair if a launch consumed it, else
+  // the stream events around the launch call.
   void begin(hipStream_t st) override {
     cur_ = take();
     if (cur_) (void)hipEventRecord(cur_, st);
+    ka_ = take();
+    kb_ = take();
+    if (ka_ && kb_) launch_events() = LaunchEvents{ka_, kb_};
   }
   void end(hipStream_t st, double b, double f) override {
-    hipEvent_t e = take();
-    if (!cur_ || !e) return;
-    (void)hipEventRecord(e, st);
-    recs_.push_back(Rec{cur_, e, b, f});
-    cur_ = nullptr;
+    LaunchEvents& le = launch_events();
+    const bool kernel_level = ka_ && kb_ && le.start == nullptr;
+    le = LaunchEvents{};
+    if (kernel_level) {
+      recs_.push_back(Rec{ka_, kb_, b, f});
+      if (cur_) free_.push_back(cur_);
+    } else {
+      if (ka_) free_.push_back(ka_);
+      if (kb_) free_.push_back(kb_);
+      hipEvent_t e = take();
+      if (cur_ && e) {
+        (void)hipEventRecord(e, st);
+        recs_.push_back(Rec{cur_, e, b, f});
+      }
+    }
+    cur_ = ka_ = kb_ = nullptr;
   }
   void flush() {
     for (auto& r : recs_) {
@@ -86,7 +105,7 @@ class EventTimer : public KernelTimer {
   }
   std::vector<hipEvent_t> free_;
   std::vector<Rec> recs_;
-  hipEvent_t cur_ = nullptr;
+  hipEvent_t cur_ = nullptr, ka_ = nullptr, kb_ = nullptr;
 };
 
 // Timer of the context-free entry points (spec_timing_enable with no context).

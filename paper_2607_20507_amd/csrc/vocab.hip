@@ -478,9 +478,9 @@ hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq*
   const bool timed = timer && timer->wants(vec ? "stats_kernel<true>" : "stats_kernel<false>");
   if (timed) timer->begin(st);
   if (vec)
-    stats_kernel<true><<<g1, kThreads, 0, st>>>(d_rows, p.V, p.chunk1, stats, p.n_chunks1);
+    launch_kernel(stats_kernel<true>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1);
   else
-    stats_kernel<false><<<g1, kThreads, 0, st>>>(d_rows, p.V, p.chunk1, stats, p.n_chunks1);
+    launch_kernel(stats_kernel<false>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1);
   if (timed) timer->end(st, 4.0 * p.n_rows * p.V, 0.0);
   dim3 g2(p.n_chunks2, p.B);
   if (vec)
