@@ -53,6 +53,76 @@ __global__ __launch_bounds__(256) void embed_kernel(int d, const int32_t* __rest
   }
 }
 
+// 8 consecutive elements widened to fp32 (16 bytes of bf16, 32 of fp32), and
+// back in the element type.
+__device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[2 * k] = __uint_as_float(w[k] << 16);
+    v[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float (&v)[8]) {
+  *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                            pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+}
+__device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+// The same gather for rows of 8-column chunks (d % 8 == 0, d <= 2048 * NCH):
+// thread t holds chunks t, t + 256, ... so that every load of the row (and of
+// the norm weight) is issued before the first store, one round trip instead
+// of one per 256 columns.  ss adds the eight squares pairwise, in the order
+// of the shuffle tree above, so both kernels give the same bits.
+template <typename T, int NCH>
+__global__ __launch_bounds__(256) void embed_vec_kernel(int d, const int32_t* __restrict__ tok_src,
+                                                        const int32_t* __restrict__ tok_pool,
+                                                        const T* __restrict__ E, float* __restrict__ h,
+                                                        int32_t* __restrict__ row_tok, T* __restrict__ hb,
+                                                        const T* __restrict__ wn, float* __restrict__ ss) {
+  const int r = blockIdx.x;
+  const int s = tok_src[r];
+  const int tok = s >= 0 ? s : tok_pool[-1 - s];
+  if (threadIdx.x == 0) row_tok[r] = tok;
+  const T* e = E + static_cast<size_t>(tok) * d;
+  const int nc = d / 8;
+  float x[NCH][8], w[NCH][8];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int j = min(static_cast<int>(threadIdx.x) + 256 * c, nc - 1);  // clamped: loads unconditional
+    load8(e + 8 * j, x[c]);
+    if (hb) load8(wn + 8 * j, w[c]);
+  }
+  float* o = h + static_cast<size_t>(r) * d;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int j = static_cast<int>(threadIdx.x) + 256 * c;
+    if (j >= nc) continue;
+    store8(o + 8 * j, x[c]);
+    if (hb) {
+      float y[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) y[k] = x[c][k] * w[c][k];
+      store8(hb + static_cast<size_t>(r) * d + 8 * j, y);
+    }
+    if (ss) {
+      float q[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) q[k] = x[c][k] * x[c][k];
+      ss[static_cast<size_t>(r) * nc + j] = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
+    }
+  }
+}
+
 // One workgroup per row.  Rows of up to 8192 columns (d % 4 == 0): thread t
 // holds 4-column chunks t, t + 256, ... of the row in registers (one round of
 // 16-byte loads, the norm weight's with them), so the row is read once and
@@ -245,6 +315,22 @@ hipError_t launch_embed(int dtype, int R, int d, const int32_t* tok_src, const i
                         float* ss) {
   if (R <= 0) return hipSuccess;
   if (ss && d % 16 != 0) return hipErrorInvalidValue;
+  const auto aligned = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+  const int nch = (d / 8 + 255) / 256;
+  if (d % 8 == 0 && nch <= 4 && aligned(E) && aligned(h) && aligned(hb) && aligned(wn)) {
+    if (dtype == 0) {
+      auto* k = nch == 1 ? embed_vec_kernel<float, 1> : nch == 2 ? embed_vec_kernel<float, 2>
+              : nch == 3 ? embed_vec_kernel<float, 3> : embed_vec_kernel<float, 4>;
+      k<<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const float*>(E), h, row_tok,
+                           static_cast<float*>(hb), static_cast<const float*>(wn), ss);
+    } else {
+      auto* k = nch == 1 ? embed_vec_kernel<bf16_t, 1> : nch == 2 ? embed_vec_kernel<bf16_t, 2>
+              : nch == 3 ? embed_vec_kernel<bf16_t, 3> : embed_vec_kernel<bf16_t, 4>;
+      k<<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const bf16_t*>(E), h, row_tok,
+                           static_cast<bf16_t*>(hb), static_cast<const bf16_t*>(wn), ss);
+    }
+    return hipGetLastError();
+  }
   if (dtype == 0)
     embed_kernel<float><<<R, 256, 0, st>>>(d, tok_src, tok_pool, static_cast<const float*>(E), h, row_tok,
                                            static_cast<float*>(hb), static_cast<const float*>(wn), ss);
