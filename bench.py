@@ -132,8 +132,7 @@ def bench_8b(args):
     lat = []
 
     def step(s, record):
-        for _ in range(k):
-            sess.draft_step([sid], [T], cfg.seed + s)
+        sess.draft_loop([sid], [T], cfg.seed + s, [k])  # k draft steps, one graph
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)

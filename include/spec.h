@@ -168,6 +168,22 @@ SPEC_API spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_i
 SPEC_API spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
                                      const float* temperature, uint64_t seed, void* stream);
 
+/* Several draft steps in one call (Section 2, speculative-decoding
+ * paragraph: the small model proposes k tokens autoregressively): sequence i
+ * takes part in steps[i] consecutive draft steps (0 <= steps[i], its draft
+ * count + steps[i] <= k_max), each exactly spec_draft_step with this seed,
+ * so the result (draft tokens, kept draft logits rows, caches) is the one
+ * steps[i] spec_draft_step calls give.  Each step's token is drawn on the
+ * device and feeds the next step there, so no step waits on the host: the
+ * draft pages of every step are taken at the start (list order), step 0 runs
+ * as one graph (the GPU starts while the host lays out the rest) and steps
+ * 1 .. max(steps) - 1 as a second one, their metadata uploaded once.
+ * temperature, steps: host [n].
+ * Errors as spec_draft_step; on an error no step has run.  Asynchronous. */
+SPEC_API spec_status spec_draft_loop(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
+                                     const float* temperature, uint64_t seed, const int32_t* steps,
+                                     void* stream);
+
 /* spec_draft_step with draft guidance, a workload-shaping hook: for each
  * sequence i with guide[i] >= 0 (host int32 [n]; -1 = none), the guide
  * token's draft logit is raised to the row maximum + boost (>= 0) before the

@@ -77,6 +77,7 @@ SIGNATURES = {
     "spec_last_logits": (c_int32, [_P, POINTER(c_void_p), _I32P]),
     "spec_set_graphs": (c_int32, [_P, c_int32]),
     "spec_draft_step_guided": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, c_float, _P]),
+    "spec_draft_loop": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, _P]),
     "spec_target_forward": (c_int32, [_P, c_int32, _I64P, _P]),
     "spec_draft_logits": (c_int32, [_P, c_int64, c_int32, _P]),
     "spec_draft_tokens": (c_int32, [_P, c_int64, _P, _P, _P]),
@@ -206,6 +207,14 @@ def spec_draft_step_guided(ctx: int, seq_ids, temperature, seed: int, guide, boo
     g = np.ascontiguousarray(np.asarray(guide, dtype=np.int32))
     check(lib().spec_draft_step_guided(ctx, len(ids), _ptr(ids, _I64P), _ptr(t, _F32P), seed, _ptr(g, _I32P),
                                        float(boost), stream_ptr(stream)), ctx)
+
+
+def spec_draft_loop(ctx: int, seq_ids, temperature, seed: int, steps, stream=None):
+    ids = _i64(seq_ids)
+    t = _f32(temperature)
+    k = np.ascontiguousarray(np.asarray(steps, dtype=np.int32))
+    check(lib().spec_draft_loop(ctx, len(ids), _ptr(ids, _I64P), _ptr(t, _F32P), seed, _ptr(k, _I32P),
+                                stream_ptr(stream)), ctx)
 
 
 def spec_target_forward(ctx: int, seq_ids, stream=None):

@@ -79,7 +79,7 @@ struct Seq {
 
 struct Ws {
   size_t h = 0, y = 0, qkv = 0, q = 0, o = 0, u = 0, logits = 0, dq = 0, dtok = 0, rowtok = 0;
-  size_t part_o = 0, part_ml = 0, vocab = 0, draft = 0, nacc = 0, otok = 0, meta = 0, gmeta = 0;
+  size_t part_o = 0, part_ml = 0, vocab = 0, draft = 0, meta = 0, gmeta = 0;
   size_t splitk = 0, splitk_bytes = 0, ss = 0;
   size_t meta_cap = 0, total = 0;
 };
@@ -150,7 +150,10 @@ struct spec_ctx {
   std::priority_queue<int, std::vector<int>, std::greater<int>> free_slots;
   Stager stager;
   int meta_next = 0;
-  int32_t* h_out = nullptr;  // pinned: n_acc [max_seqs] then tokens [max_seqs * (k_max + 1)]
+  // pinned, written by the decision pass's last kernel itself: n_acc [max_seqs]
+  // then tokens [max_seqs * (k_max + 1)]; h_out_dev is its device address
+  int32_t* h_out = nullptr;
+  int32_t* h_out_dev = nullptr;
   hipEvent_t out_ev = nullptr;
   std::string err;
   bool broken = false;
@@ -225,8 +228,6 @@ void compute_ws(spec_ctx* c) {
   const int vrows = c->max_seqs * (2 * c->k_max + 1);
   w.vocab = take(vocab_ws_bytes(vocab_plan(c->max_seqs, vrows, c->V)));
   w.draft = take(draft_ws_bytes(draft_plan(c->max_seqs, c->V)));
-  w.nacc = take(c->max_seqs * 4);
-  w.otok = take(vr * 4);
   w.splitk_bytes = gemm_splitk_bytes(c->R_max, std::max(c->qkv_max, 2 * c->ffn_max));
   w.splitk = take(w.splitk_bytes);
   // metadata bound for one call
@@ -305,7 +306,7 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   void* u = ctx->wsp + ctx->ws.u;
   // Up to 8 rows (batch-1 verify and draft steps) RMSNorm and RoPE / KV
   // append run inside the GEMMs (launch_gemm_fused): each residual-add GEMM
-  // (and the embedding) also writes bf16(h (.) w_next) into y and per-16-column
+  // (and the embedding) also writes bf16(h (.) w_next) into y and per-8-column
   // sums of squares into ss; the next GEMM reads y and scales its output rows
   // by 1/rms; the QKV GEMM applies RoPE and writes q and the KV cache itself.
   const bool fused = dt == 1 && R <= 8 && d.head_dim % 16 == 0 && d.d_model % 16 == 0;
@@ -608,8 +609,10 @@ spec_status spec_ctx_create(const spec_model_desc* target, const spec_model_desc
   c->R_max = std::max(cache->max_rows, cache->max_seqs * (cache->k_max + 1));
   for (int s = 0; s < c->max_seqs; ++s) c->free_slots.push(s);
   compute_ws(c);
+  // coherent: the kernel's stores go straight to host memory
   hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&c->h_out),
-                               sizeof(int32_t) * c->max_seqs * (c->k_max + 2), hipHostMallocDefault);
+                               sizeof(int32_t) * c->max_seqs * (c->k_max + 2), hipHostMallocCoherent);
+  if (e == hipSuccess) e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->h_out_dev), c->h_out, 0);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->out_ev, hipEventDisableTiming);
   if (e != hipSuccess) {
     g_err = std::string("hipHostMalloc/hipEventCreate: ") + hipGetErrorString(e);
@@ -834,11 +837,175 @@ spec_status draft_step_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
   return SPEC_OK;
 }
 
+// Draft steps 0 .. max(steps) - 1 of the listed sequences (sequence i in the
+// first steps[i]) as one graph, from the sequences' current state.  Callers
+// have validated the call and taken the pages of every step.  Each step is
+// the draft step above; since each step's token sources are the previous
+// step's device draws, the host lays all steps out at once: the page table is
+// shared by the steps and the metadata goes up in one block.  Metadata over
+// the call bound runs one draft_step_impl call per step instead.
+spec_status draft_steps_graph(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                              uint64_t seed, const int32_t* steps, hipStream_t st) {
+  Model& D = ctx->m[1];
+  int n_steps = 0;
+  std::vector<int> first(n);  // rows of the sequence's first step (catch-up rows after a commit)
+  for (int i = 0; i < n; ++i) {
+    const Seq& s = ctx->seqs[seq_ids[i]];
+    first[i] = s.k == 0 ? s.n() + 1 - s.len_d : 1;
+    n_steps = std::max(n_steps, steps[i]);
+  }
+  if (n_steps == 0) return SPEC_OK;
+  std::vector<const std::vector<int32_t>*> tabs;
+  for (int i = 0; i < n; ++i) tabs.push_back(&ctx->seqs[seq_ids[i]].pages_d);
+  float* dq = wsptr<float>(ctx, ctx->ws.dq);
+  MetaBlock mb;
+  std::vector<FwdOff> fo(n_steps);
+  std::vector<size_t> odr(n_steps);
+  std::vector<int> nrow(n_steps);
+  for (int j = 0; j < n_steps; ++j) {
+    Fwd f;
+    std::vector<DRow> dr;
+    for (int i = 0; i < n; ++i) {
+      if (steps[i] <= j) continue;
+      const Seq& s = ctx->seqs[seq_ids[i]];
+      const int k = s.k + j;                                           // drafts before this step
+      const int len = j == 0 ? s.len_d : s.len_d + first[i] + j - 1;  // draft cache length
+      const int c = j == 0 ? first[i] : 1;
+      f.segs.push_back(AttnSegment{i, static_cast<int32_t>(f.tok_src.size()), c, len});
+      for (int r = 0; r < c; ++r) {
+        const int pos = len + r;
+        f.tok_src.push_back(k == 0 ? s.hist[pos] : (k - 1 < s.k ? s.dsrc[k - 1] : dev_tok_ref(s.slot, ctx->k_max, k - 1)));
+        f.pos.push_back(pos);
+        f.slot.push_back(D.pool.slot(s.pages_d, pos));
+        f.seqi.push_back(i);
+      }
+      const int qidx = s.slot * ctx->k_max + k;
+      f.lm_rows.push_back(static_cast<int32_t>(f.tok_src.size()) - 1);
+      f.lm_map.push_back(qidx);
+      DRow d{};
+      d.ptr = dq + static_cast<size_t>(qidx) * ctx->V;
+      d.t = temperature[i];
+      d.pos = s.n() + k + 1;
+      d.seq_lo = static_cast<uint32_t>(static_cast<uint64_t>(s.id));
+      d.seq_hi = static_cast<uint32_t>(static_cast<uint64_t>(s.id) >> 32);
+      d.out = qidx;
+      d.guide = -1;
+      dr.push_back(d);
+    }
+    if (j == 0) build_ptab(tabs, f, ctx->max_pages);
+    fo[j] = add_forward(ctx, D, f, mb);
+    if (j > 0) {  // the page table of step 0 (row i = sequence i) serves every step
+      fo[j].pt = fo[0].pt;
+      fo[j].ptab_stride = fo[0].ptab_stride;
+    }
+    odr[j] = mb.add(dr);
+    nrow[j] = static_cast<int>(dr.size());
+  }
+  const size_t osd = mb.add(&seed, 1);
+  if (mb.size() > ctx->ws.meta_cap) {
+    for (int j = 0; j < n_steps; ++j) {
+      std::vector<int64_t> ids;
+      std::vector<float> ts;
+      for (int i = 0; i < n; ++i)
+        if (steps[i] > j) {
+          ids.push_back(seq_ids[i]);
+          ts.push_back(temperature[i]);
+        }
+      spec_status r = draft_step_impl(ctx, static_cast<int32_t>(ids.size()), ids.data(), ts.data(), seed,
+                                      nullptr, 0.f, st);
+      if (r != SPEC_OK) return r;
+    }
+    return SPEC_OK;
+  }
+  std::vector<int64_t> key = {3, n, n_steps, static_cast<int64_t>(osd)};
+  for (int j = 0; j < n_steps; ++j) {
+    key.push_back(static_cast<int64_t>(odr[j]));
+    key.push_back(nrow[j]);
+    key_forward(key, fo[j]);
+  }
+  spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
+    for (int j = 0; j < n_steps; ++j) {
+      spec_status r = launch_forward(ctx, D, fo[j], dev, dq, ls);
+      if (r != SPEC_OK) return r;
+      HIPC(launch_draft_sample(draft_plan(nrow[j], ctx->V), reinterpret_cast<const DRow*>(dev + odr[j]), seed,
+                               wsptr<int32_t>(ctx, ctx->ws.dtok), ctx->wsp + ctx->ws.draft, ls,
+                               reinterpret_cast<const uint64_t*>(dev + osd)));
+    }
+    return SPEC_OK;
+  });
+  if (s != SPEC_OK) return s;
+  for (int i = 0; i < n; ++i) {
+    Seq& q = ctx->seqs[seq_ids[i]];
+    for (int j = 0; j < steps[i]; ++j) {
+      const int qidx = q.slot * ctx->k_max + q.k;
+      q.len_d += j == 0 ? first[i] : 1;
+      q.qrow.push_back(dq + static_cast<size_t>(qidx) * ctx->V);
+      q.dsrc.push_back(dev_tok_ref(q.slot, ctx->k_max, q.k));
+      q.k += 1;
+    }
+  }
+  return SPEC_OK;
+}
+
+// Several draft steps in one call: validated as a whole (an error runs no
+// step), the pages of every step taken in list order, then step 0 on its own
+// graph, so that the GPU starts while the host lays out the later steps, and
+// steps 1 .. on one graph.
+spec_status draft_loop_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                            uint64_t seed, const int32_t* steps, void* stream) {
+  CHECK_READY();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n < 0 || (n > 0 && (!seq_ids || !temperature || !steps))) FAIL(SPEC_E_INVALID, "bad arguments");
+  if (n == 0) return SPEC_OK;
+  if (!check_ids(ctx, n, seq_ids, true)) return SPEC_E_INVALID;
+  Model& D = ctx->m[1];
+  int n_steps = 0, need = 0;
+  std::vector<int> first(n), total(n);  // rows of the first step, rows over all steps
+  for (int i = 0; i < n; ++i) {
+    Seq& s = ctx->seqs[seq_ids[i]];
+    if (!(temperature[i] >= 0.f)) FAIL(SPEC_E_INVALID, "temperature must be >= 0");
+    if (steps[i] < 0) FAIL(SPEC_E_INVALID, "steps must be >= 0");
+    if (steps[i] == 0) continue;
+    if (s.verified) FAIL(SPEC_E_STATE, "draft step after verify without commit");
+    if (s.external) FAIL(SPEC_E_STATE, "sequence holds external drafts");
+    if (s.k + steps[i] > ctx->k_max) FAIL(SPEC_E_STATE, "steps would exceed k_max drafts");
+    first[i] = s.k == 0 ? s.n() + 1 - s.len_d : 1;
+    total[i] = first[i] + steps[i] - 1;
+    if (D.pool.pages_for(s.len_d + total[i]) > ctx->max_pages)
+      FAIL(SPEC_E_INVALID, "sequence exceeds max_pages_per_seq");
+    need += D.pool.need(s.pages_d, s.len_d + total[i]);
+    n_steps = std::max(n_steps, steps[i]);
+  }
+  if (n_steps == 0) return SPEC_OK;
+  for (int j = 0; j < n_steps; ++j) {
+    int rows = 0;
+    for (int i = 0; i < n; ++i)
+      if (steps[i] > j) rows += j == 0 ? first[i] : 1;
+    if (rows > ctx->R_max) FAIL(SPEC_E_UNSUPPORTED, "draft rows exceed max_rows");
+  }
+  if (need > D.pool.free_pages()) FAIL(SPEC_E_NOPAGES, "draft KV page pool exhausted");
+  for (int i = 0; i < n; ++i)
+    if (steps[i] > 0) D.pool.ensure(ctx->seqs[seq_ids[i]].pages_d, ctx->seqs[seq_ids[i]].len_d + total[i]);
+  std::vector<int32_t> one(n), rest(n);
+  for (int i = 0; i < n; ++i) {
+    one[i] = std::min(steps[i], 1);
+    rest[i] = steps[i] - one[i];
+  }
+  spec_status s = draft_steps_graph(ctx, n, seq_ids, temperature, seed, one.data(), st);
+  if (s != SPEC_OK) return s;
+  return draft_steps_graph(ctx, n, seq_ids, temperature, seed, rest.data(), st);
+}
+
 }  // namespace
 
 spec_status spec_draft_step(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
                             uint64_t seed, void* stream) {
   return draft_step_impl(ctx, n, seq_ids, temperature, seed, nullptr, 0.f, stream);
+}
+
+spec_status spec_draft_loop(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                            uint64_t seed, const int32_t* steps, void* stream) {
+  return draft_loop_impl(ctx, n, seq_ids, temperature, seed, steps, stream);
 }
 
 spec_status spec_draft_step_guided(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
@@ -938,8 +1105,9 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   FwdOff o = add_forward(ctx, T, f, mb);
   const size_t orow = mb.add(rows), oseq = mb.add(vs);
   const size_t osd = mb.add(&seed, 1);
-  int32_t* d_nacc = wsptr<int32_t>(ctx, ctx->ws.nacc);
-  int32_t* d_otok = wsptr<int32_t>(ctx, ctx->ws.otok);
+  // the decision pass writes its outputs into pinned host memory (no copies)
+  int32_t* d_nacc = ctx->h_out_dev;
+  int32_t* d_otok = ctx->h_out_dev + ctx->max_seqs;
   const VocabPlan vp = vocab_plan(n, static_cast<int>(rows.size()), ctx->V);
   std::vector<int64_t> key = {decide ? 0 : 2, n, static_cast<int64_t>(rows.size()), static_cast<int64_t>(orow),
                               static_cast<int64_t>(oseq), static_cast<int64_t>(osd)};
@@ -957,10 +1125,14 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   ctx->last_rows = R;
   if (!decide) return SPEC_OK;
   const int W = ctx->k_max + 1;
-  HIPC(hipMemcpyAsync(ctx->h_out, d_nacc, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
-  HIPC(hipMemcpyAsync(ctx->h_out + ctx->max_seqs, d_otok, sizeof(int32_t) * n * W, hipMemcpyDeviceToHost, st));
   HIPC(hipEventRecord(ctx->out_ev, st));
-  HIPC(hipEventSynchronize(ctx->out_ev));
+  // poll instead of sleeping in hipEventSynchronize: the next draft step waits
+  // on this host round trip, and a blocking wait adds its wake-up to it
+  for (;;) {
+    const hipError_t q = hipEventQuery(ctx->out_ev);
+    if (q == hipSuccess) break;
+    if (q != hipErrorNotReady) HIPC(q);
+  }
   std::memcpy(n_accepted, ctx->h_out, sizeof(int32_t) * n);
   std::memcpy(out_tokens, ctx->h_out + ctx->max_seqs, sizeof(int32_t) * n * W);
   for (int i = 0; i < n; ++i) {

@@ -139,6 +139,10 @@ class SpecSession:
     def draft_step_guided(self, seq_ids, temps, seed: int, guide, boost: float, stream=None):
         B.spec_draft_step_guided(self.ctx, seq_ids, temps, seed, guide, boost, stream)
 
+    def draft_loop(self, seq_ids, temps, seed: int, steps, stream=None):
+        """steps[i] draft steps for sequence i in one call (one graph)."""
+        B.spec_draft_loop(self.ctx, seq_ids, temps, seed, steps, stream)
+
     def target_forward(self, seq_ids, stream=None):
         B.spec_target_forward(self.ctx, seq_ids, stream)
 
