@@ -764,43 +764,66 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
 
 // Split-K sum of a residual-add GEMM fused with the RMSNorm after it, one
 // workgroup per row m (N % 4 == 0, N <= 4 * 256 * kNormRegChunks): thread t
-// holds 4-column chunks t, t + 256, ... of the row in registers, adds the
-// partials in split order to h (as splitk_reduce does), writes h, then
+// holds the NCH 4-column chunks t, t + 256, ... of the row in registers, adds
+// the partials in split order to h (as splitk_reduce does), writes h, then
 // y[m] = bf16(h[m] / rms(h[m]) (.) w) with the sum of squares taken per
 // thread in chunk order, then over the wave and the waves in a fixed order.
+// Every load of a thread goes out before the first is used (h, w, then the
+// partials in batches of 8 / NCH splits, indexes clamped so that the loads
+// are unconditional): one or two round trips instead of one per chunk.
 constexpr int kNormRegChunks = 8;
 
+template <int NCH>
 __global__ __launch_bounds__(256) void splitk_reduce_norm(const float* __restrict__ part, int S, int R, int N,
                                                           float* __restrict__ Y, const bf16_t* __restrict__ w,
                                                           float eps, bf16_t* __restrict__ y) {
+  constexpr int B = NCH >= 8 ? 1 : 8 / NCH;  // splits per batch of loads
   const int m = blockIdx.x;
   const int nch = N / 4;
-  float4 hv[kNormRegChunks];
+  const float4* pp = reinterpret_cast<const float4*>(part) + static_cast<size_t>(m) * nch;
+  const size_t ps = static_cast<size_t>(R) * nch;  // float4 stride between splits
+  float4* hp = reinterpret_cast<float4*>(Y + static_cast<size_t>(m) * N);
+  int ch[NCH];
+  float4 h[NCH], v[NCH];
+  uint2 wv[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    ch[c] = min(static_cast<int>(threadIdx.x) + c * 256, nch - 1);
+    h[c] = hp[ch[c]];
+    wv[c] = reinterpret_cast<const uint2*>(w)[ch[c]];
+    v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  for (int s0 = 0; s0 < S; s0 += B) {
+    float4 p[B][NCH];
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) p[b][c] = pp[min(s0 + b, S - 1) * ps + ch[c]];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      if (s0 + b >= S) break;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        v[c].x += p[b][c].x;
+        v[c].y += p[b][c].y;
+        v[c].z += p[b][c].z;
+        v[c].w += p[b][c].w;
+      }
+    }
+  }
   float ss = 0.f;
 #pragma unroll
-  for (int c = 0; c < kNormRegChunks; ++c) {
-    const int ch = threadIdx.x + c * 256;
-    if (ch >= nch) continue;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s = 0; s < S; ++s) {
-      const float4 p = reinterpret_cast<const float4*>(part + (static_cast<size_t>(s) * R + m) * N)[ch];
-      v.x += p.x;
-      v.y += p.y;
-      v.z += p.z;
-      v.w += p.w;
-    }
-    float4* hp = reinterpret_cast<float4*>(Y + static_cast<size_t>(m) * N) + ch;
-    float4 h = *hp;
-    h.x += v.x;
-    h.y += v.y;
-    h.z += v.z;
-    h.w += v.w;
-    *hp = h;
-    hv[c] = h;
-    ss = fmaf(h.x, h.x, ss);
-    ss = fmaf(h.y, h.y, ss);
-    ss = fmaf(h.z, h.z, ss);
-    ss = fmaf(h.w, h.w, ss);
+  for (int c = 0; c < NCH; ++c) {
+    if (static_cast<int>(threadIdx.x) + c * 256 >= nch) continue;
+    h[c].x += v[c].x;
+    h[c].y += v[c].y;
+    h[c].z += v[c].z;
+    h[c].w += v[c].w;
+    hp[ch[c]] = h[c];
+    ss = fmaf(h[c].x, h[c].x, ss);
+    ss = fmaf(h[c].y, h[c].y, ss);
+    ss = fmaf(h[c].z, h[c].z, ss);
+    ss = fmaf(h[c].w, h[c].w, ss);
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
@@ -810,13 +833,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_norm(const float* __restric
   const float tot = s_part[0] + s_part[1] + s_part[2] + s_part[3];
   const float inv = 1.f / sqrtf(tot / static_cast<float>(N) + eps);
 #pragma unroll
-  for (int c = 0; c < kNormRegChunks; ++c) {
-    const int ch = threadIdx.x + c * 256;
-    if (ch >= nch) continue;
-    const float4 h = hv[c];
-    const float v0 = h.x * inv * bf16_to_f32(w[4 * ch]), v1 = h.y * inv * bf16_to_f32(w[4 * ch + 1]);
-    const float v2 = h.z * inv * bf16_to_f32(w[4 * ch + 2]), v3 = h.w * inv * bf16_to_f32(w[4 * ch + 3]);
-    reinterpret_cast<uint2*>(y + static_cast<size_t>(m) * N)[ch] = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+  for (int c = 0; c < NCH; ++c) {
+    if (static_cast<int>(threadIdx.x) + c * 256 >= nch) continue;
+    const float v0 = h[c].x * inv * __uint_as_float(wv[c].x << 16);
+    const float v1 = h[c].y * inv * __uint_as_float(wv[c].x & 0xFFFF0000u);
+    const float v2 = h[c].z * inv * __uint_as_float(wv[c].y << 16);
+    const float v3 = h[c].w * inv * __uint_as_float(wv[c].y & 0xFFFF0000u);
+    reinterpret_cast<uint2*>(y + static_cast<size_t>(m) * N)[ch[c]] =
+        make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
   }
 }
 
@@ -983,8 +1007,11 @@ hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* 
   launch_kernel(gemm_mfma2_bf16<EPI, MTW, NTW>, dim3(grid), dim3(256), 0, st, x, w, static_cast<void*>(nullptr), ws, R,
                 N, K, k_len, MT, NT, rm);
   if (EPI == kEpiAddF32 && norm && !rm && N % 4 == 0 && N <= 4 * 256 * kNormRegChunks) {
-    splitk_reduce_norm<<<R, 256, 0, st>>>(ws, S, R, N, static_cast<float*>(Y), static_cast<const bf16_t*>(norm->w),
-                                          norm->eps, static_cast<bf16_t*>(norm->y));
+    const int nch = (N / 4 + 255) / 256;
+    auto* k = nch <= 1 ? splitk_reduce_norm<1> : nch <= 2 ? splitk_reduce_norm<2>
+            : nch <= 4 ? splitk_reduce_norm<4> : splitk_reduce_norm<8>;
+    k<<<R, 256, 0, st>>>(ws, S, R, N, static_cast<float*>(Y), static_cast<const bf16_t*>(norm->w), norm->eps,
+                         static_cast<bf16_t*>(norm->y));
     norm->done = true;
     return hipGetLastError();
   }

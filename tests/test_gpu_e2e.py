@@ -241,14 +241,31 @@ def test_fused_small_rows_teacher_forced(which):
 
 
 
-def test_split_k_rows_teacher_forced():
+def _wide_pair(d, hd):
+    """One-layer bf16 target of width d (32 query / 8 kv heads of hd), small
+    FFN and vocabulary, with a one-layer drafter: the residual-add GEMMs of a
+    48-row verify split K and fold the RMSNorm into the split-K reduction at
+    this row width."""
+    from workloads.configs import ModelShape, PairConfig
+    t = ModelShape(f"w{d}-target", 1, d, 32, 8, hd, 1024, 2048, 5e5)
+    dr = ModelShape(f"w{d}-draft", 1, 512, 8, 8, 64, 512, 2048, 5e5)
+    return PairConfig(f"w{d}", t, dr, batch=8, context=("uniform", 40, 90), k=(5,), temperatures=(0.7,),
+                      steps=1)
+
+
+@pytest.mark.parametrize("which", ["small-2L", "d2048", "d4096"])
+def test_split_k_rows_teacher_forced(which):
     """A verify of 8 sequences (48 rows): every projection runs on the MFMA
     kernel with split-K, the residual-add GEMMs' split-K reduction also
-    applies the next RMSNorm, and rope_kv does RoPE / KV append.  Every
-    verify logits row against the oracle's no-cache forward over the same
-    tokens, within 2e-2."""
+    applies the next RMSNorm (rows of 1024, 2048 and 4096 columns: one, two
+    and four 4-column chunks per thread), and rope_kv does RoPE / KV append.
+    Every verify logits row against the oracle's no-cache forward over the
+    same tokens, within 2e-2."""
     from paper_2607_20507_amd.session import DeviceModel, SpecSession
-    cfg, lt, ld = SMALL_BF16, 2, 1
+    if which == "small-2L":
+        cfg, lt, ld = SMALL_BF16, 2, 1
+    else:
+        cfg, lt, ld = (_wide_pair(2048, 64) if which == "d2048" else _wide_pair(4096, 128)), 1, 1
     k = cfg.k[0]
     dev = device()
     tw = model_weights(cfg.target, cfg.seed, lt)
@@ -258,7 +275,7 @@ def test_split_k_rows_teacher_forced():
     tgt = Decoder(cfg.target, tw)
     ids = list(range(100, 108))
     prompts = uniform_prompts(cfg.seed + 5, [40 + 7 * i for i in range(8)], cfg.target.vocab)
-    say("split-K rows teacher-forced: prefill 8 sequences")
+    say("split-K rows teacher-forced", which, ": prefill 8 sequences")
     gpu.prefill(ids, prompts)
     rng = np.random.default_rng(9)
     keep, drafts = [], {}
