@@ -762,6 +762,63 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
   }
 }
 
+// The same sum for N % 4 == 0, 4 columns per thread: every split's loads
+// (gate and up for SwiGLU) go out in batches of 8 before the first add, and
+// the output row index with them, so that a reduction over S splits costs
+// one or two round trips rather than S.  Sums in split order, as above.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce4(const float* __restrict__ part, int S, int R, int N,
+                                                      void* __restrict__ Y, const int32_t* __restrict__ row_map) {
+  constexpr bool SW = (EPI == kEpiSwiGLU);
+  constexpr int B = 8;
+  const int n4 = N / 4, nw4 = SW ? 2 * n4 : n4;
+  const size_t ps = static_cast<size_t>(R) * nw4;  // float4 stride between splits
+  const size_t total = static_cast<size_t>(R) * n4;
+  for (size_t e = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
+       e += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    const int m = static_cast<int>(e / n4), c = static_cast<int>(e % n4);
+    const int row = row_map ? row_map[m] : m;
+    const float4* pr = reinterpret_cast<const float4*>(part) + static_cast<size_t>(m) * nw4 + c;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f), u = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; s0 < S; s0 += B) {
+      float4 p[B], q[SW ? B : 1];
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        const size_t o = static_cast<size_t>(min(s0 + b, S - 1)) * ps;
+        p[b] = pr[o];
+        if (SW) q[b] = pr[o + n4];
+      }
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        if (s0 + b >= S) break;
+        v.x += p[b].x;
+        v.y += p[b].y;
+        v.z += p[b].z;
+        v.w += p[b].w;
+        if (SW) {
+          u.x += q[b].x;
+          u.y += q[b].y;
+          u.z += q[b].z;
+          u.w += q[b].w;
+        }
+      }
+    }
+    const size_t o = static_cast<size_t>(row) * n4 + c;
+    if (EPI == kEpiStoreF32) reinterpret_cast<float4*>(Y)[o] = v;
+    if (EPI == kEpiAddF32) {
+      float4 h = reinterpret_cast<float4*>(Y)[o];
+      h.x += v.x;
+      h.y += v.y;
+      h.z += v.z;
+      h.w += v.w;
+      reinterpret_cast<float4*>(Y)[o] = h;
+    }
+    if (EPI == kEpiSwiGLU)
+      reinterpret_cast<uint2*>(Y)[o] = make_uint2(pack_bf16x2(silu(v.x) * u.x, silu(v.y) * u.y),
+                                                  pack_bf16x2(silu(v.z) * u.z, silu(v.w) * u.w));
+  }
+}
+
 // Split-K sum of a residual-add GEMM fused with the RMSNorm after it, one
 // workgroup per row m (N % 4 == 0, N <= 4 * 256 * kNormRegChunks): thread t
 // holds the NCH 4-column chunks t, t + 256, ... of the row in registers, adds
@@ -1013,6 +1070,12 @@ hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* 
     k<<<R, 256, 0, st>>>(ws, S, R, N, static_cast<float*>(Y), static_cast<const bf16_t*>(norm->w), norm->eps,
                          static_cast<bf16_t*>(norm->y));
     norm->done = true;
+    return hipGetLastError();
+  }
+  if (N % 4 == 0) {
+    const size_t total = static_cast<size_t>(R) * (N / 4);
+    const int blocks = static_cast<int>(std::min<size_t>(2048, (total + 255) / 256));
+    splitk_reduce4<EPI><<<blocks, 256, 0, st>>>(ws, S, R, N, Y, rm);
     return hipGetLastError();
   }
   const size_t total = static_cast<size_t>(R) * N;
