@@ -136,27 +136,58 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(const VRow* __restrict_
   }
 }
 
-// Merge all chunk statistics of one row.
-__device__ __forceinline__ void row_stats(const VStat* st, int n_chunks, float it, bool greedy,
-                                          float& M, float& S, int& idx) {
-  M = -INFINITY;
-  idx = INT_MAX;
-  for (int c = 0; c < n_chunks; ++c) {
-    const VStat v = st[c];
-    if (v.m > M) {  // chunks are in index order: the first chunk holding the max wins ties
-      M = v.m;
-      idx = v.idx;
-    }
-  }
-  S = 0.f;
-  if (!greedy)
-    for (int c = 0; c < n_chunks; ++c) S += scaled(st[c].s, st[c].m, M, it);
-}
-
 __device__ __forceinline__ void pick_update(float sc, int i, float& best, int& bi) {
   if (sc > best || (sc == best && i < bi)) {
     best = sc;
     bi = i;
+  }
+}
+
+// Merge all chunk statistics of one row.  Chunk records are read in batches
+// of kStatBatch (indexes clamped, so that every load of a batch is in flight
+// before the first is used) and still taken in chunk order.
+constexpr int kStatBatch = 8;
+
+__device__ __forceinline__ void row_stats(const VStat* st, int n_chunks, float it, bool greedy,
+                                          float& M, float& S, int& idx) {
+  M = -INFINITY;
+  idx = INT_MAX;
+  for (int c0 = 0; c0 < n_chunks; c0 += kStatBatch) {
+    VStat v[kStatBatch];
+#pragma unroll
+    for (int b = 0; b < kStatBatch; ++b) v[b] = st[min(c0 + b, n_chunks - 1)];
+#pragma unroll
+    for (int b = 0; b < kStatBatch; ++b)
+      if (c0 + b < n_chunks && v[b].m > M) {  // chunks in index order: the first chunk holding the max wins ties
+        M = v[b].m;
+        idx = v[b].idx;
+      }
+  }
+  S = 0.f;
+  if (!greedy)
+    for (int c0 = 0; c0 < n_chunks; c0 += kStatBatch) {
+      VStat v[kStatBatch];
+#pragma unroll
+      for (int b = 0; b < kStatBatch; ++b) v[b] = st[min(c0 + b, n_chunks - 1)];
+#pragma unroll
+      for (int b = 0; b < kStatBatch; ++b)
+        if (c0 + b < n_chunks) S += scaled(v[b].s, v[b].m, M, it);
+    }
+}
+
+// Best pick (and fallback pick) over a row's chunk records, in chunk order.
+__device__ __forceinline__ void merge_picks(const VPick* pk, int n_chunks, float& best, int& bi, float& fb,
+                                            int& fi) {
+  for (int c0 = 0; c0 < n_chunks; c0 += kStatBatch) {
+    VPick v[kStatBatch];
+#pragma unroll
+    for (int b = 0; b < kStatBatch; ++b) v[b] = pk[min(c0 + b, n_chunks - 1)];
+#pragma unroll
+    for (int b = 0; b < kStatBatch; ++b)
+      if (c0 + b < n_chunks) {
+        pick_update(v[b].score, v[b].idx, best, bi);
+        pick_update(v[b].fb_score, v[b].fb_idx, fb, fi);
+      }
   }
 }
 
@@ -295,11 +326,7 @@ __global__ void final_kernel(const VSeq* __restrict__ seqs, const int32_t* __res
   if (d.mode != kGreedy) {
     float best = -INFINITY, fb = -INFINITY;
     int bi = INT_MAX, fi = INT_MAX;
-    for (int c = 0; c < n_chunks2; ++c) {
-      const VPick p = picks[static_cast<size_t>(b) * n_chunks2 + c];
-      pick_update(p.score, p.idx, best, bi);
-      pick_update(p.fb_score, p.fb_idx, fb, fi);
-    }
+    merge_picks(picks + static_cast<size_t>(b) * n_chunks2, n_chunks2, best, bi, fb, fi);
     // an empty residual (only possible when p == q) falls back to drawing from p
     t = (best == -INFINITY) ? fi : bi;
   }
@@ -418,12 +445,9 @@ __global__ void draft_final_kernel(const DRow* __restrict__ rows, const VPick* _
                                    int n_chunks, int n, int32_t* __restrict__ tokens) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= n) return;
-  float best = -INFINITY;
-  int bi = INT_MAX;
-  for (int c = 0; c < n_chunks; ++c) {
-    const VPick p = picks[static_cast<size_t>(r) * n_chunks + c];
-    pick_update(p.score, p.idx, best, bi);
-  }
+  float best = -INFINITY, fb = -INFINITY;
+  int bi = INT_MAX, fi = INT_MAX;
+  merge_picks(picks + static_cast<size_t>(r) * n_chunks, n_chunks, best, bi, fb, fi);
   tokens[rows[r].out] = bi;
 }
 
