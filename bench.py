@@ -388,6 +388,7 @@ def bench_vocab(args):
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     tokens = 0
+    early_rows = 0
     lats = []
     for s in range(args.steps):
         a = torch.cuda.Event(enable_timing=True)
@@ -396,7 +397,11 @@ def bench_vocab(args):
         step(args.warmup + s)
         b.record(stream)
         lats.append((a, b))
-        tokens += int(na.sum().item()) + Bn
+        acc = na.cpu().numpy()
+        tokens += int(acc.sum()) + Bn
+        # early-exit accounting: rows up to the first rejection (p rows 0..a,
+        # q rows 0..min(a, k-1)); the parallel pass reads all 2k + 1 rows
+        early_rows += int(np.sum(acc + 1 + np.minimum(acc + 1, k)))
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -406,7 +411,12 @@ def bench_vocab(args):
     return {"tokens": tokens, "wall_s": wall, "event_ms": ev0.elapsed_time(ev1),
             "verify_ms_median": float(np.median(ls)), "verify_ms_p90": float(np.percentile(ls, 90)),
             "kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops,
-            "acc_hist": []}
+            "acc_hist": [],
+            "vocab_bytes": {"read_per_step": 4.0 * V * Bn * (2 * k + 1),
+                            "early_exit_per_step": 4.0 * V * early_rows / args.steps,
+                            "note": "logit rows the parallel pass reads (all k + 1 p rows and k q rows) "
+                                    "vs the rows an early-exit scan would need (p rows 0..a, q rows "
+                                    "0..min(a, k-1)); the rejected or bonus row's second read is not counted"}}
 
 
 def cpu_baseline_vocab(mean_tokens_per_step):
@@ -526,6 +536,12 @@ def main():
         "offclock_ms_per_step": info.get("offclock_ms", 0.0) / steps,
         "roofline": roofline,
     }
+    if "vocab_bytes" in info:
+        vb = dict(info["vocab_bytes"])
+        ms = line["ms_per_step"]
+        vb["read_gbs"] = vb["read_per_step"] / (ms / 1e3) / 1e9
+        vb["early_exit_gbs"] = vb["early_exit_per_step"] / (ms / 1e3) / 1e9
+        line["vocab_bytes"] = vb
     if not args.no_cpu_baseline:
         mean_tok = info["tokens"] / steps
         model, threads, aff = cpu_info()
