@@ -544,10 +544,19 @@ spec_status launch_clears(spec_ctx* ctx, const std::vector<int32_t>& ct, const s
   if (s != SPEC_OK) return s;
   const Model& T = ctx->m[0];
   const Model& D = ctx->m[1];
-  HIPC(launch_kv_clear(T.dt(), static_cast<int>(ct.size()), reinterpret_cast<const int32_t*>(dev + ot),
-                       T.kv, T.d.n_layers, T.layer_stride, T.v_off, T.d.n_kv_heads, T.d.head_dim, st));
-  HIPC(launch_kv_clear(D.dt(), static_cast<int>(cd.size()), reinterpret_cast<const int32_t*>(dev + od),
-                       D.kv, D.d.n_layers, D.layer_stride, D.v_off, D.d.n_kv_heads, D.d.head_dim, st));
+  auto job = [&](const Model& M, const std::vector<int32_t>& c, size_t off) {
+    KvClearJob j;
+    j.slots = reinterpret_cast<const int32_t*>(dev + off);
+    j.n = static_cast<int>(c.size());
+    j.kv = M.kv;
+    j.n_layers = M.d.n_layers;
+    j.layer_stride = M.layer_stride;
+    j.v_off = M.v_off;
+    j.Hkv = M.d.n_kv_heads;
+    j.hd = M.d.head_dim;
+    return j;
+  };
+  HIPC(launch_kv_clear(T.dt(), job(T, ct, ot), job(D, cd, od), st));  // one launch for both pools
   return SPEC_OK;
 }
 

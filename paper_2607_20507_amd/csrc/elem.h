@@ -29,9 +29,19 @@ hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta
                           const int32_t* pos, const int32_t* slot, void* q, void* kpool,
                           void* vpool, hipStream_t st, bool rot_tiled = false);
 
-// Zero the K and V entries of `n` flat slots in every layer of a pool whose
-// layer l holds K at kv + l * layer_stride and V at + v_off (elements).
-hipError_t launch_kv_clear(int dtype, int n, const int32_t* slots, void* kv, int n_layers,
-                           size_t layer_stride, size_t v_off, int Hkv, int hd, hipStream_t st);
+// Zero the K and V entries of `n` flat slots (device list) in every layer of
+// a pool whose layer l holds K at kv + l * layer_stride and V at + v_off
+// (elements).
+struct KvClearJob {
+  const int32_t* slots = nullptr;
+  int n = 0;
+  void* kv = nullptr;
+  int n_layers = 0;
+  size_t layer_stride = 0, v_off = 0;
+  int Hkv = 0, hd = 0;
+};
+
+// Both jobs (the target's and the drafter's pool, same dtype) in one launch.
+hipError_t launch_kv_clear(int dtype, const KvClearJob& a, const KvClearJob& b, hipStream_t st);
 
 }  // namespace spec

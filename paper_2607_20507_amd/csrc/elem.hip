@@ -2,6 +2,7 @@
 // x / sqrt(mean(x^2) + eps) * w), rotate-half RoPE fused with the paged KV
 // append, and in-place clearing of rolled-back KV slots.
 
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -293,17 +294,18 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void kv_clear_kernel(const int32_t* __restrict__ slots, T* __restrict__ kv,
-                                                       size_t layer_stride, size_t v_off, int Hkv, int hd) {
+__global__ __launch_bounds__(256) void kv_clear_kernel(KvClearJob j0, KvClearJob j1) {
+  const KvClearJob& j = blockIdx.z ? j1 : j0;
   const int i = blockIdx.x, l = blockIdx.y;
-  const int sl = slots[i];
+  if (i >= j.n || l >= j.n_layers) return;
+  const int sl = j.slots[i];
   const int page = sl >> 4, off = sl & 15;
-  T* K = kv + l * layer_stride;
-  T* V = K + v_off;
-  for (int e = threadIdx.x; e < Hkv * hd; e += blockDim.x) {
-    const int h = e / hd, dd = e % hd;
-    const size_t blk = (static_cast<size_t>(page) * Hkv + h) * 16 * hd;
-    K[blk + k_index<T>(off, dd, hd)] = T(0);
+  T* K = static_cast<T*>(j.kv) + l * j.layer_stride;
+  T* V = K + j.v_off;
+  for (int e = threadIdx.x; e < j.Hkv * j.hd; e += blockDim.x) {
+    const int h = e / j.hd, dd = e % j.hd;
+    const size_t blk = (static_cast<size_t>(page) * j.Hkv + h) * 16 * j.hd;
+    K[blk + k_index<T>(off, dd, j.hd)] = T(0);
     V[blk + v_index<T>(off, dd)] = T(0);
   }
 }
@@ -367,14 +369,14 @@ hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta
   return hipGetLastError();
 }
 
-hipError_t launch_kv_clear(int dtype, int n, const int32_t* slots, void* kv, int n_layers,
-                           size_t layer_stride, size_t v_off, int Hkv, int hd, hipStream_t st) {
+hipError_t launch_kv_clear(int dtype, const KvClearJob& a, const KvClearJob& b, hipStream_t st) {
+  const int n = std::max(a.n, b.n);
   if (n <= 0) return hipSuccess;
-  dim3 grid(n, n_layers);
+  dim3 grid(n, std::max(a.n > 0 ? a.n_layers : 0, b.n > 0 ? b.n_layers : 0), 2);
   if (dtype == 0)
-    kv_clear_kernel<float><<<grid, 256, 0, st>>>(slots, static_cast<float*>(kv), layer_stride, v_off, Hkv, hd);
+    kv_clear_kernel<float><<<grid, 256, 0, st>>>(a, b);
   else
-    kv_clear_kernel<bf16_t><<<grid, 256, 0, st>>>(slots, static_cast<bf16_t*>(kv), layer_stride, v_off, Hkv, hd);
+    kv_clear_kernel<bf16_t><<<grid, 256, 0, st>>>(a, b);
   return hipGetLastError();
 }
 
