@@ -537,16 +537,10 @@ void key_forward(std::vector<int64_t>& k, const FwdOff& o) {
 spec_status launch_clears(spec_ctx* ctx, const std::vector<int32_t>& ct, const std::vector<int32_t>& cd,
                           hipStream_t st) {
   if (ct.empty() && cd.empty()) return SPEC_OK;
-  MetaBlock mb;
-  const size_t ot = mb.add(ct), od = mb.add(cd);
-  char* dev = nullptr;
-  spec_status s = upload_meta(ctx, mb, st, &dev);
-  if (s != SPEC_OK) return s;
   const Model& T = ctx->m[0];
   const Model& D = ctx->m[1];
-  auto job = [&](const Model& M, const std::vector<int32_t>& c, size_t off) {
+  auto job = [&](const Model& M, const std::vector<int32_t>& c) {
     KvClearJob j;
-    j.slots = reinterpret_cast<const int32_t*>(dev + off);
     j.n = static_cast<int>(c.size());
     j.kv = M.kv;
     j.n_layers = M.d.n_layers;
@@ -556,7 +550,22 @@ spec_status launch_clears(spec_ctx* ctx, const std::vector<int32_t>& ct, const s
     j.hd = M.d.head_dim;
     return j;
   };
-  HIPC(launch_kv_clear(T.dt(), job(T, ct, ot), job(D, cd, od), st));  // one launch for both pools
+  KvClearJob a = job(T, ct), b = job(D, cd);
+  if (ct.size() <= static_cast<size_t>(kKvClearInline) && cd.size() <= static_cast<size_t>(kKvClearInline)) {
+    // few slots (a single sequence's commit): they travel in the kernel
+    // arguments, with no metadata upload before the launch
+    std::copy(ct.begin(), ct.end(), a.inl);
+    std::copy(cd.begin(), cd.end(), b.inl);
+  } else {
+    MetaBlock mb;
+    const size_t ot = mb.add(ct), od = mb.add(cd);
+    char* dev = nullptr;
+    spec_status s = upload_meta(ctx, mb, st, &dev);
+    if (s != SPEC_OK) return s;
+    a.slots = reinterpret_cast<const int32_t*>(dev + ot);
+    b.slots = reinterpret_cast<const int32_t*>(dev + od);
+  }
+  HIPC(launch_kv_clear(T.dt(), a, b, st));  // one launch for both pools
   return SPEC_OK;
 }
 

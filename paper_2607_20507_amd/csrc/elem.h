@@ -32,8 +32,11 @@ hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta
 // Zero the K and V entries of `n` flat slots (device list) in every layer of
 // a pool whose layer l holds K at kv + l * layer_stride and V at + v_off
 // (elements).
+constexpr int kKvClearInline = 16;
+
 struct KvClearJob {
-  const int32_t* slots = nullptr;
+  const int32_t* slots = nullptr;  // device list, or null: the first n of `inl`
+  int32_t inl[kKvClearInline] = {};
   int n = 0;
   void* kv = nullptr;
   int n_layers = 0;

@@ -298,7 +298,7 @@ __global__ __launch_bounds__(256) void kv_clear_kernel(KvClearJob j0, KvClearJob
   const KvClearJob& j = blockIdx.z ? j1 : j0;
   const int i = blockIdx.x, l = blockIdx.y;
   if (i >= j.n || l >= j.n_layers) return;
-  const int sl = j.slots[i];
+  const int sl = j.slots ? j.slots[i] : j.inl[i];
   const int page = sl >> 4, off = sl & 15;
   T* K = static_cast<T*>(j.kv) + l * j.layer_stride;
   T* V = K + j.v_off;

@@ -61,7 +61,7 @@ def _slot(pages, pos):
     return pages[pos // 16], pos % 16
 
 
-def _session(which):
+def _session(which, n_seqs):
     from paper_2607_20507_amd.session import DeviceModel, SpecSession
     cfg, lt, ld = (TINY_FP32, None, None) if which == "fp32" else (SMALL_BF16, 2, 1)
     dev = device()
@@ -69,26 +69,28 @@ def _session(which):
     dw = model_weights(cfg.draft, cfg.seed + 1, ld)
     pages = 24
     gpu = SpecSession(DeviceModel(cfg.target, tw, dev, n_layers=lt), DeviceModel(cfg.draft, dw, dev, n_layers=ld),
-                      max_seqs=2, k_max=max(cfg.k), max_pages_per_seq=pages, max_rows=256)
+                      max_seqs=n_seqs, k_max=max(cfg.k), max_pages_per_seq=pages, max_rows=256)
     Lt = cfg.target.n_layers if lt is None else lt
     Ld = cfg.draft.n_layers if ld is None else ld
-    return gpu, cfg, (Lt, Ld), 2 * pages
+    return gpu, cfg, (Lt, Ld), n_seqs * pages
 
 
-@pytest.mark.parametrize("which", ["fp32", "bf16"])
-def test_commit_and_rollback_clear_rejected_slots(which):
-    gpu, cfg, (Lt, Ld), npages = _session(which)
+# two sequences: the slots to clear travel in the kernel arguments; four or
+# five: more than 16 per pool, uploaded as call metadata
+@pytest.mark.parametrize("which,n_seqs", [("fp32", 2), ("bf16", 2), ("fp32", 5), ("bf16", 4)])
+def test_commit_and_rollback_clear_rejected_slots(which, n_seqs):
+    gpu, cfg, (Lt, Ld), npages = _session(which, n_seqs)
     k = max(cfg.k)
-    ids = [11, 12]
-    prompts = uniform_prompts(cfg.seed + 8, [37, 50], cfg.target.vocab)
+    ids = [11 + i for i in range(n_seqs)]
+    prompts = uniform_prompts(cfg.seed + 8, [37 + 13 * i for i in range(n_seqs)], cfg.target.vocab)
     say("kv clear", which, ": prefill, draft", k, "steps, verify, commit with a = 0")
     gpu.prefill(ids, prompts)
     n = {sid: gpu.seq_info(sid)["target_len"] for sid in ids}
     for _ in range(k):
-        gpu.draft_step(ids, [1.0, 1.0], 3)
-    gpu.verify(ids, [1.0, 1.0], 3)
+        gpu.draft_step(ids, [1.0] * n_seqs, 3)
+    gpu.verify(ids, [1.0] * n_seqs, 3)
     before = {sid: gpu.seq_info(sid) for sid in ids}
-    gpu.commit(ids, [0, 0])
+    gpu.commit(ids, [0] * n_seqs)
     torch.cuda.synchronize()
     tp = _Pool(gpu.kv_target, cfg.target, Lt, npages)
     dp = _Pool(gpu.kv_draft, cfg.draft, Ld, npages)
