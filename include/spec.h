@@ -226,6 +226,20 @@ SPEC_API spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_id
 SPEC_API spec_status spec_kv_commit(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
                                     const int32_t* n_accepted, void* stream);
 
+/* The tail of one speculative round and the start of the next in one call,
+ * so that the host round trip between them stays inside the library:
+ * spec_verify (verify_seed; outputs as there, on the host when the call
+ * returns), then spec_kv_commit of every listed sequence with the a the
+ * verify returned, then spec_draft_loop of the next round (draft_seed,
+ * steps[i] drafts for sequence i, host [n]).  The result equals the three
+ * calls made in that order.  On an error the calls before it have taken
+ * effect (a verify that failed commits nothing; a failed commit drafts
+ * nothing).  The drafts are asynchronous, as in spec_draft_loop. */
+SPEC_API spec_status spec_verify_commit_draft(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
+                                              const float* temperature, uint64_t verify_seed,
+                                              int32_t* n_accepted, int32_t* out_tokens,
+                                              uint64_t draft_seed, const int32_t* steps, void* stream);
+
 /* Truncate both caches of a sequence to `new_len` positions (0 <= new_len <=
  * target length); history[new_len] becomes the pending token and outstanding
  * drafts are dropped.  Cleared in place like a commit.  Asynchronous. */

@@ -78,6 +78,8 @@ SIGNATURES = {
     "spec_set_graphs": (c_int32, [_P, c_int32]),
     "spec_draft_step_guided": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, c_float, _P]),
     "spec_draft_loop": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, _P]),
+    "spec_verify_commit_draft": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, _I32P, c_uint64, _I32P,
+                                           _P]),
     "spec_target_forward": (c_int32, [_P, c_int32, _I64P, _P]),
     "spec_draft_logits": (c_int32, [_P, c_int64, c_int32, _P]),
     "spec_draft_tokens": (c_int32, [_P, c_int64, _P, _P, _P]),
@@ -237,6 +239,21 @@ def spec_verify(ctx: int, seq_ids, temperature, seed: int, k_max: int, stream=No
     ot = np.full((n, k_max + 1), -1, dtype=np.int32)
     check(lib().spec_verify(ctx, n, _ptr(ids, _I64P), _ptr(t, _F32P), seed, _ptr(na, _I32P),
                             _ptr(ot, _I32P), stream_ptr(stream)), ctx)
+    return na, ot
+
+
+def spec_verify_commit_draft(ctx: int, seq_ids, temperature, verify_seed: int, k_max: int, draft_seed: int,
+                             steps, stream=None):
+    """spec_verify, spec_kv_commit and spec_draft_loop in one call.
+    Returns (n_accepted [n], out_tokens [n, k_max + 1])."""
+    ids = _i64(seq_ids)
+    t = _f32(temperature)
+    n = len(ids)
+    k = np.ascontiguousarray(np.asarray(steps, dtype=np.int32))
+    na = np.zeros(n, dtype=np.int32)
+    ot = np.full((n, k_max + 1), -1, dtype=np.int32)
+    check(lib().spec_verify_commit_draft(ctx, n, _ptr(ids, _I64P), _ptr(t, _F32P), verify_seed, _ptr(na, _I32P),
+                                         _ptr(ot, _I32P), draft_seed, _ptr(k, _I32P), stream_ptr(stream)), ctx)
     return na, ot
 
 

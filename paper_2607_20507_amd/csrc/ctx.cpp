@@ -1259,6 +1259,17 @@ spec_status spec_kv_commit(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, con
   return launch_clears(ctx, ct, cd, st);
 }
 
+spec_status spec_verify_commit_draft(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                                     uint64_t verify_seed, int32_t* n_accepted, int32_t* out_tokens,
+                                     uint64_t draft_seed, const int32_t* steps, void* stream) {
+  if (!ctx || (n > 0 && !steps)) return SPEC_E_INVALID;
+  spec_status s = spec_verify(ctx, n, seq_ids, temperature, verify_seed, n_accepted, out_tokens, stream);
+  if (s != SPEC_OK) return s;
+  s = spec_kv_commit(ctx, n, seq_ids, n_accepted, stream);
+  if (s != SPEC_OK) return s;
+  return spec_draft_loop(ctx, n, seq_ids, temperature, draft_seed, steps, stream);
+}
+
 spec_status spec_kv_rollback(spec_ctx* ctx, int64_t seq_id, int32_t new_len, void* stream) {
   CHECK_READY();
   hipStream_t st = static_cast<hipStream_t>(stream);

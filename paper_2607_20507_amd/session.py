@@ -152,6 +152,11 @@ class SpecSession:
     def verify(self, seq_ids, temps, seed: int, stream=None):
         return B.spec_verify(self.ctx, seq_ids, temps, seed, self.k_max, stream)
 
+    def verify_commit_draft(self, seq_ids, temps, verify_seed: int, draft_seed: int, steps, stream=None):
+        """verify, commit with the accepted counts, then draft_loop of the next round, in one call."""
+        return B.spec_verify_commit_draft(self.ctx, seq_ids, temps, verify_seed, self.k_max, draft_seed, steps,
+                                          stream)
+
     def commit(self, seq_ids, n_accepted, stream=None):
         B.spec_kv_commit(self.ctx, seq_ids, n_accepted, stream)
 

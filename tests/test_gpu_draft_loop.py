@@ -97,3 +97,37 @@ def test_draft_loop_rejects_bad_steps():
     with pytest.raises(B.SpecError):
         loop.draft_loop(ids, [1.0, 1.0], 1, [1, 0])
     loop.close()
+
+
+@pytest.mark.parametrize("which", ["bf16", "fp32"])
+def test_verify_commit_draft_matches_separate_calls(which):
+    """spec_verify_commit_draft against spec_verify + spec_kv_commit +
+    spec_draft_loop made one by one in a second context: decisions, emitted
+    tokens, the next round's drafts and their logits rows, and the lengths,
+    bit for bit over 4 rounds."""
+    cfg, lt, ld, n_seqs = (SMALL_BF16, 2, 2, 3) if which == "bf16" else (TINY_FP32, None, None, 2)
+    fused, ref, k = _pair(cfg, lt, ld, max_seqs=n_seqs, pages=24)
+    ids = [int(x) for x in seq_ids_for(cfg.seed + 5, n_seqs)]
+    prompts = uniform_prompts(cfg.seed + 4, [30 + 11 * i for i in range(n_seqs)], cfg.target.vocab)
+    temps = [[0.8, 0.0, 1.0][i % 3] for i in range(n_seqs)]
+    fused.prefill(ids, prompts)
+    ref.prefill(ids, prompts)
+    steps = [k - (i % 2) for i in range(n_seqs)]
+    fused.draft_loop(ids, temps, 50, steps)
+    ref.draft_loop(ids, temps, 50, steps)
+    for r in range(4):
+        say("verify+commit+draft round", r)
+        na, oa = fused.verify_commit_draft(ids, temps, 60 + r, 51 + r, steps)
+        nb, ob = ref.verify(ids, temps, 60 + r)
+        ref.commit(ids, nb)
+        ref.draft_loop(ids, temps, 51 + r, steps)
+        assert np.array_equal(na, nb) and np.array_equal(oa, ob), f"round {r}: verify differs"
+        for sid, s in zip(ids, steps):
+            assert fused.draft_tokens(sid) == ref.draft_tokens(sid), f"round {r} seq {sid}: drafts differ"
+            for j in range(s):
+                assert torch.equal(fused.draft_logits(sid, j), ref.draft_logits(sid, j))
+            ia, ib = fused.seq_info(sid), ref.seq_info(sid)
+            for key in ("target_len", "draft_len", "pending_pos"):
+                assert ia[key] == ib[key]
+    fused.close()
+    ref.close()
