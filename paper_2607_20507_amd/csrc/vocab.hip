@@ -276,15 +276,28 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(
     }
   };
   if (VEC) {
-    for (int i4 = (beg >> 2) + threadIdx.x; i4 < (end >> 2); i4 += kThreads) {
-      const uint4 w = philox_block(key, sid, static_cast<uint32_t>(i4));
-      const float4 p = reinterpret_cast<const float4*>(zp)[i4];
-      float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (mode == kResample) q = reinterpret_cast<const float4*>(zq)[i4];
-      score(p.x, q.x, w.x, 4 * i4);
-      score(p.y, q.y, w.y, 4 * i4 + 1);
-      score(p.z, q.z, w.z, 4 * i4 + 2);
-      score(p.w, q.w, w.w, 4 * i4 + 3);
+    // batches of 4 float4 per thread (clamped loads, all in flight before the
+    // first is used), then the same per-element order as one at a time
+    const int e4 = end >> 2;
+    for (int i0 = (beg >> 2) + threadIdx.x; i0 < e4; i0 += 4 * kThreads) {
+      float4 pv[4], qv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = min(i0 + u * kThreads, e4 - 1);
+        pv[u] = reinterpret_cast<const float4*>(zp)[j];
+        qv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (mode == kResample) qv[u] = reinterpret_cast<const float4*>(zq)[j];  // zq is null otherwise
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i4 = i0 + u * kThreads;
+        if (i4 >= e4) break;
+        const uint4 w = philox_block(key, sid, static_cast<uint32_t>(i4));
+        score(pv[u].x, qv[u].x, w.x, 4 * i4);
+        score(pv[u].y, qv[u].y, w.y, 4 * i4 + 1);
+        score(pv[u].z, qv[u].z, w.z, 4 * i4 + 2);
+        score(pv[u].w, qv[u].w, w.w, 4 * i4 + 3);
+      }
     }
   } else {
     for (int i = beg + threadIdx.x; i < end; i += kThreads) {
@@ -355,19 +368,29 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
   float best = -INFINITY;
   int bi = INT_MAX;
   if (VEC) {
-    for (int i4 = (beg >> 2) + threadIdx.x; i4 < (end >> 2); i4 += kThreads) {
-      const float4 v = reinterpret_cast<const float4*>(z)[i4];
-      if (greedy) {
-        pick_update(v.x, 4 * i4, best, bi);
-        pick_update(v.y, 4 * i4 + 1, best, bi);
-        pick_update(v.z, 4 * i4 + 2, best, bi);
-        pick_update(v.w, 4 * i4 + 3, best, bi);
-      } else {
-        const uint4 w = philox_block(key, sid, static_cast<uint32_t>(i4));
-        pick_update(v.x * it + gumbel_of(w.x), 4 * i4, best, bi);
-        pick_update(v.y * it + gumbel_of(w.y), 4 * i4 + 1, best, bi);
-        pick_update(v.z * it + gumbel_of(w.z), 4 * i4 + 2, best, bi);
-        pick_update(v.w * it + gumbel_of(w.w), 4 * i4 + 3, best, bi);
+    // batches of 4 float4 per thread, as in decide_kernel
+    const int e4 = end >> 2;
+    for (int i0 = (beg >> 2) + threadIdx.x; i0 < e4; i0 += 4 * kThreads) {
+      float4 vv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) vv[u] = reinterpret_cast<const float4*>(z)[min(i0 + u * kThreads, e4 - 1)];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i4 = i0 + u * kThreads;
+        if (i4 >= e4) break;
+        const float4 v = vv[u];
+        if (greedy) {
+          pick_update(v.x, 4 * i4, best, bi);
+          pick_update(v.y, 4 * i4 + 1, best, bi);
+          pick_update(v.z, 4 * i4 + 2, best, bi);
+          pick_update(v.w, 4 * i4 + 3, best, bi);
+        } else {
+          const uint4 w = philox_block(key, sid, static_cast<uint32_t>(i4));
+          pick_update(v.x * it + gumbel_of(w.x), 4 * i4, best, bi);
+          pick_update(v.y * it + gumbel_of(w.y), 4 * i4 + 1, best, bi);
+          pick_update(v.z * it + gumbel_of(w.z), 4 * i4 + 2, best, bi);
+          pick_update(v.w * it + gumbel_of(w.w), 4 * i4 + 3, best, bi);
+        }
       }
     }
   } else {
