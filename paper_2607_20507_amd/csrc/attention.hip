@@ -271,37 +271,64 @@ __global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_bf16_kernel(Attn
 }
 
 // One workgroup per (group, kv head, 4 query vectors), one thread per (query
-// vector, head dim).  Up to kCombineOnePass parts: every part's (max, sum)
-// and output element is loaded before the first is used (one round trip),
-// then the maximum and the weighted sums.  More parts: two passes (maximum,
-// then weighted sums), each issuing batches of 8 independent loads.  Both
-// sum the parts in index order.
+// vector, DPT consecutive head dims: DPT = 4 (float4 loads of the partial
+// outputs) for head dim 128, 1 for head dim 64, as measured).  Up
+// to kCombineOnePass parts: every part's (max, sum) and output vector is
+// loaded before the first is used (one round trip), then the maximum and the
+// weighted sums.  More parts: two passes (maximum, then weighted sums), each
+// issuing batches of 8 independent loads.  Both sum the parts in index order,
+// per element as a one-element-per-thread combine would.
 constexpr int kCombineQv = 4;
 constexpr int kCombineOnePass = 32;
 
-template <int HD>
-__global__ __launch_bounds__(HD * kCombineQv) void attn_combine_kernel(AttnArgs a,
-                                                                        const AttnGroup* __restrict__ groups) {
+template <int DPT>
+struct CombVec;
+template <>
+struct CombVec<1> {
+  float v[1];
+  __device__ __forceinline__ void load(const float* p) { v[0] = *p; }
+};
+template <>
+struct CombVec<4> {
+  float v[4];
+  __device__ __forceinline__ void load(const float* p) {
+    const float4 t = *reinterpret_cast<const float4*>(p);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  }
+};
+
+template <int HD, int DPT>
+__global__ __launch_bounds__(HD / DPT * kCombineQv) void attn_combine_kernel(AttnArgs a,
+                                                                              const AttnGroup* __restrict__ groups) {
+  constexpr int TQ = HD / DPT;  // threads per query vector
   const AttnGroup gr = groups[blockIdx.x];
   const int gkv = blockIdx.y;
-  const int m = blockIdx.z * kCombineQv + static_cast<int>(threadIdx.x) / HD;
+  const int m = blockIdx.z * kCombineQv + static_cast<int>(threadIdx.x) / TQ;
   const int G = a.Hq / a.Hkv;
   if (m >= gr.nrows * G) return;
-  const int d = threadIdx.x % HD;
+  const int d0 = DPT * (threadIdx.x % TQ);  // dims d0 .. d0 + DPT - 1
   const int n = gr.nparts;
   const size_t base = static_cast<size_t>(gr.part0 * a.Hkv + gkv) * 64 + m;
   const size_t stride = static_cast<size_t>(a.Hkv) * 64;
   const float2* ml = reinterpret_cast<const float2*>(a.part_ml);
-  float num = 0.f, den = 0.f;
+  float num[DPT];
+#pragma unroll
+  for (int i = 0; i < DPT; ++i) num[i] = 0.f;
+  float den = 0.f;
+  auto acc = [&](float w, const CombVec<DPT>& o, float l) {
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) num[i] += w * o.v[i];
+    den += w * l;
+  };
   if (n <= kCombineOnePass) {
     float2 mlc[kCombineOnePass];
-    float oc[kCombineOnePass];
+    CombVec<DPT> oc[kCombineOnePass];
 #pragma unroll
     for (int j = 0; j < kCombineOnePass; ++j)
       if (j < n) {
         const size_t pm = base + j * stride;
         mlc[j] = ml[pm];
-        oc[j] = a.part_o[pm * HD + d];
+        oc[j].load(a.part_o + pm * HD + d0);
       }
     float mx = -INFINITY;
 #pragma unroll
@@ -310,11 +337,7 @@ __global__ __launch_bounds__(HD * kCombineQv) void attn_combine_kernel(AttnArgs 
     if (mx != -INFINITY) {
 #pragma unroll
       for (int j = 0; j < kCombineOnePass; ++j)
-        if (j < n) {
-          const float w = mlc[j].x != -INFINITY ? exp2f(mlc[j].x - mx) : 0.f;
-          num += w * oc[j];
-          den += w * mlc[j].y;
-        }
+        if (j < n) acc(mlc[j].x != -INFINITY ? exp2f(mlc[j].x - mx) : 0.f, oc[j], mlc[j].y);
     }
   } else {
     constexpr int B = 8;
@@ -329,24 +352,28 @@ __global__ __launch_bounds__(HD * kCombineQv) void attn_combine_kernel(AttnArgs 
     if (mx != -INFINITY) {
       for (int c0 = 0; c0 < n; c0 += B) {
         float2 mc[B];
-        float oc[B];
+        CombVec<DPT> oc[B];
 #pragma unroll
         for (int j = 0; j < B; ++j) {
           const size_t pm = base + min(c0 + j, n - 1) * stride;
           mc[j] = ml[pm];
-          oc[j] = a.part_o[pm * HD + d];
+          oc[j].load(a.part_o + pm * HD + d0);
         }
 #pragma unroll
-        for (int j = 0; j < B; ++j) {
-          const float w = (c0 + j < n && mc[j].x != -INFINITY) ? exp2f(mc[j].x - mx) : 0.f;
-          num += w * oc[j];
-          den += w * mc[j].y;
-        }
+        for (int j = 0; j < B; ++j)
+          if (c0 + j < n) acc(mc[j].x != -INFINITY ? exp2f(mc[j].x - mx) : 0.f, oc[j], mc[j].y);
       }
     }
   }
-  const size_t o = (static_cast<size_t>(gr.row0 + m / G) * a.Hq + gkv * G + m % G) * HD + d;
-  static_cast<bf16_t*>(a.out)[o] = f32_to_bf16(den > 0.f ? num / den : 0.f);
+  const size_t o = (static_cast<size_t>(gr.row0 + m / G) * a.Hq + gkv * G + m % G) * HD + d0;
+  const bool ok = den > 0.f;
+  bf16_t* out = static_cast<bf16_t*>(a.out) + o;
+  if constexpr (DPT == 4) {
+    *reinterpret_cast<uint2*>(out) = make_uint2(pack_bf16x2(ok ? num[0] / den : 0.f, ok ? num[1] / den : 0.f),
+                                                pack_bf16x2(ok ? num[2] / den : 0.f, ok ? num[3] / den : 0.f));
+  } else {
+    out[0] = f32_to_bf16(ok ? num[0] / den : 0.f);
+  }
 }
 
 // fp32: one wave per (row, head); each lane runs an online softmax over keys
@@ -421,8 +448,11 @@ hipError_t launch_bf16_hd(const AttnArgs& a, const AttnItem* items, int n_items,
     else if (nt == 2) launch_item_kernel<HD, 2>(a, items, grid, w, st);
     else launch_item_kernel<HD, 4>(a, items, grid, std::min(w, 2), st);
   }
-  if (n_groups > 0)
-    attn_combine_kernel<HD><<<dim3(n_groups, a.Hkv, 16 * nt / kCombineQv), HD * kCombineQv, 0, st>>>(a, groups);
+  if (n_groups > 0) {
+    constexpr int DPT = HD == 128 ? 4 : 1;
+    attn_combine_kernel<HD, DPT><<<dim3(n_groups, a.Hkv, 16 * nt / kCombineQv), HD / DPT * kCombineQv, 0, st>>>(
+        a, groups);
+  }
   return hipGetLastError();
 }
 
