@@ -97,6 +97,21 @@ class Session:
             out.append(x)
         return out
 
+    def draft_loop(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int,
+                   steps: Sequence[int], margins: rule.Margins = rule.Margins()):
+        """steps[i] draft steps of sequence i as one call: the draft pages of
+        all of a call's steps are taken first, sequence by sequence in list
+        order, then the steps run (step j for every sequence that takes part
+        in it, in list order), each exactly draft_step."""
+        for sid, n_steps in zip(seq_ids, steps):
+            if n_steps > 0:
+                st = self.seqs[int(sid)]
+                first = 1 if st.drafts else st.n + 1 - st.kv_d.length
+                self.pool_d.ensure(int(sid), st.kv_d.length + first + n_steps - 1)
+        for j in range(max(steps, default=0)):
+            part = [(s, t) for s, t, n_s in zip(seq_ids, temps, steps) if n_s > j]
+            self.draft_step([s for s, _ in part], [t for _, t in part], seed, margins)
+
     def set_drafts(self, sid: int, drafts: Sequence[int], zq: np.ndarray):
         """Install externally supplied drafts (tokens and their draft logits)."""
         st = self.seqs[int(sid)]
@@ -121,6 +136,17 @@ class Session:
                 res.first_excluded = 0 if res.first_excluded is None else res.first_excluded
             out.append((res, zp))
         return out
+
+    def undo_verify(self, seq_ids: Sequence[int]):
+        """Take back the last verify of the listed sequences: drop the K/V it
+        wrote (positions n..n+k) and the target pages that only it needed, so
+        that the cache and the page pool are as before the verify.  The drafts
+        stay."""
+        for sid in seq_ids:
+            sid = int(sid)
+            st = self.seqs[sid]
+            st.kv_t.truncate(st.n)
+            self.pool_t.truncate(sid, st.n)
 
     def commit(self, seq_ids: Sequence[int], results: Sequence[rule.VerifyResult]):
         for sid, res in zip(seq_ids, results):

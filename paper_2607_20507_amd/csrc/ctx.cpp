@@ -416,7 +416,10 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
     }
   }
   if (o.n_lm > 0) {
-    if (fused) {
+    // the fused GEMM takes whole 16-row tiles of W: a vocabulary that is not a
+    // multiple of 16 goes through the row-gathering RMSNorm and the plain GEMM
+    // (h holds the residual stream either way)
+    if (fused && d.vocab % 16 == 0) {
       GemmFuse fl;
       fl.ss = ss;
       fl.xrow = I(o.lmr);
@@ -1045,6 +1048,8 @@ spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k, const int3
   if (s.k > 0 && !s.external) FAIL(SPEC_E_STATE, "sequence already has drafts from spec_draft_step");
   for (int j = 0; j < k; ++j)
     if (tokens[j] < 0 || tokens[j] >= ctx->V) FAIL(SPEC_E_INVALID, "draft token out of range");
+  if (k > 0 && ctx->V % 4 == 0 && (reinterpret_cast<uintptr_t>(q_logits) & 15))
+    FAIL(SPEC_E_INVALID, "draft logits must be 16-byte aligned");
   s.k = k;
   s.external = k > 0;
   s.qrow.clear();

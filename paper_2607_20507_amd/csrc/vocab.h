@@ -44,20 +44,24 @@ struct DRow {
 
 struct VocabPlan {
   int B = 0, n_rows = 0, V = 0;
-  int chunk1 = 0, n_chunks1 = 0;  // statistics pass
-  int chunk2 = 0, n_chunks2 = 0;  // residual / bonus draw
+  int chunk1 = 0, n_chunks1 = 0;  // statistics pass (n_chunks1 <= 64)
+  int chunk2 = 0, n_chunks2 = 0;  // residual draw (n_chunks2 <= 64)
 };
 
 VocabPlan vocab_plan(int B, int n_rows, int V);
 size_t vocab_ws_bytes(const VocabPlan& p);
 
-// Full decision pass.  Outputs n_acc[B], out_tok[B * (kmax + 1)] (device).
-// d_seed (optional, device): read the Philox seed there instead of `seed`, so
-// that a captured graph of the pass takes a new seed with each replay.
+// Full decision pass: statistics, one decision per sequence, the residual or
+// bonus draw of sampled sequences, the merge of its chunk winners.  Outputs
+// n_acc[B], out_tok[B * (kmax + 1)] (device).  d_seed (optional, device): read
+// the Philox seed there instead of `seed`, so that a captured graph of the pass
+// takes a new seed with each replay.  A sequence's rows must be 16-byte aligned
+// when V % 4 == 0 (the vector path); `aligned` = false forces the scalar path.
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax,
                              int32_t* d_n_acc, int32_t* d_out_tok, void* d_ws, hipStream_t st,
-                             KernelTimer* timer = nullptr, const uint64_t* d_seed = nullptr);
+                             KernelTimer* timer = nullptr, const uint64_t* d_seed = nullptr,
+                             bool aligned = true);
 
 struct DraftPlan {
   int n = 0, V = 0, chunk = 0, n_chunks = 0;

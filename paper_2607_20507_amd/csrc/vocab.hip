@@ -4,18 +4,30 @@
 // Section 3.4): draft x~_j is accepted iff u_j * q_j(x~_j) < p_j(x~_j); at the
 // first rejection a token is drawn from norm(max(0, p_j - q_j)); if every draft
 // is accepted a bonus token is drawn from p_{k+1}.  Categorical draws use the
-// Gumbel-max trick, argmax_i (log w_i + G_i), with per-token Philox noise.
+// Gumbel-max trick with per-token Philox noise: argmax_i (log w_i + G_i), or,
+// where the weights are known only up to a factor, the equivalent exponential
+// race argmax_i w_i / E_i with E_i = -log u_i.
 //
-// Three launches, all HBM-streaming with 16-byte coalesced loads:
-//   1. stats   grid (chunks, rows): per row chunk, max, first argmax and
-//              sum exp((z - max) / T) in one online pass.
-//   2. decide  grid (chunks, seqs): every workgroup of a sequence repeats the
-//              cheap acceptance scan (one lane per draft, merged chunk stats,
-//              two gathered logits, one Philox draw), then streams its chunk
-//              of the one row that is sampled (residual or bonus).
-//   3. final   one thread per sequence: merge chunk winners, write outputs.
-// A greedy sequence (T = 0) needs no second pass: the first mismatch between
-// a draft and the target's argmax decides, and that argmax is the token.
+// Four launches:
+//   1. stats    grid (chunks, rows), HBM-streaming with 16-byte loads: per
+//               row chunk, max, first argmax and sum exp((z - max) / T) in one
+//               online pass.
+//   2. decide   one workgroup per sequence: every chunk record of the
+//               sequence's 2k + 1 rows and the gathered p(x~), q(x~) in one
+//               round of loads, then the acceptance scan (one lane per draft,
+//               one Philox draw each).  Greedy outcomes are final here; a
+//               sampled sequence leaves the row to draw from and its
+//               normalisers.
+//   3. draw     grid (chunks, sequences): only sampled sequences stream the
+//               row they draw from: a rejected (p, q) pair for the residual
+//               max(0, p - q), or the bonus row p_{k+1}.  Both by exponential
+//               race, which needs no logarithm of the weights.
+//   4. final    one wave per sampled sequence: merge the chunk winners.
+// Carrying the bonus winner along in the statistics pass (one Gumbel score
+// per token of the bonus row) measured 40 us slower at 256 x 8 x 128256: its
+// workgroups run several times longer than the others.
+// Every kernel keeps its loads of a thread in flight together and merges in a
+// fixed order, so results do not depend on timing.
 
 #include <algorithm>
 #include <climits>
@@ -30,7 +42,11 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTargetBlocks = 2048;  // enough workgroups to cover 256 CUs several times
+constexpr int kMaxChunks = 64;
+constexpr float kLog2e = 1.4426950408889634f;
 
+// Chunk record of the statistics pass: (max, sum of exp((z - max) / T),
+// first argmax).
 struct VStat {
   float m, s;
   int32_t idx, pad;
@@ -42,8 +58,12 @@ struct VPick {
   int32_t fb_idx;
 };
 enum { kGreedy = 0, kResample = 1, kBonus = 2 };
+// Decision of one sequence: accepted count, mode and, for a sampled draw,
+// the normalisers of the rows it reads (p only for the bonus).
 struct VDec {
-  int32_t a, mode, token, pad;
+  int32_t a, mode;
+  float Mp, Sp, Mq, Sq;
+  int32_t pad[2];
 };
 
 __device__ __forceinline__ float scaled(float s, float m, float M, float it) {
@@ -59,22 +79,8 @@ __device__ __forceinline__ void stat_merge(float& m, float& s, int& idx, float m
   m = M;
 }
 
-__device__ __forceinline__ void stat_update4(float4 v, int base, float it, bool greedy, float& m,
-                                             float& s, int& idx) {
-  const float vm = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
-  if (vm > m) {
-    const int j = (v.x == vm) ? 0 : (v.y == vm) ? 1 : (v.z == vm) ? 2 : 3;
-    if (!greedy) s = scaled(s, m, vm, it);
-    m = vm;
-    idx = base + j;
-  }
-  if (!greedy)
-    s += __expf((v.x - m) * it) + __expf((v.y - m) * it) + __expf((v.z - m) * it) +
-         __expf((v.w - m) * it);
-}
-
-__device__ __forceinline__ void stat_update1(float v, int i, float it, bool greedy, float& m,
-                                             float& s, int& idx) {
+__device__ __forceinline__ void stat_update1(float v, int i, float it, bool greedy, float& m, float& s,
+                                             int& idx) {
   if (v > m) {
     if (!greedy) s = scaled(s, m, v, it);
     m = v;
@@ -83,10 +89,63 @@ __device__ __forceinline__ void stat_update1(float v, int i, float it, bool gree
   if (!greedy) s += __expf((v - m) * it);
 }
 
+__device__ __forceinline__ void stat_update4(float4 v, int base, float it, bool greedy, float& m, float& s,
+                                             int& idx) {
+  const float vm = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
+  if (vm > m) {
+    const int j = (v.x == vm) ? 0 : (v.y == vm) ? 1 : (v.z == vm) ? 2 : 3;
+    if (!greedy) s = scaled(s, m, vm, it);
+    m = vm;
+    idx = base + j;
+  }
+  if (!greedy)
+    s += __expf((v.x - m) * it) + __expf((v.y - m) * it) + __expf((v.z - m) * it) + __expf((v.w - m) * it);
+}
+
+__device__ __forceinline__ void pick_update(float sc, int i, float& best, int& bi) {
+  if (sc > best || (sc == best && i < bi)) {
+    best = sc;
+    bi = i;
+  }
+}
+
+__device__ __forceinline__ uint32_t word_of(uint4 w, int e) {
+  return e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
+}
+
+__device__ __forceinline__ void wave_pick(float& best, int& bi) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float b2 = __shfl_xor(best, o, kWave);
+    const int i2 = __shfl_xor(bi, o, kWave);
+    pick_update(b2, i2, best, bi);
+  }
+}
+
+// Statistics of one row chunk.
 template <bool VEC>
-__global__ __launch_bounds__(kThreads) void stats_kernel(const VRow* __restrict__ rows, int V,
-                                                         int chunk, VStat* __restrict__ stats,
-                                                         int n_chunks) {
+__device__ __forceinline__ void stats_chunk(const float* __restrict__ z, int beg, int end, float it, bool greedy,
+                                            float& m, float& s, int& idx) {
+  if (VEC) {
+    const float4* p4 = reinterpret_cast<const float4*>(z);
+    const int b4 = beg >> 2, e4 = end >> 2;
+    int i = b4 + threadIdx.x;
+    for (; i + 3 * kThreads < e4; i += 4 * kThreads) {
+      float4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = ld_stream(p4 + i + u * kThreads);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) stat_update4(v[u], 4 * (i + u * kThreads), it, greedy, m, s, idx);
+    }
+    for (; i < e4; i += kThreads) stat_update4(p4[i], 4 * i, it, greedy, m, s, idx);
+  } else {
+    for (int i = beg + threadIdx.x; i < end; i += kThreads) stat_update1(z[i], i, it, greedy, m, s, idx);
+  }
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void stats_kernel(const VRow* __restrict__ rows, int V, int chunk,
+                                                         VStat* __restrict__ stats, int n_chunks) {
   const int r = blockIdx.y, c = blockIdx.x;
   const VRow row = rows[r];
   const float it = row.inv_t;
@@ -95,25 +154,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(const VRow* __restrict_
   const int end = min(V, beg + chunk);
   float m = -INFINITY, s = 0.f;
   int idx = INT_MAX;
-  if (VEC) {
-    const float4* p4 = reinterpret_cast<const float4*>(row.ptr + beg);
-    const int n4 = (end - beg) >> 2;
-    int i = threadIdx.x;
-    for (; i + 3 * kThreads < n4; i += 4 * kThreads) {
-      float4 v0 = ld_stream(p4 + i);
-      float4 v1 = ld_stream(p4 + i + kThreads);
-      float4 v2 = ld_stream(p4 + i + 2 * kThreads);
-      float4 v3 = ld_stream(p4 + i + 3 * kThreads);
-      stat_update4(v0, beg + 4 * i, it, greedy, m, s, idx);
-      stat_update4(v1, beg + 4 * (i + kThreads), it, greedy, m, s, idx);
-      stat_update4(v2, beg + 4 * (i + 2 * kThreads), it, greedy, m, s, idx);
-      stat_update4(v3, beg + 4 * (i + 3 * kThreads), it, greedy, m, s, idx);
-    }
-    for (; i < n4; i += kThreads) stat_update4(p4[i], beg + 4 * i, it, greedy, m, s, idx);
-  } else {
-    for (int i = beg + threadIdx.x; i < end; i += kThreads)
-      stat_update1(row.ptr[i], i, it, greedy, m, s, idx);
-  }
+  stats_chunk<VEC>(row.ptr, beg, end, it, greedy, m, s, idx);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float m2 = __shfl_xor(m, o, kWave);
@@ -136,157 +177,139 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(const VRow* __restrict_
   }
 }
 
-__device__ __forceinline__ void pick_update(float sc, int i, float& best, int& bi) {
-  if (sc > best || (sc == best && i < bi)) {
-    best = sc;
-    bi = i;
-  }
-}
+// One workgroup per sequence.  Thread t takes row t % 32 of the sequence
+// (target rows 0..k, then draft rows 0..k-1) and the chunks c = t / 32 + 8 i,
+// all its records loaded before the first is used; threads 224 + j gather
+// p and q at draft j's token meanwhile.  Partials merge through LDS in group
+// order, then one lane per draft runs the acceptance test.
+constexpr int kDecGroups = kThreads / 32;
 
-// Merge all chunk statistics of one row.  Chunk records are read in batches
-// of kStatBatch (indexes clamped, so that every load of a batch is in flight
-// before the first is used) and still taken in chunk order.
-constexpr int kStatBatch = 8;
-
-__device__ __forceinline__ void row_stats(const VStat* st, int n_chunks, float it, bool greedy,
-                                          float& M, float& S, int& idx) {
-  M = -INFINITY;
-  idx = INT_MAX;
-  for (int c0 = 0; c0 < n_chunks; c0 += kStatBatch) {
-    VStat v[kStatBatch];
-#pragma unroll
-    for (int b = 0; b < kStatBatch; ++b) v[b] = st[min(c0 + b, n_chunks - 1)];
-#pragma unroll
-    for (int b = 0; b < kStatBatch; ++b)
-      if (c0 + b < n_chunks && v[b].m > M) {  // chunks in index order: the first chunk holding the max wins ties
-        M = v[b].m;
-        idx = v[b].idx;
-      }
-  }
-  S = 0.f;
-  if (!greedy)
-    for (int c0 = 0; c0 < n_chunks; c0 += kStatBatch) {
-      VStat v[kStatBatch];
-#pragma unroll
-      for (int b = 0; b < kStatBatch; ++b) v[b] = st[min(c0 + b, n_chunks - 1)];
-#pragma unroll
-      for (int b = 0; b < kStatBatch; ++b)
-        if (c0 + b < n_chunks) S += scaled(v[b].s, v[b].m, M, it);
-    }
-}
-
-// Best pick (and fallback pick) over a row's chunk records, in chunk order.
-__device__ __forceinline__ void merge_picks(const VPick* pk, int n_chunks, float& best, int& bi, float& fb,
-                                            int& fi) {
-  for (int c0 = 0; c0 < n_chunks; c0 += kStatBatch) {
-    VPick v[kStatBatch];
-#pragma unroll
-    for (int b = 0; b < kStatBatch; ++b) v[b] = pk[min(c0 + b, n_chunks - 1)];
-#pragma unroll
-    for (int b = 0; b < kStatBatch; ++b)
-      if (c0 + b < n_chunks) {
-        pick_update(v[b].score, v[b].idx, best, bi);
-        pick_update(v[b].fb_score, v[b].fb_idx, fb, fi);
-      }
-  }
-}
-
-__device__ __forceinline__ uint32_t word_of(uint4 w, int e) {
-  return e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
-}
-
-template <bool VEC>
 __global__ __launch_bounds__(kThreads) void decide_kernel(
-    const VRow* __restrict__ rows, const VSeq* __restrict__ seqs,
-    const int32_t* __restrict__ draft_tok, const VStat* __restrict__ stats, int n_chunks1, int V,
-    int chunk2, int n_chunks2, uint64_t seed, const uint64_t* __restrict__ seed_ptr,
-    VPick* __restrict__ picks, VDec* __restrict__ decs) {
-  const int b = blockIdx.y, c = blockIdx.x;
+    const VRow* __restrict__ rows, const VSeq* __restrict__ seqs, const int32_t* __restrict__ draft_tok,
+    const VStat* __restrict__ stats, int n_chunks, int V, uint64_t seed, const uint64_t* __restrict__ seed_ptr,
+    VDec* __restrict__ decs, int kmax, int32_t* __restrict__ n_acc, int32_t* __restrict__ out_tok) {
+  const int b = blockIdx.x;
   const VSeq sq = seqs[b];
   const bool greedy = !(sq.t > 0.f);
-  const float it = greedy ? 0.f : 1.f / sq.t;
-  const uint64_t seq_id = (static_cast<uint64_t>(sq.seq_hi) << 32) | sq.seq_lo;
-  const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
-
-  __shared__ int s_a, s_tok;
-  __shared__ float s_mp, s_sp, s_mq, s_sq;
-  if (threadIdx.x < kWave) {
-    const int j = threadIdx.x;  // 0-based draft index; lane k handles the bonus row
-    bool acc = true;
-    float Mp = 0.f, Sp = 1.f, Mq = 0.f, Sq = 1.f;
-    int ap = 0, aq = 0;
-    if (j <= sq.k) {
-      row_stats(stats + static_cast<size_t>(sq.p_row + j) * n_chunks1, n_chunks1, it, greedy, Mp,
-                Sp, ap);
-    }
-    if (j < sq.k) {
-      const int x = draft_tok[sq.tok_row + j];
-      if (static_cast<unsigned>(x) >= static_cast<unsigned>(V)) {
-        acc = false;  // a draft id outside the vocabulary is never accepted
-      } else if (greedy) {
-        acc = (x == ap);
-      } else {
-        row_stats(stats + static_cast<size_t>(sq.q_row + j) * n_chunks1, n_chunks1, it, false, Mq,
-                  Sq, aq);
-        const float zp = rows[sq.p_row + j].ptr[x];
-        const float zq = rows[sq.q_row + j].ptr[x];
-        const float px = __expf((zp - Mp) * it) / Sp;
-        const float qx = __expf((zq - Mq) * it) / Sq;
-        const uint4 w = philox_block(key, stream_id(seq_id, sq.base_pos + j + 1, 1 /*ACCEPT*/), 0);
-        acc = (u01(w.x) * qx < px);
+  const float it = rows[sq.p_row].inv_t;
+  const int t = threadIdx.x;
+  const int nr = 2 * sq.k + 1;
+  __shared__ float pm[kDecGroups][32], ps[kDecGroups][32];
+  __shared__ int pi[kDecGroups][32];
+  __shared__ float rM[32], rS[32], gzp[16], gzq[16];
+  __shared__ int rI[32], gx[16];
+  {
+    const int r = t & 31, g = t >> 5;
+    float m = -INFINITY, s = 0.f;
+    int idx = INT_MAX;
+    if (r < nr) {
+      const int row = r <= sq.k ? sq.p_row + r : sq.q_row + (r - sq.k - 1);
+      const VStat* st = stats + static_cast<size_t>(row) * n_chunks;
+      VStat v[kMaxChunks / kDecGroups];
+#pragma unroll
+      for (int i = 0; i < kMaxChunks / kDecGroups; ++i) {
+        const int c = g + kDecGroups * i;
+        if (c < n_chunks) v[i] = st[c];
+      }
+#pragma unroll
+      for (int i = 0; i < kMaxChunks / kDecGroups; ++i) {
+        const int c = g + kDecGroups * i;
+        if (c < n_chunks) stat_merge(m, s, idx, v[i].m, v[i].s, v[i].idx, it, greedy);
       }
     }
-    const uint64_t rej = ~__ballot(acc);
-    const int a = (rej == 0) ? sq.k : min(sq.k, static_cast<int>(__ffsll(static_cast<long long>(rej))) - 1);
-    if (j == a) {
-      s_a = a;
-      s_tok = ap;
-      s_mp = Mp;
-      s_sp = Sp;
-      s_mq = Mq;
-      s_sq = Sq;
+    pm[g][r] = m;
+    ps[g][r] = s;
+    pi[g][r] = idx;
+    // draft tokens and the gathered logits at them
+    const int j = t - (kThreads - 32);
+    if (j >= 0 && j < sq.k) {
+      const int x = draft_tok[sq.tok_row + j];
+      gx[j] = x;
+      if (!greedy && static_cast<unsigned>(x) < static_cast<unsigned>(V)) {
+        gzp[j] = rows[sq.p_row + j].ptr[x];
+        gzq[j] = rows[sq.q_row + j].ptr[x];
+      }
     }
   }
   __syncthreads();
-  const int a = s_a;
-  const int mode = greedy ? kGreedy : (a < sq.k ? kResample : kBonus);
-  if (c == 0 && threadIdx.x == 0) decs[b] = VDec{a, mode, s_tok, 0};
-  if (mode == kGreedy) return;
-
-  const float Mp = s_mp, Sp = s_sp, Mq = s_mq, Sq = s_sq;
-  const float* zp = rows[sq.p_row + a].ptr;
-  const float* zq = (mode == kResample) ? rows[sq.q_row + a].ptr : nullptr;
-  const StreamId sid = stream_id(seq_id, sq.base_pos + a + 1, mode == kResample ? 2 : 3);
-  const float rp = 1.f / Sp, rq = 1.f / Sq;
-
-  float best = -INFINITY, fb = -INFINITY;
-  int bi = INT_MAX, fi = INT_MAX;
-  const int beg = c * chunk2;
-  const int end = min(V, beg + chunk2);
-  auto score = [&](float p_logit, float q_logit, uint32_t word, int i) {
-    const float g = gumbel_of(word);
-    const float lp = (p_logit - Mp) * it;  // log p_i + log S_p
-    if (mode == kResample) {
-      const float r = __expf(lp) * rp - __expf((q_logit - Mq) * it) * rq;
-      const float sc = (r > 0.f) ? logf(r) + g : -INFINITY;
-      pick_update(sc, i, best, bi);
-      pick_update(lp + g, i, fb, fi);
+  if (t < 32) {
+    float m = pm[0][t], s = ps[0][t];
+    int idx = pi[0][t];
+    for (int g = 1; g < kDecGroups; ++g) stat_merge(m, s, idx, pm[g][t], ps[g][t], pi[g][t], it, greedy);
+    rM[t] = m;
+    rS[t] = s;
+    rI[t] = idx;
+  }
+  __syncthreads();
+  if (t >= kWave) return;
+  const int j = t;  // 0-based draft index
+  bool acc = true;
+  if (j < sq.k) {
+    const int x = gx[j];
+    if (static_cast<unsigned>(x) >= static_cast<unsigned>(V)) {
+      acc = false;  // a draft id outside the vocabulary is never accepted
+    } else if (greedy) {
+      acc = (x == rI[j]);
     } else {
-      pick_update(lp + g, i, best, bi);
+      const float px = __expf((gzp[j] - rM[j]) * it) / rS[j];
+      const float qx = __expf((gzq[j] - rM[sq.k + 1 + j]) * it) / rS[sq.k + 1 + j];
+      const uint64_t seq_id = (static_cast<uint64_t>(sq.seq_hi) << 32) | sq.seq_lo;
+      const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
+      const uint4 w = philox_block(key, stream_id(seq_id, sq.base_pos + j + 1, 1 /*ACCEPT*/), 0);
+      acc = (u01(w.x) * qx < px);
     }
+  }
+  const uint64_t rej = ~__ballot(acc);
+  const int a = (rej == 0) ? sq.k : min(sq.k, static_cast<int>(__ffsll(static_cast<long long>(rej))) - 1);
+  const int mode = greedy ? kGreedy : (a < sq.k ? kResample : kBonus);
+  if (j == 0) {
+    VDec d{};
+    d.a = a;
+    d.mode = mode;
+    if (mode != kGreedy) {
+      d.Mp = rM[a];
+      d.Sp = rS[a];
+      if (mode == kResample) {
+        d.Mq = rM[sq.k + 1 + a];
+        d.Sq = rS[sq.k + 1 + a];
+      }
+    }
+    decs[b] = d;
+  }
+  if (mode != kGreedy) return;  // the outputs come from the draw
+  if (j == 0) n_acc[b] = a;
+  if (j <= kmax) out_tok[static_cast<size_t>(b) * (kmax + 1) + j] = j < a ? gx[j] : (j == a ? rI[a] : -1);
+}
+
+// The draw of a sampled sequence over one chunk of the row(s) it reads, by
+// exponential race with E_i = -log2 u_i: for a rejection r_i = p_i - q_i,
+// score r_i / E_i where r_i > 0, and the fallback p_i / E_i (a draw from p,
+// used only if no r_i is positive); for the bonus p_i / E_i on row k.
+template <bool VEC, bool RESID>
+__device__ __forceinline__ void draw_chunk(const float* __restrict__ zp, const float* __restrict__ zq, int beg,
+                                           int end, float cs, float dp, float dq, float rsp, float rsq,
+                                           PhiloxKey key, StreamId sid, float& best, int& bi, float& fb, int& fi) {
+  auto score = [&](float zpi, float zqi, uint32_t word, int i) {
+    const float p = __builtin_amdgcn_exp2f(fmaf(zpi, cs, -dp)) * rsp;
+    const float ie = __builtin_amdgcn_rcpf(exp2_variate(word));
+    if (RESID) {
+      const float r = p - __builtin_amdgcn_exp2f(fmaf(zqi, cs, -dq)) * rsq;
+      pick_update(r > 0.f ? r * ie : -1.f, i, best, bi);
+    }
+    pick_update(p * ie, i, fb, fi);
   };
   if (VEC) {
-    // batches of 4 float4 per thread (clamped loads, all in flight before the
-    // first is used), then the same per-element order as one at a time
+    // batches of 4 float4 of each row per thread (clamped loads, all in
+    // flight before the first is used), then the per-element order
     const int e4 = end >> 2;
     for (int i0 = (beg >> 2) + threadIdx.x; i0 < e4; i0 += 4 * kThreads) {
       float4 pv[4], qv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int j = min(i0 + u * kThreads, e4 - 1);
-        pv[u] = reinterpret_cast<const float4*>(zp)[j];
-        qv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (mode == kResample) qv[u] = reinterpret_cast<const float4*>(zq)[j];  // zq is null otherwise
+        const int jj = min(i0 + u * kThreads, e4 - 1);
+        pv[u] = reinterpret_cast<const float4*>(zp)[jj];
+        if (RESID) qv[u] = reinterpret_cast<const float4*>(zq)[jj];
+        else qv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -302,18 +325,40 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(
   } else {
     for (int i = beg + threadIdx.x; i < end; i += kThreads) {
       const uint4 w = philox_block(key, sid, static_cast<uint32_t>(i >> 2));
-      score(zp[i], zq ? zq[i] : 0.f, word_of(w, i & 3), i);
+      score(zp[i], RESID ? zq[i] : 0.f, word_of(w, i & 3), i);
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float b2 = __shfl_xor(best, o, kWave);
-    const int i2 = __shfl_xor(bi, o, kWave);
-    pick_update(b2, i2, best, bi);
-    const float f2 = __shfl_xor(fb, o, kWave);
-    const int j2 = __shfl_xor(fi, o, kWave);
-    pick_update(f2, j2, fb, fi);
-  }
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void draw_kernel(const VRow* __restrict__ rows, const VSeq* __restrict__ seqs,
+                                                        const VDec* __restrict__ decs, int V, int chunk,
+                                                        int n_chunks, uint64_t seed,
+                                                        const uint64_t* __restrict__ seed_ptr,
+                                                        VPick* __restrict__ picks) {
+  const int b = blockIdx.y, c = blockIdx.x;
+  const VDec d = decs[b];
+  if (d.mode == kGreedy) return;
+  const VSeq sq = seqs[b];
+  const bool resid = d.mode == kResample;
+  const VRow rp = rows[sq.p_row + d.a];
+  const float cs = rp.inv_t * kLog2e;  // p_i S_p = 2^(z_i cs - M cs)
+  const uint64_t seq_id = (static_cast<uint64_t>(sq.seq_hi) << 32) | sq.seq_lo;
+  const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
+  // RESAMPLE noise at the rejected position n + a + 1, BONUS at n + k + 1
+  const StreamId sid = stream_id(seq_id, sq.base_pos + d.a + 1, resid ? 2 : 3);
+  float best = -1.f, fb = -1.f;
+  int bi = INT_MAX, fi = INT_MAX;
+  const int beg = c * chunk;
+  const int end = min(V, beg + chunk);
+  if (resid)
+    draw_chunk<VEC, true>(rp.ptr, rows[sq.q_row + d.a].ptr, beg, end, cs, d.Mp * cs, d.Mq * cs, 1.f / d.Sp,
+                          1.f / d.Sq, key, sid, best, bi, fb, fi);
+  else
+    draw_chunk<VEC, false>(rp.ptr, nullptr, beg, end, cs, d.Mp * cs, 0.f, 1.f / d.Sp, 0.f, key, sid, best, bi,
+                           fb, fi);
+  wave_pick(best, bi);
+  wave_pick(fb, fi);
   __shared__ VPick sp[kThreads / kWave];
   const int wv = threadIdx.x / kWave;
   if ((threadIdx.x & (kWave - 1)) == 0) sp[wv] = VPick{best, bi, fb, fi};
@@ -323,29 +368,39 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(
       pick_update(sp[k].score, sp[k].idx, best, bi);
       pick_update(sp[k].fb_score, sp[k].fb_idx, fb, fi);
     }
-    picks[static_cast<size_t>(b) * n_chunks2 + c] = VPick{best, bi, fb, fi};
+    picks[static_cast<size_t>(b) * n_chunks + c] = VPick{best, bi, fb, fi};
   }
 }
 
-__global__ void final_kernel(const VSeq* __restrict__ seqs, const int32_t* __restrict__ draft_tok,
-                             const VDec* __restrict__ decs, const VPick* __restrict__ picks,
-                             int n_chunks2, int B, int kmax, int32_t* __restrict__ n_acc,
-                             int32_t* __restrict__ out_tok) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  const VSeq sq = seqs[b];
+// One wave per sampled sequence: lane c holds chunk c's winners (at most 64
+// chunks), merged by shuffles.
+__global__ __launch_bounds__(kWave) void final_kernel(const VSeq* __restrict__ seqs,
+                                                      const int32_t* __restrict__ draft_tok,
+                                                      const VDec* __restrict__ decs,
+                                                      const VPick* __restrict__ picks, int n_chunks, int kmax,
+                                                      int32_t* __restrict__ n_acc, int32_t* __restrict__ out_tok) {
+  const int b = blockIdx.x;
   const VDec d = decs[b];
-  int t = d.token;
-  if (d.mode != kGreedy) {
-    float best = -INFINITY, fb = -INFINITY;
-    int bi = INT_MAX, fi = INT_MAX;
-    merge_picks(picks + static_cast<size_t>(b) * n_chunks2, n_chunks2, best, bi, fb, fi);
-    // an empty residual (only possible when p == q) falls back to drawing from p
-    t = (best == -INFINITY) ? fi : bi;
+  if (d.mode == kGreedy) return;
+  const int l = threadIdx.x;
+  const VSeq sq = seqs[b];
+  float best = -1.f, fb = -1.f;
+  int bi = INT_MAX, fi = INT_MAX;
+  if (l < n_chunks) {
+    const VPick p = picks[static_cast<size_t>(b) * n_chunks + l];
+    best = p.score;
+    bi = p.idx;
+    fb = p.fb_score;
+    fi = p.fb_idx;
   }
-  n_acc[b] = d.a;
-  int32_t* o = out_tok + static_cast<size_t>(b) * (kmax + 1);
-  for (int j = 0; j <= kmax; ++j) o[j] = (j < d.a) ? draft_tok[sq.tok_row + j] : (j == d.a ? t : -1);
+  const int x = l < d.a ? draft_tok[sq.tok_row + l] : -1;
+  wave_pick(best, bi);
+  wave_pick(fb, fi);
+  // residual scores are positive; with none (only possible when p and q agree
+  // in fp32) the draw falls back to p; the bonus draws from p
+  const int t = (d.mode == kResample && best > 0.f) ? bi : fi;
+  if (l == 0) n_acc[b] = d.a;
+  if (l <= kmax) out_tok[static_cast<size_t>(b) * (kmax + 1) + l] = l < d.a ? x : (l == d.a ? t : -1);
 }
 
 // ---------------------------------------------------------------------------
@@ -368,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
   float best = -INFINITY;
   int bi = INT_MAX;
   if (VEC) {
-    // batches of 4 float4 per thread, as in decide_kernel
+    // batches of 4 float4 per thread, as in draw_chunk
     const int e4 = end >> 2;
     for (int i0 = (beg >> 2) + threadIdx.x; i0 < e4; i0 += 4 * kThreads) {
       float4 vv[4];
@@ -386,10 +441,10 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
           pick_update(v.w, 4 * i4 + 3, best, bi);
         } else {
           const uint4 w = philox_block(key, sid, static_cast<uint32_t>(i4));
-          pick_update(v.x * it + gumbel_of(w.x), 4 * i4, best, bi);
-          pick_update(v.y * it + gumbel_of(w.y), 4 * i4 + 1, best, bi);
-          pick_update(v.z * it + gumbel_of(w.z), 4 * i4 + 2, best, bi);
-          pick_update(v.w * it + gumbel_of(w.w), 4 * i4 + 3, best, bi);
+          pick_update(fmaf(v.x, it, gumbel_shift(w.x)), 4 * i4, best, bi);
+          pick_update(fmaf(v.y, it, gumbel_shift(w.y)), 4 * i4 + 1, best, bi);
+          pick_update(fmaf(v.z, it, gumbel_shift(w.z)), 4 * i4 + 2, best, bi);
+          pick_update(fmaf(v.w, it, gumbel_shift(w.w)), 4 * i4 + 3, best, bi);
         }
       }
     }
@@ -399,16 +454,11 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
         pick_update(z[i], i, best, bi);
       } else {
         const uint4 w = philox_block(key, sid, static_cast<uint32_t>(i >> 2));
-        pick_update(z[i] * it + gumbel_of(word_of(w, i & 3)), i, best, bi);
+        pick_update(fmaf(z[i], it, gumbel_shift(word_of(w, i & 3))), i, best, bi);
       }
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float b2 = __shfl_xor(best, o, kWave);
-    const int i2 = __shfl_xor(bi, o, kWave);
-    pick_update(b2, i2, best, bi);
-  }
+  wave_pick(best, bi);
   __shared__ float sb[kThreads / kWave];
   __shared__ int sbi[kThreads / kWave];
   const int wv = threadIdx.x / kWave;
@@ -423,10 +473,9 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(int V, const DRow* __re
   }
 }
 
-// One workgroup per row: row maximum, then the guide token's logit becomes
-// maximum + boost (all reads of the row finish before the write).
 // One workgroup of 1024 threads per guided row: the row maximum with 16-byte
-// streaming loads, four in flight per thread, then z[guide] = max + boost.
+// streaming loads, four in flight per thread, then z[guide] = max + boost
+// (all reads of the row finish before the write).
 constexpr int kGuideThreads = 1024;
 
 __global__ __launch_bounds__(kGuideThreads) void draft_guide_kernel(int V, const DRow* __restrict__ rows,
@@ -464,14 +513,20 @@ __global__ __launch_bounds__(kGuideThreads) void draft_guide_kernel(int V, const
   }
 }
 
-__global__ void draft_final_kernel(const DRow* __restrict__ rows, const VPick* __restrict__ picks,
-                                   int n_chunks, int n, int32_t* __restrict__ tokens) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= n) return;
-  float best = -INFINITY, fb = -INFINITY;
-  int bi = INT_MAX, fi = INT_MAX;
-  merge_picks(picks + static_cast<size_t>(r) * n_chunks, n_chunks, best, bi, fb, fi);
-  tokens[rows[r].out] = bi;
+// One wave per row: lane c holds chunk c's winner, merged by shuffles.
+__global__ __launch_bounds__(kWave) void draft_final_kernel(const DRow* __restrict__ rows,
+                                                            const VPick* __restrict__ picks, int n_chunks,
+                                                            int32_t* __restrict__ tokens) {
+  const int r = blockIdx.x, l = threadIdx.x;
+  float best = -INFINITY;
+  int bi = INT_MAX;
+  if (l < n_chunks) {
+    const VPick p = picks[static_cast<size_t>(r) * n_chunks + l];
+    best = p.score;
+    bi = p.idx;
+  }
+  wave_pick(best, bi);
+  if (l == 0) tokens[rows[r].out] = bi;
 }
 
 __global__ void philox_uniform_kernel(uint64_t seed, StreamId sid, int n, float* out) {
@@ -486,7 +541,10 @@ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255);
 void chunking(int units, int V, int& chunk, int& n_chunks) {
   int want = std::max(1, (kTargetBlocks + units - 1) / std::max(1, units));
   want = std::min(want, std::max(1, V / 4096));
-  chunk = (V + want - 1) / want;
+  // at most kMaxChunks chunks (the decision and merge kernels hold one per
+  // lane), each a multiple of 1024 elements (the vector paths need chunk
+  // starts on 16-byte boundaries)
+  chunk = std::max((V + want - 1) / want, (V + kMaxChunks - 1) / kMaxChunks);
   chunk = (chunk + 1023) / 1024 * 1024;
   n_chunks = (V + chunk - 1) / chunk;
 }
@@ -512,32 +570,43 @@ size_t vocab_ws_bytes(const VocabPlan& p) {
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax, int32_t* d_n_acc,
                              int32_t* d_out_tok, void* d_ws, hipStream_t st, KernelTimer* timer,
-                             const uint64_t* d_seed) {
+                             const uint64_t* d_seed, bool aligned) {
   if (p.B == 0) return hipSuccess;
+  if (p.n_chunks1 > kMaxChunks || p.n_chunks2 > kMaxChunks) return hipErrorInvalidValue;
   char* ws = static_cast<char*>(d_ws);
   VStat* stats = reinterpret_cast<VStat*>(ws);
   ws += align256(sizeof(VStat) * static_cast<size_t>(p.n_rows) * p.n_chunks1);
   VPick* picks = reinterpret_cast<VPick*>(ws);
   ws += align256(sizeof(VPick) * static_cast<size_t>(p.B) * p.n_chunks2);
   VDec* decs = reinterpret_cast<VDec*>(ws);
-  const bool vec = (p.V % 4) == 0;
+  const bool vec = aligned && (p.V % 4) == 0;
+  // the timer names one kernel; bytes are each launch's algorithmic HBM bytes
+  auto timed = [&](const char* name) { return timer && timer->wants(name); };
+  const char* n1 = vec ? "stats_kernel<true>" : "stats_kernel<false>";
   dim3 g1(p.n_chunks1, p.n_rows);
-  const bool timed = timer && timer->wants(vec ? "stats_kernel<true>" : "stats_kernel<false>");
-  if (timed) timer->begin(st);
+  if (timed(n1)) timer->begin(st);
   if (vec)
     launch_kernel(stats_kernel<true>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1);
   else
     launch_kernel(stats_kernel<false>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1);
-  if (timed) timer->end(st, 4.0 * p.n_rows * p.V, 0.0);
-  dim3 g2(p.n_chunks2, p.B);
+  if (timed(n1)) timer->end(st, 4.0 * p.n_rows * p.V, 0.0);
+  if (timed("decide_kernel")) timer->begin(st);
+  launch_kernel(decide_kernel, dim3(p.B), dim3(kThreads), 0, st, d_rows, d_seqs, d_draft_tok, stats, p.n_chunks1,
+                p.V, seed, d_seed, decs, kmax, d_n_acc, d_out_tok);
+  if (timed("decide_kernel")) timer->end(st, 0.0, 0.0);
+  // the draw reads one (p, q) row pair per rejected sequence, one p row per bonus
+  const char* n3 = vec ? "draw_kernel<true>" : "draw_kernel<false>";
+  dim3 g3(p.n_chunks2, p.B);
+  if (timed(n3)) timer->begin(st);
   if (vec)
-    decide_kernel<true><<<g2, kThreads, 0, st>>>(d_rows, d_seqs, d_draft_tok, stats, p.n_chunks1,
-                                                 p.V, p.chunk2, p.n_chunks2, seed, d_seed, picks, decs);
+    launch_kernel(draw_kernel<true>, g3, dim3(kThreads), 0, st, d_rows, d_seqs, decs, p.V, p.chunk2,
+                  p.n_chunks2, seed, d_seed, picks);
   else
-    decide_kernel<false><<<g2, kThreads, 0, st>>>(d_rows, d_seqs, d_draft_tok, stats, p.n_chunks1,
-                                                  p.V, p.chunk2, p.n_chunks2, seed, d_seed, picks, decs);
-  final_kernel<<<(p.B + 63) / 64, 64, 0, st>>>(d_seqs, d_draft_tok, decs, picks, p.n_chunks2, p.B,
-                                               kmax, d_n_acc, d_out_tok);
+    launch_kernel(draw_kernel<false>, g3, dim3(kThreads), 0, st, d_rows, d_seqs, decs, p.V, p.chunk2,
+                  p.n_chunks2, seed, d_seed, picks);
+  if (timed(n3)) timer->end(st, 0.0, 0.0);
+  launch_kernel(final_kernel, dim3(p.B), dim3(kWave), 0, st, d_seqs, d_draft_tok, decs, picks, p.n_chunks2, kmax,
+                d_n_acc, d_out_tok);
   return hipGetLastError();
 }
 
@@ -556,13 +625,14 @@ size_t draft_ws_bytes(const DraftPlan& p) {
 hipError_t launch_draft_sample(const DraftPlan& p, const DRow* d_rows, uint64_t seed,
                                int32_t* d_tokens, void* d_ws, hipStream_t st, const uint64_t* d_seed) {
   if (p.n == 0) return hipSuccess;
+  if (p.n_chunks > kMaxChunks) return hipErrorInvalidValue;
   VPick* picks = static_cast<VPick*>(d_ws);
   dim3 g(p.n_chunks, p.n);
   if (p.V % 4 == 0)
     draft_kernel<true><<<g, kThreads, 0, st>>>(p.V, d_rows, p.chunk, p.n_chunks, seed, d_seed, picks);
   else
     draft_kernel<false><<<g, kThreads, 0, st>>>(p.V, d_rows, p.chunk, p.n_chunks, seed, d_seed, picks);
-  draft_final_kernel<<<(p.n + 63) / 64, 64, 0, st>>>(d_rows, picks, p.n_chunks, p.n, d_tokens);
+  draft_final_kernel<<<p.n, kWave, 0, st>>>(d_rows, picks, p.n_chunks, d_tokens);
   return hipGetLastError();
 }
 

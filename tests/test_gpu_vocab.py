@@ -166,3 +166,34 @@ def test_draft_sampler(V, T):
         assert int(got[i]) == t
         agree += 1
     assert agree >= n - 1
+
+
+@pytest.mark.parametrize("T", [0.9, 0.0])
+def test_out_of_range_draft_is_rejected(T):
+    """A draft id outside the vocabulary is never accepted, and the draw at
+    that position is the ordinary one: from norm(max(0, p_j - q_j)) with the
+    RESAMPLE stream (argmax p_j when greedy), with the q row normalised as
+    usual.  Draft 0 has q = p (always accepted); draft 1 is out of range."""
+    from oracle import philox
+    dev = device()
+    b = B()
+    V, k, seed, sid, base = 1000, 3, 5, 123456789012, 700
+    g = np.random.default_rng(8)
+    p = (g.standard_normal((k + 1, V)) * 2).astype(np.float32)
+    q = (g.standard_normal((k, V)) * 2).astype(np.float32)
+    q[0] = p[0]
+    drafts = np.array([int(np.argmax(p[0])), V + 5, 3], dtype=np.int32)
+    n_acc = torch.full((1,), -7, dtype=torch.int32, device=dev)
+    out = torch.full((1, k + 1), -7, dtype=torch.int32, device=dev)
+    ws = torch.empty(b.spec_sample_workspace_bytes(1, 2 * k + 1, V), dtype=torch.uint8, device=dev)
+    b.spec_sample_verify([k], [T], [sid], [base], torch.from_numpy(p).to(dev), torch.from_numpy(q).to(dev),
+                         torch.from_numpy(drafts).to(dev), V, seed, n_acc, out, ws)
+    torch.cuda.synchronize()
+    assert int(n_acc.item()) == 1
+    if T == 0.0:
+        want = int(np.argmax(p[1]))
+    else:
+        pp, qq = rule.softmax_t(p[1], T), rule.softmax_t(q[1], T)
+        want, ex = rule.draw_residual(pp, qq, philox.gumbel(seed, sid, base + 2, philox.RESAMPLE, V), MARGINS)
+        assert not ex
+    assert out.cpu().numpy().tolist() == [[int(drafts[0]), want, -1, -1]]

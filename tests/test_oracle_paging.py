@@ -71,6 +71,31 @@ def test_session_lengths_pages_and_history():
     assert used + len(sess.pool_t.free) == 32
 
 
+def test_undo_verify_restores_cache_and_pages():
+    """A verify taken back leaves target lengths, page tables and the free
+    pool as before it; verifying a subset afterwards allocates as if the
+    other sequence had never been verified."""
+    sh = ModelShape("pg", 1, 16, 2, 2, 8, 16, 20, 1e4, dtype="f32", init_std=0.3)
+    dec = Decoder(sh, model_weights(sh, 52))
+    sess = Session(dec, dec, 32, 32, page_size=4)
+    sess.prefill([1, 2, 3], [[1, 2, 3, 4], [5, 6, 7, 8], [9, 10]])
+    for _ in range(3):
+        sess.draft_step([1, 2, 3], [0.7] * 3, seed=4)
+    before = {s: (sess.lengths(s), sess.pages(s)) for s in (1, 2, 3)}
+    free = sorted(sess.pool_t.free)
+    out1 = sess.verify([1, 2, 3], [0.7] * 3, seed=4)
+    assert sess.pages(2)[0] != before[2][1][0]
+    sess.undo_verify([1, 2, 3])
+    assert {s: (sess.lengths(s), sess.pages(s)) for s in (1, 2, 3)} == before
+    assert sorted(sess.pool_t.free) == free
+    # without sequence 1, sequence 2 takes the pages sequence 1 took before
+    taken1 = [p for p in sess.pages(1)[0]]
+    sess.release(1)
+    out2 = sess.verify([2, 3], [0.7] * 2, seed=4)
+    assert [r.tokens for r, _ in out2] == [r.tokens for r, _ in out1[1:]]
+    assert set(sess.pages(2)[0]) & set(taken1)
+
+
 def test_guided_draft_row_and_draw():
     """Draft guidance raises the guide token to max + boost in the kept q row;
     with a large boost the draw is the guide token, with guide -1 nothing changes."""
@@ -95,3 +120,25 @@ def test_guided_draft_row_and_draw():
     c = Session(Decoder(cfg.target, tw), Decoder(cfg.draft, dw), 64, 64)
     c.prefill([1], [prompt])
     assert c.draft_step([1], [1.0], 5, guide=[-1], boost=50.0) == x_b
+
+
+def test_draft_loop_takes_pages_first_in_list_order():
+    """A draft loop call takes every step's pages before any step runs, one
+    sequence after the other; per-step calls interleave them.  The drafts and
+    lengths are the same either way."""
+    sh = ModelShape("pg", 1, 16, 2, 2, 8, 16, 20, 1e4, dtype="f32", init_std=0.3)
+    dec = Decoder(sh, model_weights(sh, 53))
+    a = Session(dec, dec, 64, 64, page_size=4)
+    b = Session(dec, dec, 64, 64, page_size=4)
+    # draft caches of 6 and 4 positions: sequence 1 needs a new page at step 3
+    # (position 8), sequence 2 at step 1 (position 4)
+    prompts = [[1, 2, 3, 4, 5, 6, 7], [8, 9, 10, 11, 12]]
+    for s in (a, b):
+        s.prefill([1, 2], prompts)
+    a.draft_loop([1, 2], [0.7, 0.7], 3, [4, 4])
+    for _ in range(4):
+        b.draft_step([1, 2], [0.7, 0.7], seed=3)
+    assert a.seqs[1].drafts == b.seqs[1].drafts and a.seqs[2].drafts == b.seqs[2].drafts
+    assert a.lengths(1) == b.lengths(1) and a.lengths(2) == b.lengths(2)
+    assert a.pages(1)[1] == [0, 1, 3] and a.pages(2)[1] == [2, 4]
+    assert b.pages(1)[1] == [0, 1, 4] and b.pages(2)[1] == [2, 3]
