@@ -314,6 +314,30 @@ SPEC_API spec_status spec_sample_verify(int32_t B, const int32_t* k, const float
                                         int32_t* n_accepted, int32_t* out_tokens,
                                         void* workspace, size_t workspace_bytes, void* stream);
 
+/* The decision pass of spec_sample_verify for callers that cannot allocate
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): it calls no allocating routine and copies nothing from
+ * the host.  The per-sequence inputs are device arrays: k[B] (int32, each in
+ * 0..k_max), temperature[B] (fp32, >= 0), seq_ids[B] (int64), base_pos[B]
+ * (int32); the logits, drafts and outputs are as in spec_sample_verify, with
+ * out_tokens [B * (k_max + 1)].  Given k_max = max k[b], the outputs are bit
+ * for bit those of spec_sample_verify.  Tables and partial results live in a
+ * 512 KiB device array that the library holds on each GPU it runs on until
+ * the process ends: B <= 256 and k_max <= 15 (SPEC_E_INVALID otherwise); a
+ * shape whose tables exceed the array returns SPEC_E_UNSUPPORTED before
+ * anything is enqueued.  If any k[b] is outside 0..k_max or any temperature
+ * is negative or NaN, nothing is decided and every n_accepted[b] and token is
+ * -1 (the inputs are on the device, so this is reported there).  Every call
+ * on one GPU uses the same array: calls that overlap on one GPU (different
+ * streams, or threads) race, and must be serialised by the caller.
+ * Asynchronous on `stream`; spec_last_error(NULL) explains a failure. */
+SPEC_API spec_status spec_sample_verify_noalloc(int32_t B, int32_t k_max, const int32_t* k,
+                                                const float* temperature, const int64_t* seq_ids,
+                                                const int32_t* base_pos, const float* p_logits,
+                                                const float* q_logits, const int32_t* draft_tokens,
+                                                int32_t V, uint64_t seed, int32_t* n_accepted,
+                                                int32_t* out_tokens, void* stream);
+
 /* Draw one draft token per row: row i of `logits` (device fp32 [n, V]) is the
  * draft distribution for position pos[i] of sequence seq_ids[i] (host arrays);
  * tokens (device int32 [n]) <- Gumbel-max with DRAFT noise, argmax if T == 0. */

@@ -89,6 +89,8 @@ SIGNATURES = {
     "spec_sample_workspace_bytes": (c_size_t, [c_int32, c_int32, c_int32]),
     "spec_sample_verify": (c_int32, [c_int32, _I32P, _F32P, _I64P, _I32P, _P, _P, _P, c_int32,
                                      c_uint64, _P, _P, _P, c_size_t, _P]),
+    "spec_sample_verify_noalloc": (c_int32, [c_int32, c_int32, _P, _P, _P, _P, _P, _P, _P, c_int32, c_uint64,
+                                             _P, _P, _P]),
     "spec_sample_draft": (c_int32, [c_int32, _P, c_int32, _F32P, _I64P, _I32P, c_uint64, _P, _P,
                                     c_size_t, _P]),
     "spec_philox_uniform": (c_int32, [c_uint64, c_int64, c_int32, c_int32, c_int32, _P, _P]),
@@ -334,6 +336,14 @@ def spec_sample_verify(k, temperature, seq_ids, base_pos, p_logits, q_logits, dr
                                    _ptr(bp, _I32P), dptr(p_logits), dptr(q_logits), dptr(draft_tokens),
                                    V, seed, dptr(n_accepted), dptr(out_tokens), dptr(workspace),
                                    workspace.numel() * workspace.element_size(), stream_ptr(stream)))
+
+
+def spec_sample_verify_noalloc(k_max: int, k, temperature, seq_ids, base_pos, p_logits, q_logits, draft_tokens,
+                               V: int, seed: int, n_accepted, out_tokens, stream=None):
+    """k, temperature, seq_ids, base_pos: device tensors (int32, float32, int64, int32)."""
+    check(lib().spec_sample_verify_noalloc(k.numel(), k_max, dptr(k), dptr(temperature), dptr(seq_ids),
+                                           dptr(base_pos), dptr(p_logits), dptr(q_logits), dptr(draft_tokens),
+                                           V, seed, dptr(n_accepted), dptr(out_tokens), stream_ptr(stream)))
 
 
 def spec_sample_draft(logits, V: int, temperature, seq_ids, pos, seed: int, tokens, workspace, stream=None):

@@ -20,7 +20,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libspecverify.so")
-SOURCES = ["vocab.hip", "gemm.hip", "attention.hip", "elem.hip", "plan.cpp", "ctx.cpp", "ops.cpp"]
+SOURCES = ["vocab.hip", "gemm.hip", "attention.hip", "elem.hip", "noalloc.hip", "plan.cpp", "ctx.cpp", "ops.cpp"]
 ARCH = "gfx950"
 
 

@@ -183,6 +183,10 @@ struct spec_ctx {
 
 static thread_local std::string g_err;
 
+namespace spec {
+void set_global_error(const char* msg) { g_err = msg ? msg : ""; }
+}  // namespace spec
+
 #define FAIL(code, msg)          \
   do {                           \
     ctx->err = (msg);            \

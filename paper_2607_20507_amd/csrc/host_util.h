@@ -111,6 +111,10 @@ class EventTimer : public KernelTimer {
 // Timer of the context-free entry points (spec_timing_enable with no context).
 EventTimer& global_timer();
 
+// Message that spec_last_error(NULL) returns (the calling thread's last
+// context-free failure).
+void set_global_error(const char* msg);
+
 // A packed block of host arrays, each 256-byte aligned, uploaded in one copy.
 class MetaBlock {
  public:

@@ -108,7 +108,7 @@ spec_status spec_sample_verify(int32_t B, const int32_t* k, const float* tempera
   // the vector path reads 16-byte units from each row
   const bool aligned = (reinterpret_cast<uintptr_t>(p_logits) & 15) == 0 &&
                        (nq == 0 || (reinterpret_cast<uintptr_t>(q_logits) & 15) == 0);
-  e = launch_vocab_pass(vocab_plan(B, rows_n, V), reinterpret_cast<const VRow*>(ws + orow),
+  e = launch_vocab_pass(vocab_plan(B, rows_n, V, B * (2 * kmax + 1)), reinterpret_cast<const VRow*>(ws + orow),
                         reinterpret_cast<const VSeq*>(ws + oseq), draft_tokens, seed, kmax, n_accepted,
                         out_tokens, ws + ovoc, st, &global_timer(), nullptr, aligned);
   return hip_status(e);

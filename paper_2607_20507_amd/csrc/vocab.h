@@ -48,7 +48,10 @@ struct VocabPlan {
   int chunk2 = 0, n_chunks2 = 0;  // residual draw (n_chunks2 <= 64)
 };
 
-VocabPlan vocab_plan(int B, int n_rows, int V);
+// Chunking follows chunk_rows (default n_rows): the two context-free entry
+// points both chunk for B * (2 k_max + 1) rows, so that they compute the same
+// partial sums whatever rows a call actually has.
+VocabPlan vocab_plan(int B, int n_rows, int V, int chunk_rows = -1);
 size_t vocab_ws_bytes(const VocabPlan& p);
 
 // Full decision pass: statistics, one decision per sequence, the residual or
@@ -57,11 +60,24 @@ size_t vocab_ws_bytes(const VocabPlan& p);
 // the Philox seed there instead of `seed`, so that a captured graph of the pass
 // takes a new seed with each replay.  A sequence's rows must be 16-byte aligned
 // when V % 4 == 0 (the vector path); `aligned` = false forces the scalar path.
+// d_n_rows (optional, device): the rows that exist, when the tables were
+// built on the device (launch_vocab_setup); grid rows beyond it exit at once.
+// A sequence whose k is -1 is not decided: n_acc = -1 and tokens -1.
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax,
                              int32_t* d_n_acc, int32_t* d_out_tok, void* d_ws, hipStream_t st,
                              KernelTimer* timer = nullptr, const uint64_t* d_seed = nullptr,
-                             bool aligned = true);
+                             bool aligned = true, const int32_t* d_n_rows = nullptr);
+
+// Row and sequence tables of the decision pass built on the device from
+// device arrays (B <= 256, one workgroup): sequence b's target rows are p
+// rows sum_{c<b}(k_c + 1) .., its draft rows q rows sum_{c<b} k_c ...  If any
+// k[b] is outside 0..kmax or any temperature is negative or NaN, no row is
+// built and every sequence is marked undecided (k = -1).
+constexpr int kSetupMaxSeqs = 256;
+hipError_t launch_vocab_setup(int B, int kmax, const int32_t* d_k, const float* d_temp, const int64_t* d_ids,
+                              const int32_t* d_base, const float* d_p, const float* d_q, int V, VRow* d_rows,
+                              VSeq* d_seqs, int32_t* d_n_rows, hipStream_t st);
 
 struct DraftPlan {
   int n = 0, V = 0, chunk = 0, n_chunks = 0;

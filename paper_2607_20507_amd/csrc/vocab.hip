@@ -145,8 +145,10 @@ __device__ __forceinline__ void stats_chunk(const float* __restrict__ z, int beg
 
 template <bool VEC>
 __global__ __launch_bounds__(kThreads) void stats_kernel(const VRow* __restrict__ rows, int V, int chunk,
-                                                         VStat* __restrict__ stats, int n_chunks) {
+                                                         VStat* __restrict__ stats, int n_chunks,
+                                                         const int32_t* __restrict__ n_rows) {
   const int r = blockIdx.y, c = blockIdx.x;
+  if (n_rows && r >= *n_rows) return;
   const VRow row = rows[r];
   const float it = row.inv_t;
   const bool greedy = row.greedy != 0;
@@ -190,9 +192,17 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(
     VDec* __restrict__ decs, int kmax, int32_t* __restrict__ n_acc, int32_t* __restrict__ out_tok) {
   const int b = blockIdx.x;
   const VSeq sq = seqs[b];
+  const int t = threadIdx.x;
+  if (sq.k < 0) {  // not decided (invalid input): -1 everywhere
+    if (t == 0) {
+      n_acc[b] = -1;
+      decs[b] = VDec{-1, kGreedy, 0.f, 0.f, 0.f, 0.f, {0, 0}};
+    }
+    if (t <= kmax) out_tok[static_cast<size_t>(b) * (kmax + 1) + t] = -1;
+    return;
+  }
   const bool greedy = !(sq.t > 0.f);
   const float it = rows[sq.p_row].inv_t;
-  const int t = threadIdx.x;
   const int nr = 2 * sq.k + 1;
   __shared__ float pm[kDecGroups][32], ps[kDecGroups][32];
   __shared__ int pi[kDecGroups][32];
@@ -403,6 +413,63 @@ __global__ __launch_bounds__(kWave) void final_kernel(const VSeq* __restrict__ s
   if (l <= kmax) out_tok[static_cast<size_t>(b) * (kmax + 1) + l] = l < d.a ? x : (l == d.a ? t : -1);
 }
 
+// Tables of the decision pass from device arrays: thread b takes sequence b;
+// row offsets are exclusive prefix sums of k + 1 (target rows) and k (draft
+// rows), scanned in LDS.
+__global__ __launch_bounds__(kSetupMaxSeqs) void setup_kernel(int B, int kmax, const int32_t* __restrict__ k,
+                                                             const float* __restrict__ temp,
+                                                             const int64_t* __restrict__ ids,
+                                                             const int32_t* __restrict__ base,
+                                                             const float* __restrict__ p,
+                                                             const float* __restrict__ q, int V,
+                                                             VRow* __restrict__ rows, VSeq* __restrict__ seqs,
+                                                             int32_t* __restrict__ n_rows) {
+  __shared__ int sp[kSetupMaxSeqs], sq[kSetupMaxSeqs];
+  __shared__ int any_bad;
+  const int b = threadIdx.x;
+  if (b == 0) any_bad = 0;
+  int kb = 0;
+  float tb = 0.f;
+  if (b < B) {
+    kb = k[b];
+    tb = temp[b];
+  }
+  __syncthreads();
+  if (b < B && (kb < 0 || kb > kmax || !(tb >= 0.f))) atomicOr(&any_bad, 1);
+  sp[b] = b < B ? kb + 1 : 0;
+  sq[b] = b < B ? kb : 0;
+  __syncthreads();
+  const bool bad = any_bad != 0;
+  // inclusive Hillis-Steele scans
+  for (int o = 1; o < kSetupMaxSeqs; o <<= 1) {
+    const int ap = b >= o ? sp[b - o] : 0, aq = b >= o ? sq[b - o] : 0;
+    __syncthreads();
+    sp[b] += ap;
+    sq[b] += aq;
+    __syncthreads();
+  }
+  const int NP = sp[kSetupMaxSeqs - 1];
+  const int p_off = sp[b] - (b < B ? kb + 1 : 0), q_off = sq[b] - (b < B ? kb : 0);
+  if (b == 0) *n_rows = bad ? 0 : NP + sq[kSetupMaxSeqs - 1];
+  if (b >= B) return;
+  VSeq s{};
+  s.k = bad ? -1 : kb;
+  s.p_row = p_off;
+  s.q_row = NP + q_off;
+  s.tok_row = q_off;
+  s.base_pos = base[b];
+  s.t = tb;
+  const uint64_t id = static_cast<uint64_t>(ids[b]);
+  s.seq_lo = static_cast<uint32_t>(id);
+  s.seq_hi = static_cast<uint32_t>(id >> 32);
+  seqs[b] = s;
+  if (bad) return;
+  const float it = tb > 0.f ? 1.f / tb : 0.f;
+  const int32_t greedy = tb > 0.f ? 0 : 1;
+  for (int j = 0; j <= kb; ++j) rows[p_off + j] = VRow{p + static_cast<size_t>(p_off + j) * V, it, greedy};
+  for (int j = 0; j < kb; ++j) rows[NP + q_off + j] = VRow{q + static_cast<size_t>(q_off + j) * V, it, greedy};
+}
+
 // ---------------------------------------------------------------------------
 // Draft sampler: Gumbel-max over z / T with DRAFT noise (argmax for T = 0).
 
@@ -551,12 +618,12 @@ void chunking(int units, int V, int& chunk, int& n_chunks) {
 
 }  // namespace
 
-VocabPlan vocab_plan(int B, int n_rows, int V) {
+VocabPlan vocab_plan(int B, int n_rows, int V, int chunk_rows) {
   VocabPlan p;
   p.B = B;
   p.n_rows = n_rows;
   p.V = V;
-  chunking(n_rows, V, p.chunk1, p.n_chunks1);
+  chunking(chunk_rows >= 0 ? chunk_rows : n_rows, V, p.chunk1, p.n_chunks1);
   chunking(B, V, p.chunk2, p.n_chunks2);
   return p;
 }
@@ -570,7 +637,7 @@ size_t vocab_ws_bytes(const VocabPlan& p) {
 hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq* d_seqs,
                              const int32_t* d_draft_tok, uint64_t seed, int kmax, int32_t* d_n_acc,
                              int32_t* d_out_tok, void* d_ws, hipStream_t st, KernelTimer* timer,
-                             const uint64_t* d_seed, bool aligned) {
+                             const uint64_t* d_seed, bool aligned, const int32_t* d_n_rows) {
   if (p.B == 0) return hipSuccess;
   if (p.n_chunks1 > kMaxChunks || p.n_chunks2 > kMaxChunks) return hipErrorInvalidValue;
   char* ws = static_cast<char*>(d_ws);
@@ -586,9 +653,11 @@ hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq*
   dim3 g1(p.n_chunks1, p.n_rows);
   if (timed(n1)) timer->begin(st);
   if (vec)
-    launch_kernel(stats_kernel<true>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1);
+    launch_kernel(stats_kernel<true>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1,
+                  d_n_rows);
   else
-    launch_kernel(stats_kernel<false>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1);
+    launch_kernel(stats_kernel<false>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1,
+                  d_n_rows);
   if (timed(n1)) timer->end(st, 4.0 * p.n_rows * p.V, 0.0);
   if (timed("decide_kernel")) timer->begin(st);
   launch_kernel(decide_kernel, dim3(p.B), dim3(kThreads), 0, st, d_rows, d_seqs, d_draft_tok, stats, p.n_chunks1,
@@ -607,6 +676,15 @@ hipError_t launch_vocab_pass(const VocabPlan& p, const VRow* d_rows, const VSeq*
   if (timed(n3)) timer->end(st, 0.0, 0.0);
   launch_kernel(final_kernel, dim3(p.B), dim3(kWave), 0, st, d_seqs, d_draft_tok, decs, picks, p.n_chunks2, kmax,
                 d_n_acc, d_out_tok);
+  return hipGetLastError();
+}
+
+hipError_t launch_vocab_setup(int B, int kmax, const int32_t* d_k, const float* d_temp, const int64_t* d_ids,
+                              const int32_t* d_base, const float* d_p, const float* d_q, int V, VRow* d_rows,
+                              VSeq* d_seqs, int32_t* d_n_rows, hipStream_t st) {
+  if (B <= 0 || B > kSetupMaxSeqs) return hipErrorInvalidValue;
+  setup_kernel<<<1, kSetupMaxSeqs, 0, st>>>(B, kmax, d_k, d_temp, d_ids, d_base, d_p, d_q, V, d_rows, d_seqs,
+                                            d_n_rows);
   return hipGetLastError();
 }
 
