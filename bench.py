@@ -9,14 +9,22 @@ pass) and the KV commit / rollback.  Inputs (random-init weights, prompts)
 are synthetic, seeded and resident in HBM before the timed region.
 
 Workloads:
+  all (default) the 8b-shaped line below, with sub-objects: the same sequence
+                at T = 0 ("greedy"), plain target decode with k = 0
+                ("plain_decode"), the serving batch ("serving") and the decision
+                pass alone ("vocab_stress"), each with its own timing, roofline
+                and oracle baseline.
   8b-shaped     32-layer d=4096 target (32/8 heads, ffn 14336, vocab 128256),
                 16-layer d=2048 drafter, batch 1, 2048-token context, k = 5,
                 T = 0.8 (default) or --temperature 0 for greedy.
+  8b-serving    the same pair serving 64 sequences (contexts log-uniform in
+                [512, 4096], k in {3, 5, 7}, drafts mixed toward the target's
+                top-1 off the clock), greedy by default.
   vocab-stress  the decision pass alone: 256 sequences x (7 + 1) rows x 128256.
 
 Prints one JSON line: metric, value (verified tokens/s, whole job), latency,
 roofline of the dominant kernel (live HIP-event timing through the library's
-kernel timer), and the float64 oracle timed on a bounded sample on the host.
+kernel timer), and one whole float64 oracle step timed on the host.
 """
 
 from __future__ import annotations
@@ -105,29 +113,56 @@ def roofline_pass(B, sess, kernel, step, args):
 # ---------------------------------------------------------------------------
 # 8B-shaped pair, batch 1
 
-def bench_8b(args):
+def device_models(cfg):
+    import torch
+    from paper_2607_20507_amd.session import DeviceModel
+    log("drawing weights on device")
+    dev = torch.device("cuda:0")
+    return (DeviceModel(cfg.target, None, dev, seed=cfg.seed),
+            DeviceModel(cfg.draft, None, dev, seed=cfg.seed + 1))
+
+
+def timed_rounds(stream, n, fn):
+    """Run fn(i) for i < n between a host clock and HIP events; fn returns
+    (tokens emitted, accepted drafts).  Returns (tokens, wall s, event ms,
+    accepted list)."""
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    tokens, acc = 0, []
+    for i in range(n):
+        t, a = fn(i)
+        tokens += t
+        acc.append(a)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    return tokens, time.perf_counter() - t0, ev0.elapsed_time(ev1), acc
+
+
+def bench_8b(args, target, draft, extras=False):
     import torch
     from paper_2607_20507_amd import binding as B
-    from paper_2607_20507_amd.session import DeviceModel, SpecSession
+    from paper_2607_20507_amd.session import SpecSession
     from workloads import LLAMA8B_SHAPED, seq_ids_for, uniform_prompts
 
     cfg = LLAMA8B_SHAPED
-    dev = torch.device("cuda:0")
     k = cfg.k[0]
     T = args.temperature
     ctx_len = cfg.context[1]
-    log("drawing weights on device")
-    target = DeviceModel(cfg.target, None, dev, seed=cfg.seed)
-    draft = DeviceModel(cfg.draft, None, dev, seed=cfg.seed + 1)
     total_steps = args.warmup + 2 * args.steps + args.roof_steps + 1  # + the latency rounds and round 0
+    if extras:  # greedy rounds and plain-decode steps on the same sequence
+        total_steps += 2 * (args.warmup + args.steps) + 1
     max_len = ctx_len + total_steps * (k + 1) + 64
     pages = (max_len + 15) // 16
     sess = SpecSession(target, draft, max_seqs=1, k_max=k, max_pages_per_seq=pages, max_rows=2048)
     sid = int(seq_ids_for(cfg.seed, 1)[0])
+    stream = torch.cuda.current_stream()
     prompt = uniform_prompts(cfg.seed, [ctx_len], cfg.target.vocab)[0]
     log("prefill", ctx_len)
     sess.prefill([sid], [prompt])
-    stream = torch.cuda.current_stream()
     acc_hist = []
     lat = []
 
@@ -179,98 +214,126 @@ def bench_8b(args):
         "kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops,
         "weights_gb_per_step": (cfg.target.weight_bytes_per_forward() + k * cfg.draft.weight_bytes_per_forward()) / 1e9,
     }
+    if extras:
+        base = cfg.seed + 5000
+
+        # greedy (T = 0) rounds of the same sequence, one call per round
+        def greedy(i):
+            na, _ = sess.verify_commit_draft([sid], [0.0], base + 2 * i, base + 2 * i + 1, [k])
+            return int(na[0]) + 1, int(na[0])
+
+        for i in range(args.warmup):
+            greedy(i)
+        g_tok, g_wall, g_ev, g_acc = timed_rounds(stream, args.steps, lambda i: greedy(args.warmup + i))
+        info["greedy"] = {"value": g_tok / g_wall, "unit": "tokens/s", "ms_per_step": g_wall * 1e3 / args.steps,
+                          "event_ms_per_step": g_ev / args.steps, "steps": args.steps, "temperature": 0.0,
+                          "mean_accepted": float(np.mean(g_acc))}
+        # plain target decode (k = 0): each step is a one-row verify, which
+        # emits the target's own next token, and its commit; no drafting.
+        # The first call verifies the pending drafts and drafts none.
+        base += 1000
+        sess.verify_commit_draft([sid], [T], base, base + 1, [0])
+
+        def plain(i):
+            sess.verify_commit_draft([sid], [T], base + 2 + i, base + 3 + i, [0])
+            return 1, 0
+
+        for i in range(args.warmup):
+            plain(i)
+        p_tok, p_wall, p_ev, _ = timed_rounds(stream, args.steps, lambda i: plain(args.warmup + i))
+        info["plain_decode"] = {"value": p_tok / p_wall, "unit": "tokens/s", "ms_per_step": p_wall * 1e3 / args.steps,
+                                "event_ms_per_step": p_ev / args.steps, "steps": args.steps, "temperature": T,
+                                "what": "target alone, one token per step: spec_verify_commit_draft with k = 0 "
+                                        "(a one-row target forward, the decision pass's bonus draw, the commit)"}
     sess.close()
     return info
 
 
-def cpu_baseline_8b(mean_tokens_per_step):
-    """Time the float64 oracle on a bounded sample of the same step and scale
-    it to a whole step: one target layer on the 6 verify rows over a
-    2048-token synthetic cache, the target LM head and the rule; one drafter
-    layer on one row, the drafter LM head and a draft draw."""
+def oracle_models():
+    """The float64 oracle decoders of the 8B-shaped pair for the CPU timing.
+    Every layer of a model is the same layer, drawn from its seed (the cost of
+    a forward does not depend on the weight values, and drawing 32 distinct
+    layers would take minutes of host time); the embedding is the LM head."""
     from oracle import decoder as OD
-    from oracle import rule
     from workloads import LLAMA8B_SHAPED
     from workloads.gen import layer_weights, _normal, _ones
 
     cfg = LLAMA8B_SHAPED
-    k = cfg.k[0]
-    rng = np.random.default_rng(0)
+    log("oracle: drawing one layer + LM head of each model")
 
-    def one_layer_model(shape, seed):
+    def model(shape, seed):
         lm = _normal(seed, shape, "lm_head", 0, (shape.vocab, shape.d_model))
+        lw = layer_weights(shape, seed, 0)
         return OD.Decoder(shape, {"embed": lm, "final_norm": _ones(shape, shape.d_model), "lm_head": lm,
-                                  "layers": [layer_weights(shape, seed, 0)]})
+                                  "layers": [lw] * shape.n_layers})
 
-    def filled_kv(dec, ctx):
+    return model(cfg.target, cfg.seed), model(cfg.draft, cfg.seed + 1)
+
+
+def cpu_full_step(tdec, ddec, ctx, k, T, seed):
+    """One whole oracle step of one sequence, timed on the host: k drafter
+    forwards of one row each over a cache of ctx positions (with LM head and
+    draft draw), the target forward over the k + 1 verify rows, its LM head,
+    and the rule.  The caches hold ctx positions of random keys and values
+    (set up before the clock starts)."""
+    from oracle import rule
+
+    rng = np.random.default_rng(seed)
+
+    def filled(dec):
         kv = dec.new_kv()
         sh = dec.shape
-        kv.append(0, rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim)),
-                  rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim)))
+        for l in range(dec.n_layers):
+            kv.append(l, rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim)),
+                      rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim)))
         return kv
 
-    log("oracle sample: generating one layer + LM head of each model")
-    tdec = one_layer_model(cfg.target, cfg.seed)
-    ddec = one_layer_model(cfg.draft, cfg.seed + 1)
-    ctx = cfg.context[1]
-    toks = rng.integers(0, cfg.target.vocab, size=k + 1)
+    tkv, dkv = filled(tdec), filled(ddec)
+    pending = int(rng.integers(0, tdec.shape.vocab))
+    t0 = time.perf_counter()
+    tok, drafts, zq = pending, [], []
+    for j in range(k):
+        z = ddec.forward(dkv, [tok], [ctx + j])[0]
+        tok = rule.sample_draft(z, T, seed, 1, ctx + j + 1)[0]
+        drafts.append(int(tok))
+        zq.append(z)
+    t1 = time.perf_counter()
+    zp = tdec.forward(tkv, [pending] + drafts, ctx + np.arange(k + 1))
+    t2 = time.perf_counter()
+    res = rule.verify(zp, np.array(zq), drafts, T, seed, 1, ctx)
+    t3 = time.perf_counter()
+    return {"step_s": t3 - t0, "draft_s": t1 - t0, "target_forward_s": t2 - t1, "rule_s": t3 - t2,
+            "accepted": int(res.n_accepted)}
 
-    reps = 8  # each piece timed 8 times (mean): about 10 s of oracle work in all
 
-    def timed(fn):
-        ts = []
-        for _ in range(reps):
-            t0 = time.perf_counter()
-            out = fn()
-            ts.append(time.perf_counter() - t0)
-        return float(np.mean(ts)), out
-
-    # target: one layer over k+1 rows (hidden only), then LM head + rule
-    t_layer, _ = timed(lambda: tdec.forward(filled_kv(tdec, ctx), toks, ctx + np.arange(k + 1), logits=False))
-    h = rng.standard_normal((k + 1, cfg.target.d_model))
-    t_lm, zp = timed(lambda: OD.matmul_wt(OD.rms_norm(h, tdec.w["final_norm"], 1e-5), tdec.w["lm_head"]))
-    zq = zp[:k] + rng.standard_normal((k, cfg.target.vocab))
-    drafts = [int(np.argmax(z)) for z in zq]
-    t_rule, _ = timed(lambda: rule.verify(zp, zq, drafts, 0.8, 1, 2, ctx))
-    # drafter: one layer on one row, LM head and draw
-    t_dlayer, _ = timed(lambda: ddec.forward(filled_kv(ddec, ctx), toks[:1], np.array([ctx]), logits=False))
-    hd = rng.standard_normal((1, cfg.draft.d_model))
-    t_dlm, zd = timed(lambda: OD.matmul_wt(OD.rms_norm(hd, ddec.w["final_norm"], 1e-5), ddec.w["lm_head"]))
-    t_draw, _ = timed(lambda: rule.sample_draft(zd[0], 0.8, 1, 2, ctx + 1))
-    step_s = (cfg.target.n_layers * t_layer + t_lm + t_rule
-              + k * (cfg.draft.n_layers * t_dlayer + t_dlm + t_draw))
-    sample_s = reps * (t_layer + t_lm + t_rule + t_dlayer + t_dlm + t_draw)
-    return {
-        "value": mean_tokens_per_step / step_s,
-        "step_s": step_s,
-        "sample_s": sample_s,
-        "sample": ("one verify step estimated from timed pieces, each run 8 times (mean): 1 of 32 target "
-                   "layers on 6 rows over a 2048-token synthetic cache + LM head + rule, and 1 of 16 drafter "
-                   "layers on 1 row + drafter LM head + draw; scaled to 32/16 layers and k=5 draft steps"),
-    }
+def cpu_baseline_8b(mean_tokens_per_step, models):
+    from workloads import LLAMA8B_SHAPED
+    cfg = LLAMA8B_SHAPED
+    log("oracle: one full batch-1 step")
+    r = cpu_full_step(*models, cfg.context[1], cfg.k[0], 0.8, cfg.seed)
+    return {"value": mean_tokens_per_step / r["step_s"], "step_s": r["step_s"], "sample_s": r["step_s"],
+            "parts_s": {x: r[x] for x in ("draft_s", "target_forward_s", "rule_s")},
+            "sample": ("one whole oracle step (float64): 5 drafter steps of 16 layers + LM head + draw, the "
+                       "32-layer target forward over the 6 verify rows + LM head, and the rule, over caches of "
+                       "2048 random positions; each model's layers share one seeded layer's weights")}
 
 
 # ---------------------------------------------------------------------------
 # 8B-shaped pair, serving batch of 64 sequences
 
-def bench_serving(args):
+def bench_serving(args, target, draft, T):
     import torch
     from paper_2607_20507_amd import binding as B
-    from paper_2607_20507_amd.session import DeviceModel, SpecSession
+    from paper_2607_20507_amd.session import SpecSession
     from workloads import (SERVING_8B, context_lengths_loguniform, draft_lengths, mix_draws, seq_ids_for,
                            uniform_prompts)
 
     cfg = SERVING_8B
-    dev = torch.device("cuda:0")
-    T = args.temperature
     n = cfg.batch
     ctx = context_lengths_loguniform(cfg.seed, n, cfg.context[1], cfg.context[2])
     ks = draft_lengths(cfg.seed, n, cfg.k)
     kmax = int(max(cfg.k))
     ids = [int(x) for x in seq_ids_for(cfg.seed, n)]
-    log("drawing weights on device")
-    target = DeviceModel(cfg.target, None, dev, seed=cfg.seed)
-    draft = DeviceModel(cfg.draft, None, dev, seed=cfg.seed + 1)
     total_steps = args.warmup + args.steps + args.roof_steps
     max_len = int(ctx.max()) + total_steps * (kmax + 1) + 64
     pages = (max_len + 15) // 16
@@ -334,6 +397,8 @@ def bench_serving(args):
             on_clock.append(spans)
         return int(na.sum()) + n
 
+    for s in range(args.warmup):
+        step(s, False)
     kernel = args.kernel or "gemm_mfma2_bf16<2, 6, 8>"
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -361,7 +426,8 @@ def bench_serving(args):
             "acc_hist": acc_hist, "mix": mix, "offclock_ms": event_ms - clock_ms if mix else 0.0,
             "verify_ms_median": float(np.median(lats)), "verify_ms_p90": float(np.percentile(lats, 90)),
             "kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops,
-            "mean_ctx": float(ctx.mean()), "rows_per_verify": int((ks + 1).sum())}
+            "mean_ctx": float(ctx.mean()), "rows_per_verify": int((ks + 1).sum()),
+            "ctx": ctx, "ks": ks}
 
 
 # ---------------------------------------------------------------------------
@@ -437,22 +503,92 @@ def bench_vocab(args):
 
 
 def cpu_baseline_vocab(mean_tokens_per_step):
-    """The oracle rule (float64) on a sample of 8 of the 256 sequences."""
+    """The oracle rule (float64) on the whole batch: for each of the 256
+    sequences, its k draft draws and the acceptance / resample decision, on
+    the same synthetic logit law (drawn on the host, 32 sequences at a time,
+    outside the clock)."""
     from oracle import rule
     from workloads import VOCAB_STRESS, vocab_logits
 
     cfg = VOCAB_STRESS
-    p, q = vocab_logits(cfg.seed, range(8), cfg.k, cfg.vocab)
-    t0 = time.perf_counter()
-    for s in range(8):
-        T = cfg.temperatures[s % 3]
-        drafts = [rule.sample_draft(q[s, j], T, 1, s, 100 + j + 1)[0] for j in range(cfg.k)]
-        rule.verify(p[s], q[s], drafts, T, 1, s, 100)
-    dt = time.perf_counter() - t0
-    per_seq = dt / 8
-    return {"value": mean_tokens_per_step / (per_seq * cfg.batch), "step_s": per_seq * cfg.batch,
-            "sample_s": dt,
-            "sample": "draft draws + rule on 8 of the 256 sequences, scaled to the full batch"}
+    dt = 0.0
+    for s0 in range(0, cfg.batch, 32):
+        seqs = list(range(s0, min(cfg.batch, s0 + 32)))
+        p, q = vocab_logits(cfg.seed, seqs, cfg.k, cfg.vocab)
+        t0 = time.perf_counter()
+        for i, s in enumerate(seqs):
+            T = cfg.temperatures[s % 3]
+            drafts = [rule.sample_draft(q[i, j], T, 1, s, 100 + j + 1)[0] for j in range(cfg.k)]
+            rule.verify(p[i], q[i], drafts, T, 1, s, 100)
+        dt += time.perf_counter() - t0
+    return {"value": mean_tokens_per_step / dt, "step_s": dt, "sample_s": dt,
+            "sample": "draft draws + rule on all 256 sequences (one whole step)"}
+
+
+def roofline_of(info, bound, workload, roof_steps, note=""):
+    """Roofline object of a workload's dominant kernel from its kernel-level
+    event timing: algorithmic bytes (or flops) per launch / average launch."""
+    n = info["k_n"]
+    per_launch_ms = info["k_ms"] / max(1, n)
+    if bound == "mfma":
+        achieved = (info["k_flops"] / n) / (per_launch_ms / 1e3) / 1e12 if n else None
+        peak, unit = BF16_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        achieved = (info["k_bytes"] / n) / (per_launch_ms / 1e3) / 1e9 if n else None
+        peak, unit = HBM_PEAK_GBS, "GB/s"
+    r = {"bound": bound, "kernel": info["kernel"], "achieved": achieved, "peak": peak, "unit": unit,
+         "frac": (achieved / peak) if achieved else None, "traffic": pmc_traffic(info["kernel"], workload),
+         "launches": n, "avg_launch_us": per_launch_ms * 1e3,
+         "timing": f"kernel-level HIP events (start and end of each launch of the kernel), "
+                   f"{roof_steps} eager steps after the timed region" + note,
+         "bytes_per_launch": info["k_bytes"] / max(1, n), "flops_per_launch": info["k_flops"] / max(1, n)}
+    if bound == "hbm" and info["k_flops"] and n:
+        r["tflops"] = info["k_flops"] / (info["k_ms"] / 1e3) / 1e12
+    if bound == "mfma" and n:
+        r["gbs"] = info["k_bytes"] / (info["k_ms"] / 1e3) / 1e9
+    return r
+
+
+def cpu_line(cb, threads, model, aff):
+    out = {"value": cb["value"], "unit": "tokens/s", "cores": threads, "kind": "oracle", "sample": cb["sample"],
+           "sample_s": cb["sample_s"], "est_step_s": cb["step_s"], "cpu": model, "affinity": aff}
+    if "parts_s" in cb:
+        out["parts_s"] = cb["parts_s"]
+    return out
+
+
+def serving_config(info, T):
+    return {"workload": "8b-shaped target / 1b-shaped drafter serving 64 sequences, contexts log-uniform "
+                        "[512, 4096] in 16-token pages, k per sequence in {3,5,7}"
+                        + (", drafts mixed toward the target's top-1 at rate 0.7 (boost 2.0), off the clock"
+                           if info["mix"] else ", no draft mixing"),
+            "batch": 64, "mean_context": info["mean_ctx"], "rows_per_verify": info["rows_per_verify"],
+            "temperature": T, "draft_mixing": info["mix"]}
+
+
+def serving_cpu(info, models):
+    """The oracle runs sequences one by one: one whole step of the batch's
+    sequence with k = 5 nearest the median context, times the 64 sequences."""
+    ctx, ks = info["ctx"], info["ks"]
+    cand = [i for i in range(len(ks)) if int(ks[i]) == 5] or list(range(len(ks)))
+    med = float(np.median(ctx))
+    i = min(cand, key=lambda j: abs(float(ctx[j]) - med))
+    log("oracle: one full step of serving sequence", i, "context", int(ctx[i]))
+    r = cpu_full_step(*models, int(ctx[i]), int(ks[i]), info["T"], 1234 + i)
+    step_s = r["step_s"] * len(ks)
+    return {"value": info["tokens"] / info["steps"] / step_s, "step_s": step_s, "sample_s": r["step_s"],
+            "parts_s": {x: r[x] for x in ("draft_s", "target_forward_s", "rule_s")},
+            "sample": (f"one whole oracle step (float64) of one of the 64 sequences (context {int(ctx[i])}, "
+                       f"k = {int(ks[i])}), times 64; each model's layers share one seeded layer's weights")}
+
+
+def sub_line(info, steps, extra):
+    out = {"value": info["tokens"] / info["wall_s"], "unit": "tokens/s", "steps": steps,
+           "ms_per_step": info["wall_s"] * 1e3 / steps, "event_ms_per_step": info["event_ms"] / steps,
+           "verify_ms_median": info["verify_ms_median"], "verify_ms_p90": info["verify_ms_p90"],
+           "mean_accepted": float(np.mean(info["acc_hist"])) if info["acc_hist"] else None}
+    out.update(extra)
+    return out
 
 
 def main():
@@ -460,7 +596,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="8b-shaped", choices=["8b-shaped", "8b-serving", "vocab-stress"])
+    ap.add_argument("--workload", default="all", choices=["all", "8b-shaped", "8b-serving", "vocab-stress"],
+                    help="all (default): the 8b-shaped line with greedy, plain-decode, serving and "
+                         "vocab-stress sub-objects")
     ap.add_argument("--temperature", type=float, default=None,
                     help="sampling temperature (default 0.8; 0, greedy, for the serving workload, whose draft "
                          "mixing fixes top-1 agreement, i.e. the greedy acceptance test)")
@@ -474,8 +612,6 @@ def main():
                     help="only copy a MIB-MiB device buffer --steps times (a plain copy kernel of known "
                          "size, for scaling the profiler's FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
-    if args.temperature is None:
-        args.temperature = 0.0 if args.workload == "8b-serving" else 0.8
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs on one GPU only: sequences shard by data parallelism "
@@ -499,85 +635,91 @@ def main():
                           "bytes_written_per_copy": nbytes, "copies": args.steps}), flush=True)
         return
 
-    if args.workload == "8b-shaped":
-        info = bench_8b(args)
-        config = {"workload": "8b-shaped target / 1b-shaped drafter, batch 1, context 2048, k=5",
-                  "target": "32L d4096 32q/8kv hd128 ffn14336 V128256", "draft": "16L d2048 32q/8kv hd64 ffn8192",
-                  "batch": 1, "context": 2048, "k": 5, "temperature": args.temperature}
-        bound = "hbm"
-    elif args.workload == "8b-serving":
-        info = bench_serving(args)
-        config = {"workload": "8b-shaped target / 1b-shaped drafter serving 64 sequences, contexts log-uniform "
-                              "[512, 4096] in 16-token pages, k per sequence in {3,5,7}"
-                              + (", drafts mixed toward the target's top-1 at rate 0.7 (boost 2.0), off the clock"
-                                 if info["mix"] else ", no draft mixing"),
-                  "batch": 64, "mean_context": info["mean_ctx"], "rows_per_verify": info["rows_per_verify"],
-                  "temperature": args.temperature, "draft_mixing": info["mix"]}
-        bound = "mfma"
-    else:
-        info = bench_vocab(args)
-        config = {"workload": "vocab-stress: decision pass alone, 256 seqs x 8 rows x 128256",
-                  "batch": 256, "k": 7, "vocab": 128256, "temperatures": [0.3, 1.0, 1.5]}
-        bound = "hbm"
+    from workloads import LLAMA8B_SHAPED
+    wl = args.workload
+    serve_T = 0.0 if args.temperature is None or wl == "all" else args.temperature
+    if args.temperature is None or wl == "all":
+        args.temperature = 0.0 if wl == "8b-serving" else 0.8
     steps = args.steps
-    value = info["tokens"] / info["wall_s"]
-    per_launch_ms = info["k_ms"] / max(1, info["k_n"])
-    if bound == "mfma":
-        achieved = (info["k_flops"] / max(1, info["k_n"])) / (per_launch_ms / 1e3) / 1e12 if info["k_n"] else None
-        peak, unit = BF16_PEAK_TFLOPS, "TFLOP/s"
+    info = info_s = info_v = None
+    if wl in ("all", "8b-shaped", "8b-serving"):
+        target, draft = device_models(LLAMA8B_SHAPED)
+        if wl in ("all", "8b-shaped"):
+            info = bench_8b(args, target, draft, extras=(wl == "all"))
+        if wl in ("all", "8b-serving"):
+            log("serving workload")
+            info_s = bench_serving(args, target, draft, serve_T)
+            info_s["T"], info_s["steps"] = serve_T, steps
+        del target, draft
+        torch.cuda.empty_cache()
+    if wl in ("all", "vocab-stress"):
+        log("vocab-stress workload")
+        info_v = bench_vocab(args)
+
+    b1_config = {"workload": "8b-shaped target / 1b-shaped drafter, batch 1, context 2048, k=5",
+                 "target": "32L d4096 32q/8kv hd128 ffn14336 V128256", "draft": "16L d2048 32q/8kv hd64 ffn8192",
+                 "batch": 1, "context": 2048, "k": 5, "temperature": args.temperature}
+    vocab_config = {"workload": "vocab-stress: decision pass alone, 256 seqs x 8 rows x 128256",
+                    "batch": 256, "k": 7, "vocab": 128256, "temperatures": [0.3, 1.0, 1.5]}
+    serve_note = " (verify launches only)"
+    if info is not None:  # the headline: batch 1
+        head, bound, hw = info, "hbm", "8b-shaped"
+        config = b1_config
+    elif info_s is not None:
+        head, bound, hw = info_s, "mfma", "8b-serving"
+        config = serving_config(info_s, serve_T)
     else:
-        achieved = (info["k_bytes"] / max(1, info["k_n"])) / (per_launch_ms / 1e3) / 1e9 if info["k_n"] else None
-        peak, unit = HBM_PEAK_GBS, "GB/s"
-    roofline = {"bound": bound, "kernel": info["kernel"], "achieved": achieved, "peak": peak,
-                "unit": unit, "frac": (achieved / peak) if achieved else None,
-                "traffic": pmc_traffic(info["kernel"], args.workload),
-                "launches": info["k_n"], "avg_launch_us": per_launch_ms * 1e3,
-                "timing": f"kernel-level HIP events (start and end of each launch of the kernel), "
-                          f"{args.roof_steps} eager steps after the timed region"
-                          + (" (verify launches only)" if args.workload == "8b-serving" else ""),
-                "bytes_per_launch": info["k_bytes"] / max(1, info["k_n"]),
-                "flops_per_launch": info["k_flops"] / max(1, info["k_n"])}
-    if bound == "hbm" and info["k_flops"] and info["k_n"]:
-        roofline["tflops"] = info["k_flops"] / (info["k_ms"] / 1e3) / 1e12
-    if bound == "mfma" and info["k_n"]:
-        roofline["gbs"] = info["k_bytes"] / (info["k_ms"] / 1e3) / 1e9
+        head, bound, hw = info_v, "hbm", "vocab-stress"
+        config = vocab_config
     line = {
         "metric": "verified tokens/sec + verify-step latency (ms) at 1 MI355X; % MFMA/HBM peak",
-        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
-        "ms_per_step": info["wall_s"] * 1e3 / steps, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded random-init weights and prompts)",
-        "config": config,
-        "verify_ms_median": info["verify_ms_median"], "verify_ms_p90": info["verify_ms_p90"],
-        "verify_latency": info.get("verify_latency", "HIP events around spec_verify + spec_kv_commit of each timed step"),
-        "event_ms_per_step": info["event_ms"] / steps,
-        "mean_accepted": float(np.mean(info["acc_hist"])) if info["acc_hist"] else None,
-        "offclock_ms_per_step": info.get("offclock_ms", 0.0) / steps,
-        "roofline": roofline,
+        "value": head["tokens"] / head["wall_s"], "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": head["wall_s"] * 1e3 / steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights and prompts)", "config": config,
+        "verify_ms_median": head["verify_ms_median"], "verify_ms_p90": head["verify_ms_p90"],
+        "verify_latency": head.get("verify_latency",
+                                   "HIP events around spec_verify + spec_kv_commit of each timed step"),
+        "event_ms_per_step": head["event_ms"] / steps,
+        "mean_accepted": float(np.mean(head["acc_hist"])) if head["acc_hist"] else None,
+        "offclock_ms_per_step": head.get("offclock_ms", 0.0) / steps,
+        "roofline": roofline_of(head, bound, hw, args.roof_steps, serve_note if hw == "8b-serving" else ""),
     }
-    if "vocab_bytes" in info:
-        vb = dict(info["vocab_bytes"])
-        ms = line["ms_per_step"]
-        vb["read_gbs"] = vb["read_per_step"] / (ms / 1e3) / 1e9
-        vb["early_exit_gbs"] = vb["early_exit_per_step"] / (ms / 1e3) / 1e9
-        line["vocab_bytes"] = vb
+    if info is not None and "greedy" in info:
+        line["greedy"] = info["greedy"]
+        line["plain_decode"] = info["plain_decode"]
+        line["speculative_gain"] = {
+            "sampled": line["value"] / info["plain_decode"]["value"],
+            "greedy": info["greedy"]["value"] / info["plain_decode"]["value"],
+            "note": "verified tokens/s of draft-and-verify over plain target decode (k = 0) on the same box; "
+                    "random-init models accept few drafts, so this is a slowdown here"}
+    if info_s is not None and head is not info_s:
+        line["serving"] = sub_line(info_s, steps, {
+            "config": serving_config(info_s, serve_T),
+            "offclock_ms_per_step": info_s.get("offclock_ms", 0.0) / steps,
+            "roofline": roofline_of(info_s, "mfma", "8b-serving", args.roof_steps, serve_note)})
+    if info_v is not None and head is not info_v:
+        line["vocab_stress"] = sub_line(info_v, steps, {
+            "config": vocab_config, "roofline": roofline_of(info_v, "hbm", "vocab-stress", args.roof_steps)})
+    for obj, inf in ((line, head), (line.get("vocab_stress"), info_v)):
+        if obj is not None and inf is not None and "vocab_bytes" in inf:
+            vb = dict(inf["vocab_bytes"])
+            ms = obj["ms_per_step"]
+            vb["read_gbs"] = vb["read_per_step"] / (ms / 1e3) / 1e9
+            vb["early_exit_gbs"] = vb["early_exit_per_step"] / (ms / 1e3) / 1e9
+            obj["vocab_bytes"] = vb
     if not args.no_cpu_baseline:
-        mean_tok = info["tokens"] / steps
         model, threads, aff = cpu_info()
         log("timing the oracle on a bounded sample")
-        if args.workload == "8b-shaped":
-            cb = cpu_baseline_8b(mean_tok)
-        elif args.workload == "8b-serving":
-            # the oracle runs sequences one at a time: a serving step costs the
-            # batch-1 step estimate once per sequence
-            cb = cpu_baseline_8b(1.0)
-            cb["step_s"] *= 64
-            cb["value"] = mean_tok / cb["step_s"]
-            cb["sample"] += "; multiplied by the 64 sequences of the batch (the oracle runs them one by one)"
-        else:
-            cb = cpu_baseline_vocab(mean_tok)
-        line["cpu_baseline"] = {"value": cb["value"], "unit": "tokens/s", "cores": threads, "kind": "oracle",
-                                "sample": cb["sample"], "sample_s": cb["sample_s"],
-                                "est_step_s": cb["step_s"], "cpu": model, "affinity": aff}
+        models = oracle_models() if (info is not None or info_s is not None) else None
+        if info is not None:
+            line["cpu_baseline"] = cpu_line(cpu_baseline_8b(info["tokens"] / steps, models), threads, model, aff)
+        if info_s is not None:
+            cb = cpu_line(serving_cpu(info_s, models), threads, model, aff)
+            (line if head is info_s else line["serving"])["cpu_baseline"] = cb
+        if info_v is not None:
+            cb = cpu_line(cpu_baseline_vocab(info_v["tokens"] / steps), threads, model, aff)
+            (line if head is info_v else line["vocab_stress"])["cpu_baseline"] = cb
     print(json.dumps(line), flush=True)
 
 
