@@ -11,9 +11,10 @@ are synthetic, seeded and resident in HBM before the timed region.
 Workloads:
   all (default) the 8b-shaped line below, with sub-objects: the same sequence
                 at T = 0 ("greedy"), plain target decode with k = 0
-                ("plain_decode"), the serving batch ("serving") and the decision
-                pass alone ("vocab_stress"), each with its own timing, roofline
-                and oracle baseline.
+                ("plain_decode"), the serving batch ("serving"), the 1b-shaped
+                model decoding 64 sequences by itself ("small_decode") and the
+                decision pass alone ("vocab_stress"), each with its own timing
+                and roofline (and oracle baseline where one is timed).
   8b-shaped     32-layer d=4096 target (32/8 heads, ffn 14336, vocab 128256),
                 16-layer d=2048 drafter, batch 1, 2048-token context, k = 5,
                 T = 0.8 (default) or --temperature 0 for greedy.
@@ -431,6 +432,45 @@ def bench_serving(args, target, draft, T):
 
 
 # ---------------------------------------------------------------------------
+# the small model decoding by itself, batched
+
+def bench_small_decode(args, small):
+    """Plain batched decoding of the 1B-shaped model in a decode-only context
+    that shares its weights: 64 sequences with the serving workload's
+    contexts, T = 0.8, one token per sequence per step (spec_decode)."""
+    import torch
+    from paper_2607_20507_amd import binding as B
+    from paper_2607_20507_amd.session import SpecSession
+    from workloads import SERVING_8B, context_lengths_loguniform, seq_ids_for, uniform_prompts
+
+    cfg = SERVING_8B
+    n = cfg.batch
+    ctx = context_lengths_loguniform(cfg.seed, n, cfg.context[1], cfg.context[2])
+    ids = [int(x) for x in seq_ids_for(cfg.seed + 7, n)]
+    total = args.warmup + args.steps + args.roof_steps
+    pages = (int(ctx.max()) + total + 16 + 15) // 16
+    need = int(sum((int(c) + total + 16 + 15) // 16 for c in ctx))
+    sess = SpecSession(small, None, max_seqs=n, k_max=0, max_pages_per_seq=pages, num_pages_target=need,
+                       max_rows=4096)
+    prompts = uniform_prompts(cfg.seed + 7, [int(c) for c in ctx], cfg.draft.vocab)
+    log("small-model decode: prefill", int(ctx.sum()), "tokens")
+    sess.prefill(ids, prompts)
+    stream = torch.cuda.current_stream()
+    temps = [0.8] * n
+    sess.decode(ids, temps, cfg.seed, args.warmup)
+    # one call decodes every timed step (the library loops over the steps)
+    tok, wall, ev, _ = timed_rounds(stream, 1, lambda i: (sess.decode(ids, temps, cfg.seed + 1, args.steps).size, 0))
+    kernel = args.kernel or "attn_bf16_kernel<64, 1, 4>"
+    B.spec_timing_enable(sess.ctx, kernel)
+    sess.decode(ids, temps, cfg.seed + 2, args.roof_steps)
+    k_ms, k_n, k_bytes, k_flops = B.spec_timing_read(sess.ctx)
+    B.spec_timing_enable(sess.ctx, None)
+    sess.close()
+    return {"tokens": tok, "wall_s": wall, "event_ms": ev, "kernel": kernel, "k_ms": k_ms, "k_n": k_n,
+            "k_bytes": k_bytes, "k_flops": k_flops, "mean_ctx": float(ctx.mean())}
+
+
+# ---------------------------------------------------------------------------
 # decision pass alone
 
 def bench_vocab(args):
@@ -641,7 +681,7 @@ def main():
     if args.temperature is None or wl == "all":
         args.temperature = 0.0 if wl == "8b-serving" else 0.8
     steps = args.steps
-    info = info_s = info_v = None
+    info = info_s = info_v = info_d = None
     if wl in ("all", "8b-shaped", "8b-serving"):
         target, draft = device_models(LLAMA8B_SHAPED)
         if wl in ("all", "8b-shaped"):
@@ -650,6 +690,8 @@ def main():
             log("serving workload")
             info_s = bench_serving(args, target, draft, serve_T)
             info_s["T"], info_s["steps"] = serve_T, steps
+        if wl == "all":
+            info_d = bench_small_decode(args, draft)
         del target, draft
         torch.cuda.empty_cache()
     if wl in ("all", "vocab-stress"):
@@ -698,6 +740,15 @@ def main():
             "config": serving_config(info_s, serve_T),
             "offclock_ms_per_step": info_s.get("offclock_ms", 0.0) / steps,
             "roofline": roofline_of(info_s, "mfma", "8b-serving", args.roof_steps, serve_note)})
+    if info_d is not None:
+        line["small_decode"] = {
+            "value": info_d["tokens"] / info_d["wall_s"], "unit": "tokens/s", "steps": steps,
+            "ms_per_step": info_d["wall_s"] * 1e3 / steps, "event_ms_per_step": info_d["event_ms"] / steps,
+            "config": {"workload": "1b-shaped model decoding alone (decode-only context sharing the drafter's "
+                                   "weights), 64 sequences, contexts log-uniform [512, 4096], T = 0.8, "
+                                   "one token per sequence per step",
+                       "batch": 64, "mean_context": info_d["mean_ctx"], "temperature": 0.8},
+            "roofline": roofline_of(info_d, "hbm", "small-decode", args.roof_steps)}
     if info_v is not None and head is not info_v:
         line["vocab_stress"] = sub_line(info_v, steps, {
             "config": vocab_config, "roofline": roofline_of(info_v, "hbm", "vocab-stress", args.roof_steps)})

@@ -136,7 +136,16 @@ typedef struct spec_ctx spec_ctx;
 /* Bytes one KV pool of `num_pages` pages needs for model `m`. */
 SPEC_API size_t spec_kv_pool_bytes(const spec_model_desc* m, int32_t num_pages);
 
-/* Create a context for a target/draft pair (same vocabulary and dtype). */
+/* Create a context for a target/draft pair (same vocabulary and dtype): the
+ * two models of speculative decoding, the small one proposing tokens that the
+ * large one verifies (paper, Section 3.4 Cache-Miss Branch and the
+ * speculative-decoding paragraph of Section 2).  draft == NULL makes a
+ * decode-only context over `target` alone, for plain batched decoding with
+ * spec_decode (the small model's other role, generating on its own:
+ * Section 3.3 Cache-Hit Branch); its cache descriptor's draft pool and page
+ * count are ignored and k_max may be 0, and the draft calls return
+ * SPEC_E_STATE.  Models may share weights with another context's models
+ * (the descriptors hold the caller's device pointers). */
 SPEC_API spec_status spec_ctx_create(const spec_model_desc* target, const spec_model_desc* draft,
                                      const spec_cache_desc* cache, spec_ctx** out);
 SPEC_API void spec_ctx_destroy(spec_ctx* ctx);
@@ -239,6 +248,21 @@ SPEC_API spec_status spec_verify_commit_draft(spec_ctx* ctx, int32_t n, const in
                                               const float* temperature, uint64_t verify_seed,
                                               int32_t* n_accepted, int32_t* out_tokens,
                                               uint64_t draft_seed, const int32_t* steps, void* stream);
+
+/* Plain autoregressive decoding of the context's target model, `steps` tokens
+ * for each listed sequence (Section 3.3 Cache-Hit Branch: the small model
+ * generates by itself; in a decode-only context the target is that model).
+ * Each step feeds every sequence's pending token x_n at position n (its K/V
+ * are written), draws the next token from softmax(z/T) by Gumbel-max with
+ * BONUS noise keyed (seed, seq, n + 1) (argmax for T == 0, ties to the
+ * lowest id) and commits it: exactly a spec_verify with no drafts followed by
+ * spec_kv_commit.  The sequences must hold no drafts and no uncommitted
+ * verify (SPEC_E_STATE); every page the call needs is checked before any
+ * step runs (SPEC_E_NOPAGES).  temperature: host [n], >= 0.  out_tokens: host
+ * int32 [n][steps], row i the tokens of sequence i in order.  Blocks until
+ * the last step's tokens are on the host. */
+SPEC_API spec_status spec_decode(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                                 uint64_t seed, int32_t steps, int32_t* out_tokens, void* stream);
 
 /* Truncate both caches of a sequence to `new_len` positions (0 <= new_len <=
  * target length); history[new_len] becomes the pending token and outstanding

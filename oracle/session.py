@@ -18,6 +18,10 @@ State of one sequence (the pending-token model):
 
 A prompt of P tokens is prefilled into both caches for positions 0..P-2, and
 x_{P-1} is pending.
+
+With no draft model (``draft=None``) the session decodes the target alone
+(``decode``): each step is a verify of no drafts, whose one row's bonus draw is
+the next token, and its commit.
 """
 
 from __future__ import annotations
@@ -36,7 +40,7 @@ from . import rule
 class SeqState:
     history: List[int]
     kv_t: KVList
-    kv_d: KVList
+    kv_d: Optional[KVList]
     drafts: List[int] = field(default_factory=list)
     zq: List[np.ndarray] = field(default_factory=list)
     draft_excluded: bool = False
@@ -47,12 +51,12 @@ class SeqState:
 
 
 class Session:
-    def __init__(self, target: Decoder, draft: Decoder, num_pages_target: int,
+    def __init__(self, target: Decoder, draft: Optional[Decoder], num_pages_target: int,
                  num_pages_draft: int, page_size: int = 16):
         self.target = target
         self.draft = draft
         self.pool_t = PagePool(num_pages_target, page_size)
-        self.pool_d = PagePool(num_pages_draft, page_size)
+        self.pool_d = PagePool(num_pages_draft if draft is not None else 0, page_size)
         self.seqs: Dict[int, SeqState] = {}
 
     # ------------------------------------------------------------------
@@ -61,13 +65,15 @@ class Session:
             sid = int(sid)
             prompt = [int(t) for t in prompt]
             assert len(prompt) >= 1 and sid not in self.seqs
-            st = SeqState(prompt, self.target.new_kv(), self.draft.new_kv())
+            st = SeqState(prompt, self.target.new_kv(), self.draft.new_kv() if self.draft else None)
             P = len(prompt)
             self.pool_t.ensure(sid, P - 1)
-            self.pool_d.ensure(sid, P - 1)
+            if self.draft:
+                self.pool_d.ensure(sid, P - 1)
             if P > 1:
                 self.target.forward(st.kv_t, prompt[:-1], np.arange(P - 1), logits=False)
-                self.draft.forward(st.kv_d, prompt[:-1], np.arange(P - 1), logits=False)
+                if self.draft:
+                    self.draft.forward(st.kv_d, prompt[:-1], np.arange(P - 1), logits=False)
             self.seqs[sid] = st
 
     def draft_step(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int,
@@ -155,11 +161,12 @@ class Session:
             n, a = st.n, res.n_accepted
             st.history.extend(res.tokens)
             new_t = n + a + 1
-            new_d = min(st.kv_d.length, new_t)
             st.kv_t.truncate(new_t)
-            st.kv_d.truncate(new_d)
             self.pool_t.truncate(sid, new_t)
-            self.pool_d.truncate(sid, new_d)
+            if st.kv_d is not None:
+                new_d = min(st.kv_d.length, new_t)
+                st.kv_d.truncate(new_d)
+                self.pool_d.truncate(sid, new_d)
             st.drafts, st.zq, st.draft_excluded = [], [], False
 
     def rollback(self, sid: int, new_len: int):
@@ -169,10 +176,31 @@ class Session:
         assert 0 <= new_len <= st.kv_t.length
         del st.history[new_len + 1:]
         st.kv_t.truncate(new_len)
-        st.kv_d.truncate(min(st.kv_d.length, new_len))
         self.pool_t.truncate(int(sid), new_len)
-        self.pool_d.truncate(int(sid), st.kv_d.length)
+        if st.kv_d is not None:
+            st.kv_d.truncate(min(st.kv_d.length, new_len))
+            self.pool_d.truncate(int(sid), st.kv_d.length)
         st.drafts, st.zq, st.draft_excluded = [], [], False
+
+    def decode(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int, steps: int,
+               margins: rule.Margins = rule.Margins()):
+        """Plain decoding of the target: ``steps`` tokens per sequence, each a
+        verify with no drafts (the bonus draw from p at position n + 1, or its
+        argmax for T = 0) and its commit, step by step over the list.  Returns
+        (tokens [n][steps], excluded [n][steps], logits [steps] of [n, V])."""
+        toks = [[] for _ in seq_ids]
+        excl = [[] for _ in seq_ids]
+        logits = []
+        for _ in range(steps):
+            for sid in seq_ids:
+                assert not self.seqs[int(sid)].drafts, "decode needs sequences with no drafts"
+            out = self.verify(seq_ids, temps, seed, margins)
+            self.commit(seq_ids, [r for r, _ in out])
+            for i, (r, _) in enumerate(out):
+                toks[i].append(r.tokens[0])
+                excl[i].append(bool(r.excluded))
+            logits.append(np.stack([z[0] for _, z in out]))
+        return toks, excl, logits
 
     def release(self, sid: int):
         self.pool_t.release(int(sid))
@@ -182,7 +210,7 @@ class Session:
     # ------------------------------------------------------------------
     def lengths(self, sid: int):
         st = self.seqs[int(sid)]
-        return st.kv_t.length, st.kv_d.length
+        return st.kv_t.length, (st.kv_d.length if st.kv_d is not None else 0)
 
     def pages(self, sid: int):
         return list(self.pool_t.tables.get(int(sid), [])), list(self.pool_d.tables.get(int(sid), []))

@@ -80,6 +80,7 @@ SIGNATURES = {
     "spec_draft_loop": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, _P]),
     "spec_verify_commit_draft": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, _I32P, c_uint64, _I32P,
                                            _P]),
+    "spec_decode": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, c_int32, _I32P, _P]),
     "spec_target_forward": (c_int32, [_P, c_int32, _I64P, _P]),
     "spec_draft_logits": (c_int32, [_P, c_int64, c_int32, _P]),
     "spec_draft_tokens": (c_int32, [_P, c_int64, _P, _P, _P]),
@@ -171,10 +172,11 @@ def spec_kv_pool_bytes(desc: spec_model_desc, num_pages: int) -> int:
     return lib().spec_kv_pool_bytes(ctypes.byref(desc), num_pages)
 
 
-def spec_ctx_create(target: spec_model_desc, draft: spec_model_desc, cache: spec_cache_desc) -> int:
+def spec_ctx_create(target: spec_model_desc, draft: Optional[spec_model_desc], cache: spec_cache_desc) -> int:
+    """draft None: a decode-only context over the target model (spec_decode)."""
     out = c_void_p()
-    check(lib().spec_ctx_create(ctypes.byref(target), ctypes.byref(draft), ctypes.byref(cache),
-                                ctypes.byref(out)))
+    check(lib().spec_ctx_create(ctypes.byref(target), ctypes.byref(draft) if draft is not None else None,
+                                ctypes.byref(cache), ctypes.byref(out)))
     return out.value
 
 
@@ -257,6 +259,16 @@ def spec_verify_commit_draft(ctx: int, seq_ids, temperature, verify_seed: int, k
     check(lib().spec_verify_commit_draft(ctx, n, _ptr(ids, _I64P), _ptr(t, _F32P), verify_seed, _ptr(na, _I32P),
                                          _ptr(ot, _I32P), draft_seed, _ptr(k, _I32P), stream_ptr(stream)), ctx)
     return na, ot
+
+
+def spec_decode(ctx: int, seq_ids, temperature, seed: int, steps: int, stream=None):
+    """Plain decoding of the context's target model; returns tokens [n, steps]."""
+    ids = _i64(seq_ids)
+    t = _f32(temperature)
+    out = np.full((len(ids), max(steps, 0)), -1, dtype=np.int32)
+    check(lib().spec_decode(ctx, len(ids), _ptr(ids, _I64P), _ptr(t, _F32P), seed, steps, _ptr(out, _I32P),
+                            stream_ptr(stream)), ctx)
+    return out
 
 
 def spec_kv_commit(ctx: int, seq_ids, n_accepted, stream=None):

@@ -140,6 +140,7 @@ int unsupported_model(const spec_model_desc* m, std::string& why) {
 
 struct spec_ctx {
   Model m[2];  // 0 target, 1 draft
+  int n_models = 2;  // 1: a decode-only context (no draft model)
   spec_cache_desc cache{};
   int R_max = 0, V = 0, k_max = 0, max_seqs = 0, max_pages = 0;
   int d_max = 0, qkv_max = 0, q_max = 0, ffn_max = 0, hkv_max = 0, hd_max = 0, esz_max = 2;
@@ -591,23 +592,30 @@ spec_status spec_ctx_create(const spec_model_desc* target, const spec_model_desc
   std::string why;
   if (!out) { g_err = "null out"; return SPEC_E_INVALID; }
   *out = nullptr;
-  if (!valid_model(target, why) || !valid_model(draft, why)) { g_err = why; return SPEC_E_INVALID; }
-  if (!cache || cache->page_size != 16 || cache->num_pages_target <= 0 || cache->num_pages_draft <= 0 ||
-      cache->max_seqs <= 0 || cache->max_pages_per_seq <= 0 || cache->k_max < 1 || cache->k_max > 15 ||
-      cache->max_rows <= 0 || !cache->kv_target || !cache->kv_draft) {
-    g_err = "invalid cache descriptor (page_size must be 16, k_max in 1..15, pools non-null)";
+  const bool pair = draft != nullptr;
+  if (!valid_model(target, why) || (pair && !valid_model(draft, why))) { g_err = why; return SPEC_E_INVALID; }
+  if (!cache || cache->page_size != 16 || cache->num_pages_target <= 0 || cache->max_seqs <= 0 ||
+      cache->max_pages_per_seq <= 0 || cache->k_max < (pair ? 1 : 0) || cache->k_max > 15 ||
+      cache->max_rows <= 0 || !cache->kv_target ||
+      (pair && (cache->num_pages_draft <= 0 || !cache->kv_draft))) {
+    g_err = "invalid cache descriptor (page_size must be 16, k_max in 1..15 (0..15 without a draft model), "
+            "pools non-null)";
     return SPEC_E_INVALID;
   }
-  if (target->vocab != draft->vocab || target->dtype != draft->dtype) {
+  if (pair && (target->vocab != draft->vocab || target->dtype != draft->dtype)) {
     g_err = "target and draft must share vocab and dtype";
     return SPEC_E_INVALID;
   }
-  if (unsupported_model(target, why) || unsupported_model(draft, why)) { g_err = why; return SPEC_E_UNSUPPORTED; }
+  if (unsupported_model(target, why) || (pair && unsupported_model(draft, why))) {
+    g_err = why;
+    return SPEC_E_UNSUPPORTED;
+  }
   spec_ctx* c = new spec_ctx();
+  c->n_models = pair ? 2 : 1;
   const spec_model_desc* ms[2] = {target, draft};
   void* pools[2] = {cache->kv_target, cache->kv_draft};
-  const int np[2] = {cache->num_pages_target, cache->num_pages_draft};
-  for (int i = 0; i < 2; ++i) {
+  const int np[2] = {cache->num_pages_target, pair ? cache->num_pages_draft : 0};
+  for (int i = 0; i < c->n_models; ++i) {
     Model& M = c->m[i];
     M.d = *ms[i];
     M.layers.assign(ms[i]->layers, ms[i]->layers + ms[i]->n_layers);
@@ -699,7 +707,7 @@ spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const
     if (ctx->m[0].pool.pages_for(P + ctx->k_max + 1) > ctx->max_pages)
       FAIL(SPEC_E_INVALID, "prompt too long for max_pages_per_seq");
     need_t += ctx->m[0].pool.pages_for(P - 1);
-    need_d += ctx->m[1].pool.pages_for(P - 1);
+    if (ctx->n_models == 2) need_d += ctx->m[1].pool.pages_for(P - 1);
   }
   if (static_cast<int>(ctx->free_slots.size()) < n) FAIL(SPEC_E_INVALID, "more live sequences than max_seqs");
   if (need_t > ctx->m[0].pool.free_pages() || need_d > ctx->m[1].pool.free_pages())
@@ -724,8 +732,9 @@ spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const
     off += prompt_lens[i];
     const int P = prompt_lens[i];
     ctx->m[0].pool.ensure(s.pages_t, P - 1);
-    ctx->m[1].pool.ensure(s.pages_d, P - 1);
-    s.len_t = s.len_d = s.written_t = P - 1;
+    if (ctx->n_models == 2) ctx->m[1].pool.ensure(s.pages_d, P - 1);
+    s.len_t = s.written_t = P - 1;
+    s.len_d = ctx->n_models == 2 ? P - 1 : 0;
     ss.push_back(&(ctx->seqs[s.id] = std::move(s)));
   }
   // chunked forward of positions 0..P-2 through both models
@@ -743,7 +752,7 @@ spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const
       rows += pieces[pi].nrows;
       ++pi;
     }
-    for (int mi = 0; mi < 2; ++mi) {
+    for (int mi = 0; mi < ctx->n_models; ++mi) {
       const Model& M = ctx->m[mi];
       Fwd f;
       std::vector<const std::vector<int32_t>*> tabs;
@@ -784,6 +793,7 @@ spec_status draft_step_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (n < 0 || (n > 0 && (!seq_ids || !temperature))) FAIL(SPEC_E_INVALID, "bad arguments");
   if (n == 0) return SPEC_OK;
+  if (ctx->n_models < 2) FAIL(SPEC_E_STATE, "context has no draft model");
   if (!check_ids(ctx, n, seq_ids, true)) return SPEC_E_INVALID;
   Model& D = ctx->m[1];
   int rows = 0, need = 0;
@@ -1002,6 +1012,7 @@ spec_status draft_loop_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
     n_steps = std::max(n_steps, steps[i]);
   }
   if (n_steps == 0) return SPEC_OK;
+  if (ctx->n_models < 2) FAIL(SPEC_E_STATE, "context has no draft model");
   for (int j = 0; j < n_steps; ++j) {
     int rows = 0;
     for (int i = 0; i < n; ++i)
@@ -1048,6 +1059,7 @@ spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k, const int3
   if (it == ctx->seqs.end()) FAIL(SPEC_E_INVALID, "unknown seq_id");
   Seq& s = it->second;
   if (k < 0 || k > ctx->k_max || (k > 0 && (!tokens || !q_logits))) FAIL(SPEC_E_INVALID, "bad drafts");
+  if (k > 0 && ctx->n_models < 2) FAIL(SPEC_E_STATE, "context has no draft model");
   if (s.verified) FAIL(SPEC_E_STATE, "set_drafts after verify without commit");
   if (s.k > 0 && !s.external) FAIL(SPEC_E_STATE, "sequence already has drafts from spec_draft_step");
   for (int j = 0; j < k; ++j)
@@ -1277,6 +1289,37 @@ spec_status spec_verify_commit_draft(spec_ctx* ctx, int32_t n, const int64_t* se
   s = spec_kv_commit(ctx, n, seq_ids, n_accepted, stream);
   if (s != SPEC_OK) return s;
   return spec_draft_loop(ctx, n, seq_ids, temperature, draft_seed, steps, stream);
+}
+
+spec_status spec_decode(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
+                        uint64_t seed, int32_t steps, int32_t* out_tokens, void* stream) {
+  CHECK_READY();
+  if (n < 0 || steps < 0 || (n > 0 && steps > 0 && (!seq_ids || !temperature || !out_tokens)))
+    FAIL(SPEC_E_INVALID, "bad arguments");
+  if (n == 0 || steps == 0) return SPEC_OK;
+  if (!check_ids(ctx, n, seq_ids, true)) return SPEC_E_INVALID;
+  Model& T = ctx->m[0];
+  int need = 0;
+  for (int i = 0; i < n; ++i) {
+    const Seq& s = ctx->seqs[seq_ids[i]];
+    if (!(temperature[i] >= 0.f)) FAIL(SPEC_E_INVALID, "temperature must be >= 0");
+    if (s.k > 0 || s.verified) FAIL(SPEC_E_STATE, "decode of a sequence with drafts or an uncommitted verify");
+    if (T.pool.pages_for(s.n() + steps) > ctx->max_pages) FAIL(SPEC_E_INVALID, "sequence exceeds max_pages_per_seq");
+    need += T.pool.need(s.pages_t, s.n() + steps);
+  }
+  if (need > T.pool.free_pages()) FAIL(SPEC_E_NOPAGES, "target KV page pool exhausted");
+  // each step is a verify of no drafts (the one row's bonus draw is the next
+  // token) and its commit
+  const int W = ctx->k_max + 1;
+  std::vector<int32_t> acc(n), tok(static_cast<size_t>(n) * W), none(n, 0);
+  for (int j = 0; j < steps; ++j) {
+    spec_status s = verify_impl(ctx, n, seq_ids, temperature, seed, acc.data(), tok.data(), true, stream);
+    if (s != SPEC_OK) return s;
+    for (int i = 0; i < n; ++i) out_tokens[static_cast<size_t>(i) * steps + j] = tok[static_cast<size_t>(i) * W];
+    s = spec_kv_commit(ctx, n, seq_ids, none.data(), stream);
+    if (s != SPEC_OK) return s;
+  }
+  return SPEC_OK;
 }
 
 spec_status spec_kv_rollback(spec_ctx* ctx, int64_t seq_id, int32_t new_len, void* stream) {

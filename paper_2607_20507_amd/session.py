@@ -96,19 +96,22 @@ class DeviceModel:
 class SpecSession:
     """One library context with its pools and workspace; methods mirror the C calls."""
 
-    def __init__(self, target: DeviceModel, draft: DeviceModel, *, max_seqs: int, k_max: int,
+    def __init__(self, target: DeviceModel, draft: Optional[DeviceModel], *, max_seqs: int, k_max: int,
                  max_pages_per_seq: int, num_pages_target: Optional[int] = None,
                  num_pages_draft: Optional[int] = None, max_rows: int = 2048, graphs: bool = True):
+        """draft None: a decode-only context over `target` (decode())."""
         self.target, self.draft = target, draft
         self.k_max = k_max
         dev = target.device
         npt = num_pages_target or max_seqs * max_pages_per_seq
-        npd = num_pages_draft or max_seqs * max_pages_per_seq
+        npd = (num_pages_draft or max_seqs * max_pages_per_seq) if draft is not None else 0
         self.kv_target = torch.zeros(B.spec_kv_pool_bytes(target.desc, npt), dtype=torch.uint8, device=dev)
-        self.kv_draft = torch.zeros(B.spec_kv_pool_bytes(draft.desc, npd), dtype=torch.uint8, device=dev)
+        self.kv_draft = (torch.zeros(B.spec_kv_pool_bytes(draft.desc, npd), dtype=torch.uint8, device=dev)
+                         if draft is not None else None)
         self.cache = B.spec_cache_desc(16, npt, npd, max_seqs, max_pages_per_seq, k_max, max_rows,
-                                       self.kv_target.data_ptr(), self.kv_draft.data_ptr())
-        self.ctx = B.spec_ctx_create(target.desc, draft.desc, self.cache)
+                                       self.kv_target.data_ptr(),
+                                       self.kv_draft.data_ptr() if draft is not None else None)
+        self.ctx = B.spec_ctx_create(target.desc, draft.desc if draft is not None else None, self.cache)
         nbytes = B.spec_workspace_bytes(self.ctx)
         self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=dev)
         off = (-self.workspace.data_ptr()) % 256
@@ -156,6 +159,10 @@ class SpecSession:
         """verify, commit with the accepted counts, then draft_loop of the next round, in one call."""
         return B.spec_verify_commit_draft(self.ctx, seq_ids, temps, verify_seed, self.k_max, draft_seed, steps,
                                           stream)
+
+    def decode(self, seq_ids, temps, seed: int, steps: int, stream=None):
+        """Plain decoding of the target model: tokens [n, steps]."""
+        return B.spec_decode(self.ctx, seq_ids, temps, seed, steps, stream)
 
     def commit(self, seq_ids, n_accepted, stream=None):
         B.spec_kv_commit(self.ctx, seq_ids, n_accepted, stream)
