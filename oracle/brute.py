@@ -16,7 +16,7 @@ from typing import Callable, Dict, Tuple
 
 import numpy as np
 
-from . import rule
+from . import rule, tree
 
 Dist = Callable[[Tuple[int, ...]], np.ndarray]
 
@@ -42,6 +42,61 @@ def speculative_law(target: Dist, draft: Dist, k: int, N: int, V: int) -> Dict[T
                 ps = [target(prefix + d[:j]) for j in range(k + 1)]
                 for toks, pt in rule.outcome_law(ps, qs, d).items():
                     full = prefix + toks
+                    if len(full) >= N:
+                        key = full[:N]
+                        final[key] = final.get(key, 0.0) + pr * pt
+                    else:
+                        nxt[full] = nxt.get(full, 0.0) + pr * pt
+        frontier = nxt
+    return final
+
+
+def tree_shape(branching) -> list:
+    """Parents of a tree with branching[l] children under every node of depth
+    l (the root has depth 0), nodes numbered level by level."""
+    parents, level = [], [-1]
+    for b in branching:
+        nxt = []
+        for u in level:
+            for _ in range(b):
+                parents.append(u)
+                nxt.append(len(parents) - 1)
+        level = nxt
+    return parents
+
+
+def tree_law(target: Dist, draft: Dist, branching, N: int, V: int) -> Dict[Tuple[int, ...], float]:
+    """Joint law of the first N tokens emitted by tree verification, every
+    node's children drawn independently from the draft distribution after the
+    node's path (``tree.outcome_law_tree`` for each drawn tree)."""
+    parents = tree_shape(branching)
+    m = len(parents)
+
+    def path(i, toks):
+        out = []
+        while i >= 0:
+            out.append(toks[i])
+            i = parents[i]
+        return tuple(reversed(out))
+
+    final: Dict[Tuple[int, ...], float] = {}
+    frontier: Dict[Tuple[int, ...], float] = {(): 1.0}
+    while frontier:
+        nxt: Dict[Tuple[int, ...], float] = {}
+        for prefix, w in frontier.items():
+            for toks in itertools.product(range(V), repeat=m):
+                pr = w
+                for i in range(m):
+                    u = parents[i]
+                    pr *= draft(prefix + (path(u, toks) if u >= 0 else ()))[toks[i]]
+                    if pr == 0.0:
+                        break
+                if pr == 0.0:
+                    continue
+                ps = [target(prefix)] + [target(prefix + path(i, toks)) for i in range(m)]
+                qs = [draft(prefix)] + [draft(prefix + path(i, toks)) for i in range(m)]
+                for out, pt in tree.outcome_law_tree(ps, qs, parents, toks).items():
+                    full = prefix + out
                     if len(full) >= N:
                         key = full[:N]
                         final[key] = final.get(key, 0.0) + pr * pt

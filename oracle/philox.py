@@ -89,6 +89,13 @@ def uniform(seed: int, seq: int, pos: int, purpose: int) -> float:
     return float(to_uniform(raw_words(seed, seq, pos, purpose, 1))[0])
 
 
+def uniform_block(seed: int, seq: int, pos: int, purpose: int, block: int) -> float:
+    """Word 0 of block ``block`` of a stream as a uniform (block 0 is ``uniform``):
+    the scalar draw of candidate ``block`` among several at one position."""
+    w = philox4x32_10(stream_counter(seq, pos, purpose, [int(block)]), seed_key(seed))
+    return float(to_uniform(w[0, 0]))
+
+
 def gumbel(seed: int, seq: int, pos: int, purpose: int, n: int) -> np.ndarray:
     """Gumbel(0,1) noise G_i = -log(-log u_i) for i < n, float64."""
     u = to_uniform(raw_words(seed, seq, pos, purpose, n))

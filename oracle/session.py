@@ -33,7 +33,7 @@ import numpy as np
 
 from .decoder import Decoder, KVList
 from .paging import PagePool
-from . import rule
+from . import rule, tree
 
 
 @dataclass
@@ -44,6 +44,7 @@ class SeqState:
     drafts: List[int] = field(default_factory=list)
     zq: List[np.ndarray] = field(default_factory=list)
     draft_excluded: bool = False
+    tree_parents: Optional[List[int]] = None   # drafts form a tree (set_draft_tree)
 
     @property
     def n(self) -> int:            # position of the pending token
@@ -124,15 +125,58 @@ class Session:
         st.drafts = [int(x) for x in drafts]
         st.zq = [np.asarray(r, dtype=np.float64) for r in zq]
 
+    def set_draft_tree(self, sid: int, parents: Sequence[int], tokens: Sequence[int], zq: np.ndarray):
+        """Install a draft tree: node i has token tokens[i] and parent
+        parents[i] (-1: the pending token); zq [m+1, V] holds the draft logits
+        each node's children were drawn from (row 0: the root's)."""
+        st = self.seqs[int(sid)]
+        tree.depths(parents)
+        st.drafts = [int(x) for x in tokens]
+        st.zq = [np.asarray(r, dtype=np.float64) for r in zq]
+        st.tree_parents = [int(p) for p in parents]
+
+    def _verify_tree(self, sid: int, st: SeqState, T: float, seed: int, margins: rule.Margins):
+        """Target logits of every tree node by the plain causal forward over the
+        node's path (the root row first), then the tree rule; the cache then
+        holds the pending token and the accepted path."""
+        n, parents = st.n, st.tree_parents
+
+        def copy(kv):
+            return KVList(kv.n_layers, [None if x is None else x.copy() for x in kv.K],
+                          [None if x is None else x.copy() for x in kv.V])
+
+        def path_tokens(i):
+            out = []
+            while i >= 0:
+                out.append(st.drafts[i])
+                i = parents[i]
+            return out[::-1]
+
+        root_kv = copy(st.kv_t)
+        rows = [self.target.forward(root_kv, [st.history[-1]], [n])[0]]
+        for i in range(len(parents)):
+            pt = path_tokens(i)
+            rows.append(self.target.forward(copy(root_kv), pt, n + 1 + np.arange(len(pt)))[-1])
+        zp = np.stack(rows)
+        res = tree.verify_tree(zp, np.stack(st.zq), parents, st.drafts, T, seed, sid, n, margins)
+        acc = [st.drafts[i] for i in res.path]
+        if acc:
+            self.target.forward(root_kv, acc, n + 1 + np.arange(len(acc)), logits=False)
+        st.kv_t = root_kv
+        return res, zp
+
     def verify(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int,
                margins: rule.Margins = rule.Margins()):
-        """Returns a list of (VerifyResult, target logits [k+1, V])."""
+        """Returns a list of (VerifyResult or TreeResult, target logits [k+1, V])."""
         out = []
         for sid, T in zip(seq_ids, temps):
             sid = int(sid)
             st = self.seqs[sid]
             n, k = st.n, len(st.drafts)
             self.pool_t.ensure(sid, n + k + 1)
+            if st.tree_parents is not None:
+                out.append(self._verify_tree(sid, st, float(T), seed, margins))
+                continue
             rows = [st.history[-1]] + st.drafts
             zp = self.target.forward(st.kv_t, rows, n + np.arange(k + 1))
             zq = np.stack(st.zq) if k else np.zeros((0, zp.shape[1]))
@@ -167,7 +211,7 @@ class Session:
                 new_d = min(st.kv_d.length, new_t)
                 st.kv_d.truncate(new_d)
                 self.pool_d.truncate(sid, new_d)
-            st.drafts, st.zq, st.draft_excluded = [], [], False
+            st.drafts, st.zq, st.draft_excluded, st.tree_parents = [], [], False, None
 
     def rollback(self, sid: int, new_len: int):
         """Truncate both caches to ``new_len`` positions; history[new_len] becomes
@@ -180,7 +224,7 @@ class Session:
         if st.kv_d is not None:
             st.kv_d.truncate(min(st.kv_d.length, new_len))
             self.pool_d.truncate(int(sid), st.kv_d.length)
-        st.drafts, st.zq, st.draft_excluded = [], [], False
+        st.drafts, st.zq, st.draft_excluded, st.tree_parents = [], [], False, None
 
     def decode(self, seq_ids: Sequence[int], temps: Sequence[float], seed: int, steps: int,
                margins: rule.Margins = rule.Margins()):
