@@ -216,6 +216,30 @@ SPEC_API spec_status spec_target_forward(spec_ctx* ctx, int32_t n, const int64_t
 SPEC_API spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k,
                                      const int32_t* tokens, const float* q_logits, void* stream);
 
+/* Replace a sequence's drafts by a draft tree (tree / multi-candidate
+ * verification, which the paper's Section 2 lists among the variants of
+ * speculative decoding): m nodes (1 <= m <= k_max), node i with token
+ * tokens[i] and parent parents[i] (-1: the pending token x_n; otherwise a
+ * node with a smaller index), so that node i stands at position n + its depth;
+ * siblings are tried in index order.  q_logits: device fp32 [m + 1, vocab],
+ * row 0 the draft logits the root's children were drawn from and row i + 1
+ * those of node i's children (rows of leaves are not read); it must stay
+ * alive until the verify has run.  The next spec_verify feeds x_n and every
+ * node (node i's K/V at cache index n + 1 + i, each row attending to the
+ * committed cache and its own ancestors), then applies multi-step speculative
+ * sampling: at each node, children are accepted with probability
+ * min(1, r(x) / q(x)) (uniform of candidate j: ACCEPT noise block j at
+ * position n + depth + 1), r becoming norm(max(0, r - q)) after each
+ * rejection; when every child of a node is rejected a token is drawn from r
+ * (RESAMPLE noise), at a leaf from p (BONUS noise); greedy follows the child
+ * whose token is the argmax.  n_accepted is the accepted depth, out_tokens
+ * the accepted path's tokens and the drawn one; spec_kv_commit moves the
+ * accepted nodes' K/V to positions n + 1 .. n + a.  A chain (parents[i] =
+ * i - 1) gives exactly the results of spec_set_drafts.  Also allowed in a
+ * decode-only context (the drafts need no draft model). */
+SPEC_API spec_status spec_set_draft_tree(spec_ctx* ctx, int64_t seq_id, int32_t m, const int32_t* parents,
+                                         const int32_t* tokens, const float* q_logits, void* stream);
+
 /* Verify: feed [x_n, x~_1..x~_k] at positions n..n+k through the target (their
  * K/V are written to the cache first, then each row attends causally), produce
  * fp32 logits, and apply the speculative sampling rule per sequence with its

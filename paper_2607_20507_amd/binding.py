@@ -69,6 +69,7 @@ SIGNATURES = {
     "spec_prefill": (c_int32, [_P, c_int32, _I64P, _I32P, _I32P, _P]),
     "spec_draft_step": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _P]),
     "spec_set_drafts": (c_int32, [_P, c_int64, c_int32, _I32P, _P, _P]),
+    "spec_set_draft_tree": (c_int32, [_P, c_int64, c_int32, _I32P, _I32P, _P, _P]),
     "spec_verify": (c_int32, [_P, c_int32, _I64P, _F32P, c_uint64, _I32P, _I32P, _P]),
     "spec_kv_commit": (c_int32, [_P, c_int32, _I64P, _I32P, _P]),
     "spec_kv_rollback": (c_int32, [_P, c_int64, c_int32, _P]),
@@ -232,6 +233,14 @@ def spec_set_drafts(ctx: int, seq_id: int, tokens, q_logits, stream=None):
     tk = _i32(tokens)
     check(lib().spec_set_drafts(ctx, int(seq_id), len(tk), _ptr(tk, _I32P), dptr(q_logits),
                                 stream_ptr(stream)), ctx)
+
+
+def spec_set_draft_tree(ctx: int, seq_id: int, parents, tokens, q_logits, stream=None):
+    """q_logits: device fp32 [m + 1, V] (row 0 the root's children's draft logits)."""
+    pa = _i32(parents)
+    tk = _i32(tokens)
+    check(lib().spec_set_draft_tree(ctx, int(seq_id), len(tk), _ptr(pa, _I32P), _ptr(tk, _I32P), dptr(q_logits),
+                                    stream_ptr(stream)), ctx)
 
 
 def spec_verify(ctx: int, seq_ids, temperature, seed: int, k_max: int, stream=None):

@@ -30,6 +30,12 @@ struct AttnArgs {
   void* out;             // [R, Hq * hd]
   float* part_o;         // [parts][Hkv][64][hd]
   float* part_ml;        // [parts][Hkv][64][2]
+  // Tree verification (optional, per row): row r sees cache indices
+  // 0..tree_base[r] and tree_base[r] + 1 + j for every bit j of
+  // tree_mask[r] (its ancestors and itself in the draft tree) instead of
+  // 0..its position.  Null: causal by position.
+  const int32_t* tree_base = nullptr;
+  const uint32_t* tree_mask = nullptr;
 };
 
 // bf16: items/groups as above, nt = 16-wide query-vector tiles per item
@@ -40,11 +46,12 @@ hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int
                                  const AttnGroup* d_groups, int n_groups, int nt, int w, hipStream_t st);
 
 // fp32: one wave per (row, head); row r of sequence slot row_seq[r] at
-// position row_pos[r] attends keys 0..row_pos[r].
+// position row_pos[r] attends keys 0..row_pos[r] (or its tree keys).
 hipError_t launch_attention_f32(const AttnArgs& a, int R, const int32_t* d_row_seq,
                                 const int32_t* d_row_pos, hipStream_t st);
 
-// Profiler name of the bf16 attention kernel for (hd, nt, w).
-const char* attn_kernel_name(int hd, int nt, int w);
+// Profiler name of the bf16 attention kernel for (hd, nt, w), the tree-masked
+// variant with `tree`.
+const char* attn_kernel_name(int hd, int nt, int w, bool tree = false);
 
 }  // namespace spec

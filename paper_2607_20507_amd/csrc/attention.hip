@@ -22,6 +22,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 
 #include "attention.h"
 #include "common.h"
@@ -40,8 +41,8 @@ __device__ __forceinline__ uint32_t mask_pair(uint32_t w, int valid) {
 // W waves per workgroup share one work item: wave w takes the 32-key chunks
 // w, w + W, ... of the item's key range, and the waves' softmax states are
 // merged through LDS at the end (exact rescaling by exp2(m_w - m)).
-template <int HD, int NT, int W>
-__global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
+template <int HD, int NT, int W, bool TREE>
+__device__ __forceinline__ void attn_bf16_body(const AttnArgs& a, const AttnItem* __restrict__ items) {
   constexpr int DS = HD / 32;   // MFMA k-steps over the head dim
   constexpr int DT = HD / 16;   // 16-dim output tiles
   const AttnItem it = items[blockIdx.x];
@@ -68,13 +69,21 @@ __global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_bf16_kernel(Attn
 
   uint4 qf[NT][DS];
   int vpos[NT];
+  uint32_t tmask[NT];
   bool vval[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int m = 16 * nt + l16;
     vval[nt] = m < M;
     const int mm = vval[nt] ? m : 0;
-    vpos[nt] = it.pos0 + mm / G;
+    if constexpr (TREE) {
+      // vpos: the last index every row sees; beyond it the tree's bits
+      vpos[nt] = a.tree_base[it.row0 + mm / G];
+      tmask[nt] = a.tree_mask[it.row0 + mm / G];
+    } else {
+      vpos[nt] = it.pos0 + mm / G;
+      tmask[nt] = 0u;
+    }
     const bf16_t* base =
         q + (static_cast<size_t>(it.row0 + mm / G) * a.Hq + gkv * G + mm % G) * HD + g * 8;
 #pragma unroll
@@ -149,7 +158,13 @@ __global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_bf16_kernel(Attn
       for (int j = 0; j < 8; ++j) {
         const int t = c0 + 8 * g + j;
         const float raw = (j < 4) ? sc[nt][0][j] : sc[nt][1][j - 4];
-        const bool ok = vval[nt] && t < it.t1 && t <= vpos[nt];
+        bool ok = vval[nt] && t < it.t1;
+        if constexpr (TREE) {
+          const int rel = t - vpos[nt];
+          ok = ok && (rel <= 0 || (rel <= 32 && ((tmask[nt] >> (rel - 1)) & 1u)));
+        } else {
+          ok = ok && t <= vpos[nt];
+        }
         sv[j] = ok ? raw * scale : -INFINITY;
       }
       float mx = sv[0];
@@ -297,6 +312,18 @@ struct CombVec<4> {
   }
 };
 
+template <int HD, int NT, int W>
+__global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
+  attn_bf16_body<HD, NT, W, false>(a, items);
+}
+
+// The same with the rows' tree masks (tree verification).
+template <int HD, int NT, int W>
+__global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_tree_bf16_kernel(AttnArgs a,
+                                                                                  const AttnItem* __restrict__ items) {
+  attn_bf16_body<HD, NT, W, true>(a, items);
+}
+
 template <int HD, int DPT>
 __global__ __launch_bounds__(HD / DPT * kCombineQv) void attn_combine_kernel(AttnArgs a,
                                                                               const AttnGroup* __restrict__ groups) {
@@ -383,7 +410,12 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, const int32_t*
                                                       const int32_t* __restrict__ row_pos) {
   const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int G = a.Hq / a.Hkv, gkv = h / G;
-  const int pos = row_pos[r];
+  // causal by position, or the row's tree keys: 0..base and base + 1 + j for
+  // the bits j of its mask
+  const bool tree = a.tree_base != nullptr;
+  const int base = tree ? a.tree_base[r] : row_pos[r];
+  const uint32_t tm = tree ? a.tree_mask[r] : 0u;
+  const int tlim = base + 1 + (tm ? 32 - __clz(static_cast<int>(tm)) : 0);
   const int32_t* pt = a.page_table + static_cast<size_t>(row_seq[r]) * a.max_pages;
   const float* kp = static_cast<const float*>(a.kpool);
   const float* vp = static_cast<const float*>(a.vpool);
@@ -397,7 +429,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, const int32_t*
   float m = -INFINITY, l = 0.f, acc[HD];
 #pragma unroll
   for (int d = 0; d < HD; ++d) acc[d] = 0.f;
-  for (int t = lane; t <= pos; t += kWave) {
+  for (int t = lane; t < tlim; t += kWave) {
+    if (t > base && !((tm >> (t - base - 1)) & 1u)) continue;
     const size_t pb = static_cast<size_t>(pt[t >> 4] * a.Hkv + gkv);
     const float* kr = kp + (pb * 16 + (t & 15)) * HD;
     float s = 0.f;
@@ -434,6 +467,12 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, const int32_t*
 
 template <int HD, int NT>
 void launch_item_kernel(const AttnArgs& a, const AttnItem* items, dim3 grid, int w, hipStream_t st) {
+  if (a.tree_base) {
+    if (w >= 4) launch_kernel(attn_tree_bf16_kernel<HD, NT, 4>, grid, dim3(4 * kWave), 0, st, a, items);
+    else if (w == 2) launch_kernel(attn_tree_bf16_kernel<HD, NT, 2>, grid, dim3(2 * kWave), 0, st, a, items);
+    else launch_kernel(attn_tree_bf16_kernel<HD, NT, 1>, grid, dim3(kWave), 0, st, a, items);
+    return;
+  }
   if (w >= 4) launch_kernel(attn_bf16_kernel<HD, NT, 4>, grid, dim3(4 * kWave), 0, st, a, items);
   else if (w == 2) launch_kernel(attn_bf16_kernel<HD, NT, 2>, grid, dim3(2 * kWave), 0, st, a, items);
   else launch_kernel(attn_bf16_kernel<HD, NT, 1>, grid, dim3(kWave), 0, st, a, items);
@@ -458,7 +497,20 @@ hipError_t launch_bf16_hd(const AttnArgs& a, const AttnItem* items, int n_items,
 
 }  // namespace
 
-const char* attn_kernel_name(int hd, int nt, int w) {
+const char* attn_kernel_name(int hd, int nt, int w, bool tree) {
+  if (tree) {
+    static char tnames[2][3][3][48];
+    static bool init = false;
+    if (!init) {
+      for (int h = 0; h < 2; ++h)
+        for (int i = 0; i < 3; ++i)
+          for (int j = 0; j < 3; ++j)
+            snprintf(tnames[h][i][j], sizeof(tnames[h][i][j]), "attn_tree_bf16_kernel<%d, %d, %d>", h ? 128 : 64,
+                     1 << i, i == 2 ? std::min(2, 1 << j) : 1 << j);
+      init = true;
+    }
+    return tnames[hd == 128 ? 1 : 0][nt <= 1 ? 0 : (nt == 2 ? 1 : 2)][w <= 1 ? 0 : (w == 2 ? 1 : 2)];
+  }
   // [hd 64 / 128][nt 1 / 2 / 4][w 1 / 2 / 4]
   static const char* names[2][3][3] = {
       {{"attn_bf16_kernel<64, 1, 1>", "attn_bf16_kernel<64, 1, 2>", "attn_bf16_kernel<64, 1, 4>"},

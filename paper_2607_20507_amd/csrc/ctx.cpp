@@ -74,6 +74,9 @@ struct Seq {
   bool verified = false;
   int a_ver = 0;
   std::vector<int32_t> emitted;
+  // draft tree (spec_set_draft_tree): parent of node i (-1: the pending
+  // token), empty for a chain; the accepted nodes after a verify
+  std::vector<int32_t> tparent, tpath;
   int n() const { return static_cast<int>(hist.size()) - 1; }
 };
 
@@ -87,6 +90,8 @@ struct Ws {
 // Host description of one forward launch.
 struct Fwd {
   std::vector<int32_t> tok_src, pos, slot, seqi;
+  std::vector<int32_t> tbase;   // tree verification: per row, the last cache index all of it sees
+  std::vector<uint32_t> tmask;  // and the tree slots beyond it (bit j: index tbase + 1 + j)
   std::vector<AttnSegment> segs;
   std::vector<int32_t> ptab;
   int ptab_stride = 1;
@@ -94,7 +99,8 @@ struct Fwd {
 };
 
 struct FwdOff {
-  size_t tok, pos, slot, seqi, pt, items, groups, lmr, lmm;
+  size_t tok, pos, slot, seqi, pt, items, groups, lmr, lmm, tb = 0, tm = 0;
+  bool tree = false;
   int n_items = 0, n_groups = 0, nt = 1, w = 1, R = 0, n_lm = 0, ptab_stride = 1;
   bool lm_map = false;
   double attn_keys = 0, attn_qk = 0;  // sum of context lengths; sum over rows of (pos + 1)
@@ -151,8 +157,9 @@ struct spec_ctx {
   std::priority_queue<int, std::vector<int>, std::greater<int>> free_slots;
   Stager stager;
   int meta_next = 0;
-  // pinned, written by the decision pass's last kernel itself: n_acc [max_seqs]
-  // then tokens [max_seqs * (k_max + 1)]; h_out_dev is its device address
+  // pinned, written by the decision pass's last kernel itself: n_acc [max_seqs],
+  // tokens [max_seqs * (k_max + 1)], then the accepted tree nodes
+  // [max_seqs * k_max]; h_out_dev is its device address
   int32_t* h_out = nullptr;
   int32_t* h_out_dev = nullptr;
   hipEvent_t out_ev = nullptr;
@@ -237,7 +244,8 @@ void compute_ws(spec_ctx* c) {
   w.splitk = take(w.splitk_bytes);
   // metadata bound for one call
   size_t mc = 0;
-  mc += 6 * align_up(R * 4);
+  mc += 8 * align_up(R * 4);  // tokens, positions, slots, rows, LM rows and map; tree bases and masks
+  mc += align_up(R * sizeof(VTreeNode));
   mc += align_up(static_cast<size_t>(c->max_seqs) * c->max_pages * 4);
   mc += align_up((R + kMaxParts) * sizeof(AttnItem)) + align_up(R * sizeof(AttnGroup));
   mc += align_up(static_cast<size_t>(vrows) * sizeof(VRow)) + align_up(c->max_seqs * sizeof(VSeq));
@@ -289,6 +297,11 @@ FwdOff add_forward(spec_ctx* ctx, const Model& M, const Fwd& f, MetaBlock& mb) {
     o.attn_keys += s.pos0 + s.nrows;
     for (int r = 0; r < s.nrows; ++r) o.attn_qk += s.pos0 + r + 1;
   }
+  if (!f.tbase.empty()) {
+    o.tree = true;
+    o.tb = mb.add(f.tbase);
+    o.tm = mb.add(f.tmask);
+  }
   o.n_lm = static_cast<int>(f.lm_rows.size());
   o.lmr = mb.add(f.lm_rows);
   o.lm_map = !f.lm_map.empty();
@@ -330,6 +343,10 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
   a.out = ob;
   a.part_o = wsptr<float>(ctx, ctx->ws.part_o);
   a.part_ml = wsptr<float>(ctx, ctx->ws.part_ml);
+  if (o.tree) {
+    a.tree_base = I(o.tb);
+    a.tree_mask = reinterpret_cast<const uint32_t*>(dev + o.tm);
+  }
   EventTimer& tm = ctx->timer;
   const double esz = M.esz;
   // GEMM launch, timed when selected: algorithmic bytes = weights + inputs +
@@ -378,7 +395,7 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
     a.vpool = M.vl(l);
     if (dt == 1) {
       // bytes: every cached key and value once, queries in, output out
-      const bool timed = tm.wants(attn_kernel_name(d.head_dim, o.nt, o.w));
+      const bool timed = tm.wants(attn_kernel_name(d.head_dim, o.nt, o.w, o.tree));
       if (timed) tm.begin(st);
       HIPC(launch_attention_bf16(a, reinterpret_cast<const AttnItem*>(dev + o.items), o.n_items,
                                  reinterpret_cast<const AttnGroup*>(dev + o.groups), o.n_groups,
@@ -538,7 +555,8 @@ void key_forward(std::vector<int64_t>& k, const FwdOff& o) {
                        static_cast<int64_t>(o.slot), static_cast<int64_t>(o.seqi),
                        static_cast<int64_t>(o.pt), static_cast<int64_t>(o.items),
                        static_cast<int64_t>(o.groups), static_cast<int64_t>(o.lmr),
-                       static_cast<int64_t>(o.lmm)};
+                       static_cast<int64_t>(o.lmm), o.tree, static_cast<int64_t>(o.tb),
+                       static_cast<int64_t>(o.tm)};
   k.insert(k.end(), std::begin(v), std::end(v));
 }
 
@@ -574,6 +592,31 @@ spec_status launch_clears(spec_ctx* ctx, const std::vector<int32_t>& ct, const s
     b.slots = reinterpret_cast<const int32_t*>(dev + od);
   }
   HIPC(launch_kv_clear(T.dt(), a, b, st));  // one launch for both pools
+  return SPEC_OK;
+}
+
+// The accepted path of tree verifications to consecutive cache positions:
+// mv holds (src, dst) slot pairs, off the group (sequence) boundaries.
+spec_status launch_moves(spec_ctx* ctx, const std::vector<int32_t>& mv, const std::vector<int32_t>& off,
+                         hipStream_t st) {
+  if (mv.empty()) return SPEC_OK;
+  MetaBlock mb;
+  const size_t op = mb.add(mv), oo = mb.add(off);
+  char* dev = nullptr;
+  spec_status s = upload_meta(ctx, mb, st, &dev);
+  if (s != SPEC_OK) return s;
+  const Model& T = ctx->m[0];
+  KvMoveJob j;
+  j.pairs = reinterpret_cast<const int32_t*>(dev + op);
+  j.off = reinterpret_cast<const int32_t*>(dev + oo);
+  j.n_groups = static_cast<int>(off.size()) - 1;
+  j.kv = T.kv;
+  j.n_layers = T.d.n_layers;
+  j.layer_stride = T.layer_stride;
+  j.v_off = T.v_off;
+  j.Hkv = T.d.n_kv_heads;
+  j.hd = T.d.head_dim;
+  HIPC(launch_kv_move(T.dt(), j, st));
   return SPEC_OK;
 }
 
@@ -644,7 +687,7 @@ spec_status spec_ctx_create(const spec_model_desc* target, const spec_model_desc
   compute_ws(c);
   // coherent: the kernel's stores go straight to host memory
   hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&c->h_out),
-                               sizeof(int32_t) * c->max_seqs * (c->k_max + 2), hipHostMallocCoherent);
+                               sizeof(int32_t) * c->max_seqs * (2 * c->k_max + 2), hipHostMallocCoherent);
   if (e == hipSuccess) e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->h_out_dev), c->h_out, 0);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->out_ev, hipEventDisableTiming);
   if (e != hipSuccess) {
@@ -1059,7 +1102,6 @@ spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k, const int3
   if (it == ctx->seqs.end()) FAIL(SPEC_E_INVALID, "unknown seq_id");
   Seq& s = it->second;
   if (k < 0 || k > ctx->k_max || (k > 0 && (!tokens || !q_logits))) FAIL(SPEC_E_INVALID, "bad drafts");
-  if (k > 0 && ctx->n_models < 2) FAIL(SPEC_E_STATE, "context has no draft model");
   if (s.verified) FAIL(SPEC_E_STATE, "set_drafts after verify without commit");
   if (s.k > 0 && !s.external) FAIL(SPEC_E_STATE, "sequence already has drafts from spec_draft_step");
   for (int j = 0; j < k; ++j)
@@ -1070,10 +1112,37 @@ spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k, const int3
   s.external = k > 0;
   s.qrow.clear();
   s.dsrc.clear();
+  s.tparent.clear();
   for (int j = 0; j < k; ++j) {
     s.qrow.push_back(q_logits + static_cast<size_t>(j) * ctx->V);
     s.dsrc.push_back(tokens[j]);
   }
+  return SPEC_OK;
+}
+
+spec_status spec_set_draft_tree(spec_ctx* ctx, int64_t seq_id, int32_t m, const int32_t* parents,
+                                const int32_t* tokens, const float* q_logits, void* stream) {
+  CHECK_READY();
+  (void)stream;
+  auto it = ctx->seqs.find(seq_id);
+  if (it == ctx->seqs.end()) FAIL(SPEC_E_INVALID, "unknown seq_id");
+  Seq& s = it->second;
+  if (m < 1 || m > ctx->k_max || !parents || !tokens || !q_logits) FAIL(SPEC_E_INVALID, "bad draft tree");
+  if (s.verified) FAIL(SPEC_E_STATE, "set_draft_tree after verify without commit");
+  if (s.k > 0 && !s.external) FAIL(SPEC_E_STATE, "sequence already has drafts from spec_draft_step");
+  for (int i = 0; i < m; ++i) {
+    if (parents[i] < -1 || parents[i] >= i) FAIL(SPEC_E_INVALID, "parents[i] must be in -1 .. i - 1");
+    if (tokens[i] < 0 || tokens[i] >= ctx->V) FAIL(SPEC_E_INVALID, "draft token out of range");
+  }
+  if (ctx->V % 4 == 0 && (reinterpret_cast<uintptr_t>(q_logits) & 15))
+    FAIL(SPEC_E_INVALID, "draft logits must be 16-byte aligned");
+  s.k = m;
+  s.external = true;
+  s.qrow.clear();
+  s.dsrc.clear();
+  for (int i = 0; i <= m; ++i) s.qrow.push_back(q_logits + static_cast<size_t>(i) * ctx->V);
+  s.dsrc.assign(tokens, tokens + m);
+  s.tparent.assign(parents, parents + m);
   return SPEC_OK;
 }
 
@@ -1099,15 +1168,33 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
     need += T.pool.need(s.pages_t, s.n() + s.k + 1);
   }
   if (need > T.pool.free_pages()) FAIL(SPEC_E_NOPAGES, "target KV page pool exhausted");
+  // a batch with a draft tree runs the tree-masked attention and the tree
+  // decision for all of its sequences (a chain is the tree parents[i] = i - 1)
+  bool tree_mode = false;
+  int R_all = 0;  // rows of the call: the tree decision's q rows follow them
+  for (int i = 0; i < n; ++i) {
+    tree_mode = tree_mode || !ctx->seqs[seq_ids[i]].tparent.empty();
+    R_all += ctx->seqs[seq_ids[i]].k + 1;
+  }
   Fwd f;
   std::vector<const std::vector<int32_t>*> tabs;
-  std::vector<VRow> prow, qrow;
+  std::vector<VRow> prow, qrow, tq;
   std::vector<VSeq> vs;
+  std::vector<VTreeSeq> ts;
+  std::vector<VTreeNode> tn;
   float* logits = wsptr<float>(ctx, ctx->ws.logits);
   for (int i = 0; i < n; ++i) {
     Seq& s = ctx->seqs[seq_ids[i]];
     const int nn = s.n();
     T.pool.ensure(s.pages_t, nn + s.k + 1);
+    // parent and depth of each draft node (chain: the previous draft)
+    std::vector<int32_t> par(s.k), dep(s.k);
+    std::vector<uint32_t> anc(s.k);
+    for (int j = 0; j < s.k; ++j) {
+      par[j] = s.tparent.empty() ? j - 1 : s.tparent[j];
+      dep[j] = par[j] < 0 ? 1 : dep[par[j]] + 1;
+      anc[j] = (par[j] < 0 ? 0u : anc[par[j]]) | (1u << j);
+    }
     tabs.push_back(&s.pages_t);
     const int row0 = static_cast<int>(f.tok_src.size());
     f.segs.push_back(AttnSegment{i, row0, s.k + 1, nn});
@@ -1123,37 +1210,77 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
     q.seq_lo = static_cast<uint32_t>(static_cast<uint64_t>(s.id));
     q.seq_hi = static_cast<uint32_t>(static_cast<uint64_t>(s.id) >> 32);
     vs.push_back(q);
+    // row r: the pending token (r = 0) or draft node r - 1, at position n +
+    // its depth; its K/V go to cache index n + r
     for (int r = 0; r <= s.k; ++r) {
-      const int pos = nn + r;
       f.tok_src.push_back(r == 0 ? s.hist[nn] : s.dsrc[r - 1]);
-      f.pos.push_back(pos);
-      f.slot.push_back(T.pool.slot(s.pages_t, pos));
+      f.pos.push_back(nn + (r == 0 ? 0 : dep[r - 1]));
+      f.slot.push_back(T.pool.slot(s.pages_t, nn + r));
       f.seqi.push_back(i);
       f.lm_rows.push_back(row0 + r);
+      if (tree_mode) {
+        f.tbase.push_back(nn);
+        f.tmask.push_back(r == 0 ? 0u : anc[r - 1]);
+      }
       prow.push_back(VRow{logits + static_cast<size_t>(row0 + r) * ctx->V, it, t > 0.f ? 0 : 1});
     }
-    for (int j = 0; j < s.k; ++j) qrow.push_back(VRow{s.qrow[j], it, t > 0.f ? 0 : 1});
+    if (tree_mode) {
+      // q row of a node with children: the row its children were drawn from
+      // (chain drafts: draft j + 1's row for node j - 1; trees: row u + 1)
+      std::vector<char> kids(s.k + 1, 0);
+      for (int j = 0; j < s.k; ++j) kids[par[j] + 1] = 1;
+      auto qidx = [&](int u) -> int32_t {  // u = -1: the root
+        if (!kids[u + 1]) return -1;
+        tq.push_back(VRow{s.qrow[u + 1], it, t > 0.f ? 0 : 1});
+        return R_all + static_cast<int32_t>(tq.size()) - 1;
+      };
+      VTreeSeq tsq{};
+      tsq.m = s.k;
+      tsq.node0 = static_cast<int32_t>(tn.size());
+      tsq.p_row = row0;
+      tsq.q_row = qidx(-1);
+      tsq.base_pos = nn;
+      tsq.t = t;
+      tsq.seq_lo = q.seq_lo;
+      tsq.seq_hi = q.seq_hi;
+      ts.push_back(tsq);
+      for (int j = 0; j < s.k; ++j) tn.push_back(VTreeNode{par[j], row0 + 1 + j, qidx(j), 0});
+    } else {
+      for (int j = 0; j < s.k; ++j) qrow.push_back(VRow{s.qrow[j], it, t > 0.f ? 0 : 1});
+    }
     s.written_t = std::max(s.written_t, nn + s.k + 1);
   }
   const int R = static_cast<int>(f.tok_src.size());
   for (auto& q : vs) q.q_row += R;
   std::vector<VRow> rows = prow;
   rows.insert(rows.end(), qrow.begin(), qrow.end());
+  rows.insert(rows.end(), tq.begin(), tq.end());
   build_ptab(tabs, f, ctx->max_pages);
   MetaBlock mb;
   FwdOff o = add_forward(ctx, T, f, mb);
-  const size_t orow = mb.add(rows), oseq = mb.add(vs);
+  const size_t orow = mb.add(rows), oseq = tree_mode ? mb.add(ts) : mb.add(vs);
+  const size_t onode = mb.add(tn);
   const size_t osd = mb.add(&seed, 1);
   // the decision pass writes its outputs into pinned host memory (no copies)
   int32_t* d_nacc = ctx->h_out_dev;
   int32_t* d_otok = ctx->h_out_dev + ctx->max_seqs;
+  int32_t* d_opath = ctx->h_out_dev + ctx->max_seqs * (ctx->k_max + 2);
   const VocabPlan vp = vocab_plan(n, static_cast<int>(rows.size()), ctx->V);
   std::vector<int64_t> key = {decide ? 0 : 2, n, static_cast<int64_t>(rows.size()), static_cast<int64_t>(orow),
-                              static_cast<int64_t>(oseq), static_cast<int64_t>(osd)};
+                              static_cast<int64_t>(oseq), static_cast<int64_t>(osd), tree_mode,
+                              static_cast<int64_t>(onode)};
   key_forward(key, o);
   spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
     spec_status r = launch_forward(ctx, T, o, dev, logits, ls);
     if (r != SPEC_OK || !decide) return r;
+    if (tree_mode) {
+      HIPC(launch_tree_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
+                            reinterpret_cast<const VTreeSeq*>(dev + oseq),
+                            reinterpret_cast<const VTreeNode*>(dev + onode), wsptr<int32_t>(ctx, ctx->ws.rowtok),
+                            seed, reinterpret_cast<const uint64_t*>(dev + osd), ctx->k_max, d_nacc, d_otok,
+                            d_opath, ctx->wsp + ctx->ws.vocab, ls, &ctx->timer));
+      return SPEC_OK;
+    }
     HIPC(launch_vocab_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
                            reinterpret_cast<const VSeq*>(dev + oseq), wsptr<int32_t>(ctx, ctx->ws.rowtok),
                            seed, ctx->k_max, d_nacc, d_otok, ctx->wsp + ctx->ws.vocab, ls, &ctx->timer,
@@ -1174,11 +1301,16 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   }
   std::memcpy(n_accepted, ctx->h_out, sizeof(int32_t) * n);
   std::memcpy(out_tokens, ctx->h_out + ctx->max_seqs, sizeof(int32_t) * n * W);
+  const int32_t* h_path = ctx->h_out + ctx->max_seqs * (ctx->k_max + 2);
   for (int i = 0; i < n; ++i) {
     Seq& q = ctx->seqs[seq_ids[i]];
     q.verified = true;
     q.a_ver = n_accepted[i];
     q.emitted.assign(out_tokens + i * W, out_tokens + i * W + q.a_ver + 1);
+    if (tree_mode)
+      q.tpath.assign(h_path + static_cast<size_t>(i) * ctx->k_max, h_path + static_cast<size_t>(i) * ctx->k_max + q.a_ver);
+    else
+      q.tpath.clear();
   }
   ctx->timer.flush();
   return SPEC_OK;
@@ -1256,11 +1388,19 @@ spec_status spec_kv_commit(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, con
     if (!s.verified) FAIL(SPEC_E_STATE, "commit without verify");
     if (n_accepted[i] < 0 || n_accepted[i] > s.a_ver) FAIL(SPEC_E_INVALID, "n_accepted outside 0..verified count");
   }
-  std::vector<int32_t> ct, cd;
+  std::vector<int32_t> ct, cd, mv, moff{0};
   for (int i = 0; i < n; ++i) {
     Seq& s = ctx->seqs[seq_ids[i]];
     const int a = n_accepted[i];
     const int nn = s.n();
+    // a tree's accepted nodes sit at cache indices n + 1 + node: they move to
+    // n + 1 .. n + a, in order (an earlier move never overwrites a later source)
+    for (int j = 0; j < a && j < static_cast<int>(s.tpath.size()); ++j)
+      if (s.tpath[j] != j) {
+        mv.push_back(ctx->m[0].pool.slot(s.pages_t, nn + 1 + s.tpath[j]));
+        mv.push_back(ctx->m[0].pool.slot(s.pages_t, nn + 1 + j));
+      }
+    if (static_cast<int>(mv.size()) / 2 > moff.back()) moff.push_back(static_cast<int32_t>(mv.size() / 2));
     s.hist.insert(s.hist.end(), s.emitted.begin(), s.emitted.begin() + a + 1);
     const int new_t = nn + a + 1;
     const int new_d = std::min(s.len_d, new_t);
@@ -1276,7 +1416,11 @@ spec_status spec_kv_commit(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, con
     s.external = false;
     s.verified = false;
     s.emitted.clear();
+    s.tparent.clear();
+    s.tpath.clear();
   }
+  spec_status r = launch_moves(ctx, mv, moff, st);
+  if (r != SPEC_OK) return r;
   return launch_clears(ctx, ct, cd, st);
 }
 
@@ -1344,6 +1488,8 @@ spec_status spec_kv_rollback(spec_ctx* ctx, int64_t seq_id, int32_t new_len, voi
   s.external = false;
   s.verified = false;
   s.emitted.clear();
+  s.tparent.clear();
+  s.tpath.clear();
   return launch_clears(ctx, ct, cd, st);
 }
 

@@ -47,4 +47,20 @@ struct KvClearJob {
 // Both jobs (the target's and the drafter's pool, same dtype) in one launch.
 hipError_t launch_kv_clear(int dtype, const KvClearJob& a, const KvClearJob& b, hipStream_t st);
 
+// Moves of K/V cache entries (tree verification: the accepted path's entries
+// go to consecutive positions).  Group g holds the (src slot, dst slot) pairs
+// pairs[2 off[g]] .. pairs[2 off[g + 1] - 1], applied in order: one sequence's
+// moves may read a slot an earlier move of the group wrote, never one a later
+// move writes.  Groups touch disjoint pages.
+struct KvMoveJob {
+  const int32_t* pairs = nullptr;  // device
+  const int32_t* off = nullptr;    // device [n_groups + 1]
+  int n_groups = 0;
+  void* kv = nullptr;
+  int n_layers = 0;
+  size_t layer_stride = 0, v_off = 0;
+  int Hkv = 0, hd = 0;
+};
+hipError_t launch_kv_move(int dtype, const KvMoveJob& j, hipStream_t st);
+
 }  // namespace spec

@@ -310,7 +310,39 @@ __global__ __launch_bounds__(256) void kv_clear_kernel(KvClearJob j0, KvClearJob
   }
 }
 
+// One workgroup per (group, layer); thread e owns element e of every token,
+// so the group's moves, applied in order by each thread, see each other's
+// writes without barriers.
+template <typename T>
+__global__ __launch_bounds__(256) void kv_move_kernel(KvMoveJob j) {
+  const int g = blockIdx.x, l = blockIdx.y;
+  if (g >= j.n_groups || l >= j.n_layers) return;
+  T* K = static_cast<T*>(j.kv) + l * j.layer_stride;
+  T* V = K + j.v_off;
+  const int i0 = j.off[g], i1 = j.off[g + 1];
+  for (int e = threadIdx.x; e < j.Hkv * j.hd; e += blockDim.x) {
+    const int h = e / j.hd, dd = e % j.hd;
+    for (int i = i0; i < i1; ++i) {
+      const int src = j.pairs[2 * i], dst = j.pairs[2 * i + 1];
+      const size_t bs = (static_cast<size_t>(src >> 4) * j.Hkv + h) * 16 * j.hd;
+      const size_t bd = (static_cast<size_t>(dst >> 4) * j.Hkv + h) * 16 * j.hd;
+      K[bd + k_index<T>(dst & 15, dd, j.hd)] = K[bs + k_index<T>(src & 15, dd, j.hd)];
+      V[bd + v_index<T>(dst & 15, dd)] = V[bs + v_index<T>(src & 15, dd)];
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_kv_move(int dtype, const KvMoveJob& j, hipStream_t st) {
+  if (j.n_groups <= 0 || j.n_layers <= 0) return hipSuccess;
+  dim3 grid(j.n_groups, j.n_layers);
+  if (dtype == 0)
+    kv_move_kernel<float><<<grid, 256, 0, st>>>(j);
+  else
+    kv_move_kernel<bf16_t><<<grid, 256, 0, st>>>(j);
+  return hipGetLastError();
+}
 
 hipError_t launch_embed(int dtype, int R, int d, const int32_t* tok_src, const int32_t* tok_pool,
                         const void* E, float* h, int32_t* row_tok, hipStream_t st, void* hb, const void* wn,

@@ -79,6 +79,37 @@ hipError_t launch_vocab_setup(int B, int kmax, const int32_t* d_k, const float* 
                               const int32_t* d_base, const float* d_p, const float* d_q, int V, VRow* d_rows,
                               VSeq* d_seqs, int32_t* d_n_rows, hipStream_t st);
 
+// Tree verification (multi-step speculative sampling over a tree of sampled
+// candidates).  Node i of sequence b is nodes[node0 + i]; its parent is -1
+// (the root: the pending token) or a node with a smaller index, and siblings
+// are tried in index order.  p_row: the node's target row (its token is
+// row_tok[p_row], the token that row was fed); q_row: the row its children
+// were drawn from (-1: no children).  The root's rows are in the sequence
+// record.  A chain of k drafts is the tree parents[i] = i - 1.
+struct VTreeNode {
+  int32_t parent, p_row, q_row, pad;
+};
+struct VTreeSeq {
+  int32_t m, node0, p_row, q_row;
+  int32_t base_pos;
+  float t;
+  uint32_t seq_lo, seq_hi;
+};
+
+// Statistics of every row (p and q), then one workgroup per sequence walks
+// its tree: at a node, children are accepted while v_j q(x) < r(x) fails, r
+// becoming norm(max(0, r - q)) after each rejection (one vocabulary pass
+// each); the walk ends with a draw from r (RESAMPLE noise) at a node whose
+// children were all rejected, or from p (BONUS noise) at a leaf.  Outputs
+// n_acc[B] (accepted depth), out_tok[B * (kmax + 1)] (the path's tokens, then
+// the drawn one, -1 after), out_path[B * kmax] (the accepted node indices,
+// -1 after).  Workspace: vocab_ws_bytes(p).
+hipError_t launch_tree_pass(const VocabPlan& p, const VRow* d_rows, const VTreeSeq* d_seqs,
+                            const VTreeNode* d_nodes, const int32_t* d_row_tok, uint64_t seed,
+                            const uint64_t* d_seed, int kmax,
+                            int32_t* d_n_acc, int32_t* d_out_tok, int32_t* d_out_path, void* d_ws,
+                            hipStream_t st, KernelTimer* timer = nullptr);
+
 struct DraftPlan {
   int n = 0, V = 0, chunk = 0, n_chunks = 0;
 };

@@ -413,6 +413,211 @@ __global__ __launch_bounds__(kWave) void final_kernel(const VSeq* __restrict__ s
   if (l <= kmax) out_tok[static_cast<size_t>(b) * (kmax + 1) + l] = l < d.a ? x : (l == d.a ? t : -1);
 }
 
+// ---------------------------------------------------------------------------
+// Tree verification: one workgroup of kTreeThreads per sequence walks its
+// tree.  At node u the target distribution is r_0 = p_u; each rejected child
+// replaces r_l by r_{l+1} = max(0, r_l - q_u) / Z_{l+1}, where Z_{l+1} is the
+// residual's mass (a vocabulary pass; a residual with no mass keeps r_l), so
+// r_l(y) is evaluated from p_u(y), q_u(y) and Z_1..Z_l alone.
+
+constexpr int kTreeThreads = 1024;
+constexpr int kTreeWaves = kTreeThreads / kWave;
+constexpr int kTreeMaxNodes = 16;
+
+__device__ float tree_block_sum(float v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  const int w = threadIdx.x / kWave;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
+  __syncthreads();
+  float s = 0.f;
+  for (int i = 0; i < kTreeWaves; ++i) s += red[i];  // fixed order
+  return s;
+}
+
+__device__ void tree_block_pick(float& best, int& bi, float* redf, int* redi) {
+  wave_pick(best, bi);
+  const int w = threadIdx.x / kWave;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    redf[w] = best;
+    redi[w] = bi;
+  }
+  __syncthreads();
+  best = -1.f;
+  bi = INT_MAX;
+  for (int i = 0; i < kTreeWaves; ++i) pick_update(redf[i], redi[i], best, bi);
+}
+
+// Merged (max, sum, first argmax) of one row's chunk records, by one wave.
+__device__ void tree_row_stats(const VStat* __restrict__ st, int n_chunks, float it, bool greedy, float& m,
+                               float& s, int& idx) {
+  const int l = threadIdx.x & (kWave - 1);
+  m = -INFINITY;
+  s = 0.f;
+  idx = INT_MAX;
+  if (l < n_chunks) {
+    const VStat v = st[l];
+    m = v.m;
+    s = v.s;
+    idx = v.idx;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, kWave), s2 = __shfl_xor(s, o, kWave);
+    const int i2 = __shfl_xor(idx, o, kWave);
+    stat_merge(m, s, idx, m2, s2, i2, it, greedy);
+  }
+}
+
+__global__ __launch_bounds__(kTreeThreads) void tree_decide_kernel(
+    const VRow* __restrict__ rows, const VTreeSeq* __restrict__ seqs, const VTreeNode* __restrict__ nodes,
+    const int32_t* __restrict__ row_tok, const VStat* __restrict__ stats, int n_chunks, int V, uint64_t seed,
+    const uint64_t* __restrict__ seed_ptr, int kmax, int32_t* __restrict__ n_acc, int32_t* __restrict__ out_tok,
+    int32_t* __restrict__ out_path) {
+  const int b = blockIdx.x, t = threadIdx.x;
+  const VTreeSeq sq = seqs[b];
+  const bool greedy = !(sq.t > 0.f);
+  const float it = rows[sq.p_row].inv_t;
+  const float cs = it * kLog2e;
+  const uint64_t seq_id = (static_cast<uint64_t>(sq.seq_hi) << 32) | sq.seq_lo;
+  const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
+  __shared__ float s_red[kTreeWaves];
+  __shared__ int s_redi[kTreeWaves];
+  __shared__ float s_st[4];  // Mp, Sp, Mq, Sq of the current node
+  __shared__ int s_ip;       // first argmax of p
+  __shared__ float s_invz[kTreeMaxNodes];
+  __shared__ int s_keep[kTreeMaxNodes];
+  __shared__ int s_flag;
+  __shared__ int s_tok[kTreeMaxNodes + 1], s_path[kTreeMaxNodes];
+  int u = -1, d = 0;
+  for (;;) {
+    const int prow = u < 0 ? sq.p_row : nodes[sq.node0 + u].p_row;
+    const int qrow = u < 0 ? sq.q_row : nodes[sq.node0 + u].q_row;
+    if (t < kWave) {
+      float m, s;
+      int idx;
+      tree_row_stats(stats + static_cast<size_t>(prow) * n_chunks, n_chunks, it, greedy, m, s, idx);
+      if (t == 0) {
+        s_st[0] = m;
+        s_st[1] = s;
+        s_ip = idx;
+      }
+    } else if (t < 2 * kWave && !greedy && qrow >= 0) {
+      float m, s;
+      int idx;
+      tree_row_stats(stats + static_cast<size_t>(qrow) * n_chunks, n_chunks, it, greedy, m, s, idx);
+      if (t == kWave) {
+        s_st[2] = m;
+        s_st[3] = s;
+      }
+    }
+    __syncthreads();
+    if (greedy) {
+      const int ip = s_ip;
+      int nxt = -1;
+      for (int i = 0; i < sq.m; ++i) {
+        const VTreeNode nd = nodes[sq.node0 + i];
+        if (nd.parent == u && row_tok[nd.p_row] == ip) {
+          nxt = i;
+          break;
+        }
+      }
+      if (t == 0) {
+        s_tok[d] = ip;
+        if (nxt >= 0) s_path[d] = nxt;
+      }
+      if (nxt < 0) break;
+      u = nxt;
+      ++d;
+      __syncthreads();
+      continue;
+    }
+    const float* zp = rows[prow].ptr;
+    const float mpc = s_st[0] * cs, isp = 1.f / s_st[1];
+    const float* zq = qrow >= 0 ? rows[qrow].ptr : nullptr;
+    const float mqc = s_st[2] * cs, isq = 1.f / s_st[3];
+    // r_lv(y) from p(y), q(y) and the residual normalisers so far
+    auto r_at = [&](int y, int lv) {
+      float r = exp2f(zp[y] * cs - mpc) * isp;
+      if (lv > 0) {
+        const float q = exp2f(zq[y] * cs - mqc) * isq;
+        for (int l = 1; l <= lv; ++l)
+          if (!s_keep[l]) r = fmaxf(r - q, 0.f) * s_invz[l];
+      }
+      return r;
+    };
+    const StreamId sid_acc = stream_id(seq_id, sq.base_pos + d + 1, 1);
+    int lv = 0, acc = -1, j = 0;
+    if (qrow >= 0) {
+      for (int i = 0; i < sq.m; ++i) {
+        const VTreeNode nd = nodes[sq.node0 + i];
+        if (nd.parent != u) continue;
+        if (t == 0) {
+          const int x = row_tok[nd.p_row];
+          bool ok = false;
+          if (static_cast<unsigned>(x) < static_cast<unsigned>(V)) {  // an id outside the vocabulary is rejected
+            const float r = r_at(x, lv);
+            const float qx = exp2f(zq[x] * cs - mqc) * isq;
+            const float v = u01(philox_block(key, sid_acc, static_cast<uint32_t>(j)).x);
+            ok = v * qx < r;
+          }
+          s_flag = ok;
+        }
+        __syncthreads();
+        if (s_flag) {
+          acc = i;
+          break;
+        }
+        ++lv;
+        float part = 0.f;
+        for (int y = t; y < V; y += kTreeThreads) {
+          const float q = exp2f(zq[y] * cs - mqc) * isq;
+          part += fmaxf(r_at(y, lv - 1) - q, 0.f);
+        }
+        const float z = tree_block_sum(part, s_red);
+        if (t == 0) {
+          s_keep[lv] = !(z > 0.f);
+          s_invz[lv] = z > 0.f ? 1.f / z : 1.f;
+        }
+        __syncthreads();
+        ++j;
+      }
+    }
+    if (acc >= 0) {
+      if (t == 0) {
+        s_tok[d] = row_tok[nodes[sq.node0 + acc].p_row];
+        s_path[d] = acc;
+      }
+      u = acc;
+      ++d;
+      __syncthreads();
+      continue;
+    }
+    // the draw: from r_lv after rejections (RESAMPLE), from p at a leaf
+    // (BONUS), by exponential race over 4 tokens per Philox block
+    const StreamId sid = stream_id(seq_id, sq.base_pos + d + 1, qrow >= 0 ? 2 : 3);
+    float best = -1.f;
+    int bi = INT_MAX;
+    for (int y4 = t; 4 * y4 < V; y4 += kTreeThreads) {
+      const uint4 w = philox_block(key, sid, static_cast<uint32_t>(y4));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int y = 4 * y4 + e;
+        if (y < V) pick_update(r_at(y, lv) / exp2_variate(word_of(w, e)), y, best, bi);
+      }
+    }
+    tree_block_pick(best, bi, s_red, s_redi);
+    if (t == 0) s_tok[d] = bi;
+    break;
+  }
+  __syncthreads();
+  if (t == 0) n_acc[b] = d;
+  if (t <= kmax) out_tok[static_cast<size_t>(b) * (kmax + 1) + t] = t <= d ? s_tok[t] : -1;
+  if (t < kmax) out_path[static_cast<size_t>(b) * kmax + t] = t < d ? s_path[t] : -1;
+}
+
 // Tables of the decision pass from device arrays: thread b takes sequence b;
 // row offsets are exclusive prefix sums of k + 1 (target rows) and k (draft
 // rows), scanned in LDS.
@@ -685,6 +890,35 @@ hipError_t launch_vocab_setup(int B, int kmax, const int32_t* d_k, const float* 
   if (B <= 0 || B > kSetupMaxSeqs) return hipErrorInvalidValue;
   setup_kernel<<<1, kSetupMaxSeqs, 0, st>>>(B, kmax, d_k, d_temp, d_ids, d_base, d_p, d_q, V, d_rows, d_seqs,
                                             d_n_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_pass(const VocabPlan& p, const VRow* d_rows, const VTreeSeq* d_seqs,
+                            const VTreeNode* d_nodes, const int32_t* d_row_tok, uint64_t seed,
+                            const uint64_t* d_seed, int kmax,
+                            int32_t* d_n_acc, int32_t* d_out_tok, int32_t* d_out_path, void* d_ws,
+                            hipStream_t st, KernelTimer* timer) {
+  if (p.B == 0) return hipSuccess;
+  if (p.n_chunks1 > kMaxChunks || kmax >= kTreeMaxNodes) return hipErrorInvalidValue;
+  VStat* stats = static_cast<VStat*>(d_ws);
+  auto timed = [&](const char* name) { return timer && timer->wants(name); };
+  // the vector path needs every row 16-byte aligned: rows are whole fp32
+  // vocabulary rows of 16-byte aligned buffers when V % 4 == 0
+  const bool vec = (p.V % 4) == 0;
+  dim3 g1(p.n_chunks1, p.n_rows);
+  const char* n1 = vec ? "stats_kernel<true>" : "stats_kernel<false>";
+  if (timed(n1)) timer->begin(st);
+  if (vec)
+    launch_kernel(stats_kernel<true>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1,
+                  nullptr);
+  else
+    launch_kernel(stats_kernel<false>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1,
+                  nullptr);
+  if (timed(n1)) timer->end(st, 4.0 * p.n_rows * p.V, 0.0);
+  if (timed("tree_decide_kernel")) timer->begin(st);
+  launch_kernel(tree_decide_kernel, dim3(p.B), dim3(kTreeThreads), 0, st, d_rows, d_seqs, d_nodes, d_row_tok,
+                stats, p.n_chunks1, p.V, seed, d_seed, kmax, d_n_acc, d_out_tok, d_out_path);
+  if (timed("tree_decide_kernel")) timer->end(st, 0.0, 0.0);
   return hipGetLastError();
 }
 

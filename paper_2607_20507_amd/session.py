@@ -152,6 +152,9 @@ class SpecSession:
     def set_drafts(self, seq_id: int, tokens, q_logits, stream=None):
         B.spec_set_drafts(self.ctx, seq_id, tokens, q_logits, stream)
 
+    def set_draft_tree(self, seq_id: int, parents, tokens, q_logits, stream=None):
+        B.spec_set_draft_tree(self.ctx, seq_id, parents, tokens, q_logits, stream)
+
     def verify(self, seq_ids, temps, seed: int, stream=None):
         return B.spec_verify(self.ctx, seq_ids, temps, seed, self.k_max, stream)
 
