@@ -12,9 +12,11 @@ Workloads:
   all (default) the 8b-shaped line below, with sub-objects: the same sequence
                 at T = 0 ("greedy"), plain target decode with k = 0
                 ("plain_decode"), the serving batch ("serving"), the 1b-shaped
-                model decoding 64 sequences by itself ("small_decode") and the
-                decision pass alone ("vocab_stress"), each with its own timing
-                and roofline (and oracle baseline where one is timed).
+                model decoding 64 sequences by itself ("small_decode"), a
+                15-node draft tree against the 5-draft chain ("tree_verify"),
+                long-context prefill of 2048 to 8192 tokens ("prefill") and
+                the decision pass alone ("vocab_stress"), each with its own
+                timing (and roofline and oracle baseline where one is timed).
   8b-shaped     32-layer d=4096 target (32/8 heads, ffn 14336, vocab 128256),
                 16-layer d=2048 drafter, batch 1, 2048-token context, k = 5,
                 T = 0.8 (default) or --temperature 0 for greedy.
@@ -432,6 +434,131 @@ def bench_serving(args, target, draft, T):
 
 
 # ---------------------------------------------------------------------------
+# long-context prefill
+
+def bench_prefill(args, target):
+    """Prefill of one prompt of 2048, 4096 and 8192 tokens through the 32-layer
+    8B-shaped target (a decode-only context over the same weights; chunks of
+    up to 8192 rows), the paper's length range.  Each length is prefilled
+    `warmup` times untimed, then timed `reps` times (host clock around the
+    call, which returns when the work is done); the large-M gate/up GEMM and
+    the causal prefill attention are timed at kernel level on one more
+    prefill of 8192 tokens."""
+    import torch
+    from paper_2607_20507_amd import binding as B
+    from paper_2607_20507_amd.session import SpecSession
+    from workloads import LLAMA8B_SHAPED, uniform_prompts
+
+    cfg = LLAMA8B_SHAPED
+    V = cfg.target.vocab
+    reps = max(2, min(args.steps, 5))
+    sess = SpecSession(target, None, max_seqs=1, k_max=0, max_pages_per_seq=8192 // 16 + 2, max_rows=8192)
+    out = {}
+    for P in (2048, 4096, 8192):
+        prompt = uniform_prompts(cfg.seed + P, [P + 1], V)[0]
+        times = []
+        for r in range(max(1, args.warmup) + reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            sess.prefill([1], [prompt])
+            t = time.perf_counter() - t0
+            sess.release(1)
+            if r >= max(1, args.warmup):
+                times.append(t)
+        ms = float(np.median(times)) * 1e3
+        out[str(P)] = {"ms": ms, "tokens_per_s": P / (ms / 1e3),
+                       "tflops": 2.0 * P * cfg.target.layer_params() * cfg.target.n_layers / (ms / 1e3) / 1e12}
+    prompt = uniform_prompts(cfg.seed + 8192, [8193], V)[0]
+    roof = {}
+    for kernel, bound in (("gemm_mfma2_bf16<2, 8, 8>", "mfma"), ("attn_bf16_kernel<128, 4, 2>", "mfma")):
+        B.spec_timing_enable(sess.ctx, kernel)
+        sess.prefill([1], [prompt])
+        sess.release(1)
+        k_ms, k_n, k_bytes, k_flops = B.spec_timing_read(sess.ctx)
+        B.spec_timing_enable(sess.ctx, None)
+        info = {"kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops}
+        roof[kernel] = roofline_of(info, bound, "prefill-8192", 1, " (one 8192-token prefill)")
+    sess.close()
+    out["roofline"] = roof["gemm_mfma2_bf16<2, 8, 8>"]
+    out["attention"] = roof["attn_bf16_kernel<128, 4, 2>"]
+    out["config"] = {"workload": "8b-shaped target prefill of one prompt (2048, 4096, 8192 tokens; positions "
+                                 "0..P-1 into the paged cache, no LM head), chunks of up to 8192 rows",
+                     "tflops_counts": "2 x parameters of the 32 layers per token (attention excluded)"}
+    return out
+
+
+# ---------------------------------------------------------------------------
+# tree verification at batch 1
+
+def bench_tree(args, target, draft):
+    """Verify rounds of a 15-node draft tree (3 candidates, 2 under each, one
+    under each of those: depth 3) against the 5-draft chain, on the 8B-shaped
+    target at context 2048.  Drafts are external (seeded tokens and draft
+    logits): the measured cost is the target's forward over the tree rows and
+    the tree decision, whatever proposer made the tree."""
+    import torch
+    from paper_2607_20507_amd import binding as B
+    from paper_2607_20507_amd.session import SpecSession
+    from workloads import LLAMA8B_SHAPED, uniform_prompts
+
+    cfg = LLAMA8B_SHAPED
+    V = cfg.target.vocab
+    parents, level = [], [-1]
+    for b in (3, 2, 1):
+        nxt = []
+        for u in level:
+            for _ in range(b):
+                parents.append(u)
+                nxt.append(len(parents) - 1)
+        level = nxt
+    m = len(parents)
+    rounds = args.warmup + args.steps + args.roof_steps
+    ctx_len = cfg.context[1]
+    pages = (ctx_len + rounds * (m + 1) + 64 + 15) // 16
+    sess = SpecSession(target, draft, max_seqs=1, k_max=m, max_pages_per_seq=pages, max_rows=2048)
+    sid = 77
+    sess.prefill([sid], [uniform_prompts(cfg.seed + 3, [ctx_len], V)[0]])
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(cfg.seed)
+    zq = torch.randn(m + 1, V, generator=g, device="cuda:0")
+    rng = np.random.default_rng(cfg.seed)
+    stream = torch.cuda.current_stream()
+    out = {}
+    for name, shape in (("tree", parents), ("chain", list(range(-1, 4)))):
+        lat, acc = [], []
+        for r in range(args.warmup + args.steps):
+            toks = [int(x) for x in rng.integers(0, V, size=len(shape))]
+            sess.set_draft_tree(sid, shape, toks, zq)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            na, _ = sess.verify([sid], [0.8], cfg.seed + r)
+            sess.commit([sid], na)
+            e1.record(stream)
+            if r >= args.warmup:
+                lat.append((e0, e1))
+                acc.append(int(na[0]))
+        torch.cuda.synchronize()
+        ls = sorted(a.elapsed_time(b) for a, b in lat)
+        out[name] = {"nodes": len(shape), "verify_ms_median": float(np.median(ls)),
+                     "verify_ms_p90": float(np.percentile(ls, 90)), "mean_accepted": float(np.mean(acc))}
+    # the tree decision kernel alone (kernel-level events)
+    B.spec_timing_enable(sess.ctx, "tree_decide_kernel")
+    for r in range(args.roof_steps):
+        sess.set_draft_tree(sid, parents, [int(x) for x in rng.integers(0, V, size=m)], zq)
+        na, _ = sess.verify([sid], [0.8], cfg.seed + 500 + r)
+        sess.commit([sid], na)
+    k_ms, k_n, _, _ = B.spec_timing_read(sess.ctx)
+    B.spec_timing_enable(sess.ctx, None)
+    sess.close()
+    out["tree"]["decide_us"] = k_ms * 1e3 / max(1, k_n)
+    out["config"] = {"workload": "8b-shaped target, batch 1, context 2048, T = 0.8: a 15-node draft tree "
+                                 "(branching 3, 2, 1) against a 5-draft chain, external seeded drafts",
+                     "parents": parents}
+    return out
+
+
+# ---------------------------------------------------------------------------
 # the small model decoding by itself, batched
 
 def bench_small_decode(args, small):
@@ -681,7 +808,7 @@ def main():
     if args.temperature is None or wl == "all":
         args.temperature = 0.0 if wl == "8b-serving" else 0.8
     steps = args.steps
-    info = info_s = info_v = info_d = None
+    info = info_s = info_v = info_d = info_t = info_p = None
     if wl in ("all", "8b-shaped", "8b-serving"):
         target, draft = device_models(LLAMA8B_SHAPED)
         if wl in ("all", "8b-shaped"):
@@ -692,6 +819,10 @@ def main():
             info_s["T"], info_s["steps"] = serve_T, steps
         if wl == "all":
             info_d = bench_small_decode(args, draft)
+            log("tree verification")
+            info_t = bench_tree(args, target, draft)
+            log("long-context prefill")
+            info_p = bench_prefill(args, target)
         del target, draft
         torch.cuda.empty_cache()
     if wl in ("all", "vocab-stress"):
@@ -749,6 +880,10 @@ def main():
                                    "one token per sequence per step",
                        "batch": 64, "mean_context": info_d["mean_ctx"], "temperature": 0.8},
             "roofline": roofline_of(info_d, "hbm", "small-decode", args.roof_steps)}
+    if info_t is not None:
+        line["tree_verify"] = info_t
+    if info_p is not None:
+        line["prefill"] = info_p
     if info_v is not None and head is not info_v:
         line["vocab_stress"] = sub_line(info_v, steps, {
             "config": vocab_config, "roofline": roofline_of(info_v, "hbm", "vocab-stress", args.roof_steps)})

@@ -166,6 +166,49 @@ class Decoder:
             return y
         return matmul_wt(y, self.w["lm_head"])
 
+    def kv_at(self, tokens, rows):
+        """Every layer's K (after RoPE) and V at the listed positions of the
+        no-cache forward over ``tokens``: a list over layers of (K [r, Hkv,
+        hd], V [r, Hkv, hd]).  The same arithmetic as ``forward``, restricted
+        to what those values depend on: a layer's K/V at a row depend on the
+        layer's input at that row only, and its output at a row on its K/V
+        at the rows up to it.  So the last layer runs only at ``rows``, the
+        one before it outputs only at ``rows`` (attending over its K/V of
+        every row up to the last of them), and earlier layers run in full up
+        to that row.  (Used to check long prefills at sampled positions.)"""
+        sh = self.shape
+        tokens = np.asarray(tokens, dtype=np.int64)
+        rows = np.asarray(sorted(int(r) for r in rows), dtype=np.int64)
+        top = int(rows[-1]) + 1
+        hq, hkv, hd = sh.n_heads, sh.n_kv_heads, sh.head_dim
+        L = self.n_layers
+        idx = np.arange(top)         # rows whose layer input is known
+        h = widen(self.w["embed"][tokens[:top]])
+        out = []
+        for l, lw in enumerate(self.w["layers"]):
+            # K/V of every row of idx (all rows up to `top`, or `rows` in the last layer)
+            y = rms_norm(h, lw["attn_norm"], sh.rms_eps)
+            qkv = matmul_wt(y, lw["wqkv"])
+            n = len(idx)
+            q = rope(qkv[:, :hq * hd].reshape(n, hq, hd), idx, sh.rope_theta)
+            k = rope(qkv[:, hq * hd:(hq + hkv) * hd].reshape(n, hkv, hd), idx, sh.rope_theta)
+            v = qkv[:, (hq + hkv) * hd:].reshape(n, hkv, hd)
+            sel = np.searchsorted(idx, rows)
+            out.append((k[sel], v[sel]))
+            if l == L - 1:
+                break
+            # outputs: at `rows` when the next layer is the last, else at every row
+            orow = rows if l == L - 2 else idx
+            osel = np.searchsorted(idx, orow)
+            o = attention(q[osel], k, v, orow)
+            hh = h[osel] + matmul_wt(o.reshape(len(orow), hq * hd), lw["wo"])
+            y = rms_norm(hh, lw["mlp_norm"], sh.rms_eps)
+            gu = matmul_wt(y, lw["w_gate_up"])
+            f = sh.ffn_dim
+            h = hh + matmul_wt(silu(gu[:, :f]) * gu[:, f:], lw["w_down"])
+            idx = orow
+        return out
+
     def full_logits(self, tokens) -> np.ndarray:
         """No-cache forward over a whole token sequence (positions 0..n-1)."""
         kv = self.new_kv()

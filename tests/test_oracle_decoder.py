@@ -113,3 +113,21 @@ def test_gqa_equals_repeated_heads():
     a = D.attention(q, K, V, pos)
     b = D.attention(q, np.repeat(K, 4, axis=1), np.repeat(V, 4, axis=1), pos)
     assert np.allclose(a, b, rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("L", [1, 2, 3])
+def test_kv_at_sampled_rows_equals_the_cached_forward(L):
+    """Decoder.kv_at (every layer's K/V at chosen positions, computing only what
+    they depend on) against the K/V that the full cached forward appends."""
+    from workloads import TINY_FP32, uniform_prompts
+    sh = TINY_FP32.target
+    w = model_weights(sh, 5, L)
+    dec = D.Decoder(sh, w)
+    toks = uniform_prompts(3, [90], sh.vocab)[0]
+    rows = [0, 15, 16, 44, 88]
+    got = dec.kv_at(toks[:89], rows)
+    kv = dec.new_kv()
+    dec.forward(kv, toks[:89], np.arange(89), logits=False)
+    for l in range(L):
+        np.testing.assert_allclose(got[l][0], kv.K[l][rows], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(got[l][1], kv.V[l][rows], rtol=0, atol=1e-12)
