@@ -161,13 +161,18 @@ SPEC_API spec_status spec_set_workspace(spec_ctx* ctx, void* dev_ptr, size_t byt
 
 /* Prefill: register `n` new sequences (caller-chosen, distinct, stable ids)
  * with prompts `tokens` (host, packed, prompt_lens[i] >= 1 tokens each) and run
- * positions 0..P-2 through both models (no LM head).  The last prompt token
+ * positions 0..P-2 through both models (no LM head): the request enters the
+ * target LLM and its drafter before draft-and-verify generation starts
+ * (Section 3.4 Cache-Miss Branch; the request lengths of Section 4.7 Length
+ * Robustness set the prompt sizes).  The last prompt token
  * becomes the pending token.  Pages: lowest-numbered free page first, in list
  * order.  Blocks until the work is done. */
 SPEC_API spec_status spec_prefill(spec_ctx* ctx, int32_t n, const int64_t* seq_ids,
                                   const int32_t* prompt_lens, const int32_t* tokens, void* stream);
 
-/* One draft step for each listed sequence: the draft model consumes its
+/* One draft step for each listed sequence (Section 3.4 Cache-Miss Branch:
+ * the small model proposes candidate tokens; Section 2, speculative-decoding
+ * paragraph): the draft model consumes its
  * pending tokens (the committed tail not yet in the draft cache on the first
  * step after a commit, else the previous draft) and draws the next draft token
  * x~_j at position n+j from softmax(z/T) by Gumbel-max with DRAFT noise
@@ -193,7 +198,8 @@ SPEC_API spec_status spec_draft_loop(spec_ctx* ctx, int32_t n, const int64_t* se
                                      const float* temperature, uint64_t seed, const int32_t* steps,
                                      void* stream);
 
-/* spec_draft_step with draft guidance, a workload-shaping hook: for each
+/* WORKLOAD / TEST HOOK, not a step of the method.
+ * spec_draft_step with draft guidance, a workload-shaping hook: for each
  * sequence i with guide[i] >= 0 (host int32 [n]; -1 = none), the guide
  * token's draft logit is raised to the row maximum + boost (>= 0) before the
  * draw, and the raised row is kept as that draft's proposal q (so the rule
@@ -204,13 +210,17 @@ SPEC_API spec_status spec_draft_step_guided(spec_ctx* ctx, int32_t n, const int6
                                             const float* temperature, uint64_t seed,
                                             const int32_t* guide, float boost, void* stream);
 
-/* The verify's target forward alone: rows x_n, x~_1..x~_k at positions n..n+k
+/* WORKLOAD / TEST HOOK, not a step of the method (the verify below runs the
+ * same forward and decides).
+ * The verify's target forward alone: rows x_n, x~_1..x~_k at positions n..n+k
  * of each listed sequence (their K/V are written, as the verify that follows
  * writes them), fp32 logits where spec_last_logits points, no decision pass.
  * Committed state is unchanged; the drafts stay pending.  Asynchronous. */
 SPEC_API spec_status spec_target_forward(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, void* stream);
 
-/* Replace a sequence's drafts by externally supplied ones: k tokens (host) and
+/* WORKLOAD / TEST HOOK, not a step of the method: it stands in for the draft
+ * model when a test or bench supplies seeded drafts.
+ * Replace a sequence's drafts by externally supplied ones: k tokens (host) and
  * their draft logits rows (device fp32 [k, vocab], which must stay alive until
  * the verify has run). */
 SPEC_API spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k,
@@ -240,7 +250,11 @@ SPEC_API spec_status spec_set_drafts(spec_ctx* ctx, int64_t seq_id, int32_t k,
 SPEC_API spec_status spec_set_draft_tree(spec_ctx* ctx, int64_t seq_id, int32_t m, const int32_t* parents,
                                          const int32_t* tokens, const float* q_logits, void* stream);
 
-/* Verify: feed [x_n, x~_1..x~_k] at positions n..n+k through the target (their
+/* Verify (Section 3.4 Cache-Miss Branch: the target LLM verifies the
+ * candidates in one parallel pass and corrects or continues the generation;
+ * Section 2, speculative-decoding paragraph, with the speculative sampling
+ * rule of the works it cites, Leviathan et al. 2023 and Chen et al. 2023):
+ * feed [x_n, x~_1..x~_k] at positions n..n+k through the target (their
  * K/V are written to the cache first, then each row attends causally), produce
  * fp32 logits, and apply the speculative sampling rule per sequence with its
  * own temperature.  Outputs (host): n_accepted[i] = a_i in 0..k_i and
@@ -251,7 +265,9 @@ SPEC_API spec_status spec_verify(spec_ctx* ctx, int32_t n, const int64_t* seq_id
                                  const float* temperature, uint64_t seed,
                                  int32_t* n_accepted, int32_t* out_tokens, void* stream);
 
-/* Commit the last verify of each listed sequence with a accepted drafts
+/* Commit (Section 3.4 Cache-Miss Branch: the verified prefix and the
+ * corrected token become the generation, the rejected candidates are
+ * discarded) the last verify of each listed sequence with a accepted drafts
  * (normally the a returned by spec_verify): the target cache keeps positions
  * <= n+a, the draft cache keeps min(its length, n+a+1) positions, the emitted
  * tokens join the history, rejected K/V slots are cleared in place and pages
@@ -288,12 +304,15 @@ SPEC_API spec_status spec_verify_commit_draft(spec_ctx* ctx, int32_t n, const in
 SPEC_API spec_status spec_decode(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const float* temperature,
                                  uint64_t seed, int32_t steps, int32_t* out_tokens, void* stream);
 
-/* Truncate both caches of a sequence to `new_len` positions (0 <= new_len <=
+/* Rollback (the discard half of the commit above, Section 3.4 Cache-Miss
+ * Branch, for a caller that drops generated tokens itself).
+ * Truncate both caches of a sequence to `new_len` positions (0 <= new_len <=
  * target length); history[new_len] becomes the pending token and outstanding
  * drafts are dropped.  Cleared in place like a commit.  Asynchronous. */
 SPEC_API spec_status spec_kv_rollback(spec_ctx* ctx, int64_t seq_id, int32_t new_len, void* stream);
 
-/* Forget a sequence and free its pages. */
+/* Forget a sequence and free its pages (the request's generation has ended,
+ * Section 3.4 Cache-Miss Branch). */
 SPEC_API spec_status spec_seq_release(spec_ctx* ctx, int64_t seq_id);
 
 /* Introspection (host outputs): committed target/draft lengths, pending token
@@ -345,7 +364,10 @@ SPEC_API spec_status spec_timing_read(spec_ctx* ctx, double* total_ms, int64_t* 
                                       double* bytes, double* flops);
 
 /* ---------------------------------------------------------------------------
- * The decision pass alone, on caller-provided device logits.
+ * The decision pass alone, on caller-provided device logits: the acceptance
+ * scan, the residual resample and the bonus draw of speculative sampling
+ * (Section 3.4 Cache-Miss Branch and Section 2, speculative-decoding
+ * paragraph; the rule of the cited Leviathan et al. 2023 / Chen et al. 2023).
  *
  * B sequences; sequence b has k[b] drafts (0..15), temperature[b] >= 0,
  * stable id seq_ids[b] and pending-token position base_pos[b] (all host arrays).
@@ -386,7 +408,9 @@ SPEC_API spec_status spec_sample_verify_noalloc(int32_t B, int32_t k_max, const 
                                                 int32_t V, uint64_t seed, int32_t* n_accepted,
                                                 int32_t* out_tokens, void* stream);
 
-/* Draw one draft token per row: row i of `logits` (device fp32 [n, V]) is the
+/* The drafter's draw (Section 3.4: the small model proposes candidate
+ * tokens), for callers holding their own draft logits.
+ * Draw one draft token per row: row i of `logits` (device fp32 [n, V]) is the
  * draft distribution for position pos[i] of sequence seq_ids[i] (host arrays);
  * tokens (device int32 [n]) <- Gumbel-max with DRAFT noise, argmax if T == 0. */
 SPEC_API spec_status spec_sample_draft(int32_t n, const float* logits, int32_t V,
