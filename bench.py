@@ -402,7 +402,7 @@ def bench_serving(args, target, draft, T):
 
     for s in range(args.warmup):
         step(s, False)
-    kernel = args.kernel or "gemm_mfma2_bf16<2, 6, 8>"
+    kernel = args.kernel or "gemm_mfma3_bf16<2, 12, 4, 4>"
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0 = torch.cuda.Event(enable_timing=True)
@@ -470,7 +470,7 @@ def bench_prefill(args, target):
                        "tflops": 2.0 * P * cfg.target.layer_params() * cfg.target.n_layers / (ms / 1e3) / 1e12}
     prompt = uniform_prompts(cfg.seed + 8192, [8193], V)[0]
     roof = {}
-    for kernel, bound in (("gemm_mfma2_bf16<2, 8, 8>", "mfma"), ("attn_bf16_kernel<128, 4, 2>", "mfma")):
+    for kernel, bound in (("gemm_mfma3_bf16<2, 12, 4, 4>", "mfma"), ("attn_bf16_kernel<128, 4, 2>", "mfma")):
         B.spec_timing_enable(sess.ctx, kernel)
         sess.prefill([1], [prompt])
         sess.release(1)
@@ -479,7 +479,7 @@ def bench_prefill(args, target):
         info = {"kernel": kernel, "k_ms": k_ms, "k_n": k_n, "k_bytes": k_bytes, "k_flops": k_flops}
         roof[kernel] = roofline_of(info, bound, "prefill-8192", 1, " (one 8192-token prefill)")
     sess.close()
-    out["roofline"] = roof["gemm_mfma2_bf16<2, 8, 8>"]
+    out["roofline"] = roof["gemm_mfma3_bf16<2, 12, 4, 4>"]
     out["attention"] = roof["attn_bf16_kernel<128, 4, 2>"]
     out["config"] = {"workload": "8b-shaped target prefill of one prompt (2048, 4096, 8192 tokens; positions "
                                  "0..P-1 into the paged cache, no LM head), chunks of up to 8192 rows",

@@ -40,7 +40,9 @@
 namespace spec {
 namespace {
 
-__device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
+// x * sigmoid(x) with a hardware reciprocal (1 ulp) instead of an IEEE
+// division, which costs ten instructions per element in the epilogues.
+__device__ __forceinline__ float silu(float x) { return x * __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 
 // ---------------------------------------------------------------------------
 // tiled weight layout
@@ -739,6 +741,225 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restri
     }
 }
 
+// ---------------------------------------------------------------------------
+// MFMA bf16 with the weights streamed straight into registers, for the large
+// single-pass shapes (SwiGLU gate/up and the LM head at 160+ rows): workgroup
+// tile 16 MB rows x 4 NB 16-feature W tiles, 4 waves side by side along W
+// (wave w owns W tiles w NB .. w NB + NB - 1; SwiGLU: gate tiles w NB / 2 ..
+// and the same up tiles) against all 16 MB rows.  A W fragment is used by one
+// wave only, so it goes global -> B-operand registers with no LDS round trip
+// (tiled layout: one load is one fragment), D - 1 k-steps ahead.  The X tile
+// of a k-step (16 MB rows x 64 bytes) goes to LDS by direct-to-LDS loads, D
+// k-steps ahead, and every wave reads its A fragments from there one k-step
+// ahead (two register buffers).  The loads and fragment reads of a step are
+// spread between its MFMAs (one global load every MB NB / (NB + MB / 4)
+// MFMAs): issued together at the start of the step they held the wave at the
+// memory pipeline while its MFMAs waited (364-row gate/up: 130 -> 100 us).
+// All global loads are inline asm with explicit waits; loads complete in
+// issue order, so one s_waitcnt per k-step covers the X stage and the W
+// fragments it needs.  The epilogue transposes each 4 x 4 quad of outputs so
+// that a lane stores four consecutive columns of one row at once.
+__device__ __forceinline__ void load_reg16(u32x4& d, const void* base, uint32_t off_bytes) {
+  asm volatile("global_load_dwordx4 %0, %1, %2" : "=v"(d) : "v"(off_bytes), "s"(base));
+}
+
+// 4 x 4 transpose across each quad of lanes: lane q of a quad holds
+// v[r] = M[r][q]; afterwards it holds v[c] = M[q][c].  Two rounds of
+// neighbour exchanges (quad_perm 1,0,3,2 then 2,3,0,1), each lane keeping the
+// elements whose index agrees with its own position in the bit exchanged.
+__device__ __forceinline__ void quad_transpose(float (&v)[4]) {
+  const int q = threadIdx.x & 3;
+  float u[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float nb = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[r ^ 1]), 0xB1, 0xF, 0xF, false));
+    u[r] = ((q ^ r) & 1) ? nb : v[r];
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float nb = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(u[r ^ 2]), 0x4E, 0xF, 0xF, false));
+    v[r] = ((q ^ r) & 2) ? nb : u[r];
+  }
+}
+
+// Four consecutive outputs of a row, `left` of them inside the matrix: one
+// wide store when all four are in and the address is aligned, else element
+// by element.
+__device__ __forceinline__ void store_f32x4(float* y, const float (&v)[4], int left) {
+  if (left >= 4 && (reinterpret_cast<uintptr_t>(y) & 15) == 0) {
+    *reinterpret_cast<float4*>(y) = make_float4(v[0], v[1], v[2], v[3]);
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    if (c < left) y[c] = v[c];
+}
+__device__ __forceinline__ void store_bf16x4(bf16_t* y, const float (&v)[4], int left) {
+  if (left >= 4 && (reinterpret_cast<uintptr_t>(y) & 7) == 0) {
+    *reinterpret_cast<uint2*>(y) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    if (c < left) y[c] = f32_to_bf16(v[c]);
+}
+
+template <int EPI, int MB, int NB, int D>
+__global__ __launch_bounds__(256, 1) void gemm_mfma3_bf16(const bf16_t* __restrict__ X,
+                                                          const bf16_t* __restrict__ W, void* __restrict__ Y,
+                                                          int R, int N, int K, int MT,
+                                                          const int32_t* __restrict__ row_map) {
+  constexpr bool SW = (EPI == kEpiSwiGLU);
+  static_assert(EPI == kEpiSwiGLU || EPI == kEpiStoreF32, "store epilogues only");
+  constexpr int TM = 16 * MB;
+  constexpr int NTG = 4 * NB;   // 16-feature W tiles per workgroup
+  constexpr int LX = MB / 4;    // X loads per wave per k-step
+  constexpr int XU = TM * 4;    // 16-byte units of X per stage
+  constexpr int PER = NB + LX;  // loads per wave per k-step
+  constexpr int NM = MB * NB;   // MFMAs per wave per k-step
+  constexpr int GAP = NM / PER;
+  static_assert(MB % 4 == 0 && (!SW || NB % 2 == 0) && D % 2 == 0 && (D - 2) * PER <= 63 && GAP >= 1, "shape");
+  __shared__ u32x4 sx[D][XU];
+  const int t = threadIdx.x;
+  const int lane = t & (kWave - 1), wave = t / kWave;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int total = gridDim.x, nid = blockIdx.x;
+  const int xcd = nid & 7, slot = nid >> 3, per = total >> 3, rem = total & 7;
+  const int tix = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+  const int mt = tix % MT, nt = tix / MT;
+  const int m0 = mt * TM;
+  const int f0 = nt * (SW ? 8 * NTG : 16 * NTG);
+  const int nk = K / 32;  // a multiple of D (checked by the launcher)
+
+  // X load q of this wave: row group wave * LX + q (16 rows x 64 bytes); LDS
+  // unit u of a group holds row u / 4, chunk (u % 4) ^ (u / 16), so that an
+  // A-fragment read (16 rows, one chunk each) touches all 64 banks; rows past
+  // R clamped (read, never written back).
+  uint32_t xo[LX];
+#pragma unroll
+  for (int q = 0; q < LX; ++q)
+    xo[q] = static_cast<uint32_t>(min(m0 + (wave * LX + q) * 16 + (lane >> 2), R - 1)) * K +
+            ((lane & 3) ^ (lane >> 4)) * 8;
+  // W fragment j: lane (l16, g) of k-step e reads memory row tile * 16 +
+  // 4 ((e / 32) % 4) + g at chunk position l16 of block e / 128 (full tile);
+  // a trailing partial tile is row-major (row clamped to N - 1); tiles past N
+  // clamp to the last one.
+  const int ntiles = (N + 15) / 16;
+  uint32_t wo[NB];
+  uint32_t wfull = 0;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int tl = SW ? (f0 / 16 + wave * (NB / 2) + j % (NB / 2)) : (f0 / 16 + wave * NB + j);
+    const int tile = min(tl, ntiles - 1);
+    const uint32_t half = (SW && j >= NB / 2) ? static_cast<uint32_t>(N) * K : 0u;
+    const bool full = (tile + 1) * 16 <= N;
+    wfull |= full ? (1u << j) : 0u;
+    wo[j] = half + (full ? static_cast<uint32_t>(tile * 16 + g) * K + l16 * 8
+                         : static_cast<uint32_t>(min(tile * 16 + l16, N - 1)) * K + g * 8);
+  }
+  // k-steps past the end are clamped to the last one (redundant cache hits),
+  // so that every k-step issues the same loads and the wait counts hold
+  auto w_off = [&](int j, int k) {
+    const uint32_t e = 32 * min(k, nk - 1);
+    return (wo[j] + (((wfull >> j) & 1) ? ((e >> 5) & 3) * 4 * K + (e >> 7) * 128 : e)) * 2;
+  };
+  auto x_load = [&](int q, int s, int k) {
+    load_lds16(X, (xo[q] + 32 * min(k, nk - 1)) * 2, lds_addr(&sx[s][0]) + (wave * LX + q) * 1024);
+  };
+
+  f32x4 acc[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 wr[D][NB];
+  u32x4 fa[2][MB];
+  // prologue: X(0), then W(p), X(p + 1) for p < D - 1; A fragments of X(0)
+#pragma unroll
+  for (int q = 0; q < LX; ++q) x_load(q, 0, 0);
+#pragma unroll
+  for (int p = 0; p < D - 1; ++p) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) load_reg16(wr[p][j], W, w_off(j, p));
+#pragma unroll
+    for (int q = 0; q < LX; ++q) x_load(q, p + 1, p + 1);
+  }
+  SPEC_WAIT_VM_LDS((D - 1) * PER);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+#pragma unroll
+  for (int i = 0; i < MB; ++i) fa[0][i] = sx[0][i * 64 + l16 * 4 + (g ^ (l16 >> 2))];
+
+  // k-step k (slot s = k % D): wait until X(k + 1) has landed (and with it
+  // W(k), issued just before it) and this wave's LDS reads are done; the
+  // barrier publishes stage (k + 1) % D and ends every read of stage s.  Then
+  // the MFMAs of k, with W(k + D - 1) going into the slot W(k - 1) used,
+  // X(k + D) into stage s and the A fragments of k + 1 read in between.
+  for (int kt = 0; kt < nk; kt += D) {
+#pragma unroll
+    for (int s = 0; s < D; ++s) {
+      const int k = kt + s;
+      SPEC_WAIT_VM_LDS((D - 2) * PER);
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_barrier();
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      const int sn = (s + 1) % D;
+#pragma unroll
+      for (int u = 0; u < NM; ++u) {
+        const int i = u / NB, j = u % NB;
+        if (u % GAP == 0 && u / GAP < PER) {
+          const int q = u / GAP;
+          if (q < NB) load_reg16(wr[(s + D - 1) % D][q], W, w_off(q, k + D - 1));
+          else x_load(q - NB, s, k + D);
+        }
+        // past the end: stale data, never used
+        if (j == 0) fa[(s + 1) & 1][i] = sx[sn][i * 64 + l16 * 4 + (g ^ (l16 >> 2))];
+        mfma_acc(acc[i][j], fa[s & 1][i], wr[s][j]);
+      }
+    }
+  }
+  // The clamped loads past the end land before their registers are reused:
+  // the compiler does not see the inline-asm loads in flight, so every W
+  // register stays live (an empty asm reads it) until after the wait.
+  SPEC_WAIT_VM_LDS(0);
+#pragma unroll
+  for (int s = 0; s < D; ++s)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) asm volatile("" ::"v"(wr[s][j]));
+  {  // acc + 0 * 0 (exact), by MFMAs the compiler sees
+    const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) acc[i][j] = mfma16x16x32v(z, z, acc[i][j]);
+  }
+
+  // Lane (l16, g) holds rows 4 g + r of column l16 of each 16 x 16 block;
+  // after the quad transpose it holds row 4 g + l16 % 4, columns
+  // 4 (l16 / 4) .. + 3.
+  const int q4 = l16 & 3, c4 = (l16 >> 2) * 4;
+#pragma unroll
+  for (int i = 0; i < MB; ++i) {
+    const int m = m0 + 16 * i + 4 * g + q4;
+    const size_t mo = (m < R && row_map) ? static_cast<size_t>(row_map[m]) : static_cast<size_t>(m);
+#pragma unroll
+    for (int j = 0; j < (SW ? NB / 2 : NB); ++j) {
+      float v[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = SW ? silu(acc[i][j][r]) * acc[i][j + NB / 2][r] : acc[i][j][r];
+      quad_transpose(v);
+      const int n = f0 + 16 * (SW ? wave * (NB / 2) + j : wave * NB + j) + c4;
+      if (m >= R || n >= N) continue;
+      if (SW)
+        store_bf16x4(static_cast<bf16_t*>(Y) + mo * N + n, v, N - n);
+      else
+        store_f32x4(static_cast<float*>(Y) + mo * N + n, v, N - n);
+    }
+  }
+}
+
 // Sum split-K partials [S][R][Nw] in split order and apply the epilogue.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part, int S, int R, int N,
@@ -1094,11 +1315,39 @@ hipError_t mfma2_m(int ntw, int R, int N, int K, const bf16_t* x, const bf16_t* 
   }
 }
 
+// gemm_mfma3_bf16 (weights straight to registers, 192 x 256 tiles) for the
+// shapes it was measured to win, all in one pass over K: SwiGLU gate/up from
+// 160 rows (364-row serving verify 114 -> 97 us, 2048-row prefill 508 -> 433
+// us, 8192 rows 1966 -> 1641 us) and store-only projections of 65536+ rows
+// (the LM head: 425 -> 404 us at 364 rows), when the 192 x 256 tiles fill the
+// 256 CUs at least 3 / 4 of the way in one pass.  Elsewhere (the residual-add
+// and QKV projections, whose grids need split K) gemm_mfma2_bf16 was as fast
+// or faster.
+constexpr int kM3MB = 12, kM3NB = 4, kM3D = 4;
+
+bool use_mfma3(int R, int Nw, int K, int epi) {
+  if (R < 160 || K % (32 * kM3D)) return false;
+  if (epi != kEpiSwiGLU && !(epi == kEpiStoreF32 && Nw >= 65536)) return false;
+  if (static_cast<double>(Nw) * K >= 2147483648.0 || static_cast<double>(R) * K >= 2147483648.0) return false;
+  const int MT = (R + 16 * kM3MB - 1) / (16 * kM3MB), NT = (Nw + 64 * kM3NB - 1) / (64 * kM3NB);
+  return MT * NT >= 192;
+}
+
+template <int EPI>
+hipError_t mfma3(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st, const int32_t* rm) {
+  const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
+  const int MT = (R + 16 * kM3MB - 1) / (16 * kM3MB), NT = (Nw + 64 * kM3NB - 1) / (64 * kM3NB);
+  launch_kernel(gemm_mfma3_bf16<EPI, kM3MB, kM3NB, kM3D>, dim3(MT * NT), dim3(256), 0, st, x, w, Y, R, N, K, MT, rm);
+  return hipGetLastError();
+}
+
 template <int EPI>
 hipError_t mfma2(int R, int N, int K, const void* X, const void* W, void* Y, hipStream_t st,
                  const int32_t* rm, float* ws, size_t ws_bytes, GemmNorm* norm = nullptr) {
   const bf16_t* x = static_cast<const bf16_t*>(X);
   const bf16_t* w = static_cast<const bf16_t*>(W);
+  if constexpr (EPI == kEpiSwiGLU || EPI == kEpiStoreF32)
+    if (use_mfma3(R, EPI == kEpiSwiGLU ? 2 * N : N, K, EPI)) return mfma3<EPI>(R, N, K, x, w, Y, st, rm);
   const Mfma2Shape sh = mfma2_shape(R, N, EPI == kEpiSwiGLU ? 2 * N : N, K, ws ? ws_bytes : 0);
   switch (sh.mtw) {
     case 2: return mfma2_m<EPI, 2>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
@@ -1214,6 +1463,13 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
   if (dtype == 0) return f32[epi];
   const int Nw = epi == kEpiSwiGLU ? 2 * N : N;
   if (use_mfma(R, Nw, K)) {
+    static char m3[3][40];
+    static std::once_flag once3;
+    std::call_once(once3, [] {
+      for (int e = 0; e < 3; ++e)
+        snprintf(m3[e], sizeof(m3[e]), "gemm_mfma3_bf16<%d, %d, %d, %d>", e, kM3MB, kM3NB, kM3D);
+    });
+    if (use_mfma3(R, Nw, K, epi)) return m3[epi];
     const Mfma2Shape sh = mfma2_shape(R, N, Nw, K, splitk_bytes);
     return tiled[epi][sh.mtw / 2 - 1][sh.ntw == 2 ? 0 : (sh.ntw == 4 ? 1 : 2)];
   }

@@ -176,13 +176,19 @@ FULL = [
     (384, 6144, 4096, 0), (384, 14336, 4096, 2), (384, 4096, 14336, 1), (384, 128256, 4096, 0),
     (1, 3072, 2048, 0), (1, 8192, 2048, 2), (1, 2048, 8192, 1), (64, 128256, 2048, 0),
     (21, 128256, 2048, 0), (48, 8192, 2048, 2), (43, 2048, 8192, 1), (9, 70000, 256, 0),
+    # the register-streamed MFMA kernel: the 364-row serving verify and a
+    # 2048-row prefill chunk of the gate/up, and ragged shapes (rows not a
+    # multiple of 16, a trailing partial W tile, N % 4 != 0 for the LM-head
+    # form)
+    (364, 14336, 4096, 2), (2048, 14336, 4096, 2), (200, 24600, 256, 2), (177, 65546, 128, 0),
 ]
 
 
 @pytest.mark.parametrize("R,N,K,epi", FULL)
 def test_gemm_bf16_full_shapes_sampled(R, N, K, epi):
     dev = device()
-    cols = np.sort(np.random.default_rng(N + K).choice(N, size=min(N, 192), replace=False))
+    cols = np.random.default_rng(N + K).choice(N, size=min(N, 192), replace=False)
+    cols = np.unique(np.concatenate([cols, np.arange(max(0, N - 20), N)]))  # the ragged tail too
     got, ref = _gemm_case(B().SPEC_BF16, R, N, K, epi, dev, seed=N, cols=cols)
     tol = 1e-2 if epi == 2 else 1e-4
     assert rel_err(got, ref) < tol
