@@ -784,15 +784,23 @@ __device__ __forceinline__ void quad_transpose(float (&v)[4]) {
 
 // Four consecutive outputs of a row, `left` of them inside the matrix: one
 // wide store when all four are in and the address is aligned, else element
-// by element.
-__device__ __forceinline__ void store_f32x4(float* y, const float (&v)[4], int left) {
+// by element (add: Y += v).
+__device__ __forceinline__ void store_f32x4(float* y, const float (&v)[4], int left, bool add) {
   if (left >= 4 && (reinterpret_cast<uintptr_t>(y) & 15) == 0) {
-    *reinterpret_cast<float4*>(y) = make_float4(v[0], v[1], v[2], v[3]);
+    float4 o = make_float4(v[0], v[1], v[2], v[3]);
+    if (add) {
+      const float4 h = *reinterpret_cast<const float4*>(y);
+      o.x += h.x;
+      o.y += h.y;
+      o.z += h.z;
+      o.w += h.w;
+    }
+    *reinterpret_cast<float4*>(y) = o;
     return;
   }
 #pragma unroll
   for (int c = 0; c < 4; ++c)
-    if (c < left) y[c] = v[c];
+    if (c < left) y[c] = add ? y[c] + v[c] : v[c];
 }
 __device__ __forceinline__ void store_bf16x4(bf16_t* y, const float (&v)[4], int left) {
   if (left >= 4 && (reinterpret_cast<uintptr_t>(y) & 7) == 0) {
@@ -807,10 +815,10 @@ __device__ __forceinline__ void store_bf16x4(bf16_t* y, const float (&v)[4], int
 template <int EPI, int MB, int NB, int D>
 __global__ __launch_bounds__(256, 1) void gemm_mfma3_bf16(const bf16_t* __restrict__ X,
                                                           const bf16_t* __restrict__ W, void* __restrict__ Y,
-                                                          int R, int N, int K, int MT,
+                                                          float* __restrict__ part, int R, int N, int K,
+                                                          int k_len, int MT, int NT,
                                                           const int32_t* __restrict__ row_map) {
   constexpr bool SW = (EPI == kEpiSwiGLU);
-  static_assert(EPI == kEpiSwiGLU || EPI == kEpiStoreF32, "store epilogues only");
   constexpr int TM = 16 * MB;
   constexpr int NTG = 4 * NB;   // 16-feature W tiles per workgroup
   constexpr int LX = MB / 4;    // X loads per wave per k-step
@@ -826,10 +834,11 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma3_bf16(const bf16_t* __restri
   const int total = gridDim.x, nid = blockIdx.x;
   const int xcd = nid & 7, slot = nid >> 3, per = total >> 3, rem = total & 7;
   const int tix = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-  const int mt = tix % MT, nt = tix / MT;
+  const int mt = tix % MT, rest = tix / MT, sp = rest / NT, nt = rest % NT;
   const int m0 = mt * TM;
   const int f0 = nt * (SW ? 8 * NTG : 16 * NTG);
-  const int nk = K / 32;  // a multiple of D (checked by the launcher)
+  const int kbeg = sp * k_len;
+  const int nk = (min(K, kbeg + k_len) - kbeg) / 32;  // a multiple of D (checked by the launcher)
 
   // X load q of this wave: row group wave * LX + q (16 rows x 64 bytes); LDS
   // unit u of a group holds row u / 4, chunk (u % 4) ^ (u / 16), so that an
@@ -838,7 +847,7 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma3_bf16(const bf16_t* __restri
   uint32_t xo[LX];
 #pragma unroll
   for (int q = 0; q < LX; ++q)
-    xo[q] = static_cast<uint32_t>(min(m0 + (wave * LX + q) * 16 + (lane >> 2), R - 1)) * K +
+    xo[q] = static_cast<uint32_t>(min(m0 + (wave * LX + q) * 16 + (lane >> 2), R - 1)) * K + kbeg +
             ((lane & 3) ^ (lane >> 4)) * 8;
   // W fragment j: lane (l16, g) of k-step e reads memory row tile * 16 +
   // 4 ((e / 32) % 4) + g at chunk position l16 of block e / 128 (full tile);
@@ -860,7 +869,7 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma3_bf16(const bf16_t* __restri
   // k-steps past the end are clamped to the last one (redundant cache hits),
   // so that every k-step issues the same loads and the wait counts hold
   auto w_off = [&](int j, int k) {
-    const uint32_t e = 32 * min(k, nk - 1);
+    const uint32_t e = kbeg + 32 * min(k, nk - 1);
     return (wo[j] + (((wfull >> j) & 1) ? ((e >> 5) & 3) * 4 * K + (e >> 7) * 128 : e)) * 2;
   };
   auto x_load = [&](int q, int s, int k) {
@@ -936,6 +945,25 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma3_bf16(const bf16_t* __restri
       for (int j = 0; j < NB; ++j) acc[i][j] = mfma16x16x32v(z, z, acc[i][j]);
   }
 
+  // Split K: raw fp32 partials by W row, which splitk_reduce* sums in a fixed
+  // order, stored lane by lane (16 lanes of a row write 64 contiguous bytes;
+  // measured faster here than the transposed form below).
+  if (part) {
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + 16 * i + 4 * g + r;
+        if (m >= R) continue;
+        float* pr = part + (static_cast<size_t>(sp) * R + m) * (SW ? 2 * N : N);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const int n = f0 + 16 * (SW ? wave * (NB / 2) + j % (NB / 2) : wave * NB + j) + l16;
+          if (n < N) pr[(SW && j >= NB / 2 ? N : 0) + n] = acc[i][j][r];
+        }
+      }
+    return;
+  }
   // Lane (l16, g) holds rows 4 g + r of column l16 of each 16 x 16 block;
   // after the quad transpose it holds row 4 g + l16 % 4, columns
   // 4 (l16 / 4) .. + 3.
@@ -955,7 +983,7 @@ __global__ __launch_bounds__(256, 1) void gemm_mfma3_bf16(const bf16_t* __restri
       if (SW)
         store_bf16x4(static_cast<bf16_t*>(Y) + mo * N + n, v, N - n);
       else
-        store_f32x4(static_cast<float*>(Y) + mo * N + n, v, N - n);
+        store_f32x4(static_cast<float*>(Y) + mo * N + n, v, N - n, EPI == kEpiAddF32);
     }
   }
 }
@@ -1267,6 +1295,10 @@ Mfma2Shape mfma2_shape(int R, int N, int Nw, int K, size_t ws_bytes) {
   return best;
 }
 
+template <int EPI>
+hipError_t splitk_finish(const float* ws, int S, int R, int N, void* Y, hipStream_t st, const int32_t* rm,
+                         GemmNorm* norm);
+
 template <int EPI, int MTW, int NTW>
 hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st,
                    const int32_t* rm, float* ws, size_t ws_bytes, GemmNorm* norm = nullptr) {
@@ -1284,6 +1316,15 @@ hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* 
   }
   launch_kernel(gemm_mfma2_bf16<EPI, MTW, NTW>, dim3(grid), dim3(256), 0, st, x, w, static_cast<void*>(nullptr), ws, R,
                 N, K, k_len, MT, NT, rm);
+  return splitk_finish<EPI>(ws, S, R, N, Y, st, rm, norm);
+}
+
+// The second pass of a split-K GEMM: the partials [S][R][Nw] summed in split
+// order with the epilogue applied (for a residual add followed by RMSNorm,
+// the norm too).
+template <int EPI>
+hipError_t splitk_finish(const float* ws, int S, int R, int N, void* Y, hipStream_t st, const int32_t* rm,
+                         GemmNorm* norm) {
   if (EPI == kEpiAddF32 && norm && !rm && N % 4 == 0 && N <= 4 * 256 * kNormRegChunks) {
     const int nch = (N / 4 + 255) / 256;
     auto* k = nch <= 1 ? splitk_reduce_norm<1> : nch <= 2 ? splitk_reduce_norm<2>
@@ -1316,29 +1357,48 @@ hipError_t mfma2_m(int ntw, int R, int N, int K, const bf16_t* x, const bf16_t* 
 }
 
 // gemm_mfma3_bf16 (weights straight to registers, 192 x 256 tiles) for the
-// shapes it was measured to win, all in one pass over K: SwiGLU gate/up from
-// 160 rows (364-row serving verify 114 -> 97 us, 2048-row prefill 508 -> 433
-// us, 8192 rows 1966 -> 1641 us) and store-only projections of 65536+ rows
-// (the LM head: 425 -> 404 us at 364 rows), when the 192 x 256 tiles fill the
-// 256 CUs at least 3 / 4 of the way in one pass.  Elsewhere (the residual-add
-// and QKV projections, whose grids need split K) gemm_mfma2_bf16 was as fast
-// or faster.
+// shapes it was measured to win: SwiGLU gate/up from 160 rows in one pass
+// (364-row serving verify 114 -> 97 us, 2048-row prefill 508 -> 433 us, 8192
+// rows 1966 -> 1641 us), store-only projections of 65536+ rows in one pass
+// (the LM head: 425 -> 404 us at 364 rows), each when the tiles fill the 256
+// CUs at least 3 / 4 of the way; and residual-add projections with K >= 8192
+// whose grid splits K (the 364-row down projection: 76 -> 64 us).  Elsewhere
+// (the QKV and O projections, the unsplit 2048-row down projection)
+// gemm_mfma2_bf16 was as fast or faster.
 constexpr int kM3MB = 12, kM3NB = 4, kM3D = 4;
 
-bool use_mfma3(int R, int Nw, int K, int epi) {
+struct Mfma3Plan {
+  int MT, NT, S, k_len;
+};
+
+bool use_mfma3(int R, int Nw, int K, int epi, size_t ws_bytes, Mfma3Plan* plan = nullptr) {
   if (R < 160 || K % (32 * kM3D)) return false;
-  if (epi != kEpiSwiGLU && !(epi == kEpiStoreF32 && Nw >= 65536)) return false;
   if (static_cast<double>(Nw) * K >= 2147483648.0 || static_cast<double>(R) * K >= 2147483648.0) return false;
   const int MT = (R + 16 * kM3MB - 1) / (16 * kM3MB), NT = (Nw + 64 * kM3NB - 1) / (64 * kM3NB);
-  return MT * NT >= 192;
+  int k_len = K, S = 1;
+  bool ok;
+  if (epi == kEpiAddF32) {
+    S = mfma2_splits(MT, NT, R, Nw, K, ws_bytes, &k_len);  // k_len: a multiple of 128 = 32 D
+    ok = K >= 8192 && S >= 2;
+  } else {
+    ok = (epi == kEpiSwiGLU || (epi == kEpiStoreF32 && Nw >= 65536)) && MT * NT >= 192;
+  }
+  if (ok && plan) *plan = {MT, NT, S, k_len};
+  return ok;
 }
 
 template <int EPI>
-hipError_t mfma3(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st, const int32_t* rm) {
-  const int Nw = (EPI == kEpiSwiGLU) ? 2 * N : N;
-  const int MT = (R + 16 * kM3MB - 1) / (16 * kM3MB), NT = (Nw + 64 * kM3NB - 1) / (64 * kM3NB);
-  launch_kernel(gemm_mfma3_bf16<EPI, kM3MB, kM3NB, kM3D>, dim3(MT * NT), dim3(256), 0, st, x, w, Y, R, N, K, MT, rm);
-  return hipGetLastError();
+hipError_t mfma3(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st, const int32_t* rm,
+                 float* ws, const Mfma3Plan& p, GemmNorm* norm) {
+  auto* kern = gemm_mfma3_bf16<EPI, kM3MB, kM3NB, kM3D>;
+  if (p.S <= 1) {
+    launch_kernel(kern, dim3(p.MT * p.NT), dim3(256), 0, st, x, w, Y, static_cast<float*>(nullptr), R, N, K, K, p.MT,
+                  p.NT, rm);
+    return hipGetLastError();
+  }
+  launch_kernel(kern, dim3(p.MT * p.NT * p.S), dim3(256), 0, st, x, w, static_cast<void*>(nullptr), ws, R, N, K,
+                p.k_len, p.MT, p.NT, rm);
+  return splitk_finish<EPI>(ws, p.S, R, N, Y, st, rm, norm);
 }
 
 template <int EPI>
@@ -1346,8 +1406,9 @@ hipError_t mfma2(int R, int N, int K, const void* X, const void* W, void* Y, hip
                  const int32_t* rm, float* ws, size_t ws_bytes, GemmNorm* norm = nullptr) {
   const bf16_t* x = static_cast<const bf16_t*>(X);
   const bf16_t* w = static_cast<const bf16_t*>(W);
-  if constexpr (EPI == kEpiSwiGLU || EPI == kEpiStoreF32)
-    if (use_mfma3(R, EPI == kEpiSwiGLU ? 2 * N : N, K, EPI)) return mfma3<EPI>(R, N, K, x, w, Y, st, rm);
+  Mfma3Plan p3;
+  if (use_mfma3(R, EPI == kEpiSwiGLU ? 2 * N : N, K, EPI, ws ? ws_bytes : 0, &p3))
+    return mfma3<EPI>(R, N, K, x, w, Y, st, rm, ws, p3, norm);
   const Mfma2Shape sh = mfma2_shape(R, N, EPI == kEpiSwiGLU ? 2 * N : N, K, ws ? ws_bytes : 0);
   switch (sh.mtw) {
     case 2: return mfma2_m<EPI, 2>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
@@ -1469,7 +1530,7 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
       for (int e = 0; e < 3; ++e)
         snprintf(m3[e], sizeof(m3[e]), "gemm_mfma3_bf16<%d, %d, %d, %d>", e, kM3MB, kM3NB, kM3D);
     });
-    if (use_mfma3(R, Nw, K, epi)) return m3[epi];
+    if (use_mfma3(R, Nw, K, epi, splitk_bytes)) return m3[epi];
     const Mfma2Shape sh = mfma2_shape(R, N, Nw, K, splitk_bytes);
     return tiled[epi][sh.mtw / 2 - 1][sh.ntw == 2 ? 0 : (sh.ntw == 4 ? 1 : 2)];
   }

@@ -194,6 +194,18 @@ def test_gemm_bf16_full_shapes_sampled(R, N, K, epi):
     assert rel_err(got, ref) < tol
 
 
+# Residual-add projections with a long reduction at 160+ rows split K in the
+# register-streamed kernel (the serving verify's down projection), partials
+# summed by the fixed-order reduction; a ragged N too.
+@pytest.mark.parametrize("R,N,K", [(364, 4096, 14336), (200, 4100, 8192)])
+def test_gemm_bf16_split_add_sampled(R, N, K):
+    dev = device()
+    cols = np.random.default_rng(N + K).choice(N, size=min(N, 192), replace=False)
+    cols = np.unique(np.concatenate([cols, np.arange(max(0, N - 20), N)]))
+    got, ref = _gemm_case(B().SPEC_BF16, R, N, K, 1, dev, seed=N + 1, cols=cols, splitk=True)
+    assert rel_err(got, ref) < 1e-4
+
+
 # ---------------------------------------------------------------------------
 # RMSNorm and RoPE + KV append
 
