@@ -470,7 +470,7 @@ def bench_prefill(args, target):
                        "tflops": 2.0 * P * cfg.target.layer_params() * cfg.target.n_layers / (ms / 1e3) / 1e12}
     prompt = uniform_prompts(cfg.seed + 8192, [8193], V)[0]
     roof = {}
-    for kernel, bound in (("gemm_mfma3_bf16<2, 12, 4, 4>", "mfma"), ("attn_bf16_kernel<128, 4, 2>", "mfma")):
+    for kernel, bound in (("gemm_mfma3_bf16<2, 12, 4, 4>", "mfma"), ("attn_prefill_bf16_kernel<128>", "mfma")):
         B.spec_timing_enable(sess.ctx, kernel)
         sess.prefill([1], [prompt])
         sess.release(1)
@@ -480,7 +480,7 @@ def bench_prefill(args, target):
         roof[kernel] = roofline_of(info, bound, "prefill-8192", 1, " (one 8192-token prefill)")
     sess.close()
     out["roofline"] = roof["gemm_mfma3_bf16<2, 12, 4, 4>"]
-    out["attention"] = roof["attn_bf16_kernel<128, 4, 2>"]
+    out["attention"] = roof["attn_prefill_bf16_kernel<128>"]
     out["config"] = {"workload": "8b-shaped target prefill of one prompt (2048, 4096, 8192 tokens; positions "
                                  "0..P-1 into the paged cache, no LM head), chunks of up to 8192 rows",
                      "tflops_counts": "2 x parameters of the 32 layers per token (attention excluded)"}

@@ -45,6 +45,12 @@ struct AttnArgs {
 hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int n_items,
                                  const AttnGroup* d_groups, int n_groups, int nt, int w, hipStream_t st);
 
+// bf16 causal prefill: items from plan_attention's prefill form (blocks of
+// 256 / G consecutive rows of one sequence against keys 0 .. t1 - 1, t0 = 0,
+// part < 0), heaviest first; grid n_items x Hkv (kv head = block % Hkv).
+hipError_t launch_attention_prefill_bf16(const AttnArgs& a, const AttnItem* d_items, int n_items, hipStream_t st);
+const char* attn_prefill_kernel_name(int hd);
+
 // fp32: one wave per (row, head); row r of sequence slot row_seq[r] at
 // position row_pos[r] attends keys 0..row_pos[r] (or its tree keys).
 hipError_t launch_attention_f32(const AttnArgs& a, int R, const int32_t* d_row_seq,

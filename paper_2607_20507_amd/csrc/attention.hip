@@ -324,6 +324,233 @@ __global__ __launch_bounds__(64 * W, NT <= 2 ? 2 : 1) void attn_tree_bf16_kernel
   attn_bf16_body<HD, NT, W, true>(a, items);
 }
 
+// ---------------------------------------------------------------------------
+// Causal prefill: long runs of consecutive rows of one sequence.  One
+// workgroup of 8 waves (two per SIMD, so that one wave's softmax arithmetic
+// overlaps the other's MFMAs) per (block of 256 / G rows, kv head): its 256
+// query vectors (rows x the G query heads of the kv head) share every K / V
+// load.  The keys 0 .. last row's position are brought into LDS 64 at a time
+// (four pages of K and of V, three stage buffers, two stages in flight) by
+// direct-to-LDS loads of whole page blocks, and each wave runs both products
+// for its own 32 query vectors (2 tiles) from there, with the key permutation
+// and lane-local softmax of attn_bf16_body.  Each wave sees every key of its
+// rows, so it normalises its own output: no key splits, no combine.
+// The running maximum of a query vector is raised only when a score exceeds
+// it by more than 2^8 (scores are base-2 logits): each lane compares its own
+// 8 scores against it, and only when some lane of the wave finds a larger
+// one does the wave take the cross-lane maximum and rescale its output
+// accumulators.  Probabilities stay below 2^8 in between; the shared maximum
+// is the same in every lane of a query vector, so the products stay exact.
+// Chunks entirely at or below every row of a wave skip the causal mask.
+// Two fp32 -> bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+constexpr int kPrefillStagedPages = 1024;  // page ids kept in LDS (16384 keys)
+constexpr float kPrefillRescaleLog2 = 8.f;
+
+template <int HD>
+__global__ __launch_bounds__(512, 1) void attn_prefill_bf16_kernel(AttnArgs a, const AttnItem* __restrict__ items) {
+  constexpr int DS = HD / 32;    // MFMA k-steps over the head dim
+  constexpr int DT = HD / 16;    // 16-dim output tiles
+  constexpr int NT = 2;          // 16-vector query tiles per wave
+  constexpr int NW = 8;          // waves
+  constexpr int BU = 2 * HD;     // 16-byte units of one (page, kv head) block
+  constexpr int SU = 4 * BU;     // units of K (and of V) per 64-key stage
+  constexpr int NB = 3;          // stage buffers
+  constexpr int LPW = 2 * SU / (64 * NW);  // direct-to-LDS loads per wave per stage
+  __shared__ uint4 sk[NB][SU], sv[NB][SU];
+  __shared__ int32_t s_pt[kPrefillStagedPages];
+  const int gkv = blockIdx.x % a.Hkv;
+  const AttnItem it = items[blockIdx.x / a.Hkv];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform: load bases in SGPRs
+  const int g = lane >> 4, l16 = lane & 15;
+  const int G = a.Hq / a.Hkv;
+  const bf16_t* q = static_cast<const bf16_t*>(a.q);
+  const bf16_t* kp = static_cast<const bf16_t*>(a.kpool);
+  const bf16_t* vp = static_cast<const bf16_t*>(a.vpool);
+  const int32_t* pt = a.page_table + static_cast<size_t>(it.seq) * a.max_pages;
+  const int t1 = it.t1;                 // keys 0 .. t1 - 1 (t0 = 0)
+  const int np = (t1 + 15) >> 4;
+  const int ns = (t1 + 63) >> 6;        // stages
+  // (the planner keeps t1 <= 16 kPrefillStagedPages)
+  for (int i = threadIdx.x; i < np; i += 64 * NW) s_pt[i] = pt[i];
+  __syncthreads();
+
+  // stage j (keys 64 j ..) into buffer b: wave w moves one page block, K of
+  // page w of the stage for w < 4, V of page w - 4 after (its LPW loads of
+  // 64 units each); pages past the sequence's last clamped to it (those keys
+  // are masked)
+  static_assert(LPW * 64 == BU && NW == 8, "one page block per wave and stage");
+  const bool wv = wave >= 4;
+  const int wpg = wave & 3;
+  auto issue = [&](int j, int b) {
+    const int page = __builtin_amdgcn_readfirstlane(s_pt[min(4 * j + wpg, np - 1)]);
+    const bf16_t* blk = (wv ? vp : kp) + static_cast<size_t>(page * a.Hkv + gkv) * 16 * HD;
+    const uint32_t dst = lds_addr(wv ? &sv[b][wpg * BU] : &sk[b][wpg * BU]);
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) load_lds16(blk, (i * 64 + lane) * 16, dst + i * 1024);
+  };
+
+  uint4 qf[NT][DS];
+  bool vval[NT];
+  int vpos[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int m = 32 * wave + 16 * nt + l16;
+    vval[nt] = m / G < it.nrows;
+    const int mm = vval[nt] ? m : 0;
+    vpos[nt] = it.pos0 + mm / G;
+    const bf16_t* base = q + (static_cast<size_t>(it.row0 + mm / G) * a.Hq + gkv * G + mm % G) * HD + g * 8;
+#pragma unroll
+    for (int s = 0; s < DS; ++s)
+      qf[nt][s] = vval[nt] ? reinterpret_cast<const uint4*>(base)[4 * s] : make_uint4(0, 0, 0, 0);
+  }
+  // the last key each query vector sees (-1: none, a padding vector)
+  int klim[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) klim[nt] = vval[nt] ? min(vpos[nt], t1 - 1) : -1;
+  // the wave's rows: positions pos_lo .. pos_hi
+  const int pos_lo = it.pos0 + (32 * wave) / G;
+  const int pos_hi = it.pos0 + min((32 * wave + 31) / G, it.nrows - 1);
+  const float scale = kLog2e / sqrtf(static_cast<float>(HD));
+  float mrun[NT], lrun[NT];
+  f32x4 acc[DT][NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    mrun[nt] = -INFINITY;
+    lrun[nt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // one 32-key chunk (keys c0 .., pages 2 h, 2 h + 1 of buffer b)
+  auto chunk = [&](int b, int h, int c0) {
+    if (c0 > pos_hi) return;  // above every row of this wave
+    // every key at or below every row of the wave and inside the sequence
+    const bool full = c0 + 31 <= pos_lo && c0 + 31 < t1;
+    uint4 kf[2][DS];
+    const uint4* kb = &sk[b][(2 * h + (l16 >> 3)) * BU];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int s = 0; s < DS; ++s) kf[hh][s] = kb[((s * 2 + hh) * 4 + g) * 8 + (l16 & 7)];
+    uint4 pf[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DS; ++s) {
+        s0 = mfma16x16x32(kf[0][s], qf[nt][s], s0);
+        s1 = mfma16x16x32(kf[1][s], qf[nt][s], s1);
+      }
+      float raw[8];  // raw scores, -inf where masked
+#pragma unroll
+      for (int j = 0; j < 8; ++j) raw[j] = (j < 4) ? s0[j] : s1[j - 4];
+      if (!full) {
+        asm volatile("");  // keeps the mask a branch around diagonal chunks (not selects everywhere)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) raw[j] = (c0 + 8 * g + j <= klim[nt]) ? raw[j] : -INFINITY;
+      }
+      float mx = raw[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) mx = fmaxf(mx, raw[j]);
+      mx *= scale;  // base-2 logit (scale > 0)
+      if (__any(mx > mrun[nt] + kPrefillRescaleLog2)) {
+        // the query vector's maximum over the chunk, from all lanes holding it
+        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        const bool grow = mx > mrun[nt] + kPrefillRescaleLog2;
+        const float alpha = grow ? ((mrun[nt] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mrun[nt] - mx)) : 1.f;
+        if (grow) mrun[nt] = mx;
+        lrun[nt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) acc[dt][nt] *= alpha;
+      }
+      // p = 2^(raw scale - m): one FMA per score; with no maximum yet (no key
+      // of the query vector so far) every p is 0
+      const float mneg = (mrun[nt] == -INFINITY) ? -INFINITY : -mrun[nt];
+      float p[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) p[j] = __builtin_amdgcn_exp2f(fmaf(raw[j], scale, mneg));
+      float ps = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ps += p[j];
+      lrun[nt] += ps;
+      pf[nt] = make_uint4(cvt_pk_bf16(p[0], p[1]), cvt_pk_bf16(p[2], p[3]), cvt_pk_bf16(p[4], p[5]),
+                          cvt_pk_bf16(p[6], p[7]));
+    }
+    // V^T operands read once the probabilities are done (shorter live range)
+    uint4 vf[DT];
+    const uint4* vb = &sv[b][(2 * h + (g >> 1)) * BU];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[dt] = vb[(dt * 2 + (g & 1)) * 16 + l16];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[dt][nt] = mfma16x16x32(vf[dt], pf[nt], acc[dt][nt]);
+  };
+
+  issue(0, 0);
+  if (ns > 1) issue(1, 1);
+  for (int j = 0; j < ns; ++j) {
+    // stage j has landed (stage j + 1 may still be in flight), every wave is
+    // done with stage j - 1, whose buffer stage j + 2 now fills
+    if (j + 1 < ns) {
+      SPEC_WAIT_VM_LDS(LPW);
+    } else {
+      SPEC_WAIT_VM_LDS(0);
+    }
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (j + 2 < ns) issue(j + 2, (j + 2) % NB);
+    const int b = j % NB;
+    if (j == ns - 1 && t1 < 64 * ns) {
+      // keys past the sequence in the last stage hold stale or uninitialised
+      // V (their probabilities are 0, but 0 x NaN is not): zero them in LDS.
+      // Unit ((d / 16) 2 + k / 8) 16 + d % 16 of a page block holds keys
+      // 8 (k / 8) .. + 7 of dim d.
+      for (int u = threadIdx.x; u < SU; u += 64 * NW) {
+        const int k0 = 64 * j + (u / BU) * 16 + ((u % BU) / 16 % 2) * 8;
+        const int keep = min(max(t1 - k0, 0), 8);
+        if (keep < 8) {
+          uint4 v = sv[b][u];
+          v.x = mask_pair(v.x, keep);
+          v.y = mask_pair(v.y, keep - 2);
+          v.z = mask_pair(v.z, keep - 4);
+          v.w = mask_pair(v.w, keep - 6);
+          sv[b][u] = v;
+        }
+      }
+      __syncthreads();
+    }
+    chunk(b, 0, 64 * j);
+    chunk(b, 1, 64 * j + 32);
+  }
+
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float lt = lrun[nt];
+    lt += __shfl_xor(lt, 16, kWave);
+    lt += __shfl_xor(lt, 32, kWave);
+    const int m = 32 * wave + 16 * nt + l16;
+    if (!vval[nt]) continue;
+    const float inv = (lt > 0.f) ? 1.f / lt : 0.f;
+    bf16_t* o = static_cast<bf16_t*>(a.out) + (static_cast<size_t>(it.row0 + m / G) * a.Hq + gkv * G + m % G) * HD;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const f32x4 v = acc[dt][nt];
+      *reinterpret_cast<uint2*>(o + 16 * dt + 4 * g) =
+          make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+    }
+  }
+}
+
 template <int HD, int DPT>
 __global__ __launch_bounds__(HD / DPT * kCombineQv) void attn_combine_kernel(AttnArgs a,
                                                                               const AttnGroup* __restrict__ groups) {
@@ -530,6 +757,20 @@ hipError_t launch_attention_bf16(const AttnArgs& a, const AttnItem* d_items, int
   if (a.hd == 128) return launch_bf16_hd<128>(a, d_items, n_items, d_groups, n_groups, nt, w, st);
   if (a.hd == 64) return launch_bf16_hd<64>(a, d_items, n_items, d_groups, n_groups, nt, w, st);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_attention_prefill_bf16(const AttnArgs& a, const AttnItem* d_items, int n_items, hipStream_t st) {
+  if (n_items <= 0) return hipSuccess;
+  if (256 % (a.Hq / a.Hkv)) return hipErrorInvalidValue;
+  dim3 grid(n_items * a.Hkv);
+  if (a.hd == 128) launch_kernel(attn_prefill_bf16_kernel<128>, grid, dim3(512), 0, st, a, d_items);
+  else if (a.hd == 64) launch_kernel(attn_prefill_bf16_kernel<64>, grid, dim3(512), 0, st, a, d_items);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+const char* attn_prefill_kernel_name(int hd) {
+  return hd == 128 ? "attn_prefill_bf16_kernel<128>" : "attn_prefill_bf16_kernel<64>";
 }
 
 hipError_t launch_attention_f32(const AttnArgs& a, int R, const int32_t* d_row_seq,

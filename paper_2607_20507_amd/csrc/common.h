@@ -90,6 +90,35 @@ __device__ __forceinline__ f32x4 mfma16x16x32v(const u32x4& a, const u32x4& b, f
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS loads (global -> LDS with no register staging) and the
+// explicit waits their users issue.
+
+typedef __attribute__((address_space(3))) void* lptr_t;
+
+// One global_load_lds_dwordx4: lane i's 16 bytes at base + off_bytes land in
+// LDS at byte lds + 16 i (M0 holds the LDS address; one wait state separates
+// the M0 write from the load).  Issued as inline asm so that the compiler's
+// own wait insertion (which cannot tell the LDS stages apart and would wait
+// for every load in flight before each LDS read) leaves these loads to the
+// explicit per-stage waits of the kernel.
+__device__ __forceinline__ void load_lds16(const void* base, uint32_t off_bytes, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1" ::"v"(off_bytes),
+      "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lptr_t)(p)));
+}
+
+// s_waitcnt for at most n outstanding vector-memory operations (vmcnt bits
+// [3:0] and [15:14]) and no outstanding LDS operation (lgkmcnt 0); expcnt is
+// left at its maximum.
+#define SPEC_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4))
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));

@@ -100,7 +100,7 @@ struct Fwd {
 
 struct FwdOff {
   size_t tok, pos, slot, seqi, pt, items, groups, lmr, lmm, tb = 0, tm = 0;
-  bool tree = false;
+  bool tree = false, prefill = false;
   int n_items = 0, n_groups = 0, nt = 1, w = 1, R = 0, n_lm = 0, ptab_stride = 1;
   bool lm_map = false;
   double attn_keys = 0, attn_qk = 0;  // sum of context lengths; sum over rows of (pos + 1)
@@ -285,7 +285,8 @@ FwdOff add_forward(spec_ctx* ctx, const Model& M, const Fwd& f, MetaBlock& mb) {
   o.pt = mb.add(f.ptab);
   o.ptab_stride = f.ptab_stride;
   if (M.dt() == 1) {
-    AttnPlan p = plan_attention(f.segs, M.G(), M.d.n_kv_heads, kMaxParts);
+    AttnPlan p = plan_attention(f.segs, M.G(), M.d.n_kv_heads, kMaxParts, kAttnTargetWgs, f.tbase.empty());
+    o.prefill = p.prefill;
     o.items = mb.add(p.items);
     o.groups = mb.add(p.groups);
     o.n_items = static_cast<int>(p.items.size());
@@ -395,11 +396,15 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
     a.vpool = M.vl(l);
     if (dt == 1) {
       // bytes: every cached key and value once, queries in, output out
-      const bool timed = tm.wants(attn_kernel_name(d.head_dim, o.nt, o.w, o.tree));
+      const bool timed = tm.wants(o.prefill ? attn_prefill_kernel_name(d.head_dim)
+                                            : attn_kernel_name(d.head_dim, o.nt, o.w, o.tree));
       if (timed) tm.begin(st);
-      HIPC(launch_attention_bf16(a, reinterpret_cast<const AttnItem*>(dev + o.items), o.n_items,
-                                 reinterpret_cast<const AttnGroup*>(dev + o.groups), o.n_groups,
-                                 o.nt, o.w, st));
+      if (o.prefill)
+        HIPC(launch_attention_prefill_bf16(a, reinterpret_cast<const AttnItem*>(dev + o.items), o.n_items, st));
+      else
+        HIPC(launch_attention_bf16(a, reinterpret_cast<const AttnItem*>(dev + o.items), o.n_items,
+                                   reinterpret_cast<const AttnGroup*>(dev + o.groups), o.n_groups,
+                                   o.nt, o.w, st));
       if (timed)
         tm.end(st, (o.attn_keys * d.n_kv_heads * 2.0 + 2.0 * R * d.n_heads) * d.head_dim * esz,
                4.0 * o.attn_qk * d.n_heads * d.head_dim);
@@ -550,7 +555,7 @@ spec_status run_kernels(spec_ctx* ctx, const std::vector<int64_t>& key, const Me
 
 // Shape key of a forward: everything its grids and metadata layout depend on.
 void key_forward(std::vector<int64_t>& k, const FwdOff& o) {
-  const int64_t v[] = {o.R, o.n_items, o.n_groups, o.nt, o.w, o.n_lm, o.lm_map, o.ptab_stride,
+  const int64_t v[] = {o.R, o.n_items, o.n_groups, o.nt, o.w, o.prefill, o.n_lm, o.lm_map, o.ptab_stride,
                        static_cast<int64_t>(o.tok), static_cast<int64_t>(o.pos),
                        static_cast<int64_t>(o.slot), static_cast<int64_t>(o.seqi),
                        static_cast<int64_t>(o.pt), static_cast<int64_t>(o.items),

@@ -514,22 +514,6 @@ hipError_t gemv(int R, int N, int K, const void* X, const void* W, void* Y, hipS
 // (K % 128 == 0), so the step count is a multiple of 4 and the k-loop
 // unrolls by 4 without remainders.
 
-typedef __attribute__((address_space(3))) void* lptr_t;
-
-// One global_load_lds_dwordx4: lane i's 16 bytes at base + off_bytes land in
-// LDS at byte lds + 16 i (M0 holds the LDS address; one wait state separates
-// the M0 write from the load).  Issued as inline asm so that the compiler's
-// own wait insertion (which cannot tell the LDS stages apart and would wait
-// for every load in flight before each LDS read) leaves these loads to the
-// explicit per-stage waits of the kernel.
-__device__ __forceinline__ void load_lds16(const void* base, uint32_t off_bytes, uint32_t lds) {
-  asm volatile(
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, %1" ::"v"(off_bytes),
-      "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
-      : "memory", "m0");
-}
 // MFMA accumulating in place, as inline asm: each accumulator stays in one
 // AGPR tuple across the k-loop.  Compiler-generated MFMAs in this loop rotate
 // the loop-carried accumulators through spare AGPRs, with four copies and a
@@ -542,15 +526,6 @@ __device__ __forceinline__ void load_lds16(const void* base, uint32_t off_bytes,
 __device__ __forceinline__ void mfma_acc(f32x4& acc, const u32x4& a, const u32x4& b) {
   asm volatile("s_nop 1\n\tv_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lptr_t)(p)));
-}
-
-// s_waitcnt for at most n outstanding vector-memory operations (vmcnt bits
-// [3:0] and [15:14]) and no outstanding LDS operation (lgkmcnt 0); expcnt is
-// left at its maximum.
-#define SPEC_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4))
 
 template <int EPI, int MTW, int NTW>
 __global__ __launch_bounds__(256, 1) void gemm_mfma2_bf16(const bf16_t* __restrict__ X,

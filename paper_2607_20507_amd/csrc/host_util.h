@@ -196,6 +196,7 @@ struct AttnSegment {
 };
 
 struct AttnPlan {
+  bool prefill = false;  // items for attn_prefill_bf16_kernel (nt, w, groups unused)
   int nt = 1;
   int w = 1;  // waves per workgroup
   std::vector<AttnItem> items;
@@ -205,7 +206,12 @@ struct AttnPlan {
 
 // Tile rows into query tiles of (16 nt / G) rows and split key ranges so that
 // the launch has about `target_wgs` workgroups; at most `max_parts` partials.
+// Runs of at least kPrefillMinRows rows in every segment (prefill chunks) with
+// 256 % G == 0 and at most kPrefillMaxKeys keys take the prefill form instead: blocks of 256 / G rows against
+// all their keys, heaviest first (allow_prefill = false keeps the tiled form).
+constexpr int kPrefillMinRows = 64;
+constexpr int kPrefillMaxKeys = 16384;  // the prefill kernel stages at most 1024 page ids
 AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, int max_parts,
-                        int target_wgs = kAttnTargetWgs);
+                        int target_wgs = kAttnTargetWgs, bool allow_prefill = true);
 
 }  // namespace spec

@@ -300,6 +300,9 @@ spec_status spec_op_attention(int32_t dtype, int32_t n_seqs, const int32_t* rows
   a.part_o = reinterpret_cast<float*>(part);
   a.part_ml = reinterpret_cast<float*>(part + align_up(sizeof(float) * static_cast<size_t>(kOpMaxParts) *
                                                        n_kv_heads * 64 * head_dim));
+  if (a.dtype == 1 && plan.prefill)
+    return hip_status(launch_attention_prefill_bf16(a, reinterpret_cast<const AttnItem*>(ws + oit),
+                                                    static_cast<int>(plan.items.size()), st));
   if (a.dtype == 1)
     return hip_status(launch_attention_bf16(a, reinterpret_cast<const AttnItem*>(ws + oit),
                                             static_cast<int>(plan.items.size()),

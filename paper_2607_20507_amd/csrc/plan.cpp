@@ -7,10 +7,30 @@
 namespace spec {
 
 AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, int max_parts,
-                        int target_wgs) {
+                        int target_wgs, bool allow_prefill) {
   AttnPlan p;
-  int max_rows = 1;
-  for (const auto& s : segs) max_rows = std::max(max_rows, s.nrows);
+  int max_rows = 1, min_rows = 1 << 30;
+  for (const auto& s : segs) {
+    max_rows = std::max(max_rows, s.nrows);
+    min_rows = std::min(min_rows, s.nrows);
+  }
+  int max_keys = 0;
+  for (const auto& s : segs) max_keys = std::max(max_keys, s.pos0 + s.nrows);
+  if (allow_prefill && !segs.empty() && min_rows >= kPrefillMinRows && G >= 1 && 256 % G == 0 &&
+      max_keys <= kPrefillMaxKeys) {
+    p.prefill = true;
+    const int br = 256 / G;
+    for (const auto& s : segs)
+      for (int r = 0; r < s.nrows; r += br) {
+        const int n = std::min(br, s.nrows - r);
+        p.items.push_back(AttnItem{s.row0 + r, n, s.pos0 + r, s.seq, 0, s.pos0 + r + n, -1, 0});
+      }
+    // heaviest (most keys) first, so that the long blocks start in the first
+    // round of workgroups
+    std::stable_sort(p.items.begin(), p.items.end(),
+                     [](const AttnItem& x, const AttnItem& y) { return x.t1 > y.t1; });
+    return p;
+  }
   // query vectors per tile: rows * G <= 16 * nt, nt in {1, 2, 4}
   const int want = std::min(max_rows * G, 64);
   p.nt = want <= 16 ? 1 : (want <= 32 ? 2 : 4);

@@ -335,6 +335,13 @@ def _attn_case(dt, rows, pos0, Hq, Hkv, hd, seed, check_seqs=None):
     (1, [3, 17], [1, 33], 16, 16, 64),             # rows beyond one tile with G = 1
     (0, [5, 1], [128, 3], 4, 4, 64),               # fp32 path
     (0, [40], [0], 4, 4, 64),
+    # the prefill form (every sequence 64+ rows): blocks of 256 / G rows
+    # against all their keys, K / V staged in LDS 64 keys at a time
+    (1, [300], [0], 32, 8, 64),                    # head dim 64, a ragged last block and stage
+    (1, [200, 90], [0, 333], 32, 8, 128),          # two sequences, the second a later chunk
+    (1, [256, 70], [5, 0], 16, 16, 64),            # G = 1: 256-row blocks
+    (1, [130], [1000], 8, 2, 64),                  # a chunk continuing at position 1000
+    (1, [1024], [0], 32, 8, 128),                  # 16 blocks, 16 stages for the last
 ])
 def test_attention_small(dt, rows, pos0, Hq, Hkv, hd):
     err = _attn_case(dt, rows, pos0, Hq, Hkv, hd, seed=sum(rows) + Hq)
