@@ -429,16 +429,22 @@ __global__ __launch_bounds__(512, 1) void attn_prefill_bf16_kernel(AttnArgs a, c
   }
 
   // one 32-key chunk (keys c0 .., pages 2 h, 2 h + 1 of buffer b)
-  auto chunk = [&](int b, int h, int c0) {
-    if (c0 > pos_hi) return;  // above every row of this wave
-    // every key at or below every row of the wave and inside the sequence
-    const bool full = c0 + 31 <= pos_lo && c0 + 31 < t1;
-    uint4 kf[2][DS];
+  // K and V^T operands of chunk h of buffer b, read from LDS
+  auto read_k = [&](int b, int h, uint4 (&kf)[2][DS]) {
     const uint4* kb = &sk[b][(2 * h + (l16 >> 3)) * BU];
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
       for (int s = 0; s < DS; ++s) kf[hh][s] = kb[((s * 2 + hh) * 4 + g) * 8 + (l16 & 7)];
+  };
+  auto read_v = [&](int b, int h, uint4 (&vf)[DT]) {
+    const uint4* vb = &sv[b][(2 * h + (g >> 1)) * BU];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[dt] = vb[(dt * 2 + (g & 1)) * 16 + l16];
+  };
+  auto chunk = [&](int c0, const uint4 (&kf)[2][DS], const uint4 (&vf)[DT]) {
+    // every key at or below every row of the wave and inside the sequence
+    const bool full = c0 + 31 <= pos_lo && c0 + 31 < t1;
     uint4 pf[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -484,11 +490,6 @@ __global__ __launch_bounds__(512, 1) void attn_prefill_bf16_kernel(AttnArgs a, c
       pf[nt] = make_uint4(cvt_pk_bf16(p[0], p[1]), cvt_pk_bf16(p[2], p[3]), cvt_pk_bf16(p[4], p[5]),
                           cvt_pk_bf16(p[6], p[7]));
     }
-    // V^T operands read once the probabilities are done (shorter live range)
-    uint4 vf[DT];
-    const uint4* vb = &sv[b][(2 * h + (g >> 1)) * BU];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vf[dt] = vb[(dt * 2 + (g & 1)) * 16 + l16];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -529,8 +530,16 @@ __global__ __launch_bounds__(512, 1) void attn_prefill_bf16_kernel(AttnArgs a, c
       }
       __syncthreads();
     }
-    chunk(b, 0, 64 * j);
-    chunk(b, 1, 64 * j + 32);
+    // the first chunk's operands and the second's K read up front, so that
+    // their LDS latency hides under the first chunk's arithmetic (the
+    // second's V^T after it: registers)
+    uint4 kf0[2][DS], vf0[DT], kf1[2][DS], vf1[DT];
+    read_k(b, 0, kf0);
+    read_v(b, 0, vf0);
+    read_k(b, 1, kf1);
+    if (64 * j <= pos_hi) chunk(64 * j, kf0, vf0);  // else above every row of this wave
+    read_v(b, 1, vf1);
+    if (64 * j + 32 <= pos_hi) chunk(64 * j + 32, kf1, vf1);
   }
 
 #pragma unroll
