@@ -388,9 +388,13 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
       HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, nullptr, kEpiQKVRope, nullptr, &fq));
     } else {
       if (!normed) HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
-      HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr));
-      HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, qkv, I(o.pos),
-                          I(o.slot), q, M.kl(l), M.vl(l), st, dt == 1));
+      // a split-K QKV projection leaves its partials for rope_kv to sum
+      GemmNorm defer;
+      defer.defer = M.qkvw() % 4 == 0 && M.qkvw() <= kRopeSplitMaxWidth;
+      HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr, nullptr, &defer));
+      HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta,
+                          defer.split > 0 ? defer.part : qkv, I(o.pos), I(o.slot), q, M.kl(l), M.vl(l), st,
+                          dt == 1, defer.split));
     }
     a.kpool = M.kl(l);
     a.vpool = M.vl(l);

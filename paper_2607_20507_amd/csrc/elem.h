@@ -24,10 +24,14 @@ hipError_t launch_rmsnorm(int dtype, int R, int d, const float* h, const int32_t
 // rot_tiled: the q and k head columns of qkv are in the rotary tile order of
 // the tiled QKV weight (what the bf16 GEMMs produce from it): position
 // 16 (i / 8) + i % 8 holds dim i, and the position 8 further holds dim
-// i + hd / 2 (i < hd / 2); v columns are in plain order.
+// i + hd / 2 (i < hd / 2); v columns are in plain order.  splits > 0: qkv
+// holds that many split-K partials [splits][R][width] of the QKV GEMM (the
+// deferred reduction of GemmNorm::defer), summed here in split order; the
+// row (width = (Hq + 2 Hkv) hd floats, a multiple of 4) is staged in LDS.
+constexpr int kRopeSplitMaxWidth = 12288;
 hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta, const float* qkv,
                           const int32_t* pos, const int32_t* slot, void* q, void* kpool,
-                          void* vpool, hipStream_t st, bool rot_tiled = false);
+                          void* vpool, hipStream_t st, bool rot_tiled = false, int splits = 0);
 
 // Zero the K and V entries of `n` flat slots (device list) in every layer of
 // a pool whose layer l holds K at kv + l * layer_stride and V at + v_off

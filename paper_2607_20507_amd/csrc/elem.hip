@@ -196,17 +196,49 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int d, const float* __rest
 // One workgroup per row; thread (head, i) rotates the pair (i, i + hd/2).
 constexpr int kRopeMaxHalf = 128;  // head_dim <= 256
 
-template <typename T>
+// SPLIT: qkv holds S split-K partials [S][R][width] (split stride sstride
+// floats) of the QKV GEMM instead of its output; the row's sum over the
+// splits, in split order as splitk_reduce4 takes it, goes to LDS first (all
+// of a thread's loads of 8 splits in flight together), which saves the
+// reduction's launch and its round trip through memory.
+
+template <typename T, bool SPLIT>
 __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, float theta,
                                                       const float* __restrict__ qkv,
                                                       const int32_t* __restrict__ pos,
                                                       const int32_t* __restrict__ slot,
                                                       T* __restrict__ q, T* __restrict__ kpool,
-                                                      T* __restrict__ vpool, bool rot_tiled) {
+                                                      T* __restrict__ vpool, bool rot_tiled, int S,
+                                                      size_t sstride) {
   const int r = blockIdx.x;
   const int half = hd / 2;
   const int width = (Hq + 2 * Hkv) * hd;
+  __shared__ float4 s_row[SPLIT ? kRopeSplitMaxWidth / 4 : 1];
   const float* x = qkv + static_cast<size_t>(r) * width;
+  if constexpr (SPLIT) {
+    const float4* src = reinterpret_cast<const float4*>(x);
+    const size_t st4 = sstride / 4;
+    constexpr int B = 8;
+    for (int c = threadIdx.x; c < width / 4; c += blockDim.x) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int s0 = 0; s0 < S; s0 += B) {
+        float4 p[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) p[b] = src[static_cast<size_t>(min(s0 + b, S - 1)) * st4 + c];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+          if (s0 + b >= S) break;
+          v.x += p[b].x;
+          v.y += p[b].y;
+          v.z += p[b].z;
+          v.w += p[b].w;
+        }
+      }
+      s_row[c] = v;
+    }
+    __syncthreads();
+    x = reinterpret_cast<const float*>(s_row);
+  }
   const double p = static_cast<double>(pos[r]);
   const int sl = slot[r];
   const int page = sl >> 4, off = sl & 15;
@@ -388,16 +420,28 @@ hipError_t launch_rmsnorm(int dtype, int R, int d, const float* h, const int32_t
 
 hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta, const float* qkv,
                           const int32_t* pos, const int32_t* slot, void* q, void* kpool,
-                          void* vpool, hipStream_t st, bool rot_tiled) {
+                          void* vpool, hipStream_t st, bool rot_tiled, int splits) {
   if (R <= 0) return hipSuccess;
   if (hd % 2 != 0 || hd > 2 * kRopeMaxHalf || (rot_tiled && hd % 16 != 0)) return hipErrorInvalidValue;
-  if (dtype == 0)
-    rope_kv_kernel<float><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
-                                             static_cast<float*>(kpool), static_cast<float*>(vpool), rot_tiled);
+  const int width = (Hq + 2 * Hkv) * hd;
+  if (splits > 0 && (width % 4 || width > kRopeSplitMaxWidth)) return hipErrorInvalidValue;
+  const size_t sstride = static_cast<size_t>(R) * width;
+  if (dtype == 0 && splits > 0)
+    rope_kv_kernel<float, true><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
+                                                   static_cast<float*>(kpool), static_cast<float*>(vpool),
+                                                   rot_tiled, splits, sstride);
+  else if (dtype == 0)
+    rope_kv_kernel<float, false><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
+                                                    static_cast<float*>(kpool), static_cast<float*>(vpool),
+                                                    rot_tiled, 0, 0);
+  else if (splits > 0)
+    rope_kv_kernel<bf16_t, true><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
+                                                    static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool),
+                                                    rot_tiled, splits, sstride);
   else
-    rope_kv_kernel<bf16_t><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
-                                              static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool),
-                                              rot_tiled);
+    rope_kv_kernel<bf16_t, false><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
+                                                     static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool),
+                                                     rot_tiled, 0, 0);
   return hipGetLastError();
 }
 

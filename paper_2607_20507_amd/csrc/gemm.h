@@ -55,6 +55,13 @@ struct GemmNorm {
   float eps = 0.f;
   void* y = nullptr;        // bf16 [R][N]
   bool done = false;
+  // kEpiStoreF32 (bf16, no row map): with defer set, a launch that splits K
+  // leaves its partials [split][R][N] in the split-K workspace at `part`
+  // for the consumer to sum (launch_rope_kv) and skips the reduction;
+  // split = 0 when it did not split (Y then holds the output).
+  bool defer = false;
+  int split = 0;
+  const float* part = nullptr;
 };
 
 // dtype: 0 = fp32 (X, W, SwiGLU output fp32), 1 = bf16 (X, W, SwiGLU output bf16).

@@ -1300,6 +1300,11 @@ hipError_t mfma2_t(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* 
 template <int EPI>
 hipError_t splitk_finish(const float* ws, int S, int R, int N, void* Y, hipStream_t st, const int32_t* rm,
                          GemmNorm* norm) {
+  if (EPI == kEpiStoreF32 && norm && norm->defer && !rm) {  // the consumer sums the partials
+    norm->split = S;
+    norm->part = ws;
+    return hipSuccess;
+  }
   if (EPI == kEpiAddF32 && norm && !rm && N % 4 == 0 && N <= 4 * 256 * kNormRegChunks) {
     const int nch = (N / 4 + 255) / 256;
     auto* k = nch <= 1 ? splitk_reduce_norm<1> : nch <= 2 ? splitk_reduce_norm<2>
@@ -1515,11 +1520,16 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
 hipError_t launch_gemm(int dtype, int R, int N, int K, const void* X, const void* W, void* Y,
                        int epi, hipStream_t st, const int32_t* row_map, float* splitk_ws,
                        size_t splitk_bytes, GemmNorm* norm) {
-  if (norm) norm->done = false;
+  if (norm) {
+    norm->done = false;
+    norm->split = 0;
+    norm->part = nullptr;
+  }
   if (R <= 0 || N <= 0) return hipSuccess;
   switch (epi) {
     case kEpiStoreF32:
-      return dispatch<kEpiStoreF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes);
+      return dispatch<kEpiStoreF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes,
+                                    dtype == 1 ? norm : nullptr);
     case kEpiAddF32:
       return dispatch<kEpiAddF32>(dtype, R, N, K, X, W, Y, st, row_map, splitk_ws, splitk_bytes,
                                   dtype == 1 ? norm : nullptr);
