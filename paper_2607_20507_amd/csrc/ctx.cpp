@@ -390,7 +390,7 @@ spec_status launch_forward(spec_ctx* ctx, const Model& M, const FwdOff& o, const
       if (!normed) HIPC(launch_rmsnorm(dt, R, d.d_model, h, nullptr, L.attn_norm, d.rms_eps, y, st));
       // a split-K QKV projection leaves its partials for rope_kv to sum
       GemmNorm defer;
-      defer.defer = M.qkvw() % 4 == 0 && M.qkvw() <= kRopeSplitMaxWidth;
+      defer.defer = d.head_dim % 4 == 0 && (d.n_heads / d.n_kv_heads + 2) * d.head_dim <= kRopeSplitMaxWidth;
       HIPC(gemm(R, M.qkvw(), d.d_model, y, L.wqkv, qkv, kEpiStoreF32, nullptr, nullptr, &defer));
       HIPC(launch_rope_kv(dt, R, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta,
                           defer.split > 0 ? defer.part : qkv, I(o.pos), I(o.slot), q, M.kl(l), M.vl(l), st,

@@ -27,7 +27,8 @@ hipError_t launch_rmsnorm(int dtype, int R, int d, const float* h, const int32_t
 // i + hd / 2 (i < hd / 2); v columns are in plain order.  splits > 0: qkv
 // holds that many split-K partials [splits][R][width] of the QKV GEMM (the
 // deferred reduction of GemmNorm::defer), summed here in split order; the
-// row (width = (Hq + 2 Hkv) hd floats, a multiple of 4) is staged in LDS.
+// columns of one KV head group ((Hq / Hkv + 2) hd floats, hd % 4 == 0) are
+// staged in LDS.  One workgroup per (row, KV head).
 constexpr int kRopeSplitMaxWidth = 12288;
 hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta, const float* qkv,
                           const int32_t* pos, const int32_t* slot, void* q, void* kpool,

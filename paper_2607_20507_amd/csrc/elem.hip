@@ -193,15 +193,16 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int d, const float* __rest
   for (int i = threadIdx.x; i < d; i += blockDim.x) o[i] = Elem<T>::from_f32(x[i] * inv * Elem<T>::to_f32(w[i]));
 }
 
-// One workgroup per row; thread (head, i) rotates the pair (i, i + hd/2).
+// One workgroup per (row, KV head group): workgroup (r, g) of a grid (R, ng)
+// handles the KV heads [g Hkv / ng, (g + 1) Hkv / ng) and the query heads
+// that share them; thread (head, i) rotates the pair (i, i + hd/2).
 constexpr int kRopeMaxHalf = 128;  // head_dim <= 256
 
 // SPLIT: qkv holds S split-K partials [S][R][width] (split stride sstride
-// floats) of the QKV GEMM instead of its output; the row's sum over the
-// splits, in split order as splitk_reduce4 takes it, goes to LDS first (all
-// of a thread's loads of 8 splits in flight together), which saves the
-// reduction's launch and its round trip through memory.
-
+// floats) of the QKV GEMM instead of its output; the workgroup's columns,
+// summed over the splits in split order as splitk_reduce4 takes them, go to
+// LDS first (all of a thread's loads of 8 splits in flight together), which
+// saves the reduction's launch and its round trip through memory.
 template <typename T, bool SPLIT>
 __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, float theta,
                                                       const float* __restrict__ qkv,
@@ -213,18 +214,30 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
   const int r = blockIdx.x;
   const int half = hd / 2;
   const int width = (Hq + 2 * Hkv) * hd;
-  __shared__ float4 s_row[SPLIT ? kRopeSplitMaxWidth / 4 : 1];
+  const int kh0 = blockIdx.y * Hkv / gridDim.y, kh1 = (blockIdx.y + 1) * Hkv / gridDim.y;
+  const int qh0 = kh0 * (Hq / Hkv), qh1 = kh1 * (Hq / Hkv);
+  const int nq = qh1 - qh0, nk = kh1 - kh0;
   const float* x = qkv + static_cast<size_t>(r) * width;
+  // xq / xk / xv: the first column of query head qh0, key head kh0, value head kh0
+  const float* xq = x + qh0 * hd;
+  const float* xk = x + (Hq + kh0) * hd;
+  const float* xv = x + (Hq + Hkv + kh0) * hd;
+  __shared__ float4 s_cols[SPLIT ? kRopeSplitMaxWidth / 4 : 1];
   if constexpr (SPLIT) {
-    const float4* src = reinterpret_cast<const float4*>(x);
+    // local column lc of [q heads | k heads | v heads] comes from row column gc
+    const int nqc = nq * hd, nkc = nk * hd;
     const size_t st4 = sstride / 4;
     constexpr int B = 8;
-    for (int c = threadIdx.x; c < width / 4; c += blockDim.x) {
+    for (int c = threadIdx.x; c < (nqc + 2 * nkc) / 4; c += blockDim.x) {
+      const int lc = 4 * c;
+      const int gc = lc < nqc ? qh0 * hd + lc
+                              : (lc < nqc + nkc ? (Hq + kh0) * hd + lc - nqc : (Hq + Hkv + kh0) * hd + lc - nqc - nkc);
+      const float4* src = reinterpret_cast<const float4*>(x + gc);
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int s0 = 0; s0 < S; s0 += B) {
         float4 p[B];
 #pragma unroll
-        for (int b = 0; b < B; ++b) p[b] = src[static_cast<size_t>(min(s0 + b, S - 1)) * st4 + c];
+        for (int b = 0; b < B; ++b) p[b] = src[static_cast<size_t>(min(s0 + b, S - 1)) * st4];
 #pragma unroll
         for (int b = 0; b < B; ++b) {
           if (s0 + b >= S) break;
@@ -234,17 +247,19 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
           v.w += p[b].w;
         }
       }
-      s_row[c] = v;
+      s_cols[c] = v;
     }
     __syncthreads();
-    x = reinterpret_cast<const float*>(s_row);
+    xq = reinterpret_cast<const float*>(s_cols);
+    xk = xq + nqc;
+    xv = xk + nkc;
   }
   const double p = static_cast<double>(pos[r]);
   const int sl = slot[r];
   const int page = sl >> 4, off = sl & 15;
   const double lt = log(static_cast<double>(theta));
   // the row's rotation angles (they depend on the pair index only, not on
-  // the head), once per row in fp64
+  // the head), once per workgroup in fp64
   __shared__ float s_cos[kRopeMaxHalf], s_sin[kRopeMaxHalf];
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     double sn, cs;
@@ -266,13 +281,14 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
       reinterpret_cast<float4*>(dst)[1] = make_float4(v[4], v[5], v[6], v[7]);
     }
   };
+  // local head h < nq: query head qh0 + h; else key head kh0 + h - nq
   if (half % 8 == 0) {
     const int groups = half / 8;
-    for (int e = threadIdx.x; e < (Hq + Hkv) * groups; e += blockDim.x) {
-      const int head = e / groups, t = e % groups, i0 = 8 * t;
+    for (int e = threadIdx.x; e < (nq + nk) * groups; e += blockDim.x) {
+      const int h = e / groups, t = e % groups, i0 = 8 * t;
       // rot_tiled: the q and k columns of each head are in the rotary tile
       // order of the tiled QKV weight (rows 8t..8t+7, then hd/2+8t.. of tile t)
-      const float* src = x + head * hd;
+      const float* src = h < nq ? xq + h * hd : xk + (h - nq) * hd;
       const int ia = rot_tiled ? 16 * t : i0;
       const int ib = rot_tiled ? ia + 8 : i0 + half;
       const float4 a0 = reinterpret_cast<const float4*>(src + ia)[0], a1 = reinterpret_cast<const float4*>(src + ia)[1];
@@ -286,42 +302,39 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
         ra[j] = av[j] * c - bv[j] * sn;
         rb[j] = bv[j] * c + av[j] * sn;
       }
-      if (head < Hq) {
-        T* o = q + (static_cast<size_t>(r) * Hq + head) * hd;
+      if (h < nq) {
+        T* o = q + (static_cast<size_t>(r) * Hq + qh0 + h) * hd;
         put8(o + i0, ra);
         put8(o + i0 + half, rb);
       } else {
-        T* o = kpool + (static_cast<size_t>(page) * Hkv + (head - Hq)) * 16 * hd;
+        T* o = kpool + (static_cast<size_t>(page) * Hkv + kh0 + h - nq) * 16 * hd;
         put8(o + k_index<T>(off, i0, hd), ra);
         put8(o + k_index<T>(off, i0 + half, hd), rb);
       }
     }
   } else {
-    for (int e = threadIdx.x; e < (Hq + Hkv) * half; e += blockDim.x) {
-      const int head = e / half, i = e % half;
+    for (int e = threadIdx.x; e < (nq + nk) * half; e += blockDim.x) {
+      const int h = e / half, i = e % half;
       const float c = s_cos[i], s = s_sin[i];
-      // rot_tiled: the q and k columns of each head are in the rotary tile
-      // order of the tiled QKV weight (rows 8t..8t+7, then hd/2+8t.. of tile t)
-      const float* src = x + head * hd;
+      const float* src = h < nq ? xq + h * hd : xk + (h - nq) * hd;
       const int ia = rot_tiled ? 16 * (i / 8) + (i % 8) : i;
       const int ib = rot_tiled ? ia + 8 : i + half;
       const float a = src[ia], b = src[ib];
       const float ra = a * c - b * s, rb = b * c + a * s;
-      if (head < Hq) {
-        T* o = q + (static_cast<size_t>(r) * Hq + head) * hd;
+      if (h < nq) {
+        T* o = q + (static_cast<size_t>(r) * Hq + qh0 + h) * hd;
         o[i] = Elem<T>::from_f32(ra);
         o[i + half] = Elem<T>::from_f32(rb);
       } else {
-        T* o = kpool + (static_cast<size_t>(page) * Hkv + (head - Hq)) * 16 * hd;
+        T* o = kpool + (static_cast<size_t>(page) * Hkv + kh0 + h - nq) * 16 * hd;
         o[k_index<T>(off, i, hd)] = Elem<T>::from_f32(ra);
         o[k_index<T>(off, i + half, hd)] = Elem<T>::from_f32(rb);
       }
     }
   }
-  const float* v = x + (Hq + Hkv) * hd;
-  for (int e = threadIdx.x; e < Hkv * hd; e += blockDim.x) {
-    const int kh = e / hd, dd = e % hd;
-    vpool[(static_cast<size_t>(page) * Hkv + kh) * hd * 16 + v_index<T>(off, dd)] = Elem<T>::from_f32(v[e]);
+  for (int e = threadIdx.x; e < nk * hd; e += blockDim.x) {
+    const int kh = kh0 + e / hd, dd = e % hd;
+    vpool[(static_cast<size_t>(page) * Hkv + kh) * hd * 16 + v_index<T>(off, dd)] = Elem<T>::from_f32(xv[e]);
   }
 }
 
@@ -423,23 +436,26 @@ hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta
                           void* vpool, hipStream_t st, bool rot_tiled, int splits) {
   if (R <= 0) return hipSuccess;
   if (hd % 2 != 0 || hd > 2 * kRopeMaxHalf || (rot_tiled && hd % 16 != 0)) return hipErrorInvalidValue;
+  if (Hkv <= 0 || Hq % Hkv != 0) return hipErrorInvalidValue;
   const int width = (Hq + 2 * Hkv) * hd;
-  if (splits > 0 && (width % 4 || width > kRopeSplitMaxWidth)) return hipErrorInvalidValue;
+  // one workgroup per (row, KV head): its query heads, key head and value head
+  const dim3 grid(R, Hkv);
+  if (splits > 0 && (hd % 4 || (Hq / Hkv + 2) * hd > kRopeSplitMaxWidth)) return hipErrorInvalidValue;
   const size_t sstride = static_cast<size_t>(R) * width;
   if (dtype == 0 && splits > 0)
-    rope_kv_kernel<float, true><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
+    rope_kv_kernel<float, true><<<grid, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
                                                    static_cast<float*>(kpool), static_cast<float*>(vpool),
                                                    rot_tiled, splits, sstride);
   else if (dtype == 0)
-    rope_kv_kernel<float, false><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
+    rope_kv_kernel<float, false><<<grid, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
                                                     static_cast<float*>(kpool), static_cast<float*>(vpool),
                                                     rot_tiled, 0, 0);
   else if (splits > 0)
-    rope_kv_kernel<bf16_t, true><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
+    rope_kv_kernel<bf16_t, true><<<grid, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
                                                     static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool),
                                                     rot_tiled, splits, sstride);
   else
-    rope_kv_kernel<bf16_t, false><<<R, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
+    rope_kv_kernel<bf16_t, false><<<grid, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
                                                      static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool),
                                                      rot_tiled, 0, 0);
   return hipGetLastError();

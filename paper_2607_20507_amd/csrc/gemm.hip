@@ -1242,12 +1242,17 @@ int mfma2_splits(int MT, int NT, int R, int Nw, int K, size_t ws_bytes, int* k_l
 // projections: per-step terms for the MFMAs and the LDS loads of a
 // workgroup, times the k-steps and the rounds of workgroups over the 256
 // CUs, plus the split-K partial traffic.  Wide tiles waste rows or feed too
-// few CUs on small problems; narrow ones reload X and W more often.
+// few CUs on small problems; narrow ones reload X and W more often.  A split
+// SwiGLU pays its second pass as a launch of its own (≈ 6 us; the residual-add
+// and QKV reductions ride on launches that follow anyway: the RMSNorm and the
+// rotary embedding): with it the 41-128-row gate/up projections take narrow
+// unsplit tiles (41-row 1B-shaped gate/up 19.6 -> 16.9 us, 8B-shaped
+// 40.8 -> 36.2 us).
 struct Mfma2Shape {
   int mtw, ntw;
 };
 
-Mfma2Shape mfma2_shape(int R, int N, int Nw, int K, size_t ws_bytes) {
+Mfma2Shape mfma2_shape(int R, int N, int Nw, int K, size_t ws_bytes, bool swiglu) {
   Mfma2Shape best{2, 2};
   double best_t = 1e300;
   for (int mtw : {2, 4, 6, 8}) {
@@ -1260,7 +1265,7 @@ Mfma2Shape mfma2_shape(int R, int N, int Nw, int K, size_t ws_bytes) {
       const double steps = rounds * (k_len / 32);
       const double red_mb = S > 1 ? (S + 1.0) * R * N * 4.0 / 1e6 : 0.0;
       const double t = 0.0119 * steps * mtw * ntw + 0.0056 * steps * (32.0 * (mtw + ntw)) * 64.0 / 1024.0 +
-                       0.0574 * steps + 0.3048 * red_mb + (S > 1 ? -6.41 : 0.0);
+                       0.0574 * steps + 0.3048 * red_mb + (S > 1 ? (swiglu ? 6.0 : -6.41) : 0.0);
       if (t < best_t) {
         best_t = t;
         best = {mtw, ntw};
@@ -1389,7 +1394,7 @@ hipError_t mfma2(int R, int N, int K, const void* X, const void* W, void* Y, hip
   Mfma3Plan p3;
   if (use_mfma3(R, EPI == kEpiSwiGLU ? 2 * N : N, K, EPI, ws ? ws_bytes : 0, &p3))
     return mfma3<EPI>(R, N, K, x, w, Y, st, rm, ws, p3, norm);
-  const Mfma2Shape sh = mfma2_shape(R, N, EPI == kEpiSwiGLU ? 2 * N : N, K, ws ? ws_bytes : 0);
+  const Mfma2Shape sh = mfma2_shape(R, N, EPI == kEpiSwiGLU ? 2 * N : N, K, ws ? ws_bytes : 0, EPI == kEpiSwiGLU);
   switch (sh.mtw) {
     case 2: return mfma2_m<EPI, 2>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
     case 4: return mfma2_m<EPI, 4>(sh.ntw, R, N, K, x, w, Y, st, rm, ws, ws_bytes, norm);
@@ -1511,7 +1516,7 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
         snprintf(m3[e], sizeof(m3[e]), "gemm_mfma3_bf16<%d, %d, %d, %d>", e, kM3MB, kM3NB, kM3D);
     });
     if (use_mfma3(R, Nw, K, epi, splitk_bytes)) return m3[epi];
-    const Mfma2Shape sh = mfma2_shape(R, N, Nw, K, splitk_bytes);
+    const Mfma2Shape sh = mfma2_shape(R, N, Nw, K, splitk_bytes, epi == kEpiSwiGLU);
     return tiled[epi][sh.mtw / 2 - 1][sh.ntw == 2 ? 0 : (sh.ntw == 4 ? 1 : 2)];
   }
   return names[(std::max(R, 1) - 1) / 16][epi][0];
