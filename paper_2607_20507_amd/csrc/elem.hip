@@ -222,8 +222,8 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
   const float* xq = x + qh0 * hd;
   const float* xk = x + (Hq + kh0) * hd;
   const float* xv = x + (Hq + Hkv + kh0) * hd;
-  __shared__ float4 s_cols[SPLIT ? kRopeSplitMaxWidth / 4 : 1];
   if constexpr (SPLIT) {
+    extern __shared__ float4 s_cols[];  // (nq + 2 nk) hd floats, sized by the launch
     // local column lc of [q heads | k heads | v heads] comes from row column gc
     const int nqc = nq * hd, nkc = nk * hd;
     const size_t st4 = sstride / 4;
@@ -442,8 +442,9 @@ hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta
   const dim3 grid(R, Hkv);
   if (splits > 0 && (hd % 4 || (Hq / Hkv + 2) * hd > kRopeSplitMaxWidth)) return hipErrorInvalidValue;
   const size_t sstride = static_cast<size_t>(R) * width;
+  const size_t lds = static_cast<size_t>(Hq / Hkv + 2) * hd * sizeof(float);  // split partial sums
   if (dtype == 0 && splits > 0)
-    rope_kv_kernel<float, true><<<grid, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
+    rope_kv_kernel<float, true><<<grid, 256, lds, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<float*>(q),
                                                    static_cast<float*>(kpool), static_cast<float*>(vpool),
                                                    rot_tiled, splits, sstride);
   else if (dtype == 0)
@@ -451,7 +452,7 @@ hipError_t launch_rope_kv(int dtype, int R, int Hq, int Hkv, int hd, float theta
                                                     static_cast<float*>(kpool), static_cast<float*>(vpool),
                                                     rot_tiled, 0, 0);
   else if (splits > 0)
-    rope_kv_kernel<bf16_t, true><<<grid, 256, 0, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
+    rope_kv_kernel<bf16_t, true><<<grid, 256, lds, st>>>(Hq, Hkv, hd, theta, qkv, pos, slot, static_cast<bf16_t*>(q),
                                                     static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool),
                                                     rot_tiled, splits, sstride);
   else
