@@ -249,7 +249,6 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
       }
       s_cols[c] = v;
     }
-    __syncthreads();
     xq = reinterpret_cast<const float*>(s_cols);
     xk = xq + nqc;
     xv = xk + nkc;
@@ -259,13 +258,15 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(int Hq, int Hkv, int hd, f
   const int page = sl >> 4, off = sl & 15;
   const double lt = log(static_cast<double>(theta));
   // the row's rotation angles (they depend on the pair index only, not on
-  // the head), once per workgroup in fp64
+  // the head), once per workgroup in fp64, by the last hd / 2 threads (with
+  // the split, while the first ones wait for the partials)
   __shared__ float s_cos[kRopeMaxHalf], s_sin[kRopeMaxHalf];
-  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+  const int ai = static_cast<int>(threadIdx.x) - (static_cast<int>(blockDim.x) - half);
+  if (ai >= 0) {
     double sn, cs;
-    sincos(p * exp(-(2.0 * i / hd) * lt), &sn, &cs);
-    s_cos[i] = static_cast<float>(cs);
-    s_sin[i] = static_cast<float>(sn);
+    sincos(p * exp(-(2.0 * ai / hd) * lt), &sn, &cs);
+    s_cos[ai] = static_cast<float>(cs);
+    s_sin[ai] = static_cast<float>(sn);
   }
   __syncthreads();
   // Groups of 8 consecutive pairs (half % 8 == 0): in both column orders

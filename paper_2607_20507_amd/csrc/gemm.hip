@@ -1044,21 +1044,23 @@ __global__ __launch_bounds__(256) void splitk_reduce4(const float* __restrict__ 
 }
 
 // Split-K sum of a residual-add GEMM fused with the RMSNorm after it, one
-// workgroup per row m (N % 4 == 0, N <= 4 * 256 * kNormRegChunks): thread t
-// holds the NCH 4-column chunks t, t + 256, ... of the row in registers, adds
-// the partials in split order to h (as splitk_reduce does), writes h, then
-// y[m] = bf16(h[m] / rms(h[m]) (.) w) with the sum of squares taken per
-// thread in chunk order, then over the wave and the waves in a fixed order.
-// Every load of a thread goes out before the first is used (h, w, then the
-// partials in batches of 8 / NCH splits, indexes clamped so that the loads
-// are unconditional): one or two round trips instead of one per chunk.
-constexpr int kNormRegChunks = 8;
+// workgroup of T threads per row m (N % 4 == 0, N <= 4 * 1024 * kNormRegChunks):
+// thread t holds the NCH 4-column chunks t, t + T, ... of the row in
+// registers, adds the partials in split order to h (as splitk_reduce does),
+// writes h, then y[m] = bf16(h[m] / rms(h[m]) (.) w) with the sum of squares
+// taken per thread in chunk order, then over the wave and the waves in a
+// fixed order.  Every load of a thread goes out before the first is used (h,
+// w, then the partials in batches of 8 / NCH splits, indexes clamped so that
+// the loads are unconditional): with up to 1024 threads a row of 4096 columns
+// split 8 ways is one round trip (256 threads took four).
+constexpr int kNormRegChunks = 4;
 
-template <int NCH>
-__global__ __launch_bounds__(256) void splitk_reduce_norm(const float* __restrict__ part, int S, int R, int N,
-                                                          float* __restrict__ Y, const bf16_t* __restrict__ w,
-                                                          float eps, bf16_t* __restrict__ y) {
+template <int NCH, int T>
+__global__ __launch_bounds__(T) void splitk_reduce_norm(const float* __restrict__ part, int S, int R, int N,
+                                                        float* __restrict__ Y, const bf16_t* __restrict__ w,
+                                                        float eps, bf16_t* __restrict__ y) {
   constexpr int B = NCH >= 8 ? 1 : 8 / NCH;  // splits per batch of loads
+  constexpr int NW = T / kWave;
   const int m = blockIdx.x;
   const int nch = N / 4;
   const float4* pp = reinterpret_cast<const float4*>(part) + static_cast<size_t>(m) * nch;
@@ -1069,7 +1071,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_norm(const float* __restric
   uint2 wv[NCH];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    ch[c] = min(static_cast<int>(threadIdx.x) + c * 256, nch - 1);
+    ch[c] = min(static_cast<int>(threadIdx.x) + c * T, nch - 1);
     h[c] = hp[ch[c]];
     wv[c] = reinterpret_cast<const uint2*>(w)[ch[c]];
     v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1095,7 +1097,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_norm(const float* __restric
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    if (static_cast<int>(threadIdx.x) + c * 256 >= nch) continue;
+    if (static_cast<int>(threadIdx.x) + c * T >= nch) continue;
     h[c].x += v[c].x;
     h[c].y += v[c].y;
     h[c].z += v[c].z;
@@ -1108,14 +1110,16 @@ __global__ __launch_bounds__(256) void splitk_reduce_norm(const float* __restric
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
-  __shared__ float s_part[4];
+  __shared__ float s_part[NW];
   if ((threadIdx.x & (kWave - 1)) == 0) s_part[threadIdx.x / kWave] = ss;
   __syncthreads();
-  const float tot = s_part[0] + s_part[1] + s_part[2] + s_part[3];
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) tot += s_part[i];
   const float inv = 1.f / sqrtf(tot / static_cast<float>(N) + eps);
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    if (static_cast<int>(threadIdx.x) + c * 256 >= nch) continue;
+    if (static_cast<int>(threadIdx.x) + c * T >= nch) continue;
     const float v0 = h[c].x * inv * __uint_as_float(wv[c].x << 16);
     const float v1 = h[c].y * inv * __uint_as_float(wv[c].x & 0xFFFF0000u);
     const float v2 = h[c].z * inv * __uint_as_float(wv[c].y << 16);
@@ -1310,12 +1314,14 @@ hipError_t splitk_finish(const float* ws, int S, int R, int N, void* Y, hipStrea
     norm->part = ws;
     return hipSuccess;
   }
-  if (EPI == kEpiAddF32 && norm && !rm && N % 4 == 0 && N <= 4 * 256 * kNormRegChunks) {
-    const int nch = (N / 4 + 255) / 256;
-    auto* k = nch <= 1 ? splitk_reduce_norm<1> : nch <= 2 ? splitk_reduce_norm<2>
-            : nch <= 4 ? splitk_reduce_norm<4> : splitk_reduce_norm<8>;
-    k<<<R, 256, 0, st>>>(ws, S, R, N, static_cast<float*>(Y), static_cast<const bf16_t*>(norm->w), norm->eps,
-                         static_cast<bf16_t*>(norm->y));
+  if (EPI == kEpiAddF32 && norm && !rm && N % 4 == 0 && N <= 4 * 1024 * kNormRegChunks) {
+    const int n4 = N / 4;
+    auto* k = n4 <= 256 ? splitk_reduce_norm<1, 256> : n4 <= 512 ? splitk_reduce_norm<1, 512>
+            : n4 <= 1024 ? splitk_reduce_norm<1, 1024> : n4 <= 2048 ? splitk_reduce_norm<2, 1024>
+            : splitk_reduce_norm<4, 1024>;
+    const int T = n4 <= 256 ? 256 : n4 <= 512 ? 512 : 1024;
+    k<<<R, T, 0, st>>>(ws, S, R, N, static_cast<float*>(Y), static_cast<const bf16_t*>(norm->w), norm->eps,
+                       static_cast<bf16_t*>(norm->y));
     norm->done = true;
     return hipGetLastError();
   }
