@@ -495,13 +495,19 @@ bool check_ids(spec_ctx* ctx, int32_t n, const int64_t* ids, bool must_exist) {
 }
 
 // Run a call's kernels: eagerly through the metadata ring while kernel timing
-// is on or graphs are off, else by replaying the graph captured for `key`
+// is on, graphs are off or a forward of the call has more than
+// kGraphMaxRows rows, else by replaying the graph captured for `key`
 // (captured the second time the shape occurs; the metadata goes to that
-// graph's fixed area).
-spec_status run_kernels(spec_ctx* ctx, const std::vector<int64_t>& key, const MetaBlock& mb,
+// graph's fixed area).  Graphs pay where launches are short (batch-1 draft
+// and verify steps: 7.20 -> 7.11 ms per step); on the 64-sequence serving
+// batch the shapes drift with the contexts, each capture cost 0.3-1 ms of
+// host time and replays ran no faster than eager launches.
+constexpr int kGraphMaxRows = 16;
+
+spec_status run_kernels(spec_ctx* ctx, const std::vector<int64_t>& key, int rows, const MetaBlock& mb,
                         hipStream_t st,
                         const std::function<spec_status(const char*, hipStream_t)>& launches) {
-  if (!ctx->use_graphs || !ctx->timer.name.empty()) {
+  if (!ctx->use_graphs || !ctx->timer.name.empty() || rows > kGraphMaxRows) {
     char* dev = nullptr;
     spec_status s = upload_meta(ctx, mb, st, &dev);
     if (s != SPEC_OK) return s;
@@ -902,7 +908,7 @@ spec_status draft_step_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, co
   std::vector<int64_t> key = {1, n, static_cast<int64_t>(odr), static_cast<int64_t>(osd), guide ? 1 : 0,
                               static_cast<int64_t>(boost_bits)};
   key_forward(key, o);
-  spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
+  spec_status s = run_kernels(ctx, key, o.R, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
     spec_status r = launch_forward(ctx, D, o, dev, dq, ls);
     if (r != SPEC_OK) return r;
     if (guide) HIPC(launch_draft_guide(n, ctx->V, reinterpret_cast<const DRow*>(dev + odr), boost, ls));
@@ -1005,12 +1011,14 @@ spec_status draft_steps_graph(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, 
     return SPEC_OK;
   }
   std::vector<int64_t> key = {3, n, n_steps, static_cast<int64_t>(osd)};
+  int max_rows = 0;
   for (int j = 0; j < n_steps; ++j) {
     key.push_back(static_cast<int64_t>(odr[j]));
     key.push_back(nrow[j]);
     key_forward(key, fo[j]);
+    max_rows = std::max(max_rows, fo[j].R);
   }
-  spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
+  spec_status s = run_kernels(ctx, key, max_rows, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
     for (int j = 0; j < n_steps; ++j) {
       spec_status r = launch_forward(ctx, D, fo[j], dev, dq, ls);
       if (r != SPEC_OK) return r;
@@ -1279,7 +1287,7 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
                               static_cast<int64_t>(oseq), static_cast<int64_t>(osd), tree_mode,
                               static_cast<int64_t>(onode)};
   key_forward(key, o);
-  spec_status s = run_kernels(ctx, key, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
+  spec_status s = run_kernels(ctx, key, o.R, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
     spec_status r = launch_forward(ctx, T, o, dev, logits, ls);
     if (r != SPEC_OK || !decide) return r;
     if (tree_mode) {
