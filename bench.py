@@ -622,7 +622,7 @@ def bench_vocab(args):
     na = torch.zeros(Bn, dtype=torch.int32, device=dev)
     out = torch.zeros(Bn, k + 1, dtype=torch.int32, device=dev)
     ws = torch.empty(B.spec_sample_workspace_bytes(Bn, Bn * (2 * k + 1), V), dtype=torch.uint8, device=dev)
-    ks = [k] * Bn
+    ks = np.full(Bn, k, dtype=np.int32)  # host arrays in the C types: no per-call conversion
 
     def step(s):
         B.spec_sample_verify(ks, temps, ids, base, P, Q, drafts, V, cfg.seed + s, na, out, ws)
