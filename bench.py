@@ -763,9 +763,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="all", choices=["all", "8b-shaped", "8b-serving", "vocab-stress"],
+    ap.add_argument("--workload", default="all", choices=["all", "8b-shaped", "8b-serving", "vocab-stress", "prefill"],
                     help="all (default): the 8b-shaped line with greedy, plain-decode, serving and "
-                         "vocab-stress sub-objects")
+                         "vocab-stress sub-objects; prefill: only the long-context prefill object (for profiling)")
     ap.add_argument("--temperature", type=float, default=None,
                     help="sampling temperature (default 0.8; 0, greedy, for the serving workload, whose draft "
                          "mixing fixes top-1 agreement, i.e. the greedy acceptance test)")
@@ -809,6 +809,11 @@ def main():
         args.temperature = 0.0 if wl == "8b-serving" else 0.8
     steps = args.steps
     info = info_s = info_v = info_d = info_t = info_p = None
+    if wl == "prefill":
+        target, _ = device_models(LLAMA8B_SHAPED)
+        log("long-context prefill")
+        print(json.dumps({"workload": "prefill", "prefill": bench_prefill(args, target)}), flush=True)
+        return
     if wl in ("all", "8b-shaped", "8b-serving"):
         target, draft = device_models(LLAMA8B_SHAPED)
         if wl in ("all", "8b-shaped"):
