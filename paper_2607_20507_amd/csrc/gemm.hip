@@ -1347,7 +1347,7 @@ hipError_t mfma2_m(int ntw, int R, int N, int K, const bf16_t* x, const bf16_t* 
   }
 }
 
-// gemm_mfma3_bf16 (weights straight to registers, 192 x 256 tiles) for the
+// gemm_mfma3_bf16 (weights straight to registers), 192 x 256 tiles for the
 // shapes it was measured to win: SwiGLU gate/up from 160 rows in one pass
 // (364-row serving verify 114 -> 97 us, 2048-row prefill 508 -> 433 us, 8192
 // rows 1966 -> 1641 us), store-only projections of 65536+ rows in one pass
@@ -1357,14 +1357,49 @@ hipError_t mfma2_m(int ntw, int R, int N, int K, const bf16_t* x, const bf16_t* 
 // (the QKV and O projections, the unsplit 2048-row down projection)
 // gemm_mfma2_bf16 was as fast or faster.
 constexpr int kM3MB = 12, kM3NB = 4, kM3D = 4;
+// Small form: 64-row tiles (MB 4) of 64 NB W rows, K split to fill the CUs,
+// for the drafter's and the target's 41-128-row projections, where every
+// workgroup streams all of X: a 64-row tile streams 4 KB of X per k-step
+// through LDS against the 16 KB of the 192-row form.
+constexpr int kM3sMB = 4;
 
 struct Mfma3Plan {
   int MT, NT, S, k_len;
+  int nb;  // 0: the 192 x 256 form; else the small form with NB = nb
 };
 
+// NB of the small form for a projection of R rows, or 0 where
+// gemm_mfma2_bf16 is used (more than 128 rows; the 65536+-row LM heads).  From
+// a sweep of NB in {1, 2, 4} against gemm_mfma2_bf16 over 13-150 rows of the
+// 8B- and 1B-shaped projections: a residual add or plain store wants about 64
+// tiles (K split 4 ways), so the narrowest W tile with at most 64 tiles; a
+// SwiGLU, whose split costs a launch of its own, the widest tile that still
+// fills 192 CUs unsplit, else NB = 2.  Measured against gemm_mfma2_bf16:
+// 8B-shaped O projection at 41 rows 13.6 -> 11.3 us, gate/up at 96 rows 47.0 ->
+// 37.9 us, down at 96 rows 31.4 -> 27.6 us; 1B-shaped down at 41 rows 13.5 ->
+// 12.3 us, gate/up at 78 rows 20.1 -> 17.6 us; elsewhere within a few percent.
+int mfma3_small_nb(int R, int Nw, int K, int epi) {
+  (void)K;
+  if (R > 128 || Nw >= 65536) return 0;
+  const int MT = (R + 16 * kM3sMB - 1) / (16 * kM3sMB);
+  auto tiles = [&](int nb) { return MT * ((Nw + 64 * nb - 1) / (64 * nb)); };
+  if (epi == kEpiSwiGLU) return tiles(4) >= 192 ? 4 : 2;
+  for (int nb : {1, 2}) if (tiles(nb) <= 64) return nb;
+  return 4;
+}
+
 bool use_mfma3(int R, int Nw, int K, int epi, size_t ws_bytes, Mfma3Plan* plan = nullptr) {
-  if (R < 160 || K % (32 * kM3D)) return false;
+  if (K % (32 * kM3D)) return false;
   if (static_cast<double>(Nw) * K >= 2147483648.0 || static_cast<double>(R) * K >= 2147483648.0) return false;
+  if (R < 160) {
+    const int nb = ws_bytes ? mfma3_small_nb(R, Nw, K, epi) : 0;
+    if (nb == 0 || (epi == kEpiSwiGLU && nb % 2)) return false;
+    const int MT = (R + 16 * kM3sMB - 1) / (16 * kM3sMB), NT = (Nw + 64 * nb - 1) / (64 * nb);
+    int k_len = K;
+    const int S = mfma2_splits(MT, NT, R, Nw, K, ws_bytes, &k_len);  // k_len: a multiple of 128 = 32 D
+    if (plan) *plan = {MT, NT, S, k_len, nb};
+    return true;
+  }
   const int MT = (R + 16 * kM3MB - 1) / (16 * kM3MB), NT = (Nw + 64 * kM3NB - 1) / (64 * kM3NB);
   int k_len = K, S = 1;
   bool ok;
@@ -1374,14 +1409,26 @@ bool use_mfma3(int R, int Nw, int K, int epi, size_t ws_bytes, Mfma3Plan* plan =
   } else {
     ok = (epi == kEpiSwiGLU || (epi == kEpiStoreF32 && Nw >= 65536)) && MT * NT >= 192;
   }
-  if (ok && plan) *plan = {MT, NT, S, k_len};
+  if (ok && plan) *plan = {MT, NT, S, k_len, 0};
   return ok;
+}
+
+template <int EPI>
+auto mfma3_kernel(int nb) {
+  if constexpr (EPI == kEpiSwiGLU) {
+    return nb == 0 ? gemm_mfma3_bf16<EPI, kM3MB, kM3NB, kM3D>
+                   : nb == 2 ? gemm_mfma3_bf16<EPI, kM3sMB, 2, kM3D> : gemm_mfma3_bf16<EPI, kM3sMB, 4, kM3D>;
+  } else {
+    return nb == 0 ? gemm_mfma3_bf16<EPI, kM3MB, kM3NB, kM3D>
+                   : nb == 1 ? gemm_mfma3_bf16<EPI, kM3sMB, 1, kM3D>
+                             : nb == 2 ? gemm_mfma3_bf16<EPI, kM3sMB, 2, kM3D> : gemm_mfma3_bf16<EPI, kM3sMB, 4, kM3D>;
+  }
 }
 
 template <int EPI>
 hipError_t mfma3(int R, int N, int K, const bf16_t* x, const bf16_t* w, void* Y, hipStream_t st, const int32_t* rm,
                  float* ws, const Mfma3Plan& p, GemmNorm* norm) {
-  auto* kern = gemm_mfma3_bf16<EPI, kM3MB, kM3NB, kM3D>;
+  auto* kern = mfma3_kernel<EPI>(p.nb);
   if (p.S <= 1) {
     launch_kernel(kern, dim3(p.MT * p.NT), dim3(256), 0, st, x, w, Y, static_cast<float*>(nullptr), R, N, K, K, p.MT,
                   p.NT, rm);
@@ -1515,13 +1562,17 @@ const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused
   if (dtype == 0) return f32[epi];
   const int Nw = epi == kEpiSwiGLU ? 2 * N : N;
   if (use_mfma(R, Nw, K)) {
-    static char m3[3][40];
+    static char m3[3][5][40];  // [epi][nb: 0 the 192-row form, 1, 2, 4]
     static std::once_flag once3;
     std::call_once(once3, [] {
-      for (int e = 0; e < 3; ++e)
-        snprintf(m3[e], sizeof(m3[e]), "gemm_mfma3_bf16<%d, %d, %d, %d>", e, kM3MB, kM3NB, kM3D);
+      for (int e = 0; e < 3; ++e) {
+        snprintf(m3[e][0], sizeof(m3[e][0]), "gemm_mfma3_bf16<%d, %d, %d, %d>", e, kM3MB, kM3NB, kM3D);
+        for (int nb : {1, 2, 4})
+          snprintf(m3[e][nb], sizeof(m3[e][nb]), "gemm_mfma3_bf16<%d, %d, %d, %d>", e, kM3sMB, nb, kM3D);
+      }
     });
-    if (use_mfma3(R, Nw, K, epi, splitk_bytes)) return m3[epi];
+    Mfma3Plan p3;
+    if (use_mfma3(R, Nw, K, epi, splitk_bytes, &p3)) return m3[epi][p3.nb];
     const Mfma2Shape sh = mfma2_shape(R, N, Nw, K, splitk_bytes, epi == kEpiSwiGLU);
     return tiled[epi][sh.mtw / 2 - 1][sh.ntw == 2 ? 0 : (sh.ntw == 4 ? 1 : 2)];
   }

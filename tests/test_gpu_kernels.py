@@ -181,6 +181,11 @@ FULL = [
     # multiple of 16, a trailing partial W tile, N % 4 != 0 for the LM-head
     # form)
     (364, 14336, 4096, 2), (2048, 14336, 4096, 2), (200, 24600, 256, 2), (177, 65546, 128, 0),
+    # its 64-row form (K split, W tiles of 64 / 128 / 256 rows) at the
+    # serving draft steps' and the batch-8 verify's row counts, 32-128 rows
+    (41, 3072, 2048, 0), (64, 2048, 2048, 1), (96, 8192, 2048, 2), (100, 4096, 14336, 1),
+    (78, 6144, 4096, 0), (32, 4096, 14336, 1), (50, 14336, 4096, 2), (120, 4096, 4096, 1),
+    (128, 14336, 4096, 2), (70, 2100, 2048, 0),
 ]
 
 
