@@ -1409,6 +1409,16 @@ bool use_mfma3(int R, int Nw, int K, int epi, size_t ws_bytes, Mfma3Plan* plan =
   } else {
     ok = (epi == kEpiSwiGLU || (epi == kEpiStoreF32 && Nw >= 65536)) && MT * NT >= 192;
   }
+  if (!ok && epi == kEpiAddF32 && K < 8192 && Nw >= 4096 && Nw < 65536 && R <= 384) {
+    // the residual-add projections of the 8B-shaped target at 160-384 rows
+    // (the serving verify's O projection): the 64-row form with 256-row W
+    // tiles, K split (364 rows 29.2 -> 25.4 us against gemm_mfma2_bf16)
+    const int MTs = (R + 16 * kM3sMB - 1) / (16 * kM3sMB), NTs = (Nw + 255) / 256;
+    int kl = K;
+    const int Ss = mfma2_splits(MTs, NTs, R, Nw, K, ws_bytes, &kl);
+    if (ws_bytes && plan) *plan = {MTs, NTs, Ss, kl, 4};
+    return ws_bytes != 0;
+  }
   if (ok && plan) *plan = {MT, NT, S, k_len, 0};
   return ok;
 }

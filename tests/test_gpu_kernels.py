@@ -185,7 +185,7 @@ FULL = [
     # serving draft steps' and the batch-8 verify's row counts, 32-128 rows
     (41, 3072, 2048, 0), (64, 2048, 2048, 1), (96, 8192, 2048, 2), (100, 4096, 14336, 1),
     (78, 6144, 4096, 0), (32, 4096, 14336, 1), (50, 14336, 4096, 2), (120, 4096, 4096, 1),
-    (128, 14336, 4096, 2), (70, 2100, 2048, 0),
+    (128, 14336, 4096, 2), (70, 2100, 2048, 0), (364, 4096, 4096, 1), (170, 4100, 2048, 1),
 ]
 
 
