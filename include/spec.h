@@ -340,12 +340,14 @@ SPEC_API spec_status spec_draft_tokens(spec_ctx* ctx, int64_t seq_id, int32_t* t
 
 /* Graph replay of the draft step and the verify (on by default).  Their
  * kernel sequence depends only on the batch shape (rows, sequences, attention
- * work items), so the first call of a shape captures it into a HIP graph and
+ * work items), so the second call of a shape captures it into a HIP graph and
  * later calls of that shape upload their metadata and replay the graph: one
  * launch instead of ~10 per layer.  Up to 16 shapes are kept (least recently
- * used replaced); a new workspace drops them.  Results are identical with and
- * without graphs.  While kernel timing is on, calls run eagerly so that each
- * launch can be timed.  enable = 0 turns replay off. */
+ * used replaced); a new workspace drops them.  Calls whose forwards have more
+ * than 16 rows always launch eagerly (their kernels are long enough that a
+ * replay saves nothing, and their shapes rarely recur).  Results are
+ * identical with and without graphs.  While kernel timing is on, calls run
+ * eagerly so that each launch can be timed.  enable = 0 turns replay off. */
 SPEC_API spec_status spec_set_graphs(spec_ctx* ctx, int32_t enable);
 
 /* Kernel timing for roofline measurement.  While a kernel name is set, the
