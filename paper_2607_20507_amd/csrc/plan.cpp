@@ -77,6 +77,10 @@ AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, in
     }
     p.n_parts += c;
   }
+  // longest key ranges first: workgroups start in this order, so the short
+  // items fill in behind the long ones instead of trailing after them
+  std::stable_sort(p.items.begin(), p.items.end(),
+                   [](const AttnItem& x, const AttnItem& y) { return x.t1 - x.t0 > y.t1 - y.t0; });
   return p;
 }
 
