@@ -365,6 +365,15 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 
 constexpr int kGemvRows = 2;  // measured: the MFMA skinny kernel wins from 3 rows on
 
+// The fused one- and two-row path sends the LM head of a model with
+// d_model <= 2048 (the drafter's 128256 x 2048) to the skinny MFMA kernel
+// instead: its 16-feature tiles of 2048 columns are short enough that the
+// GEMV's per-workgroup streaming falls behind (1-row drafter LM head 87.4 ->
+// 77.8 us, 6.0 -> 6.8 TB/s); with d_model 4096 the GEMV stays ahead.
+__host__ inline bool gemv_lm_skinny(int R, int N, int K, int epi) {
+  return R <= kGemvRows && epi == kEpiStoreF32 && N >= 65536 && K <= 2048;
+}
+
 // Half tiles for residual-add projections with fewer 16-feature tiles than
 // compute units.
 bool gemv_half(int epi, int N) { return epi == kEpiAddF32 && (N + 15) / 16 < 256; }
@@ -1524,7 +1533,7 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
   if (R <= 0 || N <= 0) return hipSuccess;
   if (R > 16 || K % 128 != 0 || N % 16 != 0) return hipErrorInvalidValue;
   if (epi == kEpiQKVRope && (f.hd % 16 != 0 || N != (f.Hq + 2 * f.Hkv) * f.hd)) return hipErrorInvalidValue;
-  if (R <= kGemvRows) {
+  if (R <= kGemvRows && !gemv_lm_skinny(R, N, K, epi)) {
     switch (epi) {
       case kEpiStoreF32: return gemv<kEpiStoreF32>(R, N, K, X, W, Y, st, row_map, f);
       case kEpiAddF32: return gemv<kEpiAddF32>(R, N, K, X, W, Y, st, nullptr, f);
@@ -1545,7 +1554,7 @@ hipError_t launch_gemm_fused(int R, int N, int K, const void* X, const void* W, 
 const char* gemm_kernel_name(int dtype, int R, int N, int K, int epi, bool fused, size_t splitk_bytes) {
   static const char* gv[4] = {"gemv_bf16<0, 2, false>", "gemv_bf16<1, 2, false>", "gemv_bf16<2, 2, false>",
                               "gemv_bf16<3, 2, false>"};
-  if (dtype == 1 && R <= kGemvRows)
+  if (dtype == 1 && R <= kGemvRows && !(fused && gemv_lm_skinny(R, N, K, epi)))
     return gemv_half(epi, N) ? "gemv_bf16<1, 2, true>" : ((epi >= 0 && epi <= 3) ? gv[epi] : "");
   // skinny names [MT - 1][epi][fused]
   static char names[4][4][2][40];
