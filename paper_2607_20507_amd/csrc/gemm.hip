@@ -365,13 +365,16 @@ __global__ __launch_bounds__(kSkinnyMaxWaves * kWave) void gemm_skinny_bf16(
 
 constexpr int kGemvRows = 2;  // measured: the MFMA skinny kernel wins from 3 rows on
 
-// The fused one- and two-row path sends the LM head of a model with
-// d_model <= 2048 (the drafter's 128256 x 2048) to the skinny MFMA kernel
-// instead: its 16-feature tiles of 2048 columns are short enough that the
-// GEMV's per-workgroup streaming falls behind (1-row drafter LM head 87.4 ->
-// 77.8 us, 6.0 -> 6.8 TB/s); with d_model 4096 the GEMV stays ahead.
+// Shapes the fused one- and two-row path sends to the skinny MFMA kernel
+// instead of the GEMV, measured on the batch-1 steps: the LM head of a model
+// with d_model <= 2048 (the drafter's 128256 x 2048: 87.4 -> 77.8 us per
+// draft step, 6.0 -> 6.8 TB/s; with d_model 4096 the GEMV stays ahead), and
+// residual-add projections with K <= 2048 (the drafter's O projection:
+// batch-1 step 7.07 -> 7.03 ms).  Sending the larger-K residual-add
+// projections too was slower (7.11 ms).
 __host__ inline bool gemv_lm_skinny(int R, int N, int K, int epi) {
-  return R <= kGemvRows && epi == kEpiStoreF32 && N >= 65536 && K <= 2048;
+  if (R > kGemvRows || K > 2048) return false;
+  return (epi == kEpiStoreF32 && N >= 65536) || epi == kEpiAddF32;
 }
 
 // Half tiles for residual-add projections with fewer 16-feature tiles than
