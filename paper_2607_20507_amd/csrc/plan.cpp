@@ -34,6 +34,14 @@ AttnPlan plan_attention(const std::vector<AttnSegment>& segs, int G, int Hkv, in
   // query vectors per tile: rows * G <= 16 * nt, nt in {1, 2, 4}
   const int want = std::min(max_rows * G, 64);
   p.nt = want <= 16 ? 1 : (want <= 32 ? 2 : 4);
+  // One sequence (a batch-1 verify, draft step or tree verify: a few MB of
+  // keys and values, latency-bound): twice the items with half the query
+  // vectors each, when a row's query heads still fit the narrower tile (6
+  // rows x 4 heads per KV head, head dim 128: 8.6 -> 7.6 us per layer; the
+  // 15-node tree verify 4.76 -> 4.44 ms; halving the tree's tiles twice was
+  // no better).  Several sequences keep the wider tiles, whose items read
+  // their keys and values once for all rows.
+  if (segs.size() == 1 && p.nt >= 2 && G <= 8 * p.nt) p.nt /= 2;
   p.w = p.nt >= 4 ? 2 : 4;  // waves per workgroup (LDS of the merge bounds it at nt = 4)
   const int qt = std::max(1, 16 * p.nt / G);
 
