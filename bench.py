@@ -542,8 +542,9 @@ def bench_tree(args, target, draft):
         ls = sorted(a.elapsed_time(b) for a, b in lat)
         out[name] = {"nodes": len(shape), "verify_ms_median": float(np.median(ls)),
                      "verify_ms_p90": float(np.percentile(ls, 90)), "mean_accepted": float(np.mean(acc))}
-    # the tree decision kernel alone (kernel-level events)
-    B.spec_timing_enable(sess.ctx, "tree_decide_kernel")
+    # the tree decision after the statistics pass alone (residual-mass passes,
+    # draws and walk; kernel-level events around them)
+    B.spec_timing_enable(sess.ctx, "tree_decision")
     for r in range(args.roof_steps):
         sess.set_draft_tree(sid, parents, [int(x) for x in rng.integers(0, V, size=m)], zq)
         na, _ = sess.verify([sid], [0.8], cfg.seed + 500 + r)

@@ -356,7 +356,9 @@ SPEC_API spec_status spec_set_graphs(spec_ctx* ctx, int32_t enable);
  * kernels; other kernels: events on the call's stream around the launch).
  * Names as the profiler reports them without namespaces and argument lists,
  * e.g. "gemm_skinny_bf16<1, 2, true>", "gemm_mfma2_bf16<2, 6, 8>",
- * "attn_bf16_kernel<128, 2, 4>", "stats_kernel<true>".  It accumulates the
+ * "attn_bf16_kernel<128, 2, 4>", "stats_kernel<true>"; "tree_decision" times
+ * the tree verify's decision after its statistics pass (several kernels) as
+ * one span.  It accumulates the
  * elapsed time, the launch count and each launch's algorithmic HBM bytes and
  * flops (weights, activations and KV actually required, each read once).
  * name NULL or "" disables timing.  spec_timing_read waits for the recorded

@@ -238,8 +238,9 @@ void compute_ws(spec_ctx* c) {
   w.part_o = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * c->hd_max * 4);
   w.part_ml = take(static_cast<size_t>(kMaxParts) * c->hkv_max * 64 * 2 * 4);
   const int vrows = c->max_seqs * (2 * c->k_max + 1);
-  w.vocab = take(vocab_ws_bytes(vocab_plan(c->max_seqs, vrows, c->V)));
-  w.draft = take(draft_ws_bytes(draft_plan(c->max_seqs, c->V)));
+  // bounds over every call size (a smaller call can take more chunks per row)
+  w.vocab = take(std::max(vocab_ws_bound(c->max_seqs, vrows), tree_ws_bound(c->max_seqs, vrows)));
+  w.draft = take(draft_ws_bound(c->max_seqs));
   w.splitk_bytes = gemm_splitk_bytes(c->R_max, std::max(c->qkv_max, 2 * c->ffn_max));
   w.splitk = take(w.splitk_bytes);
   // metadata bound for one call
@@ -1199,6 +1200,7 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   std::vector<VSeq> vs;
   std::vector<VTreeSeq> ts;
   std::vector<VTreeNode> tn;
+  int max_kids = 0;  // the most children of any tree node: residual-mass levels of the tree pass
   float* logits = wsptr<float>(ctx, ctx->ws.logits);
   for (int i = 0; i < n; ++i) {
     Seq& s = ctx->seqs[seq_ids[i]];
@@ -1244,8 +1246,9 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
     if (tree_mode) {
       // q row of a node with children: the row its children were drawn from
       // (chain drafts: draft j + 1's row for node j - 1; trees: row u + 1)
-      std::vector<char> kids(s.k + 1, 0);
-      for (int j = 0; j < s.k; ++j) kids[par[j] + 1] = 1;
+      std::vector<int> kids(s.k + 1, 0);
+      for (int j = 0; j < s.k; ++j) ++kids[par[j] + 1];
+      for (int c : kids) max_kids = std::max(max_kids, c);
       auto qidx = [&](int u) -> int32_t {  // u = -1: the root
         if (!kids[u + 1]) return -1;
         tq.push_back(VRow{s.qrow[u + 1], it, t > 0.f ? 0 : 1});
@@ -1284,7 +1287,7 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
   int32_t* d_opath = ctx->h_out_dev + ctx->max_seqs * (ctx->k_max + 2);
   const VocabPlan vp = vocab_plan(n, static_cast<int>(rows.size()), ctx->V);
   std::vector<int64_t> key = {decide ? 0 : 2, n, static_cast<int64_t>(rows.size()), static_cast<int64_t>(orow),
-                              static_cast<int64_t>(oseq), static_cast<int64_t>(osd), tree_mode,
+                              static_cast<int64_t>(oseq), static_cast<int64_t>(osd), tree_mode, max_kids,
                               static_cast<int64_t>(onode)};
   key_forward(key, o);
   spec_status s = run_kernels(ctx, key, o.R, mb, st, [&](const char* dev, hipStream_t ls) -> spec_status {
@@ -1294,7 +1297,7 @@ spec_status verify_impl(spec_ctx* ctx, int32_t n, const int64_t* seq_ids, const 
       HIPC(launch_tree_pass(vp, reinterpret_cast<const VRow*>(dev + orow),
                             reinterpret_cast<const VTreeSeq*>(dev + oseq),
                             reinterpret_cast<const VTreeNode*>(dev + onode), wsptr<int32_t>(ctx, ctx->ws.rowtok),
-                            seed, reinterpret_cast<const uint64_t*>(dev + osd), ctx->k_max, d_nacc, d_otok,
+                            seed, reinterpret_cast<const uint64_t*>(dev + osd), ctx->k_max, max_kids, d_nacc, d_otok,
                             d_opath, ctx->wsp + ctx->ws.vocab, ls, &ctx->timer));
       return SPEC_OK;
     }

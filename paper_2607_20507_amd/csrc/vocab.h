@@ -96,17 +96,25 @@ struct VTreeSeq {
   uint32_t seq_lo, seq_hi;
 };
 
-// Statistics of every row (p and q), then one workgroup per sequence walks
-// its tree: at a node, children are accepted while v_j q(x) < r(x) fails, r
-// becoming norm(max(0, r - q)) after each rejection (one vocabulary pass
-// each); the walk ends with a draw from r (RESAMPLE noise) at a node whose
-// children were all rejected, or from p (BONUS noise) at a leaf.  Outputs
-// n_acc[B] (accepted depth), out_tok[B * (kmax + 1)] (the path's tokens, then
-// the drawn one, -1 after), out_path[B * kmax] (the accepted node indices,
-// -1 after).  Workspace: vocab_ws_bytes(p).
+// Statistics of every row (p and q), then the walk: at a node, children are
+// accepted while v_j q(x) < r(x) fails, r becoming norm(max(0, r - q)) after
+// each rejection; the walk ends with a draw from r (RESAMPLE noise) at a node
+// whose children were all rejected, or from p (BONUS noise) at a leaf.  The
+// residual masses of every node and level (max_kids levels: the most
+// children of any node) and every node's draw are chip-wide passes before
+// the walk.  Outputs n_acc[B] (accepted depth), out_tok[B * (kmax + 1)] (the
+// path's tokens, then the drawn one, -1 after), out_path[B * kmax] (the
+// accepted node indices, -1 after).  Workspace: tree_ws_bytes(p).
+size_t tree_ws_bytes(const VocabPlan& p);
+// Workspace that covers every plan of at most B sequences and n_rows rows
+// (decision pass, tree pass) or n draft rows: for a workspace sized once for
+// calls of varying size.
+size_t vocab_ws_bound(int B, int n_rows);
+size_t tree_ws_bound(int B, int n_rows);
+size_t draft_ws_bound(int n);
 hipError_t launch_tree_pass(const VocabPlan& p, const VRow* d_rows, const VTreeSeq* d_seqs,
                             const VTreeNode* d_nodes, const int32_t* d_row_tok, uint64_t seed,
-                            const uint64_t* d_seed, int kmax,
+                            const uint64_t* d_seed, int kmax, int max_kids,
                             int32_t* d_n_acc, int32_t* d_out_tok, int32_t* d_out_path, void* d_ws,
                             hipStream_t st, KernelTimer* timer = nullptr);
 

@@ -414,40 +414,50 @@ __global__ __launch_bounds__(kWave) void final_kernel(const VSeq* __restrict__ s
 }
 
 // ---------------------------------------------------------------------------
-// Tree verification: one workgroup of kTreeThreads per sequence walks its
-// tree.  At node u the target distribution is r_0 = p_u; each rejected child
-// replaces r_l by r_{l+1} = max(0, r_l - q_u) / Z_{l+1}, where Z_{l+1} is the
-// residual's mass (a vocabulary pass; a residual with no mass keeps r_l), so
-// r_l(y) is evaluated from p_u(y), q_u(y) and Z_1..Z_l alone.
+// Tree verification.  At node u the target distribution is r_0 = p_u; each
+// rejected child replaces r_l by r_{l+1} = max(0, r_l - q_u) / Z_{l+1}, where
+// Z_{l+1} is the residual's mass (a residual with no mass keeps r_l), so
+// r_l(y) is evaluated from p_u(y), q_u(y) and Z_1..Z_l alone.  Every child of
+// u is drawn from the same q_u, so Z_l depends on how many children were
+// rejected, not on which: the masses of every node and level, and each node's
+// final draw (from r_{c(u)} once its c(u) children are all rejected, from p
+// at a leaf), are computed for all nodes at once by chip-wide passes
+// (tree_z_kernel per level, tree_draw_kernel); one wave per sequence then
+// walks the tree with the acceptance tests alone (tree_walk_kernel).  Each
+// vocabulary pass is a grid of (chunk, node slot) workgroups; the masses are
+// chunk partials summed in chunk order wherever they are used.
 
-constexpr int kTreeThreads = 1024;
-constexpr int kTreeWaves = kTreeThreads / kWave;
-constexpr int kTreeMaxNodes = 16;
+constexpr int kTreeMaxNodes = 16;  // slots per sequence: the root and at most 15 nodes
+constexpr int kTreeWaves = kThreads / kWave;
 
-__device__ float tree_block_sum(float v, float* red) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  const int w = threadIdx.x / kWave;
-  __syncthreads();
-  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
-  __syncthreads();
-  float s = 0.f;
-  for (int i = 0; i < kTreeWaves; ++i) s += red[i];  // fixed order
-  return s;
+// Slot s of a sequence: s = 0 the root, s = i + 1 node i.
+struct TreeSlot {
+  int prow, qrow, kids, depth;
+};
+__device__ __forceinline__ TreeSlot tree_slot(const VTreeSeq& sq, const VTreeNode* __restrict__ nodes, int s) {
+  const int u = s - 1;
+  TreeSlot r;
+  r.prow = u < 0 ? sq.p_row : nodes[sq.node0 + u].p_row;
+  r.qrow = u < 0 ? sq.q_row : nodes[sq.node0 + u].q_row;
+  r.kids = 0;
+  for (int i = 0; i < sq.m; ++i) r.kids += nodes[sq.node0 + i].parent == u ? 1 : 0;
+  r.depth = 0;
+  // parents have smaller indices; at most m steps
+  for (int v = u, n = 0; v >= 0 && n < sq.m; v = nodes[sq.node0 + v].parent, ++n) ++r.depth;
+  return r;
 }
 
-__device__ void tree_block_pick(float& best, int& bi, float* redf, int* redi) {
-  wave_pick(best, bi);
-  const int w = threadIdx.x / kWave;
-  __syncthreads();
-  if ((threadIdx.x & (kWave - 1)) == 0) {
-    redf[w] = best;
-    redi[w] = bi;
-  }
-  __syncthreads();
-  best = -1.f;
-  bi = INT_MAX;
-  for (int i = 0; i < kTreeWaves; ++i) pick_update(redf[i], redi[i], best, bi);
+// Partial masses of the residuals: zpart[((b * kTreeMaxNodes + s) * kTreeMaxNodes + l - 1) * kMaxChunks + c]
+// is chunk c's share of Z_l at slot s of sequence b.
+__device__ __forceinline__ size_t tree_z_index(int b, int s, int l, int c) {
+  return ((static_cast<size_t>(b) * kTreeMaxNodes + s) * kTreeMaxNodes + (l - 1)) * kMaxChunks + c;
+}
+
+// Z_l summed over the chunks in chunk order (the same value wherever used).
+__device__ __forceinline__ float tree_z_total(const float* __restrict__ zpart, int b, int s, int l, int n_chunks) {
+  float z = 0.f;
+  for (int c = 0; c < n_chunks; ++c) z += zpart[tree_z_index(b, s, l, c)];
+  return z;
 }
 
 // Merged (max, sum, first argmax) of one row's chunk records, by one wave.
@@ -471,11 +481,161 @@ __device__ void tree_row_stats(const VStat* __restrict__ st, int n_chunks, float
   }
 }
 
-__global__ __launch_bounds__(kTreeThreads) void tree_decide_kernel(
+// The state a node's residuals are evaluated from: the p and q row statistics
+// (scaled into exp2 form) and the masses Z_1..Z_lv.
+struct TreeRes {
+  const float* zp;
+  const float* zq;
+  float cs, mpc, isp, mqc, isq;
+  float invz[kTreeMaxNodes];
+  int keep[kTreeMaxNodes];
+};
+
+// r_lv(y) from p(y), q(y) and the residual normalisers so far (levels
+// unrolled so that the tables stay in registers)
+__device__ __forceinline__ float tree_r_at(const TreeRes& R, int y, int lv) {
+  float r = exp2f(R.zp[y] * R.cs - R.mpc) * R.isp;
+  if (lv > 0) {
+    const float q = exp2f(R.zq[y] * R.cs - R.mqc) * R.isq;
+#pragma unroll
+    for (int l = 1; l < kTreeMaxNodes; ++l)
+      if (l <= lv && !R.keep[l]) r = fmaxf(r - q, 0.f) * R.invz[l];
+  }
+  return r;
+}
+
+// The residual state of slot s through level lv, for a whole workgroup (waves
+// 0 and 1 merge the p and q statistics; returns false for a greedy sequence).
+__device__ bool tree_res(const VRow* __restrict__ rows, const VTreeSeq& sq, const TreeSlot& ts,
+                         const VStat* __restrict__ stats, const float* __restrict__ zpart, int b, int s, int lv,
+                         int n_chunks, TreeRes& R) {
+  __shared__ float s_st[4];
+  __shared__ float s_z[kTreeMaxNodes];
+  const float it = rows[sq.p_row].inv_t;
+  const int t = threadIdx.x;
+  if (t < kWave) {
+    float m, sm;
+    int idx;
+    tree_row_stats(stats + static_cast<size_t>(ts.prow) * n_chunks, n_chunks, it, false, m, sm, idx);
+    if (t == 0) {
+      s_st[0] = m;
+      s_st[1] = sm;
+    }
+  } else if (t < 2 * kWave && ts.qrow >= 0) {
+    float m, sm;
+    int idx;
+    tree_row_stats(stats + static_cast<size_t>(ts.qrow) * n_chunks, n_chunks, it, false, m, sm, idx);
+    if (t == kWave) {
+      s_st[2] = m;
+      s_st[3] = sm;
+    }
+  }
+  if (t > 0 && t <= lv) s_z[t] = tree_z_total(zpart, b, s, t, n_chunks);
+  __syncthreads();
+  R.cs = it * kLog2e;
+  R.zp = rows[ts.prow].ptr;
+  R.zq = ts.qrow >= 0 ? rows[ts.qrow].ptr : nullptr;
+  R.mpc = s_st[0] * R.cs;
+  R.isp = 1.f / s_st[1];
+  R.mqc = ts.qrow >= 0 ? s_st[2] * R.cs : 0.f;
+  R.isq = ts.qrow >= 0 ? 1.f / s_st[3] : 0.f;
+#pragma unroll
+  for (int l = 1; l < kTreeMaxNodes; ++l) {
+    const float z = l <= lv ? s_z[l] : 1.f;
+    R.keep[l] = !(z > 0.f);
+    R.invz[l] = z > 0.f ? 1.f / z : 1.f;
+  }
+  return true;
+}
+
+// Chunk c's share of Z_L at every slot with at least L children.
+__global__ __launch_bounds__(kThreads) void tree_z_kernel(const VRow* __restrict__ rows,
+                                                          const VTreeSeq* __restrict__ seqs,
+                                                          const VTreeNode* __restrict__ nodes,
+                                                          const VStat* __restrict__ stats, int n_chunks, int chunk,
+                                                          int V, int L, float* __restrict__ zpart) {
+  const int c = blockIdx.x, b = blockIdx.y / kTreeMaxNodes, s = blockIdx.y % kTreeMaxNodes;
+  const VTreeSeq sq = seqs[b];
+  if (s > sq.m || !(sq.t > 0.f)) return;
+  const TreeSlot ts = tree_slot(sq, nodes, s);
+  if (ts.qrow < 0 || ts.kids < L) return;
+  TreeRes R;
+  tree_res(rows, sq, ts, stats, zpart, b, s, L - 1, n_chunks, R);
+  const int beg = c * chunk, end = min(V, beg + chunk);
+  float part = 0.f;
+  for (int y = beg + static_cast<int>(threadIdx.x); y < end; y += kThreads) {
+    const float q = exp2f(R.zq[y] * R.cs - R.mqc) * R.isq;
+    part += fmaxf(tree_r_at(R, y, L - 1) - q, 0.f);
+  }
+  // fixed-order workgroup sum
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, kWave);
+  __shared__ float red[kTreeWaves];
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = part;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float z = 0.f;
+    for (int w = 0; w < kTreeWaves; ++w) z += red[w];
+    zpart[tree_z_index(b, s, L, c)] = z;
+  }
+}
+
+// Chunk c's winner of each slot's final draw: from r_{c(u)} (RESAMPLE noise)
+// at a node with children, from p (BONUS noise) at a leaf, by exponential
+// race over 4 tokens per Philox block at stream position base + depth + 1.
+__global__ __launch_bounds__(kThreads) void tree_draw_kernel(const VRow* __restrict__ rows,
+                                                             const VTreeSeq* __restrict__ seqs,
+                                                             const VTreeNode* __restrict__ nodes,
+                                                             const VStat* __restrict__ stats, int n_chunks,
+                                                             int chunk, int V, uint64_t seed,
+                                                             const uint64_t* __restrict__ seed_ptr,
+                                                             const float* __restrict__ zpart,
+                                                             VPick* __restrict__ picks) {
+  const int c = blockIdx.x, b = blockIdx.y / kTreeMaxNodes, s = blockIdx.y % kTreeMaxNodes;
+  const VTreeSeq sq = seqs[b];
+  if (s > sq.m || !(sq.t > 0.f)) return;
+  const TreeSlot ts = tree_slot(sq, nodes, s);
+  const int lv = ts.qrow >= 0 ? ts.kids : 0;
+  TreeRes R;
+  tree_res(rows, sq, ts, stats, zpart, b, s, lv, n_chunks, R);
+  const uint64_t seq_id = (static_cast<uint64_t>(sq.seq_hi) << 32) | sq.seq_lo;
+  const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
+  const StreamId sid = stream_id(seq_id, sq.base_pos + ts.depth + 1, ts.qrow >= 0 ? 2 : 3);
+  const int beg = c * chunk, end = min(V, beg + chunk);  // chunk starts are multiples of 1024
+  float best = -1.f;
+  int bi = INT_MAX;
+  for (int y4 = beg / 4 + static_cast<int>(threadIdx.x); 4 * y4 < end; y4 += kThreads) {
+    const uint4 w = philox_block(key, sid, static_cast<uint32_t>(y4));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int y = 4 * y4 + e;
+      if (y < end) pick_update(tree_r_at(R, y, lv) / exp2_variate(word_of(w, e)), y, best, bi);
+    }
+  }
+  wave_pick(best, bi);
+  __shared__ float rf[kTreeWaves];
+  __shared__ int ri[kTreeWaves];
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    rf[threadIdx.x / kWave] = best;
+    ri[threadIdx.x / kWave] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kTreeWaves; ++w) pick_update(rf[w], ri[w], rf[0], ri[0]);
+    picks[(static_cast<size_t>(b) * kTreeMaxNodes + s) * kMaxChunks + c] = VPick{rf[0], ri[0], 0.f, 0};
+  }
+}
+
+// One wave per sequence walks its tree: at a node, children are accepted in
+// index order while v_j q(x) < r_lv(x) fails (lv = children rejected so
+// far); a greedy sequence follows the argmax of p.  The walk ends at a node
+// with no accepted child, whose token is the merged winner of its draw.  All
+// lanes take the same steps; lane 0 keeps the walk's state in LDS.
+__global__ __launch_bounds__(kWave) void tree_walk_kernel(
     const VRow* __restrict__ rows, const VTreeSeq* __restrict__ seqs, const VTreeNode* __restrict__ nodes,
     const int32_t* __restrict__ row_tok, const VStat* __restrict__ stats, int n_chunks, int V, uint64_t seed,
-    const uint64_t* __restrict__ seed_ptr, int kmax, int32_t* __restrict__ n_acc, int32_t* __restrict__ out_tok,
-    int32_t* __restrict__ out_path) {
+    const uint64_t* __restrict__ seed_ptr, const float* __restrict__ zpart, const VPick* __restrict__ picks,
+    int kmax, int32_t* __restrict__ n_acc, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_path) {
   const int b = blockIdx.x, t = threadIdx.x;
   const VTreeSeq sq = seqs[b];
   const bool greedy = !(sq.t > 0.f);
@@ -483,39 +643,18 @@ __global__ __launch_bounds__(kTreeThreads) void tree_decide_kernel(
   const float cs = it * kLog2e;
   const uint64_t seq_id = (static_cast<uint64_t>(sq.seq_hi) << 32) | sq.seq_lo;
   const PhiloxKey key = philox_key(seed_ptr ? *seed_ptr : seed);
-  __shared__ float s_red[kTreeWaves];
-  __shared__ int s_redi[kTreeWaves];
-  __shared__ float s_st[4];  // Mp, Sp, Mq, Sq of the current node
-  __shared__ int s_ip;       // first argmax of p
+  __shared__ int s_tok[kTreeMaxNodes + 1], s_path[kTreeMaxNodes];
   __shared__ float s_invz[kTreeMaxNodes];
   __shared__ int s_keep[kTreeMaxNodes];
-  __shared__ int s_flag;
-  __shared__ int s_tok[kTreeMaxNodes + 1], s_path[kTreeMaxNodes];
   int u = -1, d = 0;
   for (;;) {
+    const int s = u + 1;
     const int prow = u < 0 ? sq.p_row : nodes[sq.node0 + u].p_row;
     const int qrow = u < 0 ? sq.q_row : nodes[sq.node0 + u].q_row;
-    if (t < kWave) {
-      float m, s;
-      int idx;
-      tree_row_stats(stats + static_cast<size_t>(prow) * n_chunks, n_chunks, it, greedy, m, s, idx);
-      if (t == 0) {
-        s_st[0] = m;
-        s_st[1] = s;
-        s_ip = idx;
-      }
-    } else if (t < 2 * kWave && !greedy && qrow >= 0) {
-      float m, s;
-      int idx;
-      tree_row_stats(stats + static_cast<size_t>(qrow) * n_chunks, n_chunks, it, greedy, m, s, idx);
-      if (t == kWave) {
-        s_st[2] = m;
-        s_st[3] = s;
-      }
-    }
-    __syncthreads();
+    float mp, sp, mq = 0.f, sqs = 1.f;
+    int ip, iq;
+    tree_row_stats(stats + static_cast<size_t>(prow) * n_chunks, n_chunks, it, greedy, mp, sp, ip);
     if (greedy) {
-      const int ip = s_ip;
       int nxt = -1;
       for (int i = 0; i < sq.m; ++i) {
         const VTreeNode nd = nodes[sq.node0 + i];
@@ -531,52 +670,35 @@ __global__ __launch_bounds__(kTreeThreads) void tree_decide_kernel(
       if (nxt < 0) break;
       u = nxt;
       ++d;
-      __syncthreads();
       continue;
     }
+    if (qrow >= 0) tree_row_stats(stats + static_cast<size_t>(qrow) * n_chunks, n_chunks, it, greedy, mq, sqs, iq);
     const float* zp = rows[prow].ptr;
-    const float mpc = s_st[0] * cs, isp = 1.f / s_st[1];
     const float* zq = qrow >= 0 ? rows[qrow].ptr : nullptr;
-    const float mqc = s_st[2] * cs, isq = 1.f / s_st[3];
-    // r_lv(y) from p(y), q(y) and the residual normalisers so far
-    auto r_at = [&](int y, int lv) {
-      float r = exp2f(zp[y] * cs - mpc) * isp;
-      if (lv > 0) {
-        const float q = exp2f(zq[y] * cs - mqc) * isq;
-        for (int l = 1; l <= lv; ++l)
-          if (!s_keep[l]) r = fmaxf(r - q, 0.f) * s_invz[l];
-      }
-      return r;
-    };
+    const float mpc = mp * cs, isp = 1.f / sp, mqc = mq * cs, isq = 1.f / sqs;
     const StreamId sid_acc = stream_id(seq_id, sq.base_pos + d + 1, 1);
     int lv = 0, acc = -1, j = 0;
     if (qrow >= 0) {
       for (int i = 0; i < sq.m; ++i) {
         const VTreeNode nd = nodes[sq.node0 + i];
         if (nd.parent != u) continue;
-        if (t == 0) {
-          const int x = row_tok[nd.p_row];
-          bool ok = false;
-          if (static_cast<unsigned>(x) < static_cast<unsigned>(V)) {  // an id outside the vocabulary is rejected
-            const float r = r_at(x, lv);
-            const float qx = exp2f(zq[x] * cs - mqc) * isq;
-            const float v = u01(philox_block(key, sid_acc, static_cast<uint32_t>(j)).x);
-            ok = v * qx < r;
-          }
-          s_flag = ok;
+        const int x = row_tok[nd.p_row];
+        bool ok = false;
+        if (static_cast<unsigned>(x) < static_cast<unsigned>(V)) {  // an id outside the vocabulary is rejected
+          float r = exp2f(zp[x] * cs - mpc) * isp;
+          const float qx = exp2f(zq[x] * cs - mqc) * isq;
+          for (int l = 1; l <= lv; ++l)
+            if (!s_keep[l]) r = fmaxf(r - qx, 0.f) * s_invz[l];
+          const float v = u01(philox_block(key, sid_acc, static_cast<uint32_t>(j)).x);
+          ok = v * qx < r;
         }
-        __syncthreads();
-        if (s_flag) {
+        if (ok) {
           acc = i;
           break;
         }
         ++lv;
-        float part = 0.f;
-        for (int y = t; y < V; y += kTreeThreads) {
-          const float q = exp2f(zq[y] * cs - mqc) * isq;
-          part += fmaxf(r_at(y, lv - 1) - q, 0.f);
-        }
-        const float z = tree_block_sum(part, s_red);
+        const float z = tree_z_total(zpart, b, s, lv, n_chunks);
+        __syncthreads();
         if (t == 0) {
           s_keep[lv] = !(z > 0.f);
           s_invz[lv] = z > 0.f ? 1.f / z : 1.f;
@@ -592,23 +714,17 @@ __global__ __launch_bounds__(kTreeThreads) void tree_decide_kernel(
       }
       u = acc;
       ++d;
-      __syncthreads();
       continue;
     }
-    // the draw: from r_lv after rejections (RESAMPLE), from p at a leaf
-    // (BONUS), by exponential race over 4 tokens per Philox block
-    const StreamId sid = stream_id(seq_id, sq.base_pos + d + 1, qrow >= 0 ? 2 : 3);
+    // the node's draw: the chunk winners merged across the wave
     float best = -1.f;
     int bi = INT_MAX;
-    for (int y4 = t; 4 * y4 < V; y4 += kTreeThreads) {
-      const uint4 w = philox_block(key, sid, static_cast<uint32_t>(y4));
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int y = 4 * y4 + e;
-        if (y < V) pick_update(r_at(y, lv) / exp2_variate(word_of(w, e)), y, best, bi);
-      }
+    if (t < n_chunks) {
+      const VPick pk = picks[(static_cast<size_t>(b) * kTreeMaxNodes + s) * kMaxChunks + t];
+      best = pk.score;
+      bi = pk.idx;
     }
-    tree_block_pick(best, bi, s_red, s_redi);
+    wave_pick(best, bi);
     if (t == 0) s_tok[d] = bi;
     break;
   }
@@ -833,6 +949,29 @@ VocabPlan vocab_plan(int B, int n_rows, int V, int chunk_rows) {
   return p;
 }
 
+// Entries rows x chunks of any plan over at most `units` rows (or
+// sequences): a plan's chunk count grows as its units shrink, so the product
+// is not monotonic in the units, but a chunk count never exceeds
+// ceil(kTargetBlocks / units) nor kMaxChunks.
+static size_t chunk_entries_bound(int units) {
+  const size_t u = static_cast<size_t>(std::max(units, 0));
+  return std::min(u * kMaxChunks, static_cast<size_t>(kTargetBlocks) + u);
+}
+
+size_t vocab_ws_bound(int B, int n_rows) {
+  return align256(sizeof(VStat) * chunk_entries_bound(n_rows)) + align256(sizeof(VPick) * chunk_entries_bound(B)) +
+         align256(sizeof(VDec) * static_cast<size_t>(std::max(B, 0)));
+}
+
+size_t tree_ws_bound(int B, int n_rows) {
+  const size_t b = static_cast<size_t>(std::max(B, 0));
+  return align256(sizeof(VStat) * chunk_entries_bound(n_rows)) +
+         align256(sizeof(float) * b * kTreeMaxNodes * kTreeMaxNodes * kMaxChunks) +
+         align256(sizeof(VPick) * b * kTreeMaxNodes * kMaxChunks);
+}
+
+size_t draft_ws_bound(int n) { return align256(sizeof(VPick) * chunk_entries_bound(n)); }
+
 size_t vocab_ws_bytes(const VocabPlan& p) {
   return align256(sizeof(VStat) * static_cast<size_t>(p.n_rows) * p.n_chunks1) +
          align256(sizeof(VPick) * static_cast<size_t>(p.B) * p.n_chunks2) +
@@ -893,14 +1032,26 @@ hipError_t launch_vocab_setup(int B, int kmax, const int32_t* d_k, const float* 
   return hipGetLastError();
 }
 
+size_t tree_ws_bytes(const VocabPlan& p) {
+  return align256(sizeof(VStat) * static_cast<size_t>(p.n_rows) * p.n_chunks1) +
+         align256(sizeof(float) * static_cast<size_t>(p.B) * kTreeMaxNodes * kTreeMaxNodes * kMaxChunks) +
+         align256(sizeof(VPick) * static_cast<size_t>(p.B) * kTreeMaxNodes * kMaxChunks);
+}
+
 hipError_t launch_tree_pass(const VocabPlan& p, const VRow* d_rows, const VTreeSeq* d_seqs,
                             const VTreeNode* d_nodes, const int32_t* d_row_tok, uint64_t seed,
-                            const uint64_t* d_seed, int kmax,
+                            const uint64_t* d_seed, int kmax, int max_kids,
                             int32_t* d_n_acc, int32_t* d_out_tok, int32_t* d_out_path, void* d_ws,
                             hipStream_t st, KernelTimer* timer) {
   if (p.B == 0) return hipSuccess;
-  if (p.n_chunks1 > kMaxChunks || kmax >= kTreeMaxNodes) return hipErrorInvalidValue;
-  VStat* stats = static_cast<VStat*>(d_ws);
+  if (p.n_chunks1 > kMaxChunks || kmax >= kTreeMaxNodes || max_kids < 0 || max_kids > kmax)
+    return hipErrorInvalidValue;
+  char* ws = static_cast<char*>(d_ws);
+  VStat* stats = reinterpret_cast<VStat*>(ws);
+  ws += align256(sizeof(VStat) * static_cast<size_t>(p.n_rows) * p.n_chunks1);
+  float* zpart = reinterpret_cast<float*>(ws);
+  ws += align256(sizeof(float) * static_cast<size_t>(p.B) * kTreeMaxNodes * kTreeMaxNodes * kMaxChunks);
+  VPick* picks = reinterpret_cast<VPick*>(ws);
   auto timed = [&](const char* name) { return timer && timer->wants(name); };
   // the vector path needs every row 16-byte aligned: rows are whole fp32
   // vocabulary rows of 16-byte aligned buffers when V % 4 == 0
@@ -915,10 +1066,18 @@ hipError_t launch_tree_pass(const VocabPlan& p, const VRow* d_rows, const VTreeS
     launch_kernel(stats_kernel<false>, g1, dim3(kThreads), 0, st, d_rows, p.V, p.chunk1, stats, p.n_chunks1,
                   nullptr);
   if (timed(n1)) timer->end(st, 4.0 * p.n_rows * p.V, 0.0);
-  if (timed("tree_decide_kernel")) timer->begin(st);
-  launch_kernel(tree_decide_kernel, dim3(p.B), dim3(kTreeThreads), 0, st, d_rows, d_seqs, d_nodes, d_row_tok,
-                stats, p.n_chunks1, p.V, seed, d_seed, kmax, d_n_acc, d_out_tok, d_out_path);
-  if (timed("tree_decide_kernel")) timer->end(st, 0.0, 0.0);
+  // the decision after the statistics: a residual-mass pass per level, the
+  // draws of every node, the walk (timed together as "tree_decision")
+  if (timed("tree_decision")) timer->begin(st);
+  const dim3 g2(p.n_chunks1, p.B * kTreeMaxNodes);
+  for (int L = 1; L <= max_kids; ++L)
+    launch_kernel(tree_z_kernel, g2, dim3(kThreads), 0, st, d_rows, d_seqs, d_nodes, stats, p.n_chunks1,
+                  p.chunk1, p.V, L, zpart);
+  launch_kernel(tree_draw_kernel, g2, dim3(kThreads), 0, st, d_rows, d_seqs, d_nodes, stats, p.n_chunks1,
+                p.chunk1, p.V, seed, d_seed, zpart, picks);
+  launch_kernel(tree_walk_kernel, dim3(p.B), dim3(kWave), 0, st, d_rows, d_seqs, d_nodes, d_row_tok, stats,
+                p.n_chunks1, p.V, seed, d_seed, zpart, picks, kmax, d_n_acc, d_out_tok, d_out_path);
+  if (timed("tree_decision")) timer->end(st, 0.0, 0.0);
   return hipGetLastError();
 }
 
