@@ -794,7 +794,7 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: sequences shard by data parallelism "
+        print(json.dumps({"error": "bench.py measures one GPU only: sequences shard by data parallelism "
                                    "with no exchange, so a multi-GPU figure is N independent copies of the "
                                    "one-GPU line; run with --gpus 1"}))
         sys.exit(2)
