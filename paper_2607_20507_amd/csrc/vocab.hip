@@ -504,9 +504,10 @@ __device__ __forceinline__ float tree_r_at(const TreeRes& R, int y, int lv) {
   return r;
 }
 
-// The residual state of slot s through level lv, for a whole workgroup (waves
-// 0 and 1 merge the p and q statistics; returns false for a greedy sequence).
-__device__ bool tree_res(const VRow* __restrict__ rows, const VTreeSeq& sq, const TreeSlot& ts,
+// The residual state of slot s through level lv (a sampled sequence), for a
+// whole workgroup: waves 0 and 1 merge the p and q statistics, threads
+// 1 .. lv sum the masses.
+__device__ void tree_res(const VRow* __restrict__ rows, const VTreeSeq& sq, const TreeSlot& ts,
                          const VStat* __restrict__ stats, const float* __restrict__ zpart, int b, int s, int lv,
                          int n_chunks, TreeRes& R) {
   __shared__ float s_st[4];
@@ -545,7 +546,6 @@ __device__ bool tree_res(const VRow* __restrict__ rows, const VTreeSeq& sq, cons
     R.keep[l] = !(z > 0.f);
     R.invz[l] = z > 0.f ? 1.f / z : 1.f;
   }
-  return true;
 }
 
 // Chunk c's share of Z_L at every slot with at least L children.
@@ -652,7 +652,7 @@ __global__ __launch_bounds__(kWave) void tree_walk_kernel(
     const int prow = u < 0 ? sq.p_row : nodes[sq.node0 + u].p_row;
     const int qrow = u < 0 ? sq.q_row : nodes[sq.node0 + u].q_row;
     float mp, sp, mq = 0.f, sqs = 1.f;
-    int ip, iq;
+    int ip, iq = 0;
     tree_row_stats(stats + static_cast<size_t>(prow) * n_chunks, n_chunks, it, greedy, mp, sp, ip);
     if (greedy) {
       int nxt = -1;
